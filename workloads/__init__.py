@@ -1,0 +1,172 @@
+"""Seeded synthetic inputs for the split-search hot path.
+
+Serves both the device path and the oracle; holds none of the method's
+arithmetic (no sketching, histograms, scores or partitions).  It produces
+what a boosting step hands to split search: the binned feature matrix, the
+gradient matrix G (stored column-major, as ``G_T`` with shape (d, n)), the
+hessian column h, and the random numbers a sketch draws (k uniforms for
+Random Sampling, the d x k matrix Pi for Random Projections).
+
+Workloads (shapes of the paper's synthetic timing experiment, Appendix B.7,
+and of its multiclass / multilabel datasets, Table 5; the public datasets
+themselves are not used):
+
+===================  =========  ====  ===  ====  =====================  =====
+name                 n          m     B    d     sketch                 depth
+===================  =========  ====  ===  ====  =====================  =====
+tiny_multiclass      10,000     10    256  5     identity (k = d)       3
+mc200k_top5          200,000    50    64   20    top outputs, k=5       6
+mc2m_rs5             2,000,000  100   256  100   random sampling, k=5   6
+mc2m_d1000_rp20      2,000,000  100   256  1000  random projection k=20 6
+ml1m_top10           1,000,000  200   256  500   top outputs, k=10      8
+===================  =========  ====  ===  ====  =====================  =====
+
+Recipes: multiclass gradients are softmax(z) - onehot(y) with logits
+z ~ N(0,1) and unit hessian; tiny_multiclass / mc200k_top5 draw bins
+uniformly and labels uniformly; the 2M-row workloads draw raw features
+X ~ N(0,1), quantile-bin each feature into 256 bins (edges at the empirical
+t/256 quantiles, t = 1..255, bin = number of edges below the value) and take
+labels y = argmax(X W + eps), W ~ N(0,1)/sqrt(m), eps ~ N(0,1).  The
+multilabel workload has Y ~ Bernoulli(0.05), g = sigmoid(z) - y and
+h_i = mean_j sigmoid(z_ij)(1 - sigmoid(z_ij)).  Gradients are formed in
+fp64 and stored as fp32.  lambda = 1 everywhere.
+"""
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    n: int
+    m: int
+    n_bins: int
+    d: int
+    k: int
+    kind: str          # identity | top_outputs | random_sampling | random_projection
+    depth: int
+    lam: float
+    seed: int
+    loss: str          # softmax | sigmoid
+    binning: str       # uniform | quantile
+    min_child_weight: float = 0.0
+
+
+WORKLOADS = {
+    "tiny_multiclass": Workload("tiny_multiclass", 10_000, 10, 256, 5, 5, "identity", 3, 1.0, 0,
+                                "softmax", "uniform"),
+    "mc200k_top5": Workload("mc200k_top5", 200_000, 50, 64, 20, 5, "top_outputs", 6, 1.0, 1,
+                            "softmax", "uniform"),
+    "mc2m_rs5": Workload("mc2m_rs5", 2_000_000, 100, 256, 100, 5, "random_sampling", 6, 1.0, 2,
+                         "softmax", "quantile"),
+    "mc2m_d1000_rp20": Workload("mc2m_d1000_rp20", 2_000_000, 100, 256, 1000, 20, "random_projection", 6,
+                                1.0, 3, "softmax", "quantile"),
+    "ml1m_top10": Workload("ml1m_top10", 1_000_000, 200, 256, 500, 10, "top_outputs", 8, 1.0, 4,
+                           "sigmoid", "quantile"),
+}
+
+
+def workload(name, **overrides):
+    """A named workload, optionally with fields replaced (e.g. a smaller n)."""
+    return replace(WORKLOADS[name], **overrides)
+
+
+def quantile_bin(x, n_bins):
+    """Bins of one raw feature column: number of empirical quantile edges below x.
+
+    Edges sit at the t/n_bins quantiles (t = 1..n_bins-1) with linear
+    interpolation between order statistics.
+    """
+    xs = np.sort(x)
+    n = xs.shape[0]
+    pos = np.arange(1, n_bins, dtype=np.float64) / n_bins * (n - 1)
+    lo = np.floor(pos).astype(np.int64)
+    hi = np.minimum(lo + 1, n - 1)
+    frac = pos - lo
+    edges = xs[lo].astype(np.float64) + frac * (xs[hi].astype(np.float64) - xs[lo].astype(np.float64))
+    return np.searchsorted(edges, x.astype(np.float64), side="left").astype(np.uint8)
+
+
+@dataclass
+class Inputs:
+    bins: np.ndarray      # (n, m) uint8, row-major
+    G_T: np.ndarray       # (d, n) float32: column j of G is G_T[j]
+    h: np.ndarray         # (n,) float32
+    u: np.ndarray         # (k,) float64 uniforms in [0, 1) for random sampling
+    Pi: np.ndarray        # (d, k) float32, N(0, 1/k), for random projections
+    wl: Workload
+
+    @property
+    def G(self):
+        """The n x d gradient matrix as a (non-contiguous) view."""
+        return self.G_T.T
+
+
+def _softmax_grad_T(z, y):
+    z = z.astype(np.float64)
+    z -= z.max(axis=1, keepdims=True)
+    p = np.exp(z)
+    p /= p.sum(axis=1, keepdims=True)
+    p[np.arange(z.shape[0]), y] -= 1.0
+    return p.astype(np.float32).T
+
+
+def make_inputs(wl, chunk=100_000):
+    """Generate the inputs of workload ``wl`` (deterministic in wl.seed)."""
+    rng = np.random.default_rng(wl.seed)
+    n, m, d, k, B = wl.n, wl.m, wl.d, wl.k, wl.n_bins
+    if wl.binning == "uniform":
+        bins = rng.integers(0, B, size=(n, m), dtype=np.uint8)
+        X = None
+    else:
+        X = rng.standard_normal((n, m), dtype=np.float32)
+        bins = np.empty((n, m), dtype=np.uint8)
+        for f in range(m):
+            bins[:, f] = quantile_bin(X[:, f], B)
+    G_T = np.empty((d, n), dtype=np.float32)
+    h = np.ones(n, dtype=np.float32)
+    if wl.loss == "softmax":
+        if X is None:
+            y_all = rng.integers(0, d, size=n)
+        else:
+            W = rng.standard_normal((m, d)).astype(np.float32) / np.float32(np.sqrt(m))
+            y_all = np.empty(n, dtype=np.int64)
+        for r0 in range(0, n, chunk):
+            r1 = min(n, r0 + chunk)
+            if X is not None:
+                logits = X[r0:r1] @ W + rng.standard_normal((r1 - r0, d), dtype=np.float32)
+                y_all[r0:r1] = np.argmax(logits, axis=1)
+            z = rng.standard_normal((r1 - r0, d))
+            G_T[:, r0:r1] = _softmax_grad_T(z, y_all[r0:r1])
+    elif wl.loss == "sigmoid":
+        for r0 in range(0, n, chunk):
+            r1 = min(n, r0 + chunk)
+            y = rng.random((r1 - r0, d)) < 0.05
+            z = rng.standard_normal((r1 - r0, d))
+            s = 1.0 / (1.0 + np.exp(-z))
+            G_T[:, r0:r1] = (s - y).astype(np.float32).T
+            h[r0:r1] = np.mean(s * (1.0 - s), axis=1).astype(np.float32)
+    else:
+        raise ValueError(wl.loss)
+    u = rng.random(k)
+    Pi = (rng.standard_normal((d, k)) / np.sqrt(k)).astype(np.float32)
+    return Inputs(bins=bins, G_T=G_T, h=h, u=u, Pi=Pi, wl=wl)
+
+
+def small_case(n, m, n_bins, d, seed, h_kind="ones", k=None):
+    """A small random case for unit and parity tests (uniform bins, softmax-like G)."""
+    rng = np.random.default_rng(seed)
+    bins = rng.integers(0, n_bins, size=(n, m), dtype=np.uint8)
+    y = rng.integers(0, d, size=n)
+    z = rng.standard_normal((n, d))
+    G_T = _softmax_grad_T(z, y) if d > 1 else rng.standard_normal((1, n)).astype(np.float32)
+    if h_kind == "ones":
+        h = np.ones(n, dtype=np.float32)
+    else:
+        h = rng.uniform(0.05, 0.25, size=n).astype(np.float32)
+    k = d if k is None else k
+    u = rng.random(k)
+    Pi = (rng.standard_normal((d, k)) / np.sqrt(k)).astype(np.float32)
+    wl = Workload("small", n, m, n_bins, d, k, "identity", 3, 1.0, seed, "softmax", "uniform")
+    return Inputs(bins=bins, G_T=G_T, h=h, u=u, Pi=Pi, wl=wl)
