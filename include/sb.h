@@ -1,0 +1,249 @@
+/*
+ * sb.h -- C ABI of libsketchboost: sketched multioutput split search on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the split-search hot path of SketchBoost (Iosipoi &
+ * Vakhrushev, "SketchBoost: Fast Gradient Boosted Decision Tree for
+ * Multioutput Problems", NeurIPS 2022, arXiv 2211.12858):
+ *
+ *   sketch the n x d gradient matrix G to k columns (Section 3.1 Top Outputs,
+ *   Section 3.2 Random Sampling, Section 3.3 Random Projections) -> per node,
+ *   feature and bin histograms of the k sketch columns plus the hessian
+ *   column (Section 3.4, histogram algorithm) -> score every threshold with
+ *   S(R) = sum_t (sum_{i in R} g_it)^2 / (sum_{i in R} h_i + lambda)
+ *   (Section 2, eq. 4, in the hessian-free form S_G of Section 3) -> best
+ *   split per node -> partition the node's rows; repeated level by level
+ *   (depth-wise growth, Appendix B.1).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All array arguments are DEVICE pointers owned by the caller (for example
+ *   torch tensors).  The library never allocates or frees device memory;
+ *   scratch memory is passed in as `ws` / `ws_bytes`, sized by
+ *   sb_workspace_bytes().  `ws` must be 256-byte aligned.
+ * - Every call checks its scalar arguments and pointer presence on the host
+ *   first; on failure it returns SB_E_ARG / SB_E_SHAPE / SB_E_UNSUPPORTED
+ *   before touching the device, and sb_last_error() explains why.  Then it
+ *   enqueues kernels on `stream` (a hipStream_t; NULL = default stream) and
+ *   returns without waiting.  Outputs are valid once the stream has reached
+ *   that point.  A launch failure returns SB_E_DEVICE.
+ * - Device-resident index arguments (row indices, node offsets, build lists,
+ *   split features) are clamped into range by the kernels so that a bad
+ *   value can never make an access leave its buffer; results for such input
+ *   are unspecified.  Floating-point inputs must be finite.
+ * - Node numbering is level-local: node j of a level has children 2j (rows
+ *   with bin <= threshold, "left") and 2j+1 ("right") on the next level.
+ * - Calls on different streams may run concurrently if their workspaces and
+ *   outputs do not overlap.  Only the error text is per-thread state.
+ * - Sizes: n < 2^31 rows, m <= 65535 features, 2 <= n_bins <= 256,
+ *   1 <= k <= 255 sketch columns (k+1 channels).
+ */
+#ifndef SB_H_
+#define SB_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SB_ABI_VERSION 1
+
+/* Status codes. */
+enum {
+  SB_OK = 0,
+  SB_E_ARG = 1,          /* bad scalar or missing pointer */
+  SB_E_SHAPE = 2,        /* inconsistent sizes, strides or alignment */
+  SB_E_UNSUPPORTED = 3,  /* unknown sketch kind or size outside the supported range */
+  SB_E_DEVICE = 4        /* a HIP launch or runtime call failed */
+};
+
+/* Sketch kinds (Section 3). */
+enum {
+  SB_SKETCH_TOP_OUTPUTS = 0,       /* Section 3.1 */
+  SB_SKETCH_RANDOM_SAMPLING = 1,   /* Section 3.2 */
+  SB_SKETCH_RANDOM_PROJECTION = 2, /* Section 3.3 */
+  SB_SKETCH_IDENTITY = 3           /* k == d: full-output scoring (no sketch) */
+};
+
+/* Call identifiers for sb_workspace_bytes(). */
+enum {
+  SB_CALL_SKETCH = 0,
+  SB_CALL_BUILD_HISTOGRAMS = 1,
+  SB_CALL_SCORE_SPLITS = 2,
+  SB_CALL_PARTITION_ROWS = 3,
+  SB_CALL_GROW_TREE = 4,
+  SB_CALL_HIST_EXPONENTS = 5
+};
+
+/* Text of the last non-OK status returned on this thread ("" if none). */
+const char* sb_last_error(void);
+
+/* SB_ABI_VERSION of the loaded library. */
+int32_t sb_abi_version(void);
+
+/*
+ * Workspace bytes needed by one call.  Arguments not used by a call are
+ * ignored (pass 0).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
+ * SCORE_SPLITS, PARTITION_ROWS).  depth: tree depth (GROW_TREE).  d: output
+ * dimension (SKETCH).  Returns -1 (and sets the error text) for invalid
+ * sizes.
+ */
+int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
+                           int32_t n_nodes, int32_t depth);
+
+/*
+ * sb_sketch -- build the packed sketch GH = [G_k, h] (Section 3).
+ *
+ * G       n x d gradient matrix, column-major: element (i, j) at G[j*ld_g + i],
+ *         ld_g >= n.
+ * h       n hessian weights (the denominator weights of S; 1 for the
+ *         hessian-free score of Section 3).
+ * kind    SB_SKETCH_*.
+ *   TOP_OUTPUTS      k columns of largest ||g_j||^2 (ties: lower j first),
+ *                    scale 1 (Section 3.1).  1 <= k <= d.
+ *   RANDOM_SAMPLING  k i.i.d. draws with p_j = ||g_j||^2 / sum_l ||g_l||^2
+ *                    (Section 3.2).  Draw t takes the first j with
+ *                    C_j > u[t] * C_{d-1}, where C_j is the left-to-right fp64
+ *                    prefix sum of the norms, and scales the column by
+ *                    fp32(sqrt(C_{d-1} / (k * ||g_j||^2))) = 1/sqrt(k p_j).
+ *                    If every column is zero: cols = -1, scales = 0, zero sketch.
+ *   RANDOM_PROJECTION G_k = G Pi with Pi the given d x k matrix (Section 3.3;
+ *                    the paper draws its entries i.i.d. N(0, 1/k)).  fp32
+ *                    accumulation.  cols / scales / norm2 are not written.
+ *   IDENTITY         k == d, GH = [G, h].
+ * u       RANDOM_SAMPLING only: k uniforms in [0, 1) (fp64, device).  The
+ *         random numbers are an input so that results are reproducible.
+ * Pi      RANDOM_PROJECTION only: d x k, row-major (Pi[j*k + t]), fp32.
+ * GH      out: n records of k+1 floats, record i at GH + i*ld_gh, ld_gh >= k+1;
+ *         GH[i*ld_gh + t] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
+ *         fp32 multiply; the projection sum for RANDOM_PROJECTION) and
+ *         GH[i*ld_gh + k] = h[i].
+ * cols, scales  out (not RANDOM_PROJECTION): k entries each.
+ * norm2   out: d fp64 squared column norms; required for TOP_OUTPUTS and
+ *         RANDOM_SAMPLING, optional (may be NULL) for IDENTITY, ignored for
+ *         RANDOM_PROJECTION.
+ * qexp    out: k+1 exponents for the fixed-point histogram accumulation of
+ *         sb_build_histograms (same rule as sb_hist_exponents).
+ */
+int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_hist_exponents -- fixed-point exponents for a given GH.
+ *
+ * For channel t (t <= k) with M_t = max_i |GH[i*ld_gh + t]|:
+ *   qexp[t] = 18 - floor(log2(M_t))   (qexp[t] = 0 if M_t == 0),
+ * so every value maps to an integer rint(v * 2^qexp[t]) of magnitude <= 2^19.
+ * sb_build_histograms accumulates those integers exactly and reports sums
+ * times 2^-qexp[t]; each element therefore contributes an error of at most
+ * half a quantum, 2^-(qexp[t]+1) <= 2^-19 M_t.  Exponents must stay fixed
+ * for every level of a tree so that sibling subtraction is exact.
+ */
+int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
+                          int64_t ws_bytes, void* stream);
+
+/*
+ * sb_build_histograms -- per-node histograms of one tree level (Section 3.4).
+ *
+ * For every built node j, feature f, bin b and channel t <= k:
+ *   H[((j*m + f)*n_bins + b)*(k+1) + t] = sum over rows r of node j with
+ *       bins[r*ld_bins + f] == b of GH[r*ld_gh + t],
+ * accumulated exactly in fixed point (see sb_hist_exponents) and written as
+ * fp64.  Nodes not in the build list are left untouched.
+ *
+ * bins      n x m uint8, row-major, ld_bins >= m, ld_bins % 4 == 0, 4-byte
+ *           aligned base.  Values must be < n_bins.
+ * GH, ld_gh, k, qexp  the sketch records and exponents from sb_sketch.
+ * row_idx   n row indices grouped by node (NULL = identity order).
+ * node_off  n_nodes+1 offsets: node j owns row_idx[node_off[j] .. node_off[j+1]).
+ * build_list  n_build node ids to build (NULL = every node; n_build ignored).
+ * H         out: [n_nodes][m][n_bins][k+1] fp64.
+ */
+int32_t sb_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
+                            const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+                            const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
+                            const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
+                            void* stream);
+
+/*
+ * sb_subtract_histograms -- sibling histograms by subtraction.
+ *
+ * For parent p < n_parents with built child c = build_list[p] (2p or 2p+1):
+ *   H_child[c ^ 1] = H_parent[p] - H_child[c]   (all m*n_bins*(k+1) cells).
+ * Exact, because histograms are fixed-point sums stored in fp64.  Entries of
+ * build_list that are not 2p or 2p+1 leave that pair untouched.
+ * H_parent: [n_parents][m][n_bins][k+1]; H_child: [2*n_parents][...], updated
+ * in place.
+ */
+int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t n_parents, int32_t m,
+                               int32_t n_bins, int32_t k, const int32_t* build_list, void* stream);
+
+/*
+ * sb_score_splits -- best split of every node of a level (Section 2).
+ *
+ * For node j, feature f and threshold b in [0, n_bins-2], left = bins <= b:
+ *   GL_t, HL = prefix sums over bins 0..b; GR_t = T_t - GL_t; HR = T_h - HL;
+ *   S = sum_{t<k} GL_t^2/(HL + lambda) + GR_t^2/(HR + lambda),
+ * valid iff HL > min_child_weight and HR > min_child_weight.  The best valid
+ * candidate maximises S; ties go to the lower f, then the lower b.  Scores
+ * are evaluated in fp64.  A node without a valid candidate gets
+ * (-1, -1, -inf).
+ * H: [n_nodes][m][n_bins][k+1] fp64.  lambda > 0, min_child_weight >= 0.
+ * best_feature, best_bin, best_score: out, n_nodes entries each.
+ */
+int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins, int32_t k, double lambda,
+                        double min_child_weight, int32_t* best_feature, int32_t* best_bin, double* best_score,
+                        void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_partition_rows -- split every node's rows for the next level.
+ *
+ * Node j's rows (row_idx_in[node_off_in[j] .. node_off_in[j+1]), identity
+ * order if row_idx_in is NULL) are split stably into left (bins_cm value of
+ * feature best_feature[j] <= best_bin[j]) then right, written to the same
+ * range of row_idx_out.  best_feature[j] < 0 marks a terminal node: every row
+ * goes left and the right child is empty.
+ * bins_cm   the binned features column-major: value (r, f) at
+ *           bins_cm[f*ld_cm + r], ld_cm >= n (same values as sb_build_histograms'
+ *           row-major copy; the column-major copy makes this call read one
+ *           contiguous run per node).
+ * node_off_out  out: 2*n_nodes+1 offsets of the next level.
+ * build_list_out out: n_nodes entries; entry j is the smaller child of node j
+ *           (2j on ties), the node whose histogram the next level builds.
+ * row_idx_in and row_idx_out must not overlap.
+ */
+int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
+                          const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
+                          const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
+                          int32_t* node_off_out, int32_t* build_list_out, void* ws, int64_t ws_bytes,
+                          void* stream);
+
+/*
+ * sb_grow_tree -- the whole level loop for one tree (depth-wise growth).
+ *
+ * Runs, for level l = 0..depth-1: build histograms (all rows at l = 0, the
+ * smaller child of each pair after that), sibling subtraction, scoring and
+ * partition, entirely on the device with no host synchronisation.
+ * bins (row-major, ld_bins) and bins_cm (column-major, ld_cm) hold the same
+ * binned features; GH / qexp come from sb_sketch.
+ * tree_feature, tree_bin, tree_score: out, 2^depth - 1 entries in level
+ *   order (node j of level l at index 2^l - 1 + j).
+ * row_idx_out: out, n rows grouped by leaf; leaf_off_out: out, 2^depth + 1
+ *   offsets of the leaves (leaf j of the last level owns
+ *   row_idx_out[leaf_off_out[j] .. leaf_off_out[j+1])).
+ * 1 <= depth <= 12.
+ */
+int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_cm, int64_t ld_cm, int64_t n,
+                     int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+                     int32_t depth, double lambda, double min_child_weight, int32_t* tree_feature,
+                     int32_t* tree_bin, double* tree_score, int32_t* row_idx_out, int32_t* leaf_off_out,
+                     void* ws, int64_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SB_H_ */

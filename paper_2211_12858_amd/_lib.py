@@ -1,0 +1,170 @@
+"""Thin ctypes binding of libsketchboost.so, one Python function per C entry point.
+
+Argument marshalling only: every array argument may be a torch tensor (its
+device pointer is passed), a raw integer address, or None (NULL).  A non-zero
+status raises :class:`SBError` carrying the library's error text.  The
+functions enqueue work on ``stream`` (a torch.cuda.Stream, a raw hipStream_t
+integer, or None for torch's current stream) and return immediately.
+
+Importing this module never falls back to anything: the library must be
+built (``python -m paper_2211_12858_amd.build``).
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsketchboost.so")
+
+SB_OK, SB_E_ARG, SB_E_SHAPE, SB_E_UNSUPPORTED, SB_E_DEVICE = 0, 1, 2, 3, 4
+SB_SKETCH_TOP_OUTPUTS, SB_SKETCH_RANDOM_SAMPLING, SB_SKETCH_RANDOM_PROJECTION, SB_SKETCH_IDENTITY = 0, 1, 2, 3
+(SB_CALL_SKETCH, SB_CALL_BUILD_HISTOGRAMS, SB_CALL_SCORE_SPLITS, SB_CALL_PARTITION_ROWS, SB_CALL_GROW_TREE,
+ SB_CALL_HIST_EXPONENTS) = range(6)
+
+KIND = {
+    "top_outputs": SB_SKETCH_TOP_OUTPUTS,
+    "random_sampling": SB_SKETCH_RANDOM_SAMPLING,
+    "random_projection": SB_SKETCH_RANDOM_PROJECTION,
+    "identity": SB_SKETCH_IDENTITY,
+}
+
+# Exported C symbols (kept in step with include/sb.h).
+SYMBOLS = (
+    "sb_last_error",
+    "sb_abi_version",
+    "sb_workspace_bytes",
+    "sb_sketch",
+    "sb_hist_exponents",
+    "sb_build_histograms",
+    "sb_subtract_histograms",
+    "sb_score_splits",
+    "sb_partition_rows",
+    "sb_grow_tree",
+)
+
+
+class SBError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("libsketchboost status %d: %s" % (code, msg))
+        self.code = code
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_U64 = ctypes.c_uint64
+_F64 = ctypes.c_double
+
+_PROTOS = {
+    "sb_last_error": (ctypes.c_char_p, []),
+    "sb_abi_version": (_I32, []),
+    "sb_workspace_bytes": (_I64, [_I32, _I64, _I32, _I32, _I32, _I32, _I32, _I32]),
+    "sb_sketch": (_I32, [_I32, _P, _I64, _I32, _I64, _P, _I32, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _I64, _P]),
+    "sb_hist_exponents": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I64, _P]),
+    "sb_build_histograms": (_I32, [_P, _I64, _I32, _I64, _I32, _P, _I64, _I32, _P, _P, _P, _I32, _P, _I32, _P,
+                                   _P, _I64, _P]),
+    "sb_subtract_histograms": (_I32, [_P, _P, _I32, _I32, _I32, _I32, _P, _P]),
+    "sb_score_splits": (_I32, [_P, _I32, _I32, _I32, _I32, _F64, _F64, _P, _P, _P, _P, _I64, _P]),
+    "sb_partition_rows": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _I64, _P]),
+    "sb_grow_tree": (_I32, [_P, _I64, _P, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _I32, _F64, _F64, _P, _P,
+                            _P, _P, _P, _P, _I64, _P]),
+}
+
+_lib = None
+
+
+def load():
+    """Load the shared library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libsketchboost.so is not built: run `python -m paper_2211_12858_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _PROTOS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(rc):
+    if rc != SB_OK:
+        raise SBError(rc, sb_last_error())
+    return rc
+
+
+def sb_last_error():
+    return load().sb_last_error().decode()
+
+
+def sb_abi_version():
+    return load().sb_abi_version()
+
+
+def sb_workspace_bytes(call, n=0, m=0, n_bins=0, d=0, k=0, n_nodes=0, depth=0):
+    v = load().sb_workspace_bytes(call, n, m, n_bins, d, k, n_nodes, depth)
+    if v < 0:
+        raise SBError(SB_E_ARG, sb_last_error())
+    return v
+
+
+def sb_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws, ws_bytes, stream=None):
+    return _check(load().sb_sketch(kind, _ptr(G), n, d, ld_g, _ptr(h), k, _ptr(u), _ptr(Pi), _ptr(GH), ld_gh,
+                                   _ptr(cols), _ptr(scales), _ptr(norm2), _ptr(qexp), _ptr(ws), ws_bytes,
+                                   _stream(stream)))
+
+
+def sb_hist_exponents(GH, n, ld_gh, k, qexp, ws, ws_bytes, stream=None):
+    return _check(load().sb_hist_exponents(_ptr(GH), n, ld_gh, k, _ptr(qexp), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def sb_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes, build_list,
+                        n_build, H, ws, ws_bytes, stream=None):
+    return _check(load().sb_build_histograms(_ptr(bins), n, m, ld_bins, n_bins, _ptr(GH), ld_gh, k, _ptr(qexp),
+                                             _ptr(row_idx), _ptr(node_off), n_nodes, _ptr(build_list), n_build,
+                                             _ptr(H), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def sb_subtract_histograms(H_parent, H_child, n_parents, m, n_bins, k, build_list, stream=None):
+    return _check(load().sb_subtract_histograms(_ptr(H_parent), _ptr(H_child), n_parents, m, n_bins, k,
+                                                _ptr(build_list), _stream(stream)))
+
+
+def sb_score_splits(H, n_nodes, m, n_bins, k, lam, min_child_weight, best_feature, best_bin, best_score, ws,
+                    ws_bytes, stream=None):
+    return _check(load().sb_score_splits(_ptr(H), n_nodes, m, n_bins, k, lam, min_child_weight, _ptr(best_feature),
+                                         _ptr(best_bin), _ptr(best_score), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def sb_partition_rows(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature, best_bin, row_idx_out,
+                      node_off_out, build_list_out, ws, ws_bytes, stream=None):
+    return _check(load().sb_partition_rows(_ptr(bins_cm), n, m, ld_cm, _ptr(row_idx_in), _ptr(node_off_in), n_nodes,
+                                           _ptr(best_feature), _ptr(best_bin), _ptr(row_idx_out),
+                                           _ptr(node_off_out), _ptr(build_list_out), _ptr(ws), ws_bytes,
+                                           _stream(stream)))
+
+
+def sb_grow_tree(bins, ld_bins, bins_cm, ld_cm, n, m, n_bins, GH, ld_gh, k, qexp, depth, lam, min_child_weight,
+                 tree_feature, tree_bin, tree_score, row_idx_out, leaf_off_out, ws, ws_bytes, stream=None):
+    return _check(load().sb_grow_tree(_ptr(bins), ld_bins, _ptr(bins_cm), ld_cm, n, m, n_bins, _ptr(GH), ld_gh, k,
+                                      _ptr(qexp), depth, lam, min_child_weight, _ptr(tree_feature), _ptr(tree_bin),
+                                      _ptr(tree_score), _ptr(row_idx_out), _ptr(leaf_off_out), _ptr(ws), ws_bytes,
+                                      _stream(stream)))

@@ -1,0 +1,327 @@
+// C ABI entry points: argument checks on the host, workspace sizing, launches,
+// and the device-resident level loop of sb_grow_tree.
+#include <cmath>
+#include <cstring>
+#include <string>
+
+#include "sb_common.h"
+
+namespace sb {
+
+namespace {
+thread_local std::string g_error;
+}
+
+void set_error(const std::string& msg) { g_error = msg; }
+
+int32_t fail(int32_t code, const std::string& msg) {
+  g_error = msg;
+  return code;
+}
+
+int32_t check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(SB_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+  return SB_OK;
+}
+
+namespace {
+
+constexpr int64_t MAX_ROWS = (int64_t(1) << 31) - 1;
+constexpr int MAX_DEPTH = 12;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int32_t need_ws(void* ws, int64_t have, int64_t need, const char* call) {
+  if (need < 0) return fail(SB_E_UNSUPPORTED, std::string(call) + ": sizes outside the supported range");
+  if (need > 0 && ws == nullptr) return fail(SB_E_ARG, std::string(call) + ": workspace is NULL");
+  if (have < need)
+    return fail(SB_E_ARG, std::string(call) + ": workspace too small: need " + std::to_string(need) + " bytes, got " +
+                              std::to_string(have));
+  if (ws && !aligned(ws, 256)) return fail(SB_E_SHAPE, std::string(call) + ": workspace must be 256-byte aligned");
+  return SB_OK;
+}
+
+int32_t check_hist_shape(const char* call, int64_t n, int32_t m, int32_t n_bins, int32_t k) {
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, std::string(call) + ": n must be in [1, 2^31)");
+  if (m < 1 || m > 65535) return fail(SB_E_ARG, std::string(call) + ": m must be in [1, 65535]");
+  if (n_bins < 2 || n_bins > 256) return fail(SB_E_ARG, std::string(call) + ": n_bins must be in [2, 256]");
+  if (k < 1 || k > 255) return fail(SB_E_ARG, std::string(call) + ": k must be in [1, 255]");
+  return SB_OK;
+}
+
+int64_t grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth, int64_t* off) {
+  // off[0] H0, off[1] H1, off[2] rows tmp, off[3] level offsets, off[4] build lists, off[5] call ws
+  const int64_t maxn = int64_t(1) << (depth - 1);
+  const int64_t hbytes = align256(maxn * m * n_bins * (int64_t)(k + 1) * 8);
+  const int64_t hw = hist_ws_bytes(m, n_bins, k, (int32_t)(maxn > 1 ? maxn / 1 : 1));
+  if (hw < 0) return -1;
+  int64_t call = hw;
+  const int64_t sw = score_ws_bytes((int32_t)maxn, m);
+  const int64_t pw = partition_ws_bytes(n, (int32_t)maxn);
+  if (sw > call) call = sw;
+  if (pw > call) call = pw;
+  int64_t p = 0;
+  off[0] = p;
+  p += hbytes;
+  off[1] = p;
+  p += hbytes;
+  off[2] = p;
+  p += align256(n * 4);
+  off[3] = p;
+  p += align256(((int64_t(1) << depth) + depth) * 4);
+  off[4] = p;
+  p += align256((int64_t(1) << depth) * 4);
+  off[5] = p;
+  p += call;
+  return p;
+}
+
+__global__ void k_root_offsets(int32_t* off, int32_t n) {
+  if (threadIdx.x == 0) {
+    off[0] = 0;
+    off[1] = n;
+  }
+}
+
+}  // namespace
+}  // namespace sb
+
+using namespace sb;
+
+extern "C" {
+
+const char* sb_last_error(void) { return g_error.c_str(); }
+
+int32_t sb_abi_version(void) { return SB_ABI_VERSION; }
+
+int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
+                           int32_t n_nodes, int32_t depth) {
+  switch (call) {
+    case SB_CALL_SKETCH:
+      if (n < 1 || d < 1 || k < 1) break;
+      return sketch_ws_bytes(0, n, d, k);
+    case SB_CALL_HIST_EXPONENTS:
+      if (k < 1) break;
+      return align256((int64_t)(k + 1) * 4);
+    case SB_CALL_BUILD_HISTOGRAMS: {
+      if (m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || n_nodes < 1) break;
+      const int64_t b = hist_ws_bytes(m, n_bins, k, n_nodes);
+      if (b < 0) break;
+      return b;
+    }
+    case SB_CALL_SCORE_SPLITS:
+      if (m < 1 || n_nodes < 1) break;
+      return score_ws_bytes(n_nodes, m);
+    case SB_CALL_PARTITION_ROWS:
+      if (n < 1 || n_nodes < 1) break;
+      return partition_ws_bytes(n, n_nodes);
+    case SB_CALL_GROW_TREE: {
+      if (n < 1 || m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || depth < 1 || depth > MAX_DEPTH) break;
+      int64_t off[6];
+      const int64_t b = grow_ws_layout(n, m, n_bins, k, depth, off);
+      if (b < 0) break;
+      return b;
+    }
+    default:
+      set_error("sb_workspace_bytes: unknown call id");
+      return -1;
+  }
+  set_error("sb_workspace_bytes: sizes outside the supported range");
+  return -1;
+}
+
+int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
+  if (kind < SB_SKETCH_TOP_OUTPUTS || kind > SB_SKETCH_IDENTITY)
+    return fail(SB_E_UNSUPPORTED, "sb_sketch: unknown sketch kind " + std::to_string(kind));
+  if (!G || !h || !GH || !qexp) return fail(SB_E_ARG, "sb_sketch: G, h, GH and qexp must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_sketch: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_sketch: d must be in [1, 65535]");
+  if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_sketch: k must be in [1, 255]");
+  if (ld_g < n) return fail(SB_E_SHAPE, "sb_sketch: ld_g must be >= n");
+  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_sketch: ld_gh must be >= k + 1");
+  switch (kind) {
+    case SB_SKETCH_TOP_OUTPUTS:
+      if (k > d) return fail(SB_E_ARG, "sb_sketch: top outputs needs k <= d");
+      if (!cols || !scales || !norm2) return fail(SB_E_ARG, "sb_sketch: cols, scales and norm2 must not be NULL");
+      break;
+    case SB_SKETCH_RANDOM_SAMPLING:
+      if (!u) return fail(SB_E_ARG, "sb_sketch: random sampling needs k uniforms u");
+      if (!cols || !scales || !norm2) return fail(SB_E_ARG, "sb_sketch: cols, scales and norm2 must not be NULL");
+      break;
+    case SB_SKETCH_RANDOM_PROJECTION:
+      if (!Pi) return fail(SB_E_ARG, "sb_sketch: random projection needs Pi");
+      break;
+    case SB_SKETCH_IDENTITY:
+      if (k != d) return fail(SB_E_ARG, "sb_sketch: identity sketch needs k == d");
+      if (!cols || !scales) return fail(SB_E_ARG, "sb_sketch: cols and scales must not be NULL");
+      break;
+  }
+  int32_t rc = need_ws(ws, ws_bytes, sketch_ws_bytes(kind, n, d, k), "sb_sketch");
+  if (rc) return rc;
+  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws,
+                       static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
+                          int64_t ws_bytes, void* stream) {
+  if (!GH || !qexp) return fail(SB_E_ARG, "sb_hist_exponents: GH and qexp must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_hist_exponents: n must be in [1, 2^31)");
+  if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_hist_exponents: k must be in [1, 255]");
+  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_hist_exponents: ld_gh must be >= k + 1");
+  int32_t rc = need_ws(ws, ws_bytes, align256((int64_t)(k + 1) * 4), "sb_hist_exponents");
+  if (rc) return rc;
+  return launch_hist_exponents(GH, n, ld_gh, k, qexp, ws, static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
+                            const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+                            const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
+                            const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
+                            void* stream) {
+  const char* call = "sb_build_histograms";
+  if (!bins || !GH || !qexp || !node_off || !H)
+    return fail(SB_E_ARG, "sb_build_histograms: bins, GH, qexp, node_off and H must not be NULL");
+  int32_t rc = check_hist_shape(call, n, m, n_bins, k);
+  if (rc) return rc;
+  if (ld_bins < m || ld_bins % 4 != 0 || !aligned(bins, 4))
+    return fail(SB_E_SHAPE, "sb_build_histograms: bins needs ld_bins >= m, ld_bins % 4 == 0 and a 4-byte aligned base");
+  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_build_histograms: ld_gh must be >= k + 1");
+  if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, "sb_build_histograms: n_nodes must be in [1, 2^20]");
+  if (build_list == nullptr) n_build = n_nodes;
+  if (n_build < 1 || n_build > n_nodes || n_build > 65535)
+    return fail(SB_E_ARG, "sb_build_histograms: n_build must be in [1, min(n_nodes, 65535)]");
+  if (hist_plan(m, n_bins, k, n_build).nq == 0)
+    return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) int32 cells exceed the 160 KB LDS");
+  rc = need_ws(ws, ws_bytes, hist_ws_bytes(m, n_bins, k, n_build), call);
+  if (rc) return rc;
+  return launch_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
+                                 build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t n_parents, int32_t m,
+                               int32_t n_bins, int32_t k, const int32_t* build_list, void* stream) {
+  if (!H_parent || !H_child || !build_list)
+    return fail(SB_E_ARG, "sb_subtract_histograms: H_parent, H_child and build_list must not be NULL");
+  int32_t rc = check_hist_shape("sb_subtract_histograms", 1, m, n_bins, k);
+  if (rc) return rc;
+  if (n_parents < 1 || n_parents > 65535)
+    return fail(SB_E_ARG, "sb_subtract_histograms: n_parents must be in [1, 65535]");
+  return launch_subtract(H_parent, H_child, n_parents, (int64_t)m * n_bins * (k + 1), build_list,
+                         static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins, int32_t k, double lambda,
+                        double min_child_weight, int32_t* best_feature, int32_t* best_bin, double* best_score,
+                        void* ws, int64_t ws_bytes, void* stream) {
+  if (!H || !best_feature || !best_bin || !best_score)
+    return fail(SB_E_ARG, "sb_score_splits: H and the outputs must not be NULL");
+  int32_t rc = check_hist_shape("sb_score_splits", 1, m, n_bins, k);
+  if (rc) return rc;
+  if (n_nodes < 1 || n_nodes > 65535) return fail(SB_E_ARG, "sb_score_splits: n_nodes must be in [1, 65535]");
+  if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_score_splits: lambda must be > 0");
+  if (!(min_child_weight >= 0.0) || !std::isfinite(min_child_weight))
+    return fail(SB_E_ARG, "sb_score_splits: min_child_weight must be >= 0");
+  rc = need_ws(ws, ws_bytes, score_ws_bytes(n_nodes, m), "sb_score_splits");
+  if (rc) return rc;
+  return launch_score(H, n_nodes, m, n_bins, k, lambda, min_child_weight, best_feature, best_bin, best_score, ws,
+                      static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
+                          const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
+                          const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
+                          int32_t* node_off_out, int32_t* build_list_out, void* ws, int64_t ws_bytes,
+                          void* stream) {
+  if (!bins_cm || !node_off_in || !best_feature || !best_bin || !row_idx_out || !node_off_out || !build_list_out)
+    return fail(SB_E_ARG, "sb_partition_rows: bins_cm, node_off_in, the splits and the outputs must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_partition_rows: n must be in [1, 2^31)");
+  if (m < 1) return fail(SB_E_ARG, "sb_partition_rows: m must be >= 1");
+  if (ld_cm < n) return fail(SB_E_SHAPE, "sb_partition_rows: ld_cm must be >= n");
+  if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, "sb_partition_rows: n_nodes must be in [1, 2^20]");
+  if (row_idx_in) {
+    const char* a0 = reinterpret_cast<const char*>(row_idx_in);
+    const char* b0 = reinterpret_cast<const char*>(row_idx_out);
+    if (a0 < b0 + n * 4 && b0 < a0 + n * 4)
+      return fail(SB_E_SHAPE, "sb_partition_rows: row_idx_in and row_idx_out overlap");
+  }
+  int32_t rc = need_ws(ws, ws_bytes, partition_ws_bytes(n, n_nodes), "sb_partition_rows");
+  if (rc) return rc;
+  return launch_partition(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature, best_bin,
+                          row_idx_out, node_off_out, build_list_out, ws, static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_cm, int64_t ld_cm, int64_t n,
+                     int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+                     int32_t depth, double lambda, double min_child_weight, int32_t* tree_feature,
+                     int32_t* tree_bin, double* tree_score, int32_t* row_idx_out, int32_t* leaf_off_out,
+                     void* ws, int64_t ws_bytes, void* stream) {
+  const char* call = "sb_grow_tree";
+  if (!bins || !bins_cm || !GH || !qexp || !tree_feature || !tree_bin || !tree_score || !row_idx_out ||
+      !leaf_off_out)
+    return fail(SB_E_ARG, "sb_grow_tree: inputs and outputs must not be NULL");
+  int32_t rc = check_hist_shape(call, n, m, n_bins, k);
+  if (rc) return rc;
+  if (depth < 1 || depth > MAX_DEPTH) return fail(SB_E_ARG, "sb_grow_tree: depth must be in [1, 12]");
+  if (ld_bins < m || ld_bins % 4 != 0 || !aligned(bins, 4))
+    return fail(SB_E_SHAPE, "sb_grow_tree: bins needs ld_bins >= m, ld_bins % 4 == 0 and a 4-byte aligned base");
+  if (ld_cm < n) return fail(SB_E_SHAPE, "sb_grow_tree: ld_cm must be >= n");
+  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_grow_tree: ld_gh must be >= k + 1");
+  if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_grow_tree: lambda must be > 0");
+  if (!(min_child_weight >= 0.0) || !std::isfinite(min_child_weight))
+    return fail(SB_E_ARG, "sb_grow_tree: min_child_weight must be >= 0");
+  if (hist_plan(m, n_bins, k, 1).nq == 0)
+    return fail(SB_E_UNSUPPORTED, "sb_grow_tree: 4 features x n_bins x (k+1) int32 cells exceed the 160 KB LDS");
+  int64_t off[6];
+  const int64_t need = grow_ws_layout(n, m, n_bins, k, depth, off);
+  rc = need_ws(ws, ws_bytes, need, call);
+  if (rc) return rc;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  double* Hbuf[2] = {reinterpret_cast<double*>(w + off[0]), reinterpret_cast<double*>(w + off[1])};
+  int32_t* rows_tmp = reinterpret_cast<int32_t*>(w + off[2]);
+  int32_t* offs = reinterpret_cast<int32_t*>(w + off[3]);
+  int32_t* blists = reinterpret_cast<int32_t*>(w + off[4]);
+  void* cws = w + off[5];
+  const int64_t cws_bytes = ws_bytes - off[5];
+  const int64_t cpn = (int64_t)m * n_bins * (k + 1);
+
+  // level l offsets start at offs + (2^l - 1) + l; level l build list at blists + 2^(l-1) - 1
+  auto level_off = [&](int l) { return offs + ((int64_t(1) << l) - 1) + l; };
+  auto level_build = [&](int l) { return blists + ((int64_t(1) << (l - 1)) - 1); };
+  auto level_rows = [&](int l) -> int32_t* {  // rows of level l >= 1; level depth lands in row_idx_out
+    return ((depth - l) % 2 == 0) ? row_idx_out : rows_tmp;
+  };
+
+  hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), (int32_t)n);
+  for (int l = 0; l < depth; ++l) {
+    const int32_t nn = 1 << l;
+    double* Hcur = Hbuf[l & 1];
+    const int32_t* row_in = l == 0 ? nullptr : level_rows(l);
+    const int32_t* off_l = level_off(l);
+    if (l == 0) {
+      rc = sb_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1, nullptr, 1, Hcur,
+                               cws, cws_bytes, st);
+    } else {
+      const int32_t* bl = level_build(l);
+      rc = sb_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn, bl, nn / 2, Hcur,
+                               cws, cws_bytes, st);
+      if (!rc) rc = launch_subtract(Hbuf[(l - 1) & 1], Hcur, nn / 2, cpn, bl, st);
+    }
+    if (rc) return rc;
+    const int64_t base = (int64_t(1) << l) - 1;
+    rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
+                      tree_score + base, cws, st);
+    if (rc) return rc;
+    int32_t* off_next = (l == depth - 1) ? leaf_off_out : level_off(l + 1);
+    rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,
+                          level_rows(l + 1), off_next, level_build(l + 1), cws, st);
+    if (rc) return rc;
+  }
+  return check_launch(call);
+}
+
+}  // extern "C"

@@ -1,0 +1,118 @@
+"""Helpers for the GPU parity tests: upload seeded inputs, call the C ABI, read back.
+
+Expected values always come from ``oracle`` on the same host inputs; nothing
+here computes the method.
+"""
+import math
+
+import numpy as np
+import torch
+
+from paper_2211_12858_amd import _lib as L
+from paper_2211_12858_amd.driver import workspace
+
+DEV = torch.device("cuda:0")
+TOL = 1e-4  # relative tolerance stated for histograms and scores
+
+
+def up(x, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(DEV)
+
+
+def sync():
+    torch.cuda.synchronize()
+
+
+def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None):
+    d, n = G_T.shape
+    ld_gh = k + 1 if ld_gh is None else ld_gh
+    Gd, hd = up(G_T), up(h)
+    GH = torch.zeros((n, ld_gh), dtype=torch.float32, device=DEV)
+    cols = torch.full((k,), -7, dtype=torch.int32, device=DEV)
+    scales = torch.zeros(k, dtype=torch.float32, device=DEV)
+    norm2 = torch.zeros(d, dtype=torch.float64, device=DEV)
+    qexp = torch.zeros(k + 1, dtype=torch.int32, device=DEV)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=n, d=d, k=k), DEV)
+    ud = up(u, torch.float64) if u is not None else None
+    Pid = up(Pi, torch.float32) if Pi is not None else None
+    L.sb_sketch(L.KIND[kind], Gd, n, d, n, hd, k, ud, Pid, GH, ld_gh, cols, scales, norm2, qexp, ws, ws.numel())
+    sync()
+    return (GH[:, :k + 1].cpu().numpy(), cols.cpu().numpy(), scales.cpu().numpy(), norm2.cpu().numpy(),
+            qexp.cpu().numpy())
+
+
+def qexp_rule(GH):
+    """Exponents by the documented rule, from a host GH (not from the device)."""
+    out = []
+    for t in range(GH.shape[1]):
+        mx = float(np.max(np.abs(GH[:, t].astype(np.float64)))) if GH.shape[0] else 0.0
+        out.append(18 - math.frexp(mx)[1] + 1 if mx > 0 else 0)
+    return np.array(out, dtype=np.int32)
+
+
+def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, ld_bins=None, H=None):
+    n, m = bins.shape
+    c = GH.shape[1]
+    k = c - 1
+    ld_bins = (m + 3) // 4 * 4 if ld_bins is None else ld_bins
+    bpad = np.zeros((n, ld_bins), dtype=np.uint8)
+    bpad[:, :m] = bins
+    n_nodes = len(node_off) - 1
+    n_build = n_nodes if build_list is None else len(build_list)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=n_bins, k=k,
+                                        n_nodes=max(n_nodes, n_build)), DEV)
+    if H is None:
+        H = torch.full((n_nodes, m, n_bins, c), float("nan"), dtype=torch.float64, device=DEV)
+    L.sb_build_histograms(up(bpad), n, m, ld_bins, n_bins, up(GH, torch.float32), c, k, up(qexp, torch.int32),
+                          None if row_idx is None else up(row_idx, torch.int32), up(node_off, torch.int32), n_nodes,
+                          None if build_list is None else up(build_list, torch.int32), n_build, H, ws, ws.numel())
+    sync()
+    return H
+
+
+def hist_tolerance_ok(Hg, Ho, counts, qexp, mass, chan_max):
+    """Check a device histogram against the oracle's.
+
+    Two bars: (1) the fixed-point bound, |Hg - Ho| <= count * 2^-(qexp+1),
+    exact arithmetic plus fp64 rounding of the oracle's own sum; (2) the
+    stated 1e-4 relative bar, relative to the larger of |Ho| and the cell's
+    absolute mass (sums of mixed-sign gradients cancel), with an absolute
+    floor of 1e-4 of one maximal row of that channel (chan_max).
+    """
+    half_q = np.ldexp(1.0, -(qexp.astype(np.int64) + 1))
+    bound1 = counts[..., None] * half_q + 1e-12 * mass
+    err = np.abs(Hg - Ho)
+    ok1 = err <= bound1
+    scale = np.maximum(np.maximum(np.abs(Ho), mass), chan_max)
+    ok2 = err <= TOL * scale
+    return bool(ok1.all()), bool(ok2.all()), float((err / scale).max())
+
+
+def run_score(H_np, n_bins, k, lam=1.0, mcw=0.0):
+    n_nodes, m = H_np.shape[:2]
+    Hd = up(H_np, torch.float64)
+    bf = torch.zeros(n_nodes, dtype=torch.int32, device=DEV)
+    bb = torch.zeros(n_nodes, dtype=torch.int32, device=DEV)
+    bs = torch.zeros(n_nodes, dtype=torch.float64, device=DEV)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_SCORE_SPLITS, m=m, n_nodes=n_nodes), DEV)
+    L.sb_score_splits(Hd, n_nodes, m, n_bins, k, lam, mcw, bf, bb, bs, ws, ws.numel())
+    sync()
+    return bf.cpu().numpy(), bb.cpu().numpy(), bs.cpu().numpy()
+
+
+def run_partition(bins, row_in, node_off, bf, bb):
+    n, m = bins.shape
+    n_nodes = len(node_off) - 1
+    bins_cm = up(np.ascontiguousarray(bins.T))
+    row_out = torch.full((n,), -1, dtype=torch.int32, device=DEV)
+    off_out = torch.full((2 * n_nodes + 1,), -1, dtype=torch.int32, device=DEV)
+    bl_out = torch.full((n_nodes,), -1, dtype=torch.int32, device=DEV)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=n, n_nodes=n_nodes), DEV)
+    L.sb_partition_rows(bins_cm, n, m, n, None if row_in is None else up(row_in, torch.int32),
+                        up(node_off, torch.int32), n_nodes, up(bf, torch.int32), up(bb, torch.int32), row_out, off_out,
+                        bl_out, ws, ws.numel())
+    sync()
+    return row_out.cpu().numpy(), off_out.cpu().numpy(), bl_out.cpu().numpy()

@@ -1,0 +1,212 @@
+"""C-ABI contract checks that need no GPU.
+
+The library must load, export every function include/sb.h declares, and
+reject bad arguments on the host with the documented status before any
+device work (these calls never reach a kernel launch).
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2211_12858_amd import build as sb_build
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "sb.h")
+FAKE = 0x100000  # non-NULL address that is never dereferenced (validation fails first)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(sb_build.LIB):
+        sb_build.build()
+    from paper_2211_12858_amd import _lib
+    _lib.load()
+    return _lib
+
+
+def header_functions():
+    text = open(HDR).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**\s*(sb_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    fns = header_functions()
+    for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
+                 "sb_partition_rows", "sb_grow_tree", "sb_last_error", "sb_abi_version", "sb_workspace_bytes"):
+        assert name in fns
+
+
+def test_every_declared_symbol_is_exported(L):
+    fns = header_functions()
+    out = subprocess.run(["nm", "-D", "--defined-only", sb_build.LIB], capture_output=True, text=True, check=True).stdout
+    exported = set(ln.split()[-1] for ln in out.splitlines() if ln.strip())
+    missing = [f for f in fns if f not in exported]
+    assert not missing, missing
+    assert sorted(L.SYMBOLS) == fns
+
+
+def test_version_and_error_text(L):
+    assert L.sb_abi_version() == 1
+    assert isinstance(L.sb_last_error(), str)
+
+
+def test_workspace_bytes(L):
+    assert L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=1000, d=20, k=5) > 0
+    assert L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=1000, m=100, n_bins=256, k=5, n_nodes=16) > 0
+    assert L.sb_workspace_bytes(L.SB_CALL_SCORE_SPLITS, m=100, n_nodes=32) >= 32 * 100 * 12
+    assert L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=10_000, n_nodes=8) >= 10_000
+    assert L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10_000, m=10, n_bins=256, k=5, depth=3) > 0
+    with pytest.raises(L.SBError):
+        L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10, m=10, n_bins=256, k=5, depth=13)
+    with pytest.raises(L.SBError):
+        L.sb_workspace_bytes(99)
+    with pytest.raises(L.SBError):  # 4 features x 256 bins x 101 channels do not fit the LDS budget
+        L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=10, m=8, n_bins=256, k=100, n_nodes=1)
+
+
+def _code(fn, *args):
+    from paper_2211_12858_amd import _lib
+    with pytest.raises(_lib.SBError) as e:
+        fn(*args)
+    return e.value.code
+
+
+F = FAKE
+
+
+def sketch_args(**kw):
+    a = dict(kind=0, G=F, n=100, d=10, ld_g=100, h=F, k=3, u=F, Pi=F, GH=F, ld_gh=4, cols=F, scales=F, norm2=F,
+             qexp=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(kind=7), 3),
+    (dict(G=None), 1),
+    (dict(n=0), 1),
+    (dict(k=0), 1),
+    (dict(k=11, ld_gh=12), 1),       # top outputs needs k <= d
+    (dict(ld_g=99), 2),
+    (dict(ld_gh=3), 2),
+    (dict(kind=1, u=None), 1),
+    (dict(kind=2, Pi=None), 1),
+    (dict(kind=3, k=4, ld_gh=5), 1), # identity needs k == d
+    (dict(ws_bytes=16), 1),
+    (dict(ws=F + 8), 2),             # misaligned workspace
+    (dict(ws=None), 1),
+])
+def test_sketch_rejects(L, kw, code):
+    assert _code(L.sb_sketch, *sketch_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_sketch")
+
+
+def hist_args(**kw):
+    a = dict(bins=F, n=1000, m=10, ld_bins=12, n_bins=256, GH=F, ld_gh=6, k=5, qexp=F, row_idx=None, node_off=F,
+             n_nodes=2, build_list=F, n_build=1, H=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bins=None), 1),
+    (dict(H=None), 1),
+    (dict(n=0), 1),
+    (dict(m=0), 1),
+    (dict(n_bins=1), 1),
+    (dict(n_bins=257), 1),
+    (dict(k=0), 1),
+    (dict(ld_bins=10), 2),           # not a multiple of 4
+    (dict(ld_bins=8), 2),            # < m
+    (dict(bins=F + 2), 2),           # misaligned base
+    (dict(ld_gh=5), 2),
+    (dict(n_nodes=0), 1),
+    (dict(n_build=3), 1),            # more than n_nodes
+    (dict(k=100, ld_gh=101), 3),     # LDS budget exceeded
+    (dict(ws_bytes=100), 1),
+])
+def test_build_histograms_rejects(L, kw, code):
+    assert _code(L.sb_build_histograms, *hist_args(**kw)) == code
+
+
+def test_subtract_rejects(L):
+    assert _code(L.sb_subtract_histograms, F, F, 0, 10, 256, 5, F, 0) == 1
+    assert _code(L.sb_subtract_histograms, None, F, 1, 10, 256, 5, F, 0) == 1
+    assert _code(L.sb_subtract_histograms, F, F, 1, 10, 300, 5, F, 0) == 1
+
+
+def score_args(**kw):
+    a = dict(H=F, n_nodes=4, m=10, n_bins=256, k=5, lam=1.0, mcw=0.0, bf=F, bb=F, bs=F, ws=F, ws_bytes=1 << 30,
+             stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=None), 1),
+    (dict(bs=None), 1),
+    (dict(n_nodes=0), 1),
+    (dict(lam=0.0), 1),
+    (dict(lam=float("nan")), 1),
+    (dict(mcw=-1.0), 1),
+    (dict(ws_bytes=8), 1),
+])
+def test_score_rejects(L, kw, code):
+    assert _code(L.sb_score_splits, *score_args(**kw)) == code
+
+
+def part_args(**kw):
+    a = dict(bins_cm=F, n=1000, m=10, ld_cm=1000, row_in=F, off_in=F, n_nodes=2, bf=F, bb=F, row_out=F + 100000,
+             off_out=F, build_out=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bins_cm=None), 1),
+    (dict(row_out=None), 1),
+    (dict(n=0), 1),
+    (dict(ld_cm=999), 2),
+    (dict(n_nodes=0), 1),
+    (dict(row_out=F + 100), 2),      # overlaps row_in
+    (dict(ws_bytes=10), 1),
+])
+def test_partition_rejects(L, kw, code):
+    assert _code(L.sb_partition_rows, *part_args(**kw)) == code
+
+
+def grow_args(**kw):
+    a = dict(bins=F, ld_bins=12, bins_cm=F, ld_cm=1000, n=1000, m=10, n_bins=256, GH=F, ld_gh=6, k=5, qexp=F,
+             depth=3, lam=1.0, mcw=0.0, tf=F, tb=F, ts=F, rows=F, leaf=F, ws=F, ws_bytes=1 << 34, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bins=None), 1),
+    (dict(depth=0), 1),
+    (dict(depth=13), 1),
+    (dict(ld_cm=10), 2),
+    (dict(ld_bins=11), 2),
+    (dict(lam=-1.0), 1),
+    (dict(ws_bytes=1000), 1),
+])
+def test_grow_tree_rejects(L, kw, code):
+    assert _code(L.sb_grow_tree, *grow_args(**kw)) == code
+
+
+def test_error_text_is_per_thread(L):
+    import threading
+    _code(L.sb_grow_tree, *grow_args(depth=0))
+    seen = {}
+
+    def other():
+        seen["msg"] = L.sb_last_error()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["msg"] == ""
+    assert "depth" in L.sb_last_error()

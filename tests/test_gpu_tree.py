@@ -1,0 +1,126 @@
+"""Whole-tree parity: sketch + depth-wise level loop on the device vs the oracle.
+
+Split identity rule: where the oracle's best and runner-up scores differ by
+more than 1e-4 of the best, the device must pick the oracle's (feature, bin).
+Otherwise its pick must score within 1e-4 of the best in the oracle's own
+arithmetic, and the oracle then follows the device's pick so that the rest
+of the tree stays comparable.  Leaf row sets are compared bit-exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import make_inputs, small_case, workload
+
+pytestmark = pytest.mark.gpu
+
+import gpu_util as gu  # noqa: E402
+from paper_2211_12858_amd.driver import SplitSearch  # noqa: E402
+
+
+def grow_on_device(inp, kind, k, depth, lam=1.0, mcw=0.0, interleave=True, n_bins=None):
+    n_bins = inp.wl.n_bins if n_bins is None else n_bins
+    ss = SplitSearch(inp.bins, n_bins, k, depth, lam, mcw, device=gu.DEV, interleave=interleave)
+    G_T = gu.up(inp.G_T)
+    h = gu.up(inp.h)
+    u = gu.up(inp.u[:k], torch.float64)
+    Pi = gu.up(inp.Pi[:, :k] if inp.Pi.shape[1] >= k else inp.Pi, torch.float32)
+    ss.step(kind, G_T, h, u=u, Pi=Pi)
+    gu.sync()
+    return ss
+
+
+def check_tree(inp, kind, k, depth, lam=1.0, mcw=0.0, interleave=True, n_bins=None):
+    n_bins = inp.wl.n_bins if n_bins is None else n_bins
+    ss = grow_on_device(inp, kind, k, depth, lam, mcw, interleave, n_bins)
+    dev = ss.tree()
+    GH_dev = ss.gh()
+    GH_o, cols, scales, _ = oracle.sketch(kind, inp.G, inp.h, k, u=inp.u[:k], Pi=inp.Pi)
+    if kind != "random_projection":
+        assert np.array_equal(ss.cols.cpu().numpy(), cols)
+        assert np.array_equal(GH_dev.view(np.uint32), GH_o.view(np.uint32))
+    stats = {"near_ties": 0, "nodes": 0}
+
+    def choose(level, j, f, b, s1, s2, S, valid):
+        gf, gb, gs = int(dev["feature"][level][j]), int(dev["bin"][level][j]), float(dev["score"][level][j])
+        stats["nodes"] += 1
+        if f < 0:
+            assert (gf, gb) == (-1, -1) and gs == -np.inf, (level, j)
+            return f, b
+        assert gf >= 0 and valid[gf, gb], (level, j, gf, gb)
+        if s1 - s2 > gu.TOL * s1:
+            assert (gf, gb) == (f, b), (level, j, (gf, gb), (f, b), s1, s2)
+        else:
+            stats["near_ties"] += 1
+            assert S[gf, gb] >= s1 * (1 - gu.TOL), (level, j)
+        assert abs(gs - S[gf, gb]) <= gu.TOL * max(s1, 1e-30), (level, j, gs, S[gf, gb])
+        return gf, gb
+
+    tree = oracle.grow_tree(inp.bins, GH_o, depth, lam, n_bins, mcw, choose=choose)
+    sizes = [len(s) for s in tree["segments"]]
+    assert np.array_equal(dev["leaf_off"], np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32))
+    assert np.array_equal(dev["row_idx"], np.concatenate(tree["segments"]).astype(np.int32))
+    return stats
+
+
+def test_tree_tiny_multiclass_full():
+    wl = workload("tiny_multiclass")
+    check_tree(make_inputs(wl), "identity", wl.k, wl.depth)
+
+
+def test_tree_200k_top_outputs_full():
+    wl = workload("mc200k_top5")
+    check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth)
+
+
+def test_tree_2m_random_sampling_reduced():
+    wl = workload("mc2m_rs5", n=60_001)
+    check_tree(make_inputs(wl), "random_sampling", wl.k, wl.depth)
+
+
+def test_tree_d1000_random_projection_reduced():
+    wl = workload("mc2m_d1000_rp20", n=20_000)
+    check_tree(make_inputs(wl), "random_projection", wl.k, wl.depth)
+
+
+def test_tree_multilabel_top10_reduced():
+    wl = workload("ml1m_top10", n=30_000)
+    check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth)
+
+
+def test_tree_separate_gh_layout():
+    wl = workload("mc200k_top5", n=50_000)
+    check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth, interleave=False)
+
+
+@pytest.mark.parametrize("n,m,B,d,depth", [(1, 1, 2, 2, 3), (7, 2, 2, 3, 4), (300, 5, 3, 2, 5), (4099, 9, 16, 4, 7)])
+def test_tree_edge_shapes(n, m, B, d, depth):
+    # tiny and ragged inputs, depth beyond what the rows can split (terminal
+    # nodes and empty children on deep levels)
+    check_tree(small_case(n, m, B, d, seed=n), "identity", d, depth, n_bins=B)
+
+
+def test_tree_constant_features_are_terminal():
+    case = small_case(5000, 4, 8, 3, seed=1)
+    case.bins[:] = 3
+    ss = grow_on_device(case, "identity", 3, 3, n_bins=8)
+    dev = ss.tree()
+    assert all((f == -1).all() for f in dev["feature"])
+    assert dev["leaf_off"][1] == 5000 and (dev["leaf_off"][1:] == 5000).all()
+    assert np.array_equal(dev["row_idx"], np.arange(5000, dtype=np.int32))
+
+
+def test_tree_deterministic_repeat():
+    wl = workload("mc200k_top5", n=100_000)
+    inp = make_inputs(wl)
+    ss = grow_on_device(inp, "top_outputs", wl.k, wl.depth)
+    a = ss.tree()
+    for _ in range(3):
+        ss.step("top_outputs", gu.up(inp.G_T), gu.up(inp.h))
+        gu.sync()
+        b = ss.tree()
+        for key in ("feature", "bin", "score"):
+            for x, y in zip(a[key], b[key]):
+                assert np.array_equal(x, y)
+        assert np.array_equal(a["row_idx"], b["row_idx"])
