@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark of the sketched split-search hot path on one MI355X.
+
+One step is one tree: the sketch of the gradient matrix (taken once per tree)
+followed by the depth-wise level loop (histograms of the built nodes, sibling
+subtraction, scoring, partition) for every level.  Workload: 2,000,000 rows,
+100 features quantile-binned to 256 bins, 100 softmax outputs, Random
+Sampling sketch with k = 5, depth 6, lambda = 1 (the shape of the paper's
+synthetic timing experiment, Appendix B.7).  Inputs are generated on the
+host, uploaded once, and resident in HBM when timing starts; each tree uses
+its own k uniforms.
+
+Prints one JSON line on stdout.  Besides seconds per tree it reports the
+histogram kernel's algorithmic bandwidth against the 8 TB/s HBM peak
+(``roofline``) and the CPU oracle timed on this host (``cpu_baseline``).
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBPS = 8000.0
+METRIC = "sec per tree (depth 6) + histogram-build HBM GB/s (% of peak)"
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "hist_traffic.json")
+HIST_SRC = os.path.join(HERE, "paper_2211_12858_amd", "csrc", "sb_hist.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def level_sizes(leaf_off, depth):
+    """Node sizes of every level, from the leaf offsets of the finished tree."""
+    leaf_off = np.asarray(leaf_off, dtype=np.int64)
+    out = []
+    for l in range(depth):
+        span = 1 << (depth - l)
+        edges = leaf_off[::span]
+        out.append(np.diff(edges))
+    return out
+
+
+def hist_algorithmic_bytes(leaf_off, depth, m, n_bins, c):
+    """Algorithmic bytes of the histogram kernel over one tree, per launch.
+
+    Per level: every built row is read once (m bin bytes + 4c sketch bytes)
+    and every built node's histogram is written once (m * n_bins * c * 4).
+    Level 0 builds the root; level l >= 1 builds the smaller child of each
+    pair (ties: left), the other child coming from subtraction.
+    """
+    sizes = level_sizes(leaf_off, depth)
+    per_launch = []
+    for l in range(depth):
+        s = sizes[l]
+        if l == 0:
+            rows, nodes = int(s.sum()), 1
+        else:
+            left, right = s[0::2], s[1::2]
+            rows, nodes = int(np.minimum(left, right).sum()), len(left)
+        per_launch.append(rows * (m + 4 * c) + nodes * m * n_bins * c * 4)
+    return per_launch
+
+
+def traffic_for_current_kernel():
+    """Counter-measured HBM bytes per histogram launch, if taken on this kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        src = hashlib.sha256(open(HIST_SRC, "rb").read()).hexdigest()
+        if rec.get("kernel_source_sha256") != src:
+            return None
+        return rec.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(inp, wl, sample_rows):
+    """Time the oracle (as it stands) for one tree on the first sample_rows rows."""
+    import oracle
+    ns = min(sample_rows, wl.n)
+    bins = inp.bins[:ns]
+    G = inp.G_T[:, :ns].T
+    h = inp.h[:ns]
+    t0 = time.perf_counter()
+    GH, _, _, _ = oracle.sketch(wl.kind, G, h, wl.k, u=inp.u, Pi=inp.Pi)
+    oracle.grow_tree(bins, GH, wl.depth, wl.lam, wl.n_bins, wl.min_child_weight)
+    dt = time.perf_counter() - t0
+    scale = wl.n / ns
+    return {
+        "value": dt * scale,
+        "unit": "s/tree",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": "one tree (sketch + %d levels) on the first %d of %d rows, %.2f s measured, scaled x%.1f "
+                  "(the oracle's work is linear in rows); numpy, single thread; host has %d cores"
+                  % (wl.depth, ns, wl.n, dt, scale, len(os.sched_getaffinity(0))),
+    }
+
+
+def copy_probe(nbytes):
+    """A plain device copy of known size, the reference for scaling HBM counters."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mc2m_rs5")
+    ap.add_argument("--cpu-sample-rows", type=int, default=800_000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
+    ap.add_argument("--layout", choices=("separate", "interleaved"), default="separate",
+                    help="sketch records in their own array, or inside 128-byte row records with the bins")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU; --gpus %d is not supported (multi-GPU is design only)"
+              % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    import torch
+    sys.path.insert(0, HERE)
+    from workloads import make_inputs, workload
+    from paper_2211_12858_amd import _lib as L
+    from paper_2211_12858_amd.driver import SplitSearch
+
+    L.load()  # fails loudly if the HIP library is not built
+    wl = workload(args.workload)
+    t0 = time.perf_counter()
+    log("bench: generating %s (n=%d m=%d d=%d)" % (wl.name, wl.n, wl.m, wl.d))
+    inp = make_inputs(wl)
+    log("bench: inputs ready in %.1f s" % (time.perf_counter() - t0))
+
+    dev = torch.device("cuda:0")
+    ss = SplitSearch(inp.bins, wl.n_bins, wl.k, wl.depth, wl.lam, wl.min_child_weight, device=dev,
+                     interleave=args.layout == "interleaved")
+    G_T = torch.from_numpy(inp.G_T).to(dev)
+    h = torch.from_numpy(inp.h).to(dev)
+    Pi = torch.from_numpy(inp.Pi).to(dev)
+    K, W = args.steps, args.warmup
+    rng = np.random.default_rng(wl.seed + 1000)
+    u_all = torch.from_numpy(rng.random((K + W, wl.k))).to(dev)
+    torch.cuda.synchronize()
+    log("bench: resident in HBM; %d warmup + %d timed trees" % (W, K))
+
+    for s in range(W):
+        ss.step(wl.kind, G_T, h, u=u_all[s], Pi=Pi)
+    torch.cuda.synchronize()
+
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    L.sb_profile_begin()
+    start.record()
+    for s in range(K):
+        ss.step(wl.kind, G_T, h, u=u_all[W + s], Pi=Pi)
+    stop.record()
+    torch.cuda.synchronize()
+    hist_ms, launches = L.sb_profile_end()
+    total_ms = start.elapsed_time(stop)
+    log("bench: %d trees in %.3f ms; histogram kernel %.3f ms over %d launches" % (K, total_ms, hist_ms, launches))
+
+    # algorithmic bytes of every timed histogram launch (trees are deterministic
+    # in their uniforms, so replaying one reproduces its node sizes)
+    alg = []
+    for s in range(K):
+        ss.step(wl.kind, G_T, h, u=u_all[W + s], Pi=Pi)
+        torch.cuda.synchronize()
+        alg += hist_algorithmic_bytes(ss.leaf_off.cpu().numpy(), wl.depth, wl.m, wl.n_bins, wl.k + 1)
+    assert len(alg) == launches, (len(alg), launches)
+    bytes_per_launch = float(np.mean(alg))
+    ms_per_launch = hist_ms / launches
+    achieved = bytes_per_launch / (ms_per_launch * 1e-3) / 1e9
+    traffic = traffic_for_current_kernel()
+
+    sec_per_tree = total_ms / K / 1e3
+    out = {
+        "metric": METRIC,
+        "value": sec_per_tree,
+        "unit": "s/tree",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": total_ms / K,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 sketch, i32 fixed-point histogram accumulation, f64 scores",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: n=%d rows, m=%d features, %d quantile bins, d=%d softmax outputs, %s sketch k=%d, "
+                        "depth %d, lambda=%g" % (wl.name, wl.n, wl.m, wl.n_bins, wl.d, wl.kind.replace("_", " "),
+                                                 wl.k, wl.depth, wl.lam),
+            "layout": args.layout,
+        },
+        "hist_GBps": achieved,
+        "hist_pct_peak": 100.0 * achieved / HBM_PEAK_GBPS,
+        "hist_ms_per_tree": hist_ms / K,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "kernel": "k_hist",
+            "bytes_per_launch": bytes_per_launch,
+            "ms_per_launch": ms_per_launch,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_sample_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -242,6 +242,18 @@ int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_c
                      int32_t* tree_bin, double* tree_score, int32_t* row_idx_out, int32_t* leaf_off_out,
                      void* ws, int64_t ws_bytes, void* stream);
 
+/*
+ * Kernel timing for benchmarks.  Between sb_profile_begin() and
+ * sb_profile_end() on one host thread, every launch of the histogram kernel
+ * (the LDS-accumulation kernel inside sb_build_histograms and sb_grow_tree)
+ * is bracketed by a pair of HIP events recorded on the same stream.
+ * sb_profile_end() waits for the last event, returns the summed kernel time
+ * in milliseconds and the number of launches, and releases the events.
+ * Creating events is host-side work; no device memory is allocated.
+ */
+int32_t sb_profile_begin(void);
+int32_t sb_profile_end(double* hist_kernel_ms, int64_t* hist_launches);
+
 #ifdef __cplusplus
 }
 #endif

@@ -39,6 +39,8 @@ SYMBOLS = (
     "sb_score_splits",
     "sb_partition_rows",
     "sb_grow_tree",
+    "sb_profile_begin",
+    "sb_profile_end",
 )
 
 
@@ -68,6 +70,9 @@ _PROTOS = {
     "sb_grow_tree": (_I32, [_P, _I64, _P, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _I32, _F64, _F64, _P, _P,
                             _P, _P, _P, _P, _I64, _P]),
 }
+
+_PROTOS["sb_profile_begin"] = (_I32, [])
+_PROTOS["sb_profile_end"] = (_I32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)])
 
 _lib = None
 
@@ -168,3 +173,15 @@ def sb_grow_tree(bins, ld_bins, bins_cm, ld_cm, n, m, n_bins, GH, ld_gh, k, qexp
                                       _ptr(qexp), depth, lam, min_child_weight, _ptr(tree_feature), _ptr(tree_bin),
                                       _ptr(tree_score), _ptr(row_idx_out), _ptr(leaf_off_out), _ptr(ws), ws_bytes,
                                       _stream(stream)))
+
+
+def sb_profile_begin():
+    return _check(load().sb_profile_begin())
+
+
+def sb_profile_end():
+    """Returns (summed histogram-kernel milliseconds, number of launches)."""
+    ms = ctypes.c_double(0.0)
+    cnt = ctypes.c_int64(0)
+    _check(load().sb_profile_end(ctypes.byref(ms), ctypes.byref(cnt)))
+    return ms.value, cnt.value

@@ -3,6 +3,8 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <utility>
+#include <vector>
 
 #include "sb_common.h"
 
@@ -10,7 +12,15 @@ namespace sb {
 
 namespace {
 thread_local std::string g_error;
-}
+struct Profile {
+  bool on = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> hist;
+};
+thread_local Profile g_prof;
+}  // namespace
+
+bool profile_on() { return g_prof.on; }
+void profile_record(hipEvent_t start, hipEvent_t stop) { g_prof.hist.emplace_back(start, stop); }
 
 void set_error(const std::string& msg) { g_error = msg; }
 
@@ -94,6 +104,37 @@ extern "C" {
 const char* sb_last_error(void) { return g_error.c_str(); }
 
 int32_t sb_abi_version(void) { return SB_ABI_VERSION; }
+
+int32_t sb_profile_begin(void) {
+  for (auto& pr : g_prof.hist) {
+    (void)hipEventDestroy(pr.first);
+    (void)hipEventDestroy(pr.second);
+  }
+  g_prof.hist.clear();
+  g_prof.on = true;
+  return SB_OK;
+}
+
+int32_t sb_profile_end(double* hist_kernel_ms, int64_t* hist_launches) {
+  g_prof.on = false;
+  double total = 0.0;
+  int32_t rc = SB_OK;
+  if (!g_prof.hist.empty() && hipEventSynchronize(g_prof.hist.back().second) != hipSuccess)
+    rc = fail(SB_E_DEVICE, "sb_profile_end: event synchronisation failed");
+  for (auto& pr : g_prof.hist) {
+    float ms = 0.0f;
+    if (rc == SB_OK && hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+      rc = fail(SB_E_DEVICE, "sb_profile_end: hipEventElapsedTime failed");
+    total += ms;
+    (void)hipEventDestroy(pr.first);
+    (void)hipEventDestroy(pr.second);
+  }
+  const int64_t count = (int64_t)g_prof.hist.size();
+  g_prof.hist.clear();
+  if (hist_kernel_ms) *hist_kernel_ms = total;
+  if (hist_launches) *hist_launches = count;
+  return rc;
+}
 
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
                            int32_t n_nodes, int32_t depth) {

@@ -21,17 +21,20 @@ constexpr int QBITS = 19;
 // LDS cells are int32 running sums read back into int64 every window; the
 // change between two reads spans at most two windows, so
 // 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
-constexpr int WINDOW_ROWS = 1024;
+constexpr int WINDOW_ROWS = 1536;
 static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point window overflow");
 
 // ---------------------------------------------------------------- histogram plan
-// One histogram workgroup: 1024 threads (16 waves, 4 per SIMD, so at most
-// 128 VGPRs per lane) and up to 30 int32 LDS cells per thread (120 KB of the
-// 160 KB LDS).  Each thread keeps the int64 totals of its 30 cells in 60
-// VGPRs; more cells would spill them to scratch.
-constexpr int HIST_THREADS = 1024;
-constexpr int HIST_MAX_CELLS_PER_THREAD = 30;
+// One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
+// VGPRs per lane) and up to 40 int32 LDS cells per thread (120 KB of the
+// 160 KB LDS).  Each thread keeps the int64 totals of its 40 cells in 80
+// VGPRs next to the double-buffered row data of the step loop; with 4 waves
+// per SIMD (128 VGPRs) they would spill to scratch.
+constexpr int HIST_THREADS = 768;
+constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
 constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
+// A lane holds the bin words of up to 16 quads (64 features) of its row.
+constexpr int HIST_MAX_QUADS = 16;
 
 struct HistPlan {
   int c;          // channels k+1
@@ -70,6 +73,11 @@ int64_t partition_ws_bytes(int64_t n, int32_t n_nodes);
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
                          int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st);
+
+// ---------------------------------------------------------------- profiling
+// Event pairs around histogram-kernel launches while profiling is on (per thread).
+bool profile_on();
+void profile_record(hipEvent_t start, hipEvent_t stop);
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 

@@ -28,13 +28,13 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   int nq_max = (int)(HIST_LDS_BYTES / quad_bytes);
   const int quads_total = (m + 3) / 4;
   if (nq_max > quads_total) nq_max = quads_total;
-  if (nq_max > 64) nq_max = 64;
+  if (nq_max > HIST_MAX_QUADS) nq_max = HIST_MAX_QUADS;
   if (nq_max < 1) nq_max = 0;  // does not fit: caller rejects
   if (nq_max == 0) return p;
   p.slices = (quads_total + nq_max - 1) / nq_max;
   p.nq = (quads_total + p.slices - 1) / p.slices;
   p.f = 4 * p.nq;
-  p.rows_wave = 64 / p.nq;
+  p.rows_wave = 64;  // one lane per row; the lane covers the whole slice
   p.cells = p.f * n_bins * p.c;
   int q = 256 / p.slices;
   if (q < 1) q = 1;
@@ -124,19 +124,152 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
 
 // Thread t owns the contiguous cells [t*MAXC, t*MAXC + MAXC) (MAXC =
 // HIST_MAX_CELLS_PER_THREAD), so one base address plus immediate offsets
-// reaches all of them.
+// reaches all of them.  Cells are folded 8 at a time with compiler barriers in
+// between, which keeps the scheduler from holding all the reads in registers
+// at once on top of the 2*MAXC registers of totals.
 __device__ inline void fold_cells(const int32_t* lds, int64_t* tot, int cells) {
   const int e0 = threadIdx.x * HIST_MAX_CELLS_PER_THREAD;
 #pragma unroll
-  for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
-    if (e0 + jj < cells) {
-      const uint32_t cur = (uint32_t)lds[e0 + jj];
-      const int32_t delta = (int32_t)(cur - (uint32_t)tot[jj]);
-      tot[jj] += delta;
+  for (int j0 = 0; j0 < HIST_MAX_CELLS_PER_THREAD; j0 += 8) {
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int jj = j0; jj < j0 + 8 && jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
+      if (e0 + jj < cells) {
+        const uint32_t cur = (uint32_t)lds[e0 + jj];
+        const int32_t delta = (int32_t)(cur - (uint32_t)tot[jj]);
+        tot[jj] += delta;
+      }
+    }
+  }
+  asm volatile("" ::: "memory");
+}
+
+// Barrier for the window folds: waits for this wave's LDS operations only, so
+// global prefetches stay in flight across it (a plain __syncthreads also
+// drains them).  0xc07f is s_waitcnt lgkmcnt(0) in the gfx9 encoding.
+__device__ inline void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One row of one lane: the slice's bins (4 per word) and the row's channel
+// values, loaded together so their latencies overlap.
+template <int CMAX, int NQMAX>
+struct RowData {
+  uint32_t word[NQMAX];
+  float g[CMAX];
+};
+
+// A lane's position in a step: `raw` is the row index as loaded (not yet
+// clamped, so that issuing the load never waits for it) and `on` says whether
+// the position exists.
+struct RowRef {
+  int32_t raw;
+  bool on;
+};
+
+// EXACT: CMAX channels and NQMAX quads exactly (no per-element tests, so the
+// load path has no branches and the compiler can count outstanding loads).
+// Lanes without a row load row 0 and never use the data.
+template <int CMAX, int NQMAX, bool EXACT>
+__device__ inline void load_row(const HistArgs& a, RowRef ref, int f0, int nq, int c, RowData<CMAX, NQMAX>& d) {
+  int64_t row = ref.on ? (int64_t)ref.raw : 0;
+  row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
+  const uint32_t* wp = reinterpret_cast<const uint32_t*>(a.bins + row * a.ld_bins + f0);
+#pragma unroll
+  for (int qq = 0; qq < NQMAX; ++qq)
+    if (EXACT || qq < nq) d.word[qq] = wp[qq];
+  const float* ghr = a.GH + row * a.ld_gh;
+#pragma unroll
+  for (int t = 0; t < CMAX; ++t)
+    if (EXACT || t < c) d.g[t] = ghr[t];
+}
+
+// LDS cells are laid out [t][feature in slice][bin]: for a fixed channel and
+// feature the 64 lanes of a wave hit lds[base + bin], so random bins spread
+// over all the banks.  All four features of a quad are accumulated; features
+// past m (m not a multiple of 4) read padding bytes of the row and land in
+// cells the reduction never reads.
+template <int CMAX, int NQMAX, bool EXACT>
+__device__ inline void add_row(int32_t* lds, const RowData<CMAX, NQMAX>& d, const int* qe, int nq, int B, int FB,
+                               int c) {
+  int32_t vq[CMAX];
+#pragma unroll
+  for (int t = 0; t < CMAX; ++t) vq[t] = (EXACT || t < c) ? (int32_t)rintf(ldexpf(d.g[t], qe[t])) : 0;
+#pragma unroll
+  for (int qq = 0; qq < NQMAX; ++qq) {
+    if (EXACT || qq < nq) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        int bin = (int)((d.word[qq] >> (8 * u)) & 0xffu);
+        bin = bin < B ? bin : B - 1;
+        int32_t* cell = lds + (4 * qq + u) * B + bin;
+#pragma unroll
+        for (int t = 0; t < CMAX; ++t)
+          if (EXACT || t < c) atomicAdd(cell + t * FB, vq[t]);
+      }
     }
   }
 }
 
+// Accumulate the lane's rows of virtual positions [v, vend) of one node
+// (segment start seg0, first virtual position pstart) into the LDS cells,
+// folding into `tot` at every window.  HAS_IDX: rows come through row_idx
+// (otherwise the position is the row).  The row-index load of a lane is
+// unconditional (positions past the end are clamped into the segment and
+// marked off), so the load path has no branches and the compiler's count of
+// outstanding loads stays exact.
+template <int CMAX, int NQMAX, bool EXACT, bool HAS_IDX>
+__device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot, const int* qe, int64_t v,
+                                   int64_t vend, int64_t pstart, int64_t seg0, int wave, int lane, int f0, int nq,
+                                   int B, int FB, int c) {
+  const int rows_step = HIST_THREADS;
+  const int64_t win_rows = (int64_t)a.steps_per_window * rows_step;
+  const int64_t last_pos = seg0 + (vend - 1 - pstart);
+  auto row_at = [&](int64_t vs, int64_t lim) -> RowRef {
+    const int64_t vv = vs + (int64_t)wave * 64 + lane;
+    RowRef r;
+    r.on = vv < lim;
+    int64_t pos = seg0 + (vv - pstart);
+    pos = pos < last_pos ? pos : last_pos;
+    r.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
+    return r;
+  };
+  // Windows of steps_per_window steps.  The prefetch pipeline runs inside a
+  // window and is empty at its end, so nothing but the totals is live across
+  // the fold.
+#pragma unroll 1
+  for (int64_t ws = v; ws < vend; ws += win_rows) {
+    const int64_t we = (ws + win_rows < vend) ? ws + win_rows : vend;
+    RowRef r_cur = row_at(ws, we);
+    RowData<CMAX, NQMAX> cur;
+    load_row<CMAX, NQMAX, EXACT>(a, r_cur, f0, nq, c, cur);
+    RowRef r_nxt = row_at(ws + rows_step, we);
+#pragma unroll 1
+    for (int64_t vs = ws; vs < we; vs += rows_step) {
+      // Loads return in issue order, so the row index two steps ahead is
+      // issued before this step's data loads: waiting for it later never
+      // waits for them.
+      const RowRef r_after = row_at(vs + 2 * rows_step, we);
+      RowData<CMAX, NQMAX> nxt;
+      load_row<CMAX, NQMAX, EXACT>(a, r_nxt, f0, nq, c, nxt);
+      if (r_cur.on) add_row<CMAX, NQMAX, EXACT>(lds, cur, qe, nq, B, FB, c);
+      r_cur = r_nxt;
+      cur = nxt;
+      r_nxt = r_after;
+    }
+    lds_barrier();
+    fold_cells(lds, tot, a.cells);
+  }
+}
+
+// One lane per row; each lane accumulates all F = 4*nq features of its slice
+// for its row.  Each step a wave covers 64 rows: it issues the loads of its
+// next rows and the row indices of the step after, then performs the current
+// rows' LDS atomics, so memory latency hides behind LDS work.
+template <int CMAX, int NQMAX, bool EXACT>
 __global__ void __launch_bounds__(HIST_THREADS)
 k_hist(HistArgs a) {
   extern __shared__ int32_t lds[];
@@ -161,12 +294,15 @@ k_hist(HistArgs a) {
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int rr = lane / a.nq, qd = lane - rr * a.nq;
-  const bool lane_on = rr < a.rows_wave;
   const int f0 = s * a.f;
-  const int fq = f0 + 4 * qd;  // first feature of this lane's quad
-  const int B = a.n_bins, c = a.c;
-  const int rows_step = (HIST_THREADS / 64) * a.rows_wave;
+  // quads of this slice (the last slice may hold fewer; EXACT launches only
+  // when every slice holds NQMAX)
+  const int nq = EXACT ? NQMAX : ((a.m - f0 + 3) / 4 < a.nq ? (a.m - f0 + 3) / 4 : a.nq);
+  const int B = a.n_bins, c = EXACT ? CMAX : a.c;
+  const int FB = a.f * B;
+  int qe[CMAX];  // wave-uniform: kept in scalar registers
+#pragma unroll
+  for (int t = 0; t < CMAX; ++t) qe[t] = __builtin_amdgcn_readfirstlane(t < c ? a.qexp[t] : 0);
 
   int64_t tot[HIST_MAX_CELLS_PER_THREAD];
 #pragma unroll
@@ -180,37 +316,10 @@ k_hist(HistArgs a) {
     const int64_t pstart = a.pre[p];
     const int64_t vend = v1 < a.pre[p + 1] ? v1 : a.pre[p + 1];
     const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
-    int steps = 0;
-    for (int64_t vs = v; vs < vend; vs += rows_step) {
-      const int64_t vv = vs + (int64_t)wave * a.rows_wave + rr;
-      if (lane_on && vv < vend && fq < a.m) {
-        const int64_t pos = seg0 + (vv - pstart);
-        int64_t row = a.row_idx ? (int64_t)a.row_idx[pos] : pos;
-        row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
-        const uint32_t word = *reinterpret_cast<const uint32_t*>(a.bins + row * a.ld_bins + fq);
-        int base[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          int bin = (int)((word >> (8 * u)) & 0xffu);
-          bin = bin < B ? bin : B - 1;
-          base[u] = ((4 * qd + u) * B + bin) * c;
-        }
-        const int nf = (a.m - fq) < 4 ? (a.m - fq) : 4;
-        const float* ghr = a.GH + row * a.ld_gh;
-        for (int t = 0; t < c; ++t) {
-          const int32_t vq = (int32_t)rintf(ldexpf(ghr[t], a.qexp[t]));
-          atomicAdd(&lds[base[0] + t], vq);
-          if (nf > 1) atomicAdd(&lds[base[1] + t], vq);
-          if (nf > 2) atomicAdd(&lds[base[2] + t], vq);
-          if (nf > 3) atomicAdd(&lds[base[3] + t], vq);
-        }
-      }
-      if (++steps == a.steps_per_window) {
-        steps = 0;
-        __syncthreads();
-        fold_cells(lds, tot, a.cells);
-      }
-    }
+    if (a.row_idx)
+      run_segment<CMAX, NQMAX, EXACT, true>(a, lds, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
+    else
+      run_segment<CMAX, NQMAX, EXACT, false>(a, lds, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
     // end of this node's part: final fold, write the partial, reset
     __syncthreads();
     fold_cells(lds, tot, a.cells);
@@ -233,17 +342,19 @@ k_hist(HistArgs a) {
 
 __device__ inline int64_t group_of(int64_t x, int64_t T, int64_t Q) { return ((x + 1) * Q - 1) / T; }
 
-// H[node][f][b][t] = sum of the partials of the row groups that covered the node.
+// H[node][f][b][t] = sum of the partials of the row groups that covered the
+// node.  Partial cell e is laid out [t][feature in slice][bin] like the LDS.
 __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   const int p = blockIdx.y, s = blockIdx.z;
   if (e >= a.cells) return;
   const int32_t j = node_of(a, p);
   if (j < 0 || j >= a.n_nodes) return;
-  const int bc = a.n_bins * a.c;
-  const int fl = e / bc;
-  const int rem = e - fl * bc;
-  const int t = rem % a.c;
+  const int FB = a.f * a.n_bins;
+  const int t = e / FB;
+  const int rem = e - t * FB;
+  const int fl = rem / a.n_bins;
+  const int bin = rem - fl * a.n_bins;
   const int f = s * a.f + fl;
   if (f >= a.m) return;
   const int64_t T = a.pre[a.n_build];
@@ -256,7 +367,7 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
         sum += a.partial[((int64_t)s * a.slots + q + p) * a.cells + e];
     }
   }
-  a.H[((int64_t)j * a.m + f) * bc + rem] = ldexp((double)sum, -a.qexp[t]);
+  a.H[(((int64_t)j * a.m + f) * a.n_bins + bin) * a.c + t] = ldexp((double)sum, -a.qexp[t]);
 }
 
 __global__ void __launch_bounds__(256)
@@ -305,14 +416,41 @@ int32_t launch_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64
   a.cells = pl.cells;
   a.q = pl.q;
   a.cpt = (pl.cells + HIST_THREADS - 1) / HIST_THREADS;
-  const int rows_step = (HIST_THREADS / 64) * pl.rows_wave;
+  const int rows_step = HIST_THREADS;
   a.steps_per_window = WINDOW_ROWS / rows_step > 0 ? WINDOW_ROWS / rows_step : 1;
   a.slots = pl.slots;
   if (rows_step > WINDOW_ROWS) return fail(SB_E_UNSUPPORTED, "histogram step exceeds the fixed-point window");
 
   hipLaunchKernelGGL(k_hist_plan, dim3(1), dim3(1024), 0, st, a);
   const int grid = pl.q_pad * pl.slices;
-  hipLaunchKernelGGL(k_hist, dim3(grid), dim3(HIST_THREADS), (size_t)pl.cells * 4, st, a);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;
+  if (prof) (void)hipEventRecord(e0, st);
+  const size_t lds_bytes = (size_t)pl.cells * 4;
+  const int cm = pl.c <= 4 ? 4 : pl.c <= 8 ? 8 : pl.c <= 16 ? 16 : 24;
+  const int nm = pl.nq <= 4 ? 4 : pl.nq <= 8 ? 8 : 16;
+  // exact shapes: every slice holds nq quads and there are exactly c channels
+  const bool even = pl.slices * pl.nq * 4 - m < 4;
+#define SB_HIST_EXACT(C, NQ)                                                                        \
+  if (even && pl.c == C && pl.nq == NQ) {                                                           \
+    hipLaunchKernelGGL((k_hist<C, NQ, true>), dim3(grid), dim3(HIST_THREADS), lds_bytes, st, a); \
+  } else
+#define SB_HIST_CASE(CM, NM)                                                                         \
+  if (cm == CM && nm == NM) {                                                                        \
+    hipLaunchKernelGGL((k_hist<CM, NM, false>), dim3(grid), dim3(HIST_THREADS), lds_bytes, st, a); \
+  } else
+  SB_HIST_EXACT(6, 5) SB_HIST_EXACT(6, 3) SB_HIST_EXACT(6, 13) SB_HIST_EXACT(11, 2) SB_HIST_EXACT(21, 1)
+  SB_HIST_CASE(4, 4) SB_HIST_CASE(4, 8) SB_HIST_CASE(4, 16)
+  SB_HIST_CASE(8, 4) SB_HIST_CASE(8, 8) SB_HIST_CASE(8, 16)
+  SB_HIST_CASE(16, 4) SB_HIST_CASE(16, 8) SB_HIST_CASE(16, 16)
+  SB_HIST_CASE(24, 4) SB_HIST_CASE(24, 8) SB_HIST_CASE(24, 16)
+  return fail(SB_E_UNSUPPORTED, "sb_build_histograms: more than 24 channels (k > 23)");
+#undef SB_HIST_EXACT
+#undef SB_HIST_CASE
+  if (prof) {
+    (void)hipEventRecord(e1, st);
+    profile_record(e0, e1);
+  }
   dim3 rg((pl.cells + 255) / 256, n_build, pl.slices);
   hipLaunchKernelGGL(k_hist_reduce, rg, dim3(256), 0, st, a);
   return check_launch("sb_build_histograms");

@@ -8,10 +8,14 @@
 //   right row at i -> o_j + nleft_j + (i - o_j) - (L[i] - Lb_j),
 // which keeps the original order inside each child.
 //   k_part_flags   : flag per position (column-major bins: one contiguous run
-//                    of a single feature column per node), left counts per
-//                    tile and per node (integer atomics: order-free).
-//   k_part_scan    : tile offsets, Lb, child offsets, next build list.
-//   k_part_scatter : block scan of the tile's flags and the scatter.
+//                    of a single feature column per node) and left count per
+//                    tile of 4096 positions.
+//   k_part_scan    : exclusive scan of the tile counts (one block).
+//   k_part_bounds  : Lb_j = L[o_j] for every node boundary, from the tile
+//                    offset plus the flags of the boundary's own tile.
+//   k_part_scatter : block scan of the tile's flags and the scatter; block 0
+//                    also writes the child offsets and the next build list.
+// No counter is shared between workgroups, so nothing serialises on atomics.
 #include "sb_common.h"
 
 namespace sb {
@@ -33,9 +37,8 @@ struct PartArgs {
   int32_t* build_out;
   uint8_t* flags;
   int32_t* tile_cnt;
-  int32_t* tile_off;
-  int32_t* nleft;
-  int32_t* Lb;
+  int32_t* tile_off;  // n_tiles + 1 entries (last = total)
+  int32_t* Lb;        // n_nodes + 1 entries
   int64_t n;
   int32_t m, n_nodes, n_tiles;
 };
@@ -56,17 +59,13 @@ __device__ inline int find_node(const PartArgs& a, int64_t i) {
   return lo;
 }
 
-__global__ void k_part_zero(int32_t* p, int cnt) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < cnt; i += gridDim.x * blockDim.x) p[i] = 0;
-}
-
 __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   __shared__ int32_t wsum[PT_THREADS / 64];
   const int64_t i0 = (int64_t)blockIdx.x * PT_TILE + (int64_t)threadIdx.x * PT_PER_THREAD;
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
   int j = find_node(a, i0);
   int64_t jend = off_at(a, j + 1);
-  int cnt_tile = 0, cnt_node = 0;
+  int cnt_tile = 0;
   uint32_t packed[PT_PER_THREAD / 4];
 #pragma unroll
   for (int w = 0; w < PT_PER_THREAD / 4; ++w) packed[w] = 0u;
@@ -76,8 +75,6 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
     uint32_t left = 0u;
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
-        if (cnt_node) atomicAdd(&a.nleft[j], cnt_node);
-        cnt_node = 0;
         ++j;
         jend = off_at(a, j + 1);
       }
@@ -89,12 +86,10 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
       } else {
         left = a.bins_cm[(int64_t)f * a.ld_cm + row] <= a.best_b[j] ? 1u : 0u;
       }
-      cnt_node += (int)left;
       cnt_tile += (int)left;
     }
     packed[r >> 2] |= left << (8 * (r & 3));
   }
-  if (cnt_node) atomicAdd(&a.nleft[j], cnt_node);
   // 16 flag bytes per thread, written as 4 words (tile base is 4096-aligned)
   if (i0 < a.n) {
     uint32_t* dst = reinterpret_cast<uint32_t*>(a.flags + i0);
@@ -138,16 +133,28 @@ __device__ void block_excl_scan(const int32_t* cnt, int32_t* out, int N, int32_t
 __global__ void __launch_bounds__(1024) k_part_scan(PartArgs a) {
   __shared__ int32_t sh[1024];
   block_excl_scan(a.tile_cnt, a.tile_off, a.n_tiles, sh);
-  block_excl_scan(a.nleft, a.Lb, a.n_nodes, sh);
-  for (int j = threadIdx.x; j < a.n_nodes; j += 1024) {
-    const int64_t o0 = off_at(a, j), o1 = off_at(a, j + 1);
-    const int64_t size = o1 > o0 ? o1 - o0 : 0;
-    const int64_t nl = a.nleft[j];
-    a.off_out[2 * j] = (int32_t)o0;
-    a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
-    a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
+  if (threadIdx.x == 0) a.tile_off[a.n_tiles] = a.tile_off[a.n_tiles - 1] + a.tile_cnt[a.n_tiles - 1];
+}
+
+// Lb[j] = number of left rows at positions < off[j], j = 0..n_nodes.
+__global__ void __launch_bounds__(PT_THREADS) k_part_bounds(PartArgs a) {
+  __shared__ int32_t wsum[PT_THREADS / 64];
+  const int j = blockIdx.x;
+  const int64_t x = off_at(a, j);
+  const int64_t t = x / PT_TILE;
+  int cnt = 0;
+  if (t < a.n_tiles) {
+    const int64_t base = t * PT_TILE;
+    for (int64_t i = base + threadIdx.x; i < x; i += PT_THREADS) cnt += a.flags[i];
   }
-  if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
+  for (int off = 32; off > 0; off >>= 1) cnt += __shfl_down(cnt, off, 64);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < PT_THREADS / 64; ++w) s += wsum[w];
+    a.Lb[j] = a.tile_off[t < a.n_tiles ? t : a.n_tiles] + (t < a.n_tiles ? s : 0);
+  }
 }
 
 __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
@@ -176,6 +183,17 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
     __syncthreads();
   }
   int64_t L = (int64_t)a.tile_off[blockIdx.x] + sh[threadIdx.x] - mine;
+  if (blockIdx.x == 0) {
+    for (int j = threadIdx.x; j < a.n_nodes; j += PT_THREADS) {
+      const int64_t o0 = off_at(a, j), o1 = off_at(a, j + 1);
+      const int64_t size = o1 > o0 ? o1 - o0 : 0;
+      const int64_t nl = (int64_t)a.Lb[j + 1] - a.Lb[j];
+      a.off_out[2 * j] = (int32_t)o0;
+      a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
+      a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
+    }
+    if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
+  }
   if (i0 >= a.n) return;
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
   int j = find_node(a, i0);
@@ -193,7 +211,8 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
       int64_t row = a.row_in ? (int64_t)a.row_in[i] : i;
       row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
       const int64_t lrel = L - a.Lb[j];
-      int64_t dest = left ? jstart + lrel : jstart + a.nleft[j] + (i - jstart) - lrel;
+      const int64_t nleft = a.Lb[j + 1] - a.Lb[j];
+      int64_t dest = left ? jstart + lrel : jstart + nleft + (i - jstart) - lrel;
       dest = dest < 0 ? 0 : (dest >= a.n ? a.n - 1 : dest);
       a.row_out[dest] = (int32_t)row;
     }
@@ -203,10 +222,10 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
 
 }  // namespace
 
-// Workspace: [flags n][tile_cnt][tile_off][nleft][Lb]
+// Workspace: [flags n][tile_cnt][tile_off][Lb]
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes) {
   const int64_t tiles = (n + PT_TILE - 1) / PT_TILE;
-  return align256(tiles * PT_TILE) + 2 * align256(tiles * 4) + 2 * align256((int64_t)(n_nodes + 1) * 4);
+  return align256(tiles * PT_TILE) + 2 * align256((tiles + 1) * 4) + align256((int64_t)(n_nodes + 1) * 4);
 }
 
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
@@ -227,19 +246,17 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.flags = reinterpret_cast<uint8_t*>(w);
   w += align256(tiles * PT_TILE);
   a.tile_cnt = reinterpret_cast<int32_t*>(w);
-  w += align256(tiles * 4);
+  w += align256((tiles + 1) * 4);
   a.tile_off = reinterpret_cast<int32_t*>(w);
-  w += align256(tiles * 4);
-  a.nleft = reinterpret_cast<int32_t*>(w);
-  w += align256((int64_t)(n_nodes + 1) * 4);
+  w += align256((tiles + 1) * 4);
   a.Lb = reinterpret_cast<int32_t*>(w);
   a.n = n;
   a.m = m;
   a.n_nodes = n_nodes;
   a.n_tiles = (int32_t)tiles;
-  hipLaunchKernelGGL(k_part_zero, dim3((n_nodes + 255) / 256), dim3(256), 0, st, a.nleft, n_nodes);
   hipLaunchKernelGGL(k_part_flags, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
   hipLaunchKernelGGL(k_part_scan, dim3(1), dim3(1024), 0, st, a);
+  hipLaunchKernelGGL(k_part_bounds, dim3(n_nodes + 1), dim3(PT_THREADS), 0, st, a);
   hipLaunchKernelGGL(k_part_scatter, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
   return check_launch("sb_partition_rows");
 }

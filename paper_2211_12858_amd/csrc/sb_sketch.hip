@@ -67,14 +67,21 @@ k_colnorm_partial(const float* __restrict__ G, int64_t n, int64_t ld, int parts,
   if (threadIdx.x == 0) part[(int64_t)j * parts + p] = s;
 }
 
-__global__ void k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __restrict__ n2,
-                                double* __restrict__ n2_user) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+// One wave per column: lane l sums partials l, l+64, ... in order, then a
+// fixed shuffle tree; the result depends only on the number of partials.
+__global__ void __launch_bounds__(256)
+k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __restrict__ n2,
+                double* __restrict__ n2_user) {
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   if (j >= d) return;
   double s = 0.0;
-  for (int p = 0; p < parts; ++p) s += part[(int64_t)j * parts + p];
-  n2[j] = s;
-  if (n2_user) n2_user[j] = s;
+  for (int p = lane; p < parts; p += 64) s += part[(int64_t)j * parts + p];
+  s = wave_sum(s);
+  if (lane == 0) {
+    n2[j] = s;
+    if (n2_user) n2_user[j] = s;
+  }
 }
 
 // One block.  Also clears the per-channel max bits used by k_pack.
@@ -307,7 +314,7 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
     int64_t chunk = (n + P - 1) / P;
     chunk = (chunk + 3) & ~int64_t(3);
     hipLaunchKernelGGL(k_colnorm_partial, dim3(P, d), dim3(NORM_THREADS), 0, st, G, n, ld_g, P, chunk, part);
-    hipLaunchKernelGGL(k_colnorm_final, dim3((d + 255) / 256), dim3(256), 0, st, part, d, P, n2, norm2);
+    hipLaunchKernelGGL(k_colnorm_final, dim3((d + 3) / 4), dim3(256), 0, st, part, d, P, n2, norm2);
     hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, n2, d, k, u, cols, scales, C, maxbits);
     const int64_t rows_per_block = (int64_t)PACK_THREADS * PACK_ROWS_PER_THREAD;
     const int64_t blocks = (n + rows_per_block - 1) / rows_per_block;

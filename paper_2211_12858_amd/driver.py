@@ -5,9 +5,10 @@ the kernels read:
 
 * row records for the histogram kernel: row i occupies ``rec_stride`` bytes,
   its m bin bytes first and, when ``interleave`` is set, its k+1 sketch
-  floats right after them (at a 4-byte aligned offset).  With m + 4(k+1) <=
-  128, as for 100 features and k = 5, each row is exactly one 128-byte cache
-  line, so gathering the rows of a node fetches nothing it does not use;
+  floats after them (at an 8-byte aligned offset).  With 100 features and
+  k = 5 each row is exactly one 128-byte cache line, so gathering the rows
+  of a node fetches nothing it does not use.  Otherwise the sketch lives in
+  its own compact (n, k+1) array;
 * a column-major copy (feature-major, ``bins_cm[f, i]``) for the partition,
   which then reads one contiguous run of one feature column per node.
 
@@ -40,8 +41,8 @@ class SplitSearch:
         n, m, c = self.n, self.m, self.c
         self.ld_bins = _round_up(m, 4)
         if interleave:
-            self.gh_offset = self.ld_bins
-            self.rec_stride = _round_up(self.ld_bins + 4 * c, 128)
+            self.gh_offset = _round_up(self.ld_bins, 8)
+            self.rec_stride = _round_up(self.gh_offset + 4 * c, 128)
         else:
             self.gh_offset = None
             self.rec_stride = self.ld_bins

@@ -31,6 +31,7 @@ multilabel workload has Y ~ Bernoulli(0.05), g = sigmoid(z) - y and
 h_i = mean_j sigmoid(z_ij)(1 - sigmoid(z_ij)).  Gradients are formed in
 fp64 and stored as fp32.  lambda = 1 everywhere.
 """
+import os
 from dataclasses import dataclass, replace
 
 import numpy as np
@@ -103,52 +104,75 @@ class Inputs:
         return self.G_T.T
 
 
+def _softmax_grad_cols(z_T, y):
+    """Column-major softmax-CE gradient block: z_T is (d, rows) fp64 logits."""
+    z_T = z_T - z_T.max(axis=0, keepdims=True)
+    p = np.exp(z_T)
+    p /= p.sum(axis=0, keepdims=True)
+    p[y, np.arange(z_T.shape[1])] -= 1.0
+    return p.astype(np.float32)
+
+
 def _softmax_grad_T(z, y):
-    z = z.astype(np.float64)
-    z -= z.max(axis=1, keepdims=True)
-    p = np.exp(z)
-    p /= p.sum(axis=1, keepdims=True)
-    p[np.arange(z.shape[0]), y] -= 1.0
-    return p.astype(np.float32).T
+    """Row-major logits (rows, d) -> column-major fp32 gradient block (d, rows)."""
+    return _softmax_grad_cols(np.ascontiguousarray(np.asarray(z, dtype=np.float64).T), y)
 
 
-def make_inputs(wl, chunk=100_000):
-    """Generate the inputs of workload ``wl`` (deterministic in wl.seed)."""
-    rng = np.random.default_rng(wl.seed)
+def _pool():
+    from concurrent.futures import ThreadPoolExecutor
+    return ThreadPoolExecutor(max_workers=min(16, len(os.sched_getaffinity(0))))
+
+
+def make_inputs(wl, chunk=65_536):
+    """Generate the inputs of workload ``wl``.
+
+    Deterministic in wl.seed and independent of the thread count: every
+    feature column and every row chunk draws from its own child generator
+    (numpy SeedSequence keyed by (seed, stream, index)).
+    """
     n, m, d, k, B = wl.n, wl.m, wl.d, wl.k, wl.n_bins
-    if wl.binning == "uniform":
-        bins = rng.integers(0, B, size=(n, m), dtype=np.uint8)
-        X = None
-    else:
-        X = rng.standard_normal((n, m), dtype=np.float32)
-        bins = np.empty((n, m), dtype=np.uint8)
-        for f in range(m):
-            bins[:, f] = quantile_bin(X[:, f], B)
-    G_T = np.empty((d, n), dtype=np.float32)
-    h = np.ones(n, dtype=np.float32)
-    if wl.loss == "softmax":
-        if X is None:
-            y_all = rng.integers(0, d, size=n)
+    rng = np.random.default_rng(wl.seed)
+    chunks = [(r0, min(n, r0 + chunk)) for r0 in range(0, n, chunk)]
+    bins = np.empty((n, m), dtype=np.uint8)
+    X_cm = None
+    with _pool() as pool:
+        if wl.binning == "uniform":
+            def one_bins(f):
+                bins[:, f] = np.random.default_rng([wl.seed, 1, f]).integers(0, B, size=n, dtype=np.uint8)
+            list(pool.map(one_bins, range(m)))
         else:
-            W = rng.standard_normal((m, d)).astype(np.float32) / np.float32(np.sqrt(m))
-            y_all = np.empty(n, dtype=np.int64)
-        for r0 in range(0, n, chunk):
-            r1 = min(n, r0 + chunk)
-            if X is not None:
-                logits = X[r0:r1] @ W + rng.standard_normal((r1 - r0, d), dtype=np.float32)
-                y_all[r0:r1] = np.argmax(logits, axis=1)
-            z = rng.standard_normal((r1 - r0, d))
-            G_T[:, r0:r1] = _softmax_grad_T(z, y_all[r0:r1])
-    elif wl.loss == "sigmoid":
-        for r0 in range(0, n, chunk):
-            r1 = min(n, r0 + chunk)
-            y = rng.random((r1 - r0, d)) < 0.05
-            z = rng.standard_normal((r1 - r0, d))
-            s = 1.0 / (1.0 + np.exp(-z))
-            G_T[:, r0:r1] = (s - y).astype(np.float32).T
-            h[r0:r1] = np.mean(s * (1.0 - s), axis=1).astype(np.float32)
-    else:
-        raise ValueError(wl.loss)
+            X_cm = np.empty((m, n), dtype=np.float32)
+
+            def one_feature(f):
+                X_cm[f] = np.random.default_rng([wl.seed, 2, f]).standard_normal(n, dtype=np.float32)
+                bins[:, f] = quantile_bin(X_cm[f], B)
+            list(pool.map(one_feature, range(m)))
+        G_T = np.empty((d, n), dtype=np.float32)
+        h = np.ones(n, dtype=np.float32)
+        if wl.loss == "softmax":
+            W = (rng.standard_normal((m, d)) / np.sqrt(m)).astype(np.float32) if X_cm is not None else None
+
+            def one_chunk(ci):
+                r0, r1 = chunks[ci]
+                g = np.random.default_rng([wl.seed, 3, ci])
+                if X_cm is None:
+                    y = g.integers(0, d, size=r1 - r0)
+                else:
+                    logits = W.T @ X_cm[:, r0:r1] + g.standard_normal((d, r1 - r0), dtype=np.float32)
+                    y = np.argmax(logits, axis=0)
+                G_T[:, r0:r1] = _softmax_grad_cols(g.standard_normal((d, r1 - r0)), y)
+            list(pool.map(one_chunk, range(len(chunks))))
+        elif wl.loss == "sigmoid":
+            def one_chunk(ci):
+                r0, r1 = chunks[ci]
+                g = np.random.default_rng([wl.seed, 4, ci])
+                y = g.random((d, r1 - r0)) < 0.05
+                sg = 1.0 / (1.0 + np.exp(-g.standard_normal((d, r1 - r0))))
+                G_T[:, r0:r1] = (sg - y).astype(np.float32)
+                h[r0:r1] = np.mean(sg * (1.0 - sg), axis=0).astype(np.float32)
+            list(pool.map(one_chunk, range(len(chunks))))
+        else:
+            raise ValueError(wl.loss)
     u = rng.random(k)
     Pi = (rng.standard_normal((d, k)) / np.sqrt(k)).astype(np.float32)
     return Inputs(bins=bins, G_T=G_T, h=h, u=u, Pi=Pi, wl=wl)
