@@ -33,6 +33,8 @@ static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point win
 constexpr int HIST_THREADS = 768;
 constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
 constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
+// MI355X: 8 XCDs of 32 CUs; workgroup b is dispatched to XCD b % 8.
+constexpr int HIST_CUS_PER_XCD = 32;
 // A lane holds the bin words of up to 16 quads (64 features) of its row.
 constexpr int HIST_MAX_QUADS = 16;
 

@@ -36,11 +36,14 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   p.f = 4 * p.nq;
   p.rows_wave = 64;  // one lane per row; the lane covers the whole slice
   p.cells = p.f * n_bins * p.c;
-  int q = 256 / p.slices;
-  if (q < 1) q = 1;
-  p.q = q;
-  p.q_pad = (q + 7) & ~7;
-  p.slots = (int64_t)q + n_build;
+  // Workgroup b runs on XCD b % 8 and a row group's slices share its XCD, so
+  // an XCD hosts (q/8) * slices workgroups; keep that within its 32 CUs (one
+  // histogram workgroup per CU) so that every workgroup starts at once.
+  int per_xcd = HIST_CUS_PER_XCD / p.slices;
+  if (per_xcd < 1) per_xcd = 1;
+  p.q = 8 * per_xcd;
+  p.q_pad = p.q;
+  p.slots = (int64_t)p.q + n_build;
   return p;
 }
 
@@ -123,22 +126,24 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
 }
 
 // Thread t owns the contiguous cells [t*MAXC, t*MAXC + MAXC) (MAXC =
-// HIST_MAX_CELLS_PER_THREAD), so one base address plus immediate offsets
-// reaches all of them.  Cells are folded 8 at a time with compiler barriers in
-// between, which keeps the scheduler from holding all the reads in registers
-// at once on top of the 2*MAXC registers of totals.
-__device__ inline void fold_cells(const int32_t* lds, int64_t* tot, int cells) {
-  const int e0 = threadIdx.x * HIST_MAX_CELLS_PER_THREAD;
+// HIST_MAX_CELLS_PER_THREAD, a multiple of 4), read as 128-bit words.  The
+// LDS always holds MAXC cells per thread (cells past the plan's count stay
+// zero), so the reads need no bounds tests.  Cells are folded 8 at a time with
+// compiler barriers in between, which bounds the registers the reads hold on
+// top of the 2*MAXC registers of totals.
+__device__ inline void fold_cells(const int32_t* lds, int64_t* tot) {
+  static_assert(HIST_MAX_CELLS_PER_THREAD % 8 == 0, "fold reads 8 cells at a time");
+  const int4* src = reinterpret_cast<const int4*>(lds + threadIdx.x * HIST_MAX_CELLS_PER_THREAD);
 #pragma unroll
   for (int j0 = 0; j0 < HIST_MAX_CELLS_PER_THREAD; j0 += 8) {
     asm volatile("" ::: "memory");
+    const int4 x = src[j0 / 4];
+    const int4 y = src[j0 / 4 + 1];
+    const int32_t cur[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
 #pragma unroll
-    for (int jj = j0; jj < j0 + 8 && jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
-      if (e0 + jj < cells) {
-        const uint32_t cur = (uint32_t)lds[e0 + jj];
-        const int32_t delta = (int32_t)(cur - (uint32_t)tot[jj]);
-        tot[jj] += delta;
-      }
+    for (int jj = 0; jj < 8; ++jj) {
+      const int32_t delta = (int32_t)((uint32_t)cur[jj] - (uint32_t)tot[j0 + jj]);
+      tot[j0 + jj] += delta;
     }
   }
   asm volatile("" ::: "memory");
@@ -226,7 +231,6 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
                                    int64_t vend, int64_t pstart, int64_t seg0, int wave, int lane, int f0, int nq,
                                    int B, int FB, int c) {
   const int rows_step = HIST_THREADS;
-  const int64_t win_rows = (int64_t)a.steps_per_window * rows_step;
   const int64_t last_pos = seg0 + (vend - 1 - pstart);
   auto row_at = [&](int64_t vs, int64_t lim) -> RowRef {
     const int64_t vv = vs + (int64_t)wave * 64 + lane;
@@ -237,31 +241,30 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
     r.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
     return r;
   };
-  // Windows of steps_per_window steps.  The prefetch pipeline runs inside a
-  // window and is empty at its end, so nothing but the totals is live across
-  // the fold.
+  // The prefetch pipeline runs through the whole segment; every
+  // steps_per_window steps all waves meet at a barrier and fold their cells
+  // (the data of the next step stays in flight across the fold).
+  RowRef r_cur = row_at(v, vend);
+  RowData<CMAX, NQMAX> cur;
+  load_row<CMAX, NQMAX, EXACT>(a, r_cur, f0, nq, c, cur);
+  RowRef r_nxt = row_at(v + rows_step, vend);
+  int steps = 0;
 #pragma unroll 1
-  for (int64_t ws = v; ws < vend; ws += win_rows) {
-    const int64_t we = (ws + win_rows < vend) ? ws + win_rows : vend;
-    RowRef r_cur = row_at(ws, we);
-    RowData<CMAX, NQMAX> cur;
-    load_row<CMAX, NQMAX, EXACT>(a, r_cur, f0, nq, c, cur);
-    RowRef r_nxt = row_at(ws + rows_step, we);
-#pragma unroll 1
-    for (int64_t vs = ws; vs < we; vs += rows_step) {
-      // Loads return in issue order, so the row index two steps ahead is
-      // issued before this step's data loads: waiting for it later never
-      // waits for them.
-      const RowRef r_after = row_at(vs + 2 * rows_step, we);
-      RowData<CMAX, NQMAX> nxt;
-      load_row<CMAX, NQMAX, EXACT>(a, r_nxt, f0, nq, c, nxt);
-      if (r_cur.on) add_row<CMAX, NQMAX, EXACT>(lds, cur, qe, nq, B, FB, c);
-      r_cur = r_nxt;
-      cur = nxt;
-      r_nxt = r_after;
+  for (int64_t vs = v; vs < vend; vs += rows_step) {
+    // Loads return in issue order, so the row index two steps ahead is issued
+    // before this step's data loads: waiting for it later never waits for them.
+    const RowRef r_after = row_at(vs + 2 * rows_step, vend);
+    RowData<CMAX, NQMAX> nxt;
+    load_row<CMAX, NQMAX, EXACT>(a, r_nxt, f0, nq, c, nxt);
+    if (r_cur.on) add_row<CMAX, NQMAX, EXACT>(lds, cur, qe, nq, B, FB, c);
+    r_cur = r_nxt;
+    cur = nxt;
+    r_nxt = r_after;
+    if (++steps == a.steps_per_window) {
+      steps = 0;
+      lds_barrier();
+      fold_cells(lds, tot);
     }
-    lds_barrier();
-    fold_cells(lds, tot, a.cells);
   }
 }
 
@@ -307,7 +310,7 @@ k_hist(HistArgs a) {
   int64_t tot[HIST_MAX_CELLS_PER_THREAD];
 #pragma unroll
   for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) tot[jj] = 0;
-  for (int e = tid; e < a.cells; e += HIST_THREADS) lds[e] = 0;
+  for (int e = tid; e < HIST_THREADS * HIST_MAX_CELLS_PER_THREAD; e += HIST_THREADS) lds[e] = 0;
   __syncthreads();
 
   int64_t v = v0;
@@ -322,15 +325,13 @@ k_hist(HistArgs a) {
       run_segment<CMAX, NQMAX, EXACT, false>(a, lds, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
     // end of this node's part: final fold, write the partial, reset
     __syncthreads();
-    fold_cells(lds, tot, a.cells);
+    fold_cells(lds, tot);
     int64_t* dst = a.partial + ((int64_t)s * a.slots + q + p) * a.cells;
 #pragma unroll
     for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
       const int e = tid * HIST_MAX_CELLS_PER_THREAD + jj;
-      if (e < a.cells) {
-        dst[e] = tot[jj];
-        lds[e] = 0;
-      }
+      if (e < a.cells) dst[e] = tot[jj];
+      lds[e] = 0;
       tot[jj] = 0;
     }
     __syncthreads();
@@ -426,7 +427,7 @@ int32_t launch_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64
   hipEvent_t e0 = nullptr, e1 = nullptr;
   const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;
   if (prof) (void)hipEventRecord(e0, st);
-  const size_t lds_bytes = (size_t)pl.cells * 4;
+  const size_t lds_bytes = (size_t)HIST_LDS_BYTES;
   const int cm = pl.c <= 4 ? 4 : pl.c <= 8 ? 8 : pl.c <= 16 ? 16 : 24;
   const int nm = pl.nq <= 4 ? 4 : pl.nq <= 8 ? 8 : 16;
   // exact shapes: every slice holds nq quads and there are exactly c channels
