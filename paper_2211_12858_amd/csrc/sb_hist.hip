@@ -241,25 +241,46 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
     r.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
     return r;
   };
-  // The prefetch pipeline runs through the whole segment; every
-  // steps_per_window steps all waves meet at a barrier and fold their cells
-  // (the data of the next step stays in flight across the fold).
-  RowRef r_cur = row_at(v, vend);
-  RowData<CMAX, NQMAX> cur;
-  load_row<CMAX, NQMAX, EXACT>(a, r_cur, f0, nq, c, cur);
-  RowRef r_nxt = row_at(v + rows_step, vend);
+  // The prefetch pipeline runs through the whole segment.  With two-step
+  // prefetch (row data two steps ahead, row indices three), used when a row's
+  // data fits in 12 registers, loads stay in flight across more than one step
+  // of LDS work (the loaded memory latency is longer than one step); wider
+  // rows prefetch one step ahead to stay within the register budget.  Every
+  // steps_per_window steps all waves meet at a barrier and fold their cells;
+  // the prefetched data stays in flight across the fold.  Row indices are
+  // issued before the data loads of the same step: loads return in issue
+  // order, so waiting for an index later never waits for data behind it.
+  constexpr bool DEEP = CMAX + NQMAX <= 12;
+  RowRef r0 = row_at(v, vend);
+  RowRef r1 = row_at(v + rows_step, vend);
+  RowData<CMAX, NQMAX> d0, d1;
+  load_row<CMAX, NQMAX, EXACT>(a, r0, f0, nq, c, d0);
+  RowRef r2;
+  if constexpr (DEEP) {
+    r2 = row_at(v + 2 * rows_step, vend);
+    load_row<CMAX, NQMAX, EXACT>(a, r1, f0, nq, c, d1);
+  }
   int steps = 0;
 #pragma unroll 1
   for (int64_t vs = v; vs < vend; vs += rows_step) {
-    // Loads return in issue order, so the row index two steps ahead is issued
-    // before this step's data loads: waiting for it later never waits for them.
-    const RowRef r_after = row_at(vs + 2 * rows_step, vend);
-    RowData<CMAX, NQMAX> nxt;
-    load_row<CMAX, NQMAX, EXACT>(a, r_nxt, f0, nq, c, nxt);
-    if (r_cur.on) add_row<CMAX, NQMAX, EXACT>(lds, cur, qe, nq, B, FB, c);
-    r_cur = r_nxt;
-    cur = nxt;
-    r_nxt = r_after;
+    if constexpr (DEEP) {
+      const RowRef r3 = row_at(vs + 3 * rows_step, vend);
+      RowData<CMAX, NQMAX> d2;
+      load_row<CMAX, NQMAX, EXACT>(a, r2, f0, nq, c, d2);
+      if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
+      r0 = r1;
+      d0 = d1;
+      r1 = r2;
+      d1 = d2;
+      r2 = r3;
+    } else {
+      const RowRef r2n = row_at(vs + 2 * rows_step, vend);
+      load_row<CMAX, NQMAX, EXACT>(a, r1, f0, nq, c, d1);
+      if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
+      r0 = r1;
+      d0 = d1;
+      r1 = r2n;
+    }
     if (++steps == a.steps_per_window) {
       steps = 0;
       lds_barrier();
