@@ -125,8 +125,6 @@ def main():
     ap.add_argument("--cpu-sample-rows", type=int, default=800_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
-    ap.add_argument("--layout", choices=("separate", "interleaved"), default="separate",
-                    help="sketch records in their own array, or inside 128-byte row records with the bins")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -152,8 +150,7 @@ def main():
     log("bench: inputs ready in %.1f s" % (time.perf_counter() - t0))
 
     dev = torch.device("cuda:0")
-    ss = SplitSearch(inp.bins, wl.n_bins, wl.k, wl.depth, wl.lam, wl.min_child_weight, device=dev,
-                     interleave=args.layout == "interleaved")
+    ss = SplitSearch(inp.bins, wl.n_bins, wl.k, wl.depth, wl.lam, wl.min_child_weight, device=dev)
     G_T = torch.from_numpy(inp.G_T).to(dev)
     h = torch.from_numpy(inp.h).to(dev)
     Pi = torch.from_numpy(inp.Pi).to(dev)
@@ -210,7 +207,6 @@ def main():
             "workload": "%s: n=%d rows, m=%d features, %d quantile bins, d=%d softmax outputs, %s sketch k=%d, "
                         "depth %d, lambda=%g" % (wl.name, wl.n, wl.m, wl.n_bins, wl.d, wl.kind.replace("_", " "),
                                                  wl.k, wl.depth, wl.lam),
-            "layout": args.layout,
         },
         "hist_GBps": achieved,
         "hist_pct_peak": 100.0 * achieved / HBM_PEAK_GBPS,

@@ -37,6 +37,30 @@
  *   outputs do not overlap.  Only the error text is per-thread state.
  * - Sizes: n < 2^31 rows, m <= 65535 features, 2 <= n_bins <= 256,
  *   1 <= k <= 255 sketch columns (k+1 channels).
+ *
+ * Data layouts (device memory; the layouts are this library's choice, made
+ * so that each kernel reads whole cache lines of what it needs)
+ * ----------------------------------------------------------------------
+ * - QUAD-MAJOR BINS (bins4, ld4): the uint32 word q of row i is
+ *   bins4[q*ld4 + i], ld4 >= n, and its byte u (little-endian) is the bin of
+ *   feature 4q+u.  A row has Q = ceil(m/4) words; bytes of features >= m are
+ *   ignored.  The histogram kernel reads this layout: the 64 lanes of a wave
+ *   take 64 consecutive rows and read 256 contiguous bytes per word.
+ * - COLUMN-MAJOR BINS (bins_cm, ld_cm): the bin of (row i, feature f) is the
+ *   byte bins_cm[f*ld_cm + i], ld_cm >= n.  The partition reads it: the rows
+ *   of a node are read in one run of the split feature's column.
+ * - ROW RECORDS (rec, ld_rec, rec_gh): row i owns the ld_rec bytes at
+ *   rec + i*ld_rec; its m bins are bytes 0..m-1 and, once sb_sketch has
+ *   written the sketch into the records, channel t of its sketch is the
+ *   float at byte rec_gh + 4t.  Requirements: 16-byte aligned base,
+ *   ld_rec % 16 == 0, rec_gh % 4 == 0, rec_gh >= m, rec_gh + 4(k+1) <= ld_rec.
+ *   The histograms of the deeper levels read it through row indices: one
+ *   row is one contiguous record (exactly one 128-byte line for m = 100,
+ *   k = 5).
+ * - CHANNEL-MAJOR SKETCH (GH, ld_gh): channel t of row i is GH[t*ld_gh + i],
+ *   ld_gh >= n.  Channels 0..k-1 are the sketch columns, channel k is the
+ *   hessian weight h.
+ * sb_layout_bins() builds the three bin layouts from a row-major matrix.
  */
 #ifndef SB_H_
 #define SB_H_
@@ -48,7 +72,7 @@
 extern "C" {
 #endif
 
-#define SB_ABI_VERSION 1
+#define SB_ABI_VERSION 2
 
 /* Status codes. */
 enum {
@@ -88,13 +112,28 @@ int32_t sb_abi_version(void);
  * ignored (pass 0).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
  * SCORE_SPLITS, PARTITION_ROWS).  depth: tree depth (GROW_TREE).  d: output
  * dimension (SKETCH).  Returns -1 (and sets the error text) for invalid
- * sizes.
+ * sizes.  sb_layout_bins and sb_subtract_histograms need no workspace.
  */
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
                            int32_t n_nodes, int32_t depth);
 
 /*
- * sb_sketch -- build the packed sketch GH = [G_k, h] (Section 3).
+ * sb_layout_bins -- the three bin layouts from a row-major bin matrix.
+ *
+ * bins     n x m uint8 bins, row-major: (i, f) at bins[i*ld_bins + f],
+ *          ld_bins >= m.  Values must be < n_bins of the later calls.
+ * bins4    out (may be NULL): quad-major bins, ld4 >= n.  Bytes of features
+ *          >= m are written as 0.
+ * bins_cm  out (may be NULL): column-major bins, ld_cm >= n.
+ * rec      out (may be NULL): row records, ld_rec % 16 == 0, ld_rec >= m,
+ *          16-byte aligned.  Only bytes 0..m-1 of each record are written.
+ * Setup work, once per dataset (not on the per-tree path).
+ */
+int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, uint32_t* bins4, int64_t ld4,
+                       uint8_t* bins_cm, int64_t ld_cm, uint8_t* rec, int64_t ld_rec, void* stream);
+
+/*
+ * sb_sketch -- build the sketch GH = [G_k, h] (Section 3).
  *
  * G       n x d gradient matrix, column-major: element (i, j) at G[j*ld_g + i],
  *         ld_g >= n.
@@ -116,10 +155,14 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
  * u       RANDOM_SAMPLING only: k uniforms in [0, 1) (fp64, device).  The
  *         random numbers are an input so that results are reproducible.
  * Pi      RANDOM_PROJECTION only: d x k, row-major (Pi[j*k + t]), fp32.
- * GH      out: n records of k+1 floats, record i at GH + i*ld_gh, ld_gh >= k+1;
- *         GH[i*ld_gh + t] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
+ * GH      out: channel-major sketch, ld_gh >= n:
+ *         GH[t*ld_gh + i] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
  *         fp32 multiply; the projection sum for RANDOM_PROJECTION) and
- *         GH[i*ld_gh + k] = h[i].
+ *         GH[k*ld_gh + i] = h[i].
+ * rec, ld_rec, rec_gh  optional (rec may be NULL): the same k+1 values are
+ *         also written into the row records (float t of row i at byte
+ *         i*ld_rec + rec_gh + 4t), where the histograms of the deeper levels
+ *         read them.
  * cols, scales  out (not RANDOM_PROJECTION): k entries each.
  * norm2   out: d fp64 squared column norms; required for TOP_OUTPUTS and
  *         RANDOM_SAMPLING, optional (may be NULL) for IDENTITY, ignored for
@@ -128,13 +171,14 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
  *         sb_build_histograms (same rule as sb_hist_exponents).
  */
 int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream);
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
+                  int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
+                  int64_t ws_bytes, void* stream);
 
 /*
- * sb_hist_exponents -- fixed-point exponents for a given GH.
+ * sb_hist_exponents -- fixed-point exponents for a given GH (channel-major).
  *
- * For channel t (t <= k) with M_t = max_i |GH[i*ld_gh + t]|:
+ * For channel t (t <= k) with M_t = max_i |GH[t*ld_gh + i]|:
  *   qexp[t] = 18 - floor(log2(M_t))   (qexp[t] = 0 if M_t == 0),
  * so every value maps to an integer rint(v * 2^qexp[t]) of magnitude <= 2^19.
  * sb_build_histograms accumulates those integers exactly and reports sums
@@ -149,22 +193,28 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  * sb_build_histograms -- per-node histograms of one tree level (Section 3.4).
  *
  * For every built node j, feature f, bin b and channel t <= k:
- *   H[((j*m + f)*n_bins + b)*(k+1) + t] = sum over rows r of node j with
- *       bins[r*ld_bins + f] == b of GH[r*ld_gh + t],
+ *   H[((j*m + f)*n_bins + b)*(k+1) + t] = sum over the rows r of node j whose
+ *       feature f has bin b of channel t of r's sketch,
  * accumulated exactly in fixed point (see sb_hist_exponents) and written as
  * fp64.  Nodes not in the build list are left untouched.
  *
- * bins      n x m uint8, row-major, ld_bins >= m, ld_bins % 4 == 0, 4-byte
- *           aligned base.  Values must be < n_bins.
- * GH, ld_gh, k, qexp  the sketch records and exponents from sb_sketch.
- * row_idx   n row indices grouped by node (NULL = identity order).
- * node_off  n_nodes+1 offsets: node j owns row_idx[node_off[j] .. node_off[j+1]).
+ * The rows are read from one of two sources:
+ * row_idx == NULL: node j's rows are the positions node_off[j] ..
+ *           node_off[j+1] of the arrays bins4 (quad-major, ld4 >= n, 4-byte
+ *           aligned) and GH (channel-major, ld_gh >= n); every load is
+ *           coalesced.  rec may be NULL.
+ * row_idx != NULL: node j's rows are row_idx[node_off[j] .. node_off[j+1]),
+ *           each < n, read from their row records (rec, ld_rec, rec_gh; the
+ *           sketch must have been written into them by sb_sketch): one record
+ *           per row.  bins4 and GH may be NULL.
+ * k, qexp   sketch columns and the exponents from sb_sketch.
+ * node_off  n_nodes+1 offsets.
  * build_list  n_build node ids to build (NULL = every node; n_build ignored).
  * H         out: [n_nodes][m][n_bins][k+1] fp64.
  */
-int32_t sb_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
-                            const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
-                            const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
+int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t rec_gh,
+                            int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+                            const int32_t* qexp, const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                             const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
                             void* stream);
 
@@ -202,16 +252,13 @@ int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_b
  * sb_partition_rows -- split every node's rows for the next level.
  *
  * Node j's rows (row_idx_in[node_off_in[j] .. node_off_in[j+1]), identity
- * order if row_idx_in is NULL) are split stably into left (bins_cm value of
- * feature best_feature[j] <= best_bin[j]) then right, written to the same
+ * order if row_idx_in is NULL) are split stably into left (column-major bin
+ * of feature best_feature[j] <= best_bin[j]) then right, written to the same
  * range of row_idx_out.  best_feature[j] < 0 marks a terminal node: every row
  * goes left and the right child is empty.
- * bins_cm   the binned features column-major: value (r, f) at
- *           bins_cm[f*ld_cm + r], ld_cm >= n (same values as sb_build_histograms'
- *           row-major copy; the column-major copy makes this call read one
- *           contiguous run per node).
- * node_off_out  out: 2*n_nodes+1 offsets of the next level.
- * build_list_out out: n_nodes entries; entry j is the smaller child of node j
+ * bins_cm, ld_cm  column-major bins (ld_cm >= n).
+ * node_off_out    out: 2*n_nodes+1 offsets of the next level.
+ * build_list_out  out: n_nodes entries; entry j is the smaller child of node j
  *           (2j on ties), the node whose histogram the next level builds.
  * row_idx_in and row_idx_out must not overlap.
  */
@@ -224,11 +271,13 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
 /*
  * sb_grow_tree -- the whole level loop for one tree (depth-wise growth).
  *
- * Runs, for level l = 0..depth-1: build histograms (all rows at l = 0, the
- * smaller child of each pair after that), sibling subtraction, scoring and
- * partition, entirely on the device with no host synchronisation.
- * bins (row-major, ld_bins) and bins_cm (column-major, ld_cm) hold the same
- * binned features; GH / qexp come from sb_sketch.
+ * Runs, for level l = 0..depth-1: histograms (all rows at l = 0, read from
+ * bins4 and GH; from l = 1 on, the smaller child of each pair, read from the
+ * row records), sibling subtraction, scoring and partition, entirely on the
+ * device with no host synchronisation.
+ * bins4 / bins_cm / rec hold the same binned features in the three layouts;
+ * GH (channel-major) and the sketch inside rec come from one sb_sketch call;
+ * qexp from the same call.
  * tree_feature, tree_bin, tree_score: out, 2^depth - 1 entries in level
  *   order (node j of level l at index 2^l - 1 + j).
  * row_idx_out: out, n rows grouped by leaf; leaf_off_out: out, 2^depth + 1
@@ -236,11 +285,11 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
  *   row_idx_out[leaf_off_out[j] .. leaf_off_out[j+1])).
  * 1 <= depth <= 12.
  */
-int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_cm, int64_t ld_cm, int64_t n,
-                     int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
-                     int32_t depth, double lambda, double min_child_weight, int32_t* tree_feature,
-                     int32_t* tree_bin, double* tree_score, int32_t* row_idx_out, int32_t* leaf_off_out,
-                     void* ws, int64_t ws_bytes, void* stream);
+int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm, int64_t ld_cm, const uint8_t* rec,
+                     int64_t ld_rec, int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH,
+                     int64_t ld_gh, int32_t k, const int32_t* qexp, int32_t depth, double lambda,
+                     double min_child_weight, int32_t* tree_feature, int32_t* tree_bin, double* tree_score,
+                     int32_t* row_idx_out, int32_t* leaf_off_out, void* ws, int64_t ws_bytes, void* stream);
 
 /*
  * Kernel timing for benchmarks.  Between sb_profile_begin() and

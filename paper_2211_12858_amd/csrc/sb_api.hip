@@ -60,31 +60,48 @@ int32_t check_hist_shape(const char* call, int64_t n, int32_t m, int32_t n_bins,
   return SB_OK;
 }
 
-int64_t grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth, int64_t* off) {
-  // off[0] H0, off[1] H1, off[2] rows tmp, off[3] level offsets, off[4] build lists, off[5] call ws
+struct GrowLayout {
+  int64_t H0, H1, rows_tmp, offs, blists, call, total;
+};
+
+GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth) {
+  GrowLayout L{};
   const int64_t maxn = int64_t(1) << (depth - 1);
   const int64_t hbytes = align256(maxn * m * n_bins * (int64_t)(k + 1) * 8);
-  const int64_t hw = hist_ws_bytes(m, n_bins, k, (int32_t)(maxn > 1 ? maxn / 1 : 1));
-  if (hw < 0) return -1;
+  const int64_t hw = hist_ws_bytes(m, n_bins, k, (int32_t)maxn);
+  if (hw < 0) {
+    L.total = -1;
+    return L;
+  }
   int64_t call = hw;
   const int64_t sw = score_ws_bytes((int32_t)maxn, m);
   const int64_t pw = partition_ws_bytes(n, (int32_t)maxn);
   if (sw > call) call = sw;
   if (pw > call) call = pw;
+  const int64_t level_offs = align256(((int64_t(1) << depth) + depth) * 4);
   int64_t p = 0;
-  off[0] = p;
+  L.H0 = p;
   p += hbytes;
-  off[1] = p;
+  L.H1 = p;
   p += hbytes;
-  off[2] = p;
+  L.rows_tmp = p;
   p += align256(n * 4);
-  off[3] = p;
-  p += align256(((int64_t(1) << depth) + depth) * 4);
-  off[4] = p;
+  L.offs = p;
+  p += level_offs;
+  L.blists = p;
   p += align256((int64_t(1) << depth) * 4);
-  off[5] = p;
+  L.call = p;
   p += call;
-  return p;
+  L.total = p;
+  return L;
+}
+
+int32_t check_rec(const char* call, const void* rec, int64_t ld_rec, int64_t rec_gh, int32_t m, int32_t k) {
+  if (!aligned(rec, 16) || ld_rec % 16 != 0 || rec_gh % 4 != 0 || rec_gh < m || rec_gh + 4ll * (k + 1) > ld_rec)
+    return fail(SB_E_SHAPE, std::string(call) +
+                                ": row records need a 16-byte aligned base, ld_rec % 16 == 0, rec_gh % 4 == 0, "
+                                "rec_gh >= m and rec_gh + 4(k+1) <= ld_rec");
+  return SB_OK;
 }
 
 __global__ void k_root_offsets(int32_t* off, int32_t n) {
@@ -143,8 +160,8 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
       if (n < 1 || d < 1 || k < 1) break;
       return sketch_ws_bytes(0, n, d, k);
     case SB_CALL_HIST_EXPONENTS:
-      if (k < 1) break;
-      return align256((int64_t)(k + 1) * 4);
+      if (k < 1 || k > 255) break;
+      return hist_exponents_ws_bytes(k);
     case SB_CALL_BUILD_HISTOGRAMS: {
       if (m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || n_nodes < 1) break;
       const int64_t b = hist_ws_bytes(m, n_bins, k, n_nodes);
@@ -159,8 +176,7 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
       return partition_ws_bytes(n, n_nodes);
     case SB_CALL_GROW_TREE: {
       if (n < 1 || m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || depth < 1 || depth > MAX_DEPTH) break;
-      int64_t off[6];
-      const int64_t b = grow_ws_layout(n, m, n_bins, k, depth, off);
+      const int64_t b = grow_ws_layout(n, m, n_bins, k, depth).total;
       if (b < 0) break;
       return b;
     }
@@ -172,9 +188,25 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
   return -1;
 }
 
+int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, uint32_t* bins4, int64_t ld4,
+                       uint8_t* bins_cm, int64_t ld_cm, uint8_t* rec, int64_t ld_rec, void* stream) {
+  if (!bins) return fail(SB_E_ARG, "sb_layout_bins: bins must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_layout_bins: n must be in [1, 2^31)");
+  if (m < 1 || m > 65535) return fail(SB_E_ARG, "sb_layout_bins: m must be in [1, 65535]");
+  if (ld_bins < m) return fail(SB_E_SHAPE, "sb_layout_bins: ld_bins must be >= m");
+  if (bins4 && (ld4 < n || !aligned(bins4, 4)))
+    return fail(SB_E_SHAPE, "sb_layout_bins: bins4 needs ld4 >= n and a 4-byte aligned base");
+  if (bins_cm && ld_cm < n) return fail(SB_E_SHAPE, "sb_layout_bins: ld_cm must be >= n");
+  if (rec && (ld_rec < m || ld_rec % 16 != 0 || !aligned(rec, 16)))
+    return fail(SB_E_SHAPE, "sb_layout_bins: rec needs ld_rec >= m, ld_rec % 16 == 0 and a 16-byte aligned base");
+  return launch_layout(bins, n, m, ld_bins, bins4, ld4, bins_cm, ld_cm, rec, ld_rec,
+                       static_cast<hipStream_t>(stream));
+}
+
 int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
+                  int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
+                  int64_t ws_bytes, void* stream) {
   if (kind < SB_SKETCH_TOP_OUTPUTS || kind > SB_SKETCH_IDENTITY)
     return fail(SB_E_UNSUPPORTED, "sb_sketch: unknown sketch kind " + std::to_string(kind));
   if (!G || !h || !GH || !qexp) return fail(SB_E_ARG, "sb_sketch: G, h, GH and qexp must not be NULL");
@@ -182,7 +214,11 @@ int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld
   if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_sketch: d must be in [1, 65535]");
   if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_sketch: k must be in [1, 255]");
   if (ld_g < n) return fail(SB_E_SHAPE, "sb_sketch: ld_g must be >= n");
-  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_sketch: ld_gh must be >= k + 1");
+  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_sketch: ld_gh must be >= n (GH is channel-major)");
+  if (rec) {
+    const int32_t rr = check_rec("sb_sketch", rec, ld_rec, rec_gh, 0, k);
+    if (rr) return rr;
+  }
   switch (kind) {
     case SB_SKETCH_TOP_OUTPUTS:
       if (k > d) return fail(SB_E_ARG, "sb_sketch: top outputs needs k <= d");
@@ -202,8 +238,8 @@ int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld
   }
   int32_t rc = need_ws(ws, ws_bytes, sketch_ws_bytes(kind, n, d, k), "sb_sketch");
   if (rc) return rc;
-  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws,
-                       static_cast<hipStream_t>(stream));
+  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, rec, ld_rec, rec_gh, cols, scales, norm2, qexp,
+                       ws, static_cast<hipStream_t>(stream));
 }
 
 int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
@@ -211,35 +247,41 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
   if (!GH || !qexp) return fail(SB_E_ARG, "sb_hist_exponents: GH and qexp must not be NULL");
   if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_hist_exponents: n must be in [1, 2^31)");
   if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_hist_exponents: k must be in [1, 255]");
-  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_hist_exponents: ld_gh must be >= k + 1");
-  int32_t rc = need_ws(ws, ws_bytes, align256((int64_t)(k + 1) * 4), "sb_hist_exponents");
+  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_hist_exponents: ld_gh must be >= n (GH is channel-major)");
+  int32_t rc = need_ws(ws, ws_bytes, hist_exponents_ws_bytes(k), "sb_hist_exponents");
   if (rc) return rc;
   return launch_hist_exponents(GH, n, ld_gh, k, qexp, ws, static_cast<hipStream_t>(stream));
 }
 
-int32_t sb_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
-                            const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
-                            const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
+int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t rec_gh,
+                            int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+                            const int32_t* qexp, const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                             const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
                             void* stream) {
   const char* call = "sb_build_histograms";
-  if (!bins || !GH || !qexp || !node_off || !H)
-    return fail(SB_E_ARG, "sb_build_histograms: bins, GH, qexp, node_off and H must not be NULL");
+  if (!qexp || !node_off || !H) return fail(SB_E_ARG, "sb_build_histograms: qexp, node_off and H must not be NULL");
   int32_t rc = check_hist_shape(call, n, m, n_bins, k);
   if (rc) return rc;
-  if (ld_bins < m || ld_bins % 4 != 0 || !aligned(bins, 4))
-    return fail(SB_E_SHAPE, "sb_build_histograms: bins needs ld_bins >= m, ld_bins % 4 == 0 and a 4-byte aligned base");
-  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_build_histograms: ld_gh must be >= k + 1");
+  if (row_idx) {
+    if (!rec) return fail(SB_E_ARG, "sb_build_histograms: rows through row_idx are read from rec, which is NULL");
+    rc = check_rec(call, rec, ld_rec, rec_gh, m, k);
+    if (rc) return rc;
+  } else {
+    if (!bins4 || !GH) return fail(SB_E_ARG, "sb_build_histograms: without row_idx, bins4 and GH must not be NULL");
+    if (ld4 < n || !aligned(bins4, 4))
+      return fail(SB_E_SHAPE, "sb_build_histograms: bins4 needs ld4 >= n and a 4-byte aligned base");
+    if (ld_gh < n) return fail(SB_E_SHAPE, "sb_build_histograms: ld_gh must be >= n (GH is channel-major)");
+  }
   if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, "sb_build_histograms: n_nodes must be in [1, 2^20]");
   if (build_list == nullptr) n_build = n_nodes;
   if (n_build < 1 || n_build > n_nodes || n_build > 65535)
     return fail(SB_E_ARG, "sb_build_histograms: n_build must be in [1, min(n_nodes, 65535)]");
   if (hist_plan(m, n_bins, k, n_build).nq == 0)
-    return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) int32 cells exceed the 160 KB LDS");
+    return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) cells exceed the LDS budget");
   rc = need_ws(ws, ws_bytes, hist_ws_bytes(m, n_bins, k, n_build), call);
   if (rc) return rc;
-  return launch_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
-                                 build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
+  return launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off,
+                                 n_nodes, build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
 }
 
 int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t n_parents, int32_t m,
@@ -294,43 +336,44 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
                           row_idx_out, node_off_out, build_list_out, ws, static_cast<hipStream_t>(stream));
 }
 
-int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_cm, int64_t ld_cm, int64_t n,
-                     int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
-                     int32_t depth, double lambda, double min_child_weight, int32_t* tree_feature,
-                     int32_t* tree_bin, double* tree_score, int32_t* row_idx_out, int32_t* leaf_off_out,
-                     void* ws, int64_t ws_bytes, void* stream) {
+int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm, int64_t ld_cm, const uint8_t* rec,
+                     int64_t ld_rec, int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH,
+                     int64_t ld_gh, int32_t k, const int32_t* qexp, int32_t depth, double lambda,
+                     double min_child_weight, int32_t* tree_feature, int32_t* tree_bin, double* tree_score,
+                     int32_t* row_idx_out, int32_t* leaf_off_out, void* ws, int64_t ws_bytes, void* stream) {
   const char* call = "sb_grow_tree";
-  if (!bins || !bins_cm || !GH || !qexp || !tree_feature || !tree_bin || !tree_score || !row_idx_out ||
+  if (!bins4 || !bins_cm || !rec || !GH || !qexp || !tree_feature || !tree_bin || !tree_score || !row_idx_out ||
       !leaf_off_out)
     return fail(SB_E_ARG, "sb_grow_tree: inputs and outputs must not be NULL");
   int32_t rc = check_hist_shape(call, n, m, n_bins, k);
   if (rc) return rc;
   if (depth < 1 || depth > MAX_DEPTH) return fail(SB_E_ARG, "sb_grow_tree: depth must be in [1, 12]");
-  if (ld_bins < m || ld_bins % 4 != 0 || !aligned(bins, 4))
-    return fail(SB_E_SHAPE, "sb_grow_tree: bins needs ld_bins >= m, ld_bins % 4 == 0 and a 4-byte aligned base");
+  if (ld4 < n || !aligned(bins4, 4))
+    return fail(SB_E_SHAPE, "sb_grow_tree: bins4 needs ld4 >= n and a 4-byte aligned base");
   if (ld_cm < n) return fail(SB_E_SHAPE, "sb_grow_tree: ld_cm must be >= n");
-  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_grow_tree: ld_gh must be >= k + 1");
+  rc = check_rec(call, rec, ld_rec, rec_gh, m, k);
+  if (rc) return rc;
+  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_grow_tree: ld_gh must be >= n (GH is channel-major)");
   if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_grow_tree: lambda must be > 0");
   if (!(min_child_weight >= 0.0) || !std::isfinite(min_child_weight))
     return fail(SB_E_ARG, "sb_grow_tree: min_child_weight must be >= 0");
   if (hist_plan(m, n_bins, k, 1).nq == 0)
     return fail(SB_E_UNSUPPORTED, "sb_grow_tree: 4 features x n_bins x (k+1) int32 cells exceed the 160 KB LDS");
-  int64_t off[6];
-  const int64_t need = grow_ws_layout(n, m, n_bins, k, depth, off);
-  rc = need_ws(ws, ws_bytes, need, call);
+  const GrowLayout G = grow_ws_layout(n, m, n_bins, k, depth);
+  rc = need_ws(ws, ws_bytes, G.total, call);
   if (rc) return rc;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(ws);
-  double* Hbuf[2] = {reinterpret_cast<double*>(w + off[0]), reinterpret_cast<double*>(w + off[1])};
-  int32_t* rows_tmp = reinterpret_cast<int32_t*>(w + off[2]);
-  int32_t* offs = reinterpret_cast<int32_t*>(w + off[3]);
-  int32_t* blists = reinterpret_cast<int32_t*>(w + off[4]);
-  void* cws = w + off[5];
-  const int64_t cws_bytes = ws_bytes - off[5];
+  double* Hbuf[2] = {reinterpret_cast<double*>(w + G.H0), reinterpret_cast<double*>(w + G.H1)};
+  int32_t* rows_tmp = reinterpret_cast<int32_t*>(w + G.rows_tmp);
+  int32_t* offs = reinterpret_cast<int32_t*>(w + G.offs);
+  int32_t* blists = reinterpret_cast<int32_t*>(w + G.blists);
+  void* cws = w + G.call;
   const int64_t cpn = (int64_t)m * n_bins * (k + 1);
 
-  // level l offsets start at offs + (2^l - 1) + l; level l build list at blists + 2^(l-1) - 1
+  // level l node offsets start at offs + (2^l - 1) + l (2^l + 1 entries), its
+  // build list at blists + 2^(l-1) - 1
   auto level_off = [&](int l) { return offs + ((int64_t(1) << l) - 1) + l; };
   auto level_build = [&](int l) { return blists + ((int64_t(1) << (l - 1)) - 1); };
   auto level_rows = [&](int l) -> int32_t* {  // rows of level l >= 1; level depth lands in row_idx_out
@@ -344,12 +387,12 @@ int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_c
     const int32_t* row_in = l == 0 ? nullptr : level_rows(l);
     const int32_t* off_l = level_off(l);
     if (l == 0) {
-      rc = sb_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1, nullptr, 1, Hcur,
-                               cws, cws_bytes, st);
+      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l,
+                                   1, nullptr, 1, Hcur, cws, st);
     } else {
       const int32_t* bl = level_build(l);
-      rc = sb_build_histograms(bins, n, m, ld_bins, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn, bl, nn / 2, Hcur,
-                               cws, cws_bytes, st);
+      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l,
+                                   nn, bl, nn / 2, Hcur, cws, st);
       if (!rc) rc = launch_subtract(Hbuf[(l - 1) & 1], Hcur, nn / 2, cpn, bl, st);
     }
     if (rc) return rc;
@@ -357,9 +400,9 @@ int32_t sb_grow_tree(const uint8_t* bins, int64_t ld_bins, const uint8_t* bins_c
     rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
                       tree_score + base, cws, st);
     if (rc) return rc;
-    int32_t* off_next = (l == depth - 1) ? leaf_off_out : level_off(l + 1);
+    const bool last = l == depth - 1;
     rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,
-                          level_rows(l + 1), off_next, level_build(l + 1), cws, st);
+                          level_rows(l + 1), last ? leaf_off_out : level_off(l + 1), level_build(l + 1), cws, st);
     if (rc) return rc;
   }
   return check_launch(call);

@@ -26,10 +26,11 @@ static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point win
 
 // ---------------------------------------------------------------- histogram plan
 // One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
-// VGPRs per lane) and up to 40 int32 LDS cells per thread (120 KB of the
-// 160 KB LDS).  Each thread keeps the int64 totals of its 40 cells in 80
-// VGPRs next to the double-buffered row data of the step loop; with 4 waves
-// per SIMD (128 VGPRs) they would spill to scratch.
+// VGPRs per lane) and up to 40 channel cells per thread (20 64-bit LDS cells
+// of two channels each: 120 KB of the 160 KB LDS).  Each thread keeps the
+// int64 totals of its 40 channel cells in 80 VGPRs next to the prefetched
+// row data of the step loop; with 4 waves per SIMD (128 VGPRs) they would
+// spill to scratch.
 constexpr int HIST_THREADS = 768;
 constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
 constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
@@ -40,11 +41,12 @@ constexpr int HIST_MAX_QUADS = 16;
 
 struct HistPlan {
   int c;          // channels k+1
+  int pairs;      // 64-bit LDS cells per (feature, bin): ceil(c/2)
   int nq;         // 4-feature quads per slice
   int f;          // features per slice (4*nq)
   int slices;     // feature slices
   int rows_wave;  // rows one wave handles per step (64 / nq)
-  int cells;      // f * n_bins * c int32 cells per workgroup
+  int cells;      // 2 * pairs * f * n_bins channel cells per workgroup
   int q;          // row groups per slice
   int q_pad;      // q rounded up to a multiple of 8 (XCD-aware mapping)
   int64_t slots;  // partial slots per slice: q + n_build
@@ -53,15 +55,21 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
 int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
 
 // ---------------------------------------------------------------- launches (stream-ordered)
+int32_t launch_layout(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, uint32_t* bins4, int64_t ld4,
+                      uint8_t* bins_cm, int64_t ld_cm, uint8_t* rec, int64_t ld_rec, hipStream_t st);
+
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                      const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                      double* norm2, int32_t* qexp, void* ws, hipStream_t st);
+                      const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
+                      int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
+                      hipStream_t st);
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k);
+int64_t hist_exponents_ws_bytes(int32_t k);
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
                               hipStream_t st);
 
-int32_t launch_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
-                                const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec,
+                                int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
+                                int32_t k, const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st);
 int32_t launch_subtract(const double* Hp, double* Hc, int32_t n_parents, int64_t cells_per_node,

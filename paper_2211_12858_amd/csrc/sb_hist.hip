@@ -1,19 +1,29 @@
 // Per-node histograms of one tree level (Section 3.4) and sibling subtraction.
 //
-// Design for gfx950 (measured: ds_add_f32 retires ~0.33 lanes/clk/CU while
-// ds_add_u32 retires 10-14 lanes/clk/CU):
+// Design for gfx950.  The scatter-add of random bins into LDS is the roof of
+// this kernel, and it is set by LDS bank conflicts.  Measured on MI355X with
+// uniformly random bins, 768 threads and 120 KB of cells per CU:
+// ds_add_u32 retires 6.5 channel-adds/clk/CU and ds_add_u64 carrying two
+// channels 8.9 (conflict-free bins reach 14.9; ds_add_f32 only ~0.3).  So:
 //  * every sketch value is quantised to an integer rint(v * 2^qexp[t]) of
-//    magnitude <= 2^QBITS and accumulated with int32 LDS atomics;
-//  * each LDS cell is a running sum modulo 2^32.  Its owner thread reads it
-//    back every window of <= WINDOW_ROWS rows and adds the wrapped difference
-//    into an int64 register total, so no cell can overflow;
-//  * a workgroup owns one feature slice (F features, LDS = F*B*(k+1) int32
-//    cells) and a contiguous range of the rows of the built nodes, taken in
-//    build-list order; it writes one int64 partial per node it touched;
+//    magnitude <= 2^QBITS;
+//  * channels are packed in pairs into 64-bit LDS cells holding
+//    hi * 2^32 + lo as a two's-complement sum, one ds_add_u64 per pair;
+//  * each cell is a running sum modulo 2^64.  Its owner thread reads it back
+//    every window of <= WINDOW_ROWS rows, splits the change into the two
+//    channel changes (each below 2^31 in magnitude, so the split is exact)
+//    and adds them into int64 register totals;
+//  * a workgroup owns one feature slice (F features, F * n_bins cells per
+//    channel pair) and a contiguous range of the rows of the built nodes,
+//    taken in build-list order; it writes one int64 partial per node it
+//    touched;
 //  * k_hist_reduce sums the partials of each node (integer, so the result is
 //    independent of the grid and of the order of the atomics) and writes the
 //    fp64 histogram.  Sums of fixed-point values are exact in fp64, which
 //    makes sibling subtraction exact as well.
+// Rows come either as positions of contiguous data (quad-major bins and a
+// channel-major sketch: every load is 256 contiguous bytes per wave) or
+// through row indices from the row records (one record line per row).
 // Workgroups that share a row range but own different slices are placed on
 // the same XCD (dispatch is round-robin over the 8 XCDs by block index) so
 // the rows they all read stay in that XCD's L2.
@@ -24,7 +34,8 @@ namespace sb {
 HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   HistPlan p{};
   p.c = k + 1;
-  const int64_t quad_bytes = 4ll * n_bins * p.c * 4;
+  p.pairs = (p.c + 1) / 2;
+  const int64_t quad_bytes = 4ll * n_bins * p.pairs * 8;
   int nq_max = (int)(HIST_LDS_BYTES / quad_bytes);
   const int quads_total = (m + 3) / 4;
   if (nq_max > quads_total) nq_max = quads_total;
@@ -35,7 +46,7 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   p.nq = (quads_total + p.slices - 1) / p.slices;
   p.f = 4 * p.nq;
   p.rows_wave = 64;  // one lane per row; the lane covers the whole slice
-  p.cells = p.f * n_bins * p.c;
+  p.cells = 2 * p.pairs * p.f * n_bins;  // channel cells, the odd channel's partner included
   // Workgroup b runs on XCD b % 8 and a row group's slices share its XCD, so
   // an XCD hosts (q/8) * slices workgroups; keep that within its 32 CUs (one
   // histogram workgroup per CU) so that every workgroup starts at once.
@@ -57,10 +68,12 @@ int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
 namespace {
 
 struct HistArgs {
-  const uint8_t* bins;
-  int64_t ld_bins;
+  const uint32_t* bins4;
+  int64_t ld4;
   const float* GH;
   int64_t ld_gh;
+  const uint8_t* rec;
+  int64_t ld_rec, rec_gh;
   const int32_t* qexp;
   const int32_t* row_idx;
   const int32_t* node_off;
@@ -69,7 +82,7 @@ struct HistArgs {
   int64_t* partial;
   double* H;
   int64_t n;
-  int32_t m, n_bins, c, n_nodes, n_build;
+  int32_t m, n_bins, c, pairs, n_nodes, n_build;
   int32_t nq, f, slices, rows_wave, cells, q, cpt, steps_per_window;
   int64_t slots;
 };
@@ -125,25 +138,39 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
   if (threadIdx.x == 1023) a.pre[a.n_build] = part[1023];
 }
 
-// Thread t owns the contiguous cells [t*MAXC, t*MAXC + MAXC) (MAXC =
-// HIST_MAX_CELLS_PER_THREAD, a multiple of 4), read as 128-bit words.  The
-// LDS always holds MAXC cells per thread (cells past the plan's count stay
-// zero), so the reads need no bounds tests.  Cells are folded 8 at a time with
-// compiler barriers in between, which bounds the registers the reads hold on
-// top of the 2*MAXC registers of totals.
-__device__ inline void fold_cells(const int32_t* lds, int64_t* tot) {
-  static_assert(HIST_MAX_CELLS_PER_THREAD % 8 == 0, "fold reads 8 cells at a time");
-  const int4* src = reinterpret_cast<const int4*>(lds + threadIdx.x * HIST_MAX_CELLS_PER_THREAD);
+// Thread t owns the contiguous 64-bit cells [t*H, t*H + H), H =
+// HIST_MAX_CELLS_PER_THREAD / 2, read as 128-bit words; cell j carries the
+// channel cells 2j (low half) and 2j+1 (high half) of the thread's totals.
+// The LDS always holds H cells per thread (cells past the plan's count stay
+// zero), so the reads need no bounds tests.  Cells are folded 4 at a time
+// with compiler barriers in between, which bounds the registers the reads
+// hold on top of the 2*MAXC registers of totals.
+//
+// A cell holds S = Hi * 2^32 + Lo (mod 2^64), Hi and Lo the exact running
+// channel sums, and the totals hold the sums as of the previous read, so
+// the change D = S - (tot_hi * 2^32 + tot_lo) is dHi * 2^32 + dLo with
+// |dLo|, |dHi| < 2^31: dLo is the sign-extended low word of D and dHi the
+// arithmetic high word of D - dLo.
+__device__ inline void fold_cells(const uint64_t* lds64, int64_t* tot) {
+  constexpr int H = HIST_MAX_CELLS_PER_THREAD / 2;
+  static_assert(H % 4 == 0, "fold reads 4 cells at a time");
+  const uint4* src = reinterpret_cast<const uint4*>(lds64 + threadIdx.x * H);
 #pragma unroll
-  for (int j0 = 0; j0 < HIST_MAX_CELLS_PER_THREAD; j0 += 8) {
+  for (int j0 = 0; j0 < H; j0 += 4) {
     asm volatile("" ::: "memory");
-    const int4 x = src[j0 / 4];
-    const int4 y = src[j0 / 4 + 1];
-    const int32_t cur[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+    const uint4 x = src[j0 / 2];
+    const uint4 y = src[j0 / 2 + 1];
+    const uint64_t cur[4] = {(uint64_t)x.x | ((uint64_t)x.y << 32), (uint64_t)x.z | ((uint64_t)x.w << 32),
+                             (uint64_t)y.x | ((uint64_t)y.y << 32), (uint64_t)y.z | ((uint64_t)y.w << 32)};
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      const int32_t delta = (int32_t)((uint32_t)cur[jj] - (uint32_t)tot[j0 + jj]);
-      tot[j0 + jj] += delta;
+    for (int jj = 0; jj < 4; ++jj) {
+      const int i = 2 * (j0 + jj);
+      const uint64_t last = ((uint64_t)tot[i + 1] << 32) + (uint64_t)tot[i];
+      const uint64_t d = cur[jj] - last;
+      const int64_t dlo = (int64_t)(int32_t)(uint32_t)d;
+      const int64_t dhi = (int64_t)(d - (uint64_t)dlo) >> 32;
+      tot[i] += dlo;
+      tot[i + 1] += dhi;
     }
   }
   asm volatile("" ::: "memory");
@@ -160,7 +187,10 @@ __device__ inline void lds_barrier() {
 }
 
 // One row of one lane: the slice's bins (4 per word) and the row's channel
-// values, loaded together so their latencies overlap.
+// values, loaded together so their latencies overlap.  Both layouts are
+// word-per-row (quad-major bins, channel-major sketch), so each of these
+// loads is one 256-byte contiguous access per wave when the wave's rows are
+// consecutive.
 template <int CMAX, int NQMAX>
 struct RowData {
   uint32_t word[NQMAX];
@@ -177,32 +207,53 @@ struct RowRef {
 
 // EXACT: CMAX channels and NQMAX quads exactly (no per-element tests, so the
 // load path has no branches and the compiler can count outstanding loads).
-// Lanes without a row load row 0 and never use the data.
-template <int CMAX, int NQMAX, bool EXACT>
+// Lanes without a row load row 0 and never use the data.  FROM_REC: the row
+// is read from its record (bins at byte 0, sketch at byte rec_gh), else from
+// the quad-major bins and the channel-major sketch.
+template <int CMAX, int NQMAX, bool EXACT, bool FROM_REC>
 __device__ inline void load_row(const HistArgs& a, RowRef ref, int f0, int nq, int c, RowData<CMAX, NQMAX>& d) {
   int64_t row = ref.on ? (int64_t)ref.raw : 0;
   row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
-  const uint32_t* wp = reinterpret_cast<const uint32_t*>(a.bins + row * a.ld_bins + f0);
+  if constexpr (FROM_REC) {
+    const uint8_t* r = a.rec + row * a.ld_rec;
+    const uint32_t* wp = reinterpret_cast<const uint32_t*>(r) + (f0 >> 2);
 #pragma unroll
-  for (int qq = 0; qq < NQMAX; ++qq)
-    if (EXACT || qq < nq) d.word[qq] = wp[qq];
-  const float* ghr = a.GH + row * a.ld_gh;
+    for (int qq = 0; qq < NQMAX; ++qq)
+      if (EXACT || qq < nq) d.word[qq] = wp[qq];
+    const float* ghr = reinterpret_cast<const float*>(r + a.rec_gh);
 #pragma unroll
-  for (int t = 0; t < CMAX; ++t)
-    if (EXACT || t < c) d.g[t] = ghr[t];
+    for (int t = 0; t < CMAX; ++t)
+      if (EXACT || t < c) d.g[t] = ghr[t];
+  } else {
+    const uint32_t* wp = a.bins4 + (int64_t)(f0 >> 2) * a.ld4 + row;
+#pragma unroll
+    for (int qq = 0; qq < NQMAX; ++qq)
+      if (EXACT || qq < nq) d.word[qq] = wp[(int64_t)qq * a.ld4];
+    const float* ghr = a.GH + row;
+#pragma unroll
+    for (int t = 0; t < CMAX; ++t)
+      if (EXACT || t < c) d.g[t] = ghr[(int64_t)t * a.ld_gh];
+  }
 }
 
-// LDS cells are laid out [t][feature in slice][bin]: for a fixed channel and
-// feature the 64 lanes of a wave hit lds[base + bin], so random bins spread
-// over all the banks.  All four features of a quad are accumulated; features
-// past m (m not a multiple of 4) read padding bytes of the row and land in
-// cells the reduction never reads.
+// LDS cells are laid out [channel pair][feature in slice][bin] (64-bit): for
+// a fixed pair and feature the 64 lanes of a wave hit lds64[base + bin].  All
+// four features of a quad are accumulated; features past m (m not a multiple
+// of 4) read the padding bytes of the last word and land in cells the
+// reduction never reads.  An odd channel count pairs the last channel with a
+// zero.
 template <int CMAX, int NQMAX, bool EXACT>
-__device__ inline void add_row(int32_t* lds, const RowData<CMAX, NQMAX>& d, const int* qe, int nq, int B, int FB,
+__device__ inline void add_row(uint64_t* lds64, const RowData<CMAX, NQMAX>& d, const int* qe, int nq, int B, int FB,
                                int c) {
-  int32_t vq[CMAX];
+  constexpr int PMAX = (CMAX + 1) / 2;
+  int32_t vq[2 * PMAX];
 #pragma unroll
-  for (int t = 0; t < CMAX; ++t) vq[t] = (EXACT || t < c) ? (int32_t)rintf(ldexpf(d.g[t], qe[t])) : 0;
+  for (int t = 0; t < 2 * PMAX; ++t)
+    vq[t] = (t < CMAX && (EXACT || t < c)) ? (int32_t)rintf(ldexpf(d.g[t < CMAX ? t : 0], qe[t < CMAX ? t : 0])) : 0;
+  uint64_t pk[PMAX];
+#pragma unroll
+  for (int p = 0; p < PMAX; ++p)
+    pk[p] = ((uint64_t)(uint32_t)vq[2 * p + 1] << 32) + (uint64_t)(int64_t)vq[2 * p];
 #pragma unroll
   for (int qq = 0; qq < NQMAX; ++qq) {
     if (EXACT || qq < nq) {
@@ -210,10 +261,10 @@ __device__ inline void add_row(int32_t* lds, const RowData<CMAX, NQMAX>& d, cons
       for (int u = 0; u < 4; ++u) {
         int bin = (int)((d.word[qq] >> (8 * u)) & 0xffu);
         bin = bin < B ? bin : B - 1;
-        int32_t* cell = lds + (4 * qq + u) * B + bin;
+        uint64_t* cell = lds64 + (4 * qq + u) * B + bin;
 #pragma unroll
-        for (int t = 0; t < CMAX; ++t)
-          if (EXACT || t < c) atomicAdd(cell + t * FB, vq[t]);
+        for (int p = 0; p < PMAX; ++p)
+          if (EXACT || 2 * p < c) atomicAdd(reinterpret_cast<unsigned long long*>(cell + p * FB), pk[p]);
       }
     }
   }
@@ -222,12 +273,13 @@ __device__ inline void add_row(int32_t* lds, const RowData<CMAX, NQMAX>& d, cons
 // Accumulate the lane's rows of virtual positions [v, vend) of one node
 // (segment start seg0, first virtual position pstart) into the LDS cells,
 // folding into `tot` at every window.  HAS_IDX: rows come through row_idx
-// (otherwise the position is the row).  The row-index load of a lane is
+// and are read from their records (otherwise the position is the row of the
+// contiguous data).  The row-index load of a lane is
 // unconditional (positions past the end are clamped into the segment and
 // marked off), so the load path has no branches and the compiler's count of
 // outstanding loads stays exact.
 template <int CMAX, int NQMAX, bool EXACT, bool HAS_IDX>
-__device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot, const int* qe, int64_t v,
+__device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* tot, const int* qe, int64_t v,
                                    int64_t vend, int64_t pstart, int64_t seg0, int wave, int lane, int f0, int nq,
                                    int B, int FB, int c) {
   const int rows_step = HIST_THREADS;
@@ -254,11 +306,11 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
   RowRef r0 = row_at(v, vend);
   RowRef r1 = row_at(v + rows_step, vend);
   RowData<CMAX, NQMAX> d0, d1;
-  load_row<CMAX, NQMAX, EXACT>(a, r0, f0, nq, c, d0);
+  load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r0, f0, nq, c, d0);
   RowRef r2;
   if constexpr (DEEP) {
     r2 = row_at(v + 2 * rows_step, vend);
-    load_row<CMAX, NQMAX, EXACT>(a, r1, f0, nq, c, d1);
+    load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r1, f0, nq, c, d1);
   }
   int steps = 0;
 #pragma unroll 1
@@ -266,7 +318,7 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
     if constexpr (DEEP) {
       const RowRef r3 = row_at(vs + 3 * rows_step, vend);
       RowData<CMAX, NQMAX> d2;
-      load_row<CMAX, NQMAX, EXACT>(a, r2, f0, nq, c, d2);
+      load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r2, f0, nq, c, d2);
       if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
       r0 = r1;
       d0 = d1;
@@ -275,7 +327,7 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
       r2 = r3;
     } else {
       const RowRef r2n = row_at(vs + 2 * rows_step, vend);
-      load_row<CMAX, NQMAX, EXACT>(a, r1, f0, nq, c, d1);
+      load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r1, f0, nq, c, d1);
       if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
       r0 = r1;
       d0 = d1;
@@ -296,7 +348,8 @@ __device__ inline void run_segment(const HistArgs& a, int32_t* lds, int64_t* tot
 template <int CMAX, int NQMAX, bool EXACT>
 __global__ void __launch_bounds__(HIST_THREADS)
 k_hist(HistArgs a) {
-  extern __shared__ int32_t lds[];
+  extern __shared__ uint64_t lds64[];
+  int32_t* lds = reinterpret_cast<int32_t*>(lds64);
   const int b = blockIdx.x;
   const int xcd = b & 7, g = b >> 3;
   const int q = (g / a.slices) * 8 + xcd;
@@ -341,12 +394,12 @@ k_hist(HistArgs a) {
     const int64_t vend = v1 < a.pre[p + 1] ? v1 : a.pre[p + 1];
     const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
     if (a.row_idx)
-      run_segment<CMAX, NQMAX, EXACT, true>(a, lds, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
+      run_segment<CMAX, NQMAX, EXACT, true>(a, lds64, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
     else
-      run_segment<CMAX, NQMAX, EXACT, false>(a, lds, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
+      run_segment<CMAX, NQMAX, EXACT, false>(a, lds64, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
     // end of this node's part: final fold, write the partial, reset
     __syncthreads();
-    fold_cells(lds, tot);
+    fold_cells(lds64, tot);
     int64_t* dst = a.partial + ((int64_t)s * a.slots + q + p) * a.cells;
 #pragma unroll
     for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
@@ -365,7 +418,8 @@ k_hist(HistArgs a) {
 __device__ inline int64_t group_of(int64_t x, int64_t T, int64_t Q) { return ((x + 1) * Q - 1) / T; }
 
 // H[node][f][b][t] = sum of the partials of the row groups that covered the
-// node.  Partial cell e is laid out [t][feature in slice][bin] like the LDS.
+// node.  Partial channel cell e = 2 * e64 + half, with 64-bit LDS cell e64
+// laid out [channel pair][feature in slice][bin] and t = 2 * pair + half.
 __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   const int p = blockIdx.y, s = blockIdx.z;
@@ -373,12 +427,14 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   const int32_t j = node_of(a, p);
   if (j < 0 || j >= a.n_nodes) return;
   const int FB = a.f * a.n_bins;
-  const int t = e / FB;
-  const int rem = e - t * FB;
+  const int e64 = e >> 1;
+  const int pair = e64 / FB;
+  const int rem = e64 - pair * FB;
   const int fl = rem / a.n_bins;
   const int bin = rem - fl * a.n_bins;
+  const int t = 2 * pair + (e & 1);
   const int f = s * a.f + fl;
-  if (f >= a.m) return;
+  if (f >= a.m || t >= a.c) return;
   const int64_t T = a.pre[a.n_build];
   const int64_t lo = a.pre[p], hi = a.pre[p + 1];
   int64_t sum = 0;
@@ -407,14 +463,18 @@ k_subtract(const double* __restrict__ Hp, double* __restrict__ Hc, int64_t cpn, 
 
 }  // namespace
 
-int32_t launch_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, int32_t n_bins,
-                                const float* GH, int64_t ld_gh, int32_t k, const int32_t* qexp,
+int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec,
+                                int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
+                                int32_t k, const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build);
   HistArgs a{};
-  a.bins = bins;
-  a.ld_bins = ld_bins;
+  a.bins4 = bins4;
+  a.ld4 = ld4;
+  a.rec = rec;
+  a.ld_rec = ld_rec;
+  a.rec_gh = rec_gh;
   a.GH = GH;
   a.ld_gh = ld_gh;
   a.qexp = qexp;
@@ -429,6 +489,7 @@ int32_t launch_build_histograms(const uint8_t* bins, int64_t n, int32_t m, int64
   a.m = m;
   a.n_bins = n_bins;
   a.c = pl.c;
+  a.pairs = pl.pairs;
   a.n_nodes = n_nodes;
   a.n_build = n_build;
   a.nq = pl.nq;

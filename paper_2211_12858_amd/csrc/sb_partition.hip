@@ -7,14 +7,17 @@
 //   left  row at i -> o_j + (L[i] - Lb_j)
 //   right row at i -> o_j + nleft_j + (i - o_j) - (L[i] - Lb_j),
 // which keeps the original order inside each child.
-//   k_part_flags   : flag per position (column-major bins: one contiguous run
-//                    of a single feature column per node) and left count per
-//                    tile of 4096 positions.
-//   k_part_scan    : exclusive scan of the tile counts (one block).
-//   k_part_bounds  : Lb_j = L[o_j] for every node boundary, from the tile
-//                    offset plus the flags of the boundary's own tile.
-//   k_part_scatter : block scan of the tile's flags and the scatter; block 0
-//                    also writes the child offsets and the next build list.
+//   k_part_flags   : per tile of 4096 positions, the flags as 64-bit wave
+//                    ballots (bit = lane = position) and the tile's left count.
+//                    Lanes take consecutive positions, so the row-index reads
+//                    are coalesced; the bin is one byte of the split feature's
+//                    column.
+//   k_part_bounds  : one block: tile offsets (scan of the counts), Lb_j at
+//                    every node boundary (tile offset + popcounts of the
+//                    ballots before it), child offsets and the next build
+//                    list.
+//   k_part_scatter : per tile, L[i] from the tile offset and the ballots,
+//                    then the scatter of the row indices.
 // No counter is shared between workgroups, so nothing serialises on atomics.
 #include "sb_common.h"
 
@@ -22,8 +25,9 @@ namespace sb {
 namespace {
 
 constexpr int PT_THREADS = 256;
-constexpr int PT_PER_THREAD = 16;
-constexpr int PT_TILE = PT_THREADS * PT_PER_THREAD;  // 4096 positions
+constexpr int PT_ITERS = 16;
+constexpr int PT_TILE = PT_THREADS * PT_ITERS;  // 4096 positions
+constexpr int PT_MASKS = PT_TILE / 64;          // 64 ballots per tile
 
 struct PartArgs {
   const uint8_t* bins_cm;
@@ -35,10 +39,10 @@ struct PartArgs {
   int32_t* row_out;
   int32_t* off_out;
   int32_t* build_out;
-  uint8_t* flags;
-  int32_t* tile_cnt;
-  int32_t* tile_off;  // n_tiles + 1 entries (last = total)
-  int32_t* Lb;        // n_nodes + 1 entries
+  uint64_t* masks;      // n_tiles * PT_MASKS
+  int32_t* tile_cnt;    // n_tiles
+  int32_t* tile_off;    // n_tiles + 1 entries (last = total)
+  int32_t* Lb;          // n_nodes + 1 entries
   int64_t n;
   int32_t m, n_nodes, n_tiles;
 };
@@ -59,20 +63,20 @@ __device__ inline int find_node(const PartArgs& a, int64_t i) {
   return lo;
 }
 
+__device__ inline int32_t popc64(uint64_t x) { return __popcll(x); }
+
 __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   __shared__ int32_t wsum[PT_THREADS / 64];
-  const int64_t i0 = (int64_t)blockIdx.x * PT_TILE + (int64_t)threadIdx.x * PT_PER_THREAD;
+  const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
-  int j = find_node(a, i0);
+  int64_t i = t0 + threadIdx.x;
+  int j = find_node(a, i);
   int64_t jend = off_at(a, j + 1);
-  int cnt_tile = 0;
-  uint32_t packed[PT_PER_THREAD / 4];
-#pragma unroll
-  for (int w = 0; w < PT_PER_THREAD / 4; ++w) packed[w] = 0u;
-#pragma unroll
-  for (int r = 0; r < PT_PER_THREAD; ++r) {
-    const int64_t i = i0 + r;
-    uint32_t left = 0u;
+  int cnt = 0;
+#pragma unroll 4
+  for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
+    bool left = false;
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
         ++j;
@@ -81,23 +85,15 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
       int64_t row = a.row_in ? (int64_t)a.row_in[i] : i;
       row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
       const int32_t f = a.best_f[j];
-      if (f < 0 || f >= a.m) {
-        left = 1u;
-      } else {
-        left = a.bins_cm[(int64_t)f * a.ld_cm + row] <= a.best_b[j] ? 1u : 0u;
-      }
-      cnt_tile += (int)left;
+      left = (f < 0 || f >= a.m) ? true : (int32_t)a.bins_cm[(int64_t)f * a.ld_cm + row] <= a.best_b[j];
     }
-    packed[r >> 2] |= left << (8 * (r & 3));
+    const uint64_t mask = __ballot(left);
+    if (lane == 0) {
+      a.masks[(int64_t)blockIdx.x * PT_MASKS + it * (PT_THREADS / 64) + wave] = mask;
+      cnt += popc64(mask);
+    }
   }
-  // 16 flag bytes per thread, written as 4 words (tile base is 4096-aligned)
-  if (i0 < a.n) {
-    uint32_t* dst = reinterpret_cast<uint32_t*>(a.flags + i0);
-#pragma unroll
-    for (int w = 0; w < PT_PER_THREAD / 4; ++w) dst[w] = packed[w];
-  }
-  for (int off = 32; off > 0; off >>= 1) cnt_tile += __shfl_down(cnt_tile, off, 64);
-  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = cnt_tile;
+  if (lane == 0) wsum[wave] = cnt;
   __syncthreads();
   if (threadIdx.x == 0) {
     int s = 0;
@@ -106,126 +102,132 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   }
 }
 
-// Exclusive scan of cnt[0..N) into out[0..N) by one 1024-thread block.
-__device__ void block_excl_scan(const int32_t* cnt, int32_t* out, int N, int32_t* sh) {
+// Exclusive scan over v(0..N-1) by one 1024-thread block; out(i, prefix) is
+// called for every i, and the total is returned to every thread.
+template <typename V, typename O>
+__device__ int64_t block_excl_scan(int N, V v, O out, int64_t* sh) {
   const int per = (N + 1023) / 1024;
   const int p0 = threadIdx.x * per;
-  int32_t local = 0;
+  int64_t local = 0;
   for (int i = 0; i < per; ++i)
-    if (p0 + i < N) local += cnt[p0 + i];
+    if (p0 + i < N) local += v(p0 + i);
+  __syncthreads();
   sh[threadIdx.x] = local;
   __syncthreads();
   for (int off = 1; off < 1024; off <<= 1) {
-    int32_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
+    int64_t x = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
     __syncthreads();
-    sh[threadIdx.x] += v;
+    sh[threadIdx.x] += x;
     __syncthreads();
   }
-  int32_t run = threadIdx.x ? sh[threadIdx.x - 1] : 0;
+  int64_t run = threadIdx.x ? sh[threadIdx.x - 1] : 0;
   for (int i = 0; i < per; ++i)
     if (p0 + i < N) {
-      out[p0 + i] = run;
-      run += cnt[p0 + i];
+      out(p0 + i, run);
+      run += v(p0 + i);
     }
+  const int64_t total = sh[1023];
   __syncthreads();
+  return total;
 }
 
-__global__ void __launch_bounds__(1024) k_part_scan(PartArgs a) {
-  __shared__ int32_t sh[1024];
-  block_excl_scan(a.tile_cnt, a.tile_off, a.n_tiles, sh);
-  if (threadIdx.x == 0) a.tile_off[a.n_tiles] = a.tile_off[a.n_tiles - 1] + a.tile_cnt[a.n_tiles - 1];
+// Left rows of node j, clamped to its size.
+__device__ inline int64_t node_left(const PartArgs& a, int j, int64_t* size_out) {
+  const int64_t o0 = off_at(a, j), o1 = off_at(a, j + 1);
+  const int64_t size = o1 > o0 ? o1 - o0 : 0;
+  int64_t nl = (int64_t)a.Lb[j + 1] - a.Lb[j];
+  *size_out = size;
+  return nl < 0 ? 0 : (nl > size ? size : nl);
 }
 
-// Lb[j] = number of left rows at positions < off[j], j = 0..n_nodes.
-__global__ void __launch_bounds__(PT_THREADS) k_part_bounds(PartArgs a) {
-  __shared__ int32_t wsum[PT_THREADS / 64];
-  const int j = blockIdx.x;
-  const int64_t x = off_at(a, j);
-  const int64_t t = x / PT_TILE;
-  int cnt = 0;
-  if (t < a.n_tiles) {
-    const int64_t base = t * PT_TILE;
-    for (int64_t i = base + threadIdx.x; i < x; i += PT_THREADS) cnt += a.flags[i];
-  }
-  for (int off = 32; off > 0; off >>= 1) cnt += __shfl_down(cnt, off, 64);
-  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = cnt;
+__global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
+  __shared__ int64_t sh[1024];
+  // 1. tile offsets
+  const int64_t total = block_excl_scan(
+      a.n_tiles, [&](int t) -> int64_t { return a.tile_cnt[t]; },
+      [&](int t, int64_t pre) { a.tile_off[t] = (int32_t)pre; }, sh);
+  if (threadIdx.x == 0) a.tile_off[a.n_tiles] = (int32_t)total;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int s = 0;
-    for (int w = 0; w < PT_THREADS / 64; ++w) s += wsum[w];
-    a.Lb[j] = a.tile_off[t < a.n_tiles ? t : a.n_tiles] + (t < a.n_tiles ? s : 0);
+  // 2. Lb_j = left rows before each node boundary
+  for (int j = threadIdx.x; j <= a.n_nodes; j += 1024) {
+    const int64_t x = off_at(a, j);
+    const int64_t t = x / PT_TILE;
+    int64_t lb;
+    if (t >= a.n_tiles) {
+      lb = total;
+    } else {
+      const int w = (int)(x - t * PT_TILE);
+      const uint64_t* mk = a.masks + t * PT_MASKS;
+      lb = a.tile_off[t];
+      for (int q = 0; q < (w >> 6); ++q) lb += popc64(mk[q]);
+      if (w & 63) lb += popc64(mk[w >> 6] & ((uint64_t(1) << (w & 63)) - 1));
+    }
+    a.Lb[j] = (int32_t)lb;
   }
+  __syncthreads();
+  // 3. children and build list
+  for (int j = threadIdx.x; j < a.n_nodes; j += 1024) {
+    int64_t size;
+    const int64_t nl = node_left(a, j, &size);
+    const int64_t o0 = off_at(a, j);
+    a.off_out[2 * j] = (int32_t)o0;
+    a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
+    a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
+  }
+  if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
 }
 
 __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
-  __shared__ int32_t sh[PT_THREADS];
-  const int64_t i0 = (int64_t)blockIdx.x * PT_TILE + (int64_t)threadIdx.x * PT_PER_THREAD;
-  uint32_t packed[PT_PER_THREAD / 4];
-  int32_t mine = 0;
-  if (i0 < a.n) {
-    const uint32_t* src = reinterpret_cast<const uint32_t*>(a.flags + i0);
-#pragma unroll
-    for (int w = 0; w < PT_PER_THREAD / 4; ++w) {
-      packed[w] = src[w];
-      mine += __popc(packed[w]);  // flags are 0/1 bytes
-    }
-  } else {
-#pragma unroll
-    for (int w = 0; w < PT_PER_THREAD / 4; ++w) packed[w] = 0u;
-  }
-  // block exclusive scan of the per-thread left counts
-  sh[threadIdx.x] = mine;
+  __shared__ uint64_t mk[PT_MASKS];
+  __shared__ int32_t pre[PT_MASKS];
+  const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (threadIdx.x < PT_MASKS) mk[threadIdx.x] = a.masks[(int64_t)blockIdx.x * PT_MASKS + threadIdx.x];
   __syncthreads();
-  for (int off = 1; off < PT_THREADS; off <<= 1) {
-    int32_t v = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
-    __syncthreads();
-    sh[threadIdx.x] += v;
-    __syncthreads();
-  }
-  int64_t L = (int64_t)a.tile_off[blockIdx.x] + sh[threadIdx.x] - mine;
-  if (blockIdx.x == 0) {
-    for (int j = threadIdx.x; j < a.n_nodes; j += PT_THREADS) {
-      const int64_t o0 = off_at(a, j), o1 = off_at(a, j + 1);
-      const int64_t size = o1 > o0 ? o1 - o0 : 0;
-      const int64_t nl = (int64_t)a.Lb[j + 1] - a.Lb[j];
-      a.off_out[2 * j] = (int32_t)o0;
-      a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
-      a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
+  if (threadIdx.x == 0) {
+    int32_t r = a.tile_off[blockIdx.x];
+    for (int q = 0; q < PT_MASKS; ++q) {
+      pre[q] = r;
+      r += popc64(mk[q]);
     }
-    if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
   }
-  if (i0 >= a.n) return;
+  __syncthreads();
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
-  int j = find_node(a, i0);
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  int64_t i = t0 + threadIdx.x;
+  int j = find_node(a, i);
   int64_t jstart = off_at(a, j), jend = off_at(a, j + 1);
-#pragma unroll
-  for (int r = 0; r < PT_PER_THREAD; ++r) {
-    const int64_t i = i0 + r;
-    const uint32_t left = (packed[r >> 2] >> (8 * (r & 3))) & 0xffu;
+  int64_t lbj = a.Lb[j], nleft = (int64_t)a.Lb[j + 1] - lbj;
+#pragma unroll 4
+  for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
         ++j;
         jstart = jend;
         jend = off_at(a, j + 1);
+        lbj = a.Lb[j];
+        nleft = (int64_t)a.Lb[j + 1] - lbj;
       }
+      const int q = it * (PT_THREADS / 64) + wave;
+      const uint64_t m = mk[q];
+      const bool left = (m >> lane) & 1u;
+      const int64_t L = (int64_t)pre[q] + popc64(m & below);
       int64_t row = a.row_in ? (int64_t)a.row_in[i] : i;
       row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
-      const int64_t lrel = L - a.Lb[j];
-      const int64_t nleft = a.Lb[j + 1] - a.Lb[j];
+      const int64_t lrel = L - lbj;
       int64_t dest = left ? jstart + lrel : jstart + nleft + (i - jstart) - lrel;
       dest = dest < 0 ? 0 : (dest >= a.n ? a.n - 1 : dest);
       a.row_out[dest] = (int32_t)row;
     }
-    L += left;
   }
 }
 
 }  // namespace
 
-// Workspace: [flags n][tile_cnt][tile_off][Lb]
+// Workspace: [masks][tile_cnt][tile_off][Lb]
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes) {
   const int64_t tiles = (n + PT_TILE - 1) / PT_TILE;
-  return align256(tiles * PT_TILE) + 2 * align256((tiles + 1) * 4) + align256((int64_t)(n_nodes + 1) * 4);
+  return align256(tiles * PT_MASKS * 8) + 2 * align256((tiles + 1) * 4) + align256((int64_t)(n_nodes + 1) * 4);
 }
 
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
@@ -243,8 +245,8 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.off_out = off_out;
   a.build_out = build_out;
   char* w = static_cast<char*>(ws);
-  a.flags = reinterpret_cast<uint8_t*>(w);
-  w += align256(tiles * PT_TILE);
+  a.masks = reinterpret_cast<uint64_t*>(w);
+  w += align256(tiles * PT_MASKS * 8);
   a.tile_cnt = reinterpret_cast<int32_t*>(w);
   w += align256((tiles + 1) * 4);
   a.tile_off = reinterpret_cast<int32_t*>(w);
@@ -255,8 +257,7 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.n_nodes = n_nodes;
   a.n_tiles = (int32_t)tiles;
   hipLaunchKernelGGL(k_part_flags, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
-  hipLaunchKernelGGL(k_part_scan, dim3(1), dim3(1024), 0, st, a);
-  hipLaunchKernelGGL(k_part_bounds, dim3(n_nodes + 1), dim3(PT_THREADS), 0, st, a);
+  hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
   hipLaunchKernelGGL(k_part_scatter, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
   return check_launch("sb_partition_rows");
 }

@@ -5,9 +5,11 @@
 //       p_j proportional to it).
 //   k_select   : Top Outputs ranks, Random Sampling inverse-CDF draws from
 //       given uniforms, identity.
-//   k_pack     : GH[i, t] = fp32(G[i, col_t] * scale_t), GH[i, k] = h_i, plus
-//       the per-channel max |value| for the fixed-point histogram exponents.
-//   k_project  : GH[i, 0:k] = G[i, :] Pi (Section 3.3), fp32 accumulation.
+//   k_pack     : GH[t, i] = fp32(G[i, col_t] * scale_t), GH[k, i] = h_i
+//       (channel-major, optionally also into the row records), plus per-block
+//       maxima of |value| for the fixed-point histogram exponents.
+//   k_project  : GH[0:k, i] = (G Pi)[i, :] (Section 3.3), fp32 accumulation.
+//   k_qexp     : per-channel maximum over the blocks and the exponents.
 //
 // G is column-major, so every kernel reads whole columns with lanes on
 // consecutive rows (coalesced 256-byte wave loads).
@@ -84,12 +86,10 @@ k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __res
   }
 }
 
-// One block.  Also clears the per-channel max bits used by k_pack.
+// One block.
 __global__ void __launch_bounds__(1024)
 k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __restrict__ u,
-         int32_t* __restrict__ cols, float* __restrict__ scales, double* __restrict__ C,
-         uint32_t* __restrict__ maxbits) {
-  for (int t = threadIdx.x; t <= k; t += blockDim.x) maxbits[t] = 0u;
+         int32_t* __restrict__ cols, float* __restrict__ scales, double* __restrict__ C) {
   if (kind == SB_SKETCH_IDENTITY) {
     for (int t = threadIdx.x; t < k; t += blockDim.x) {
       cols[t] = t;
@@ -147,48 +147,97 @@ __device__ inline uint32_t wave_max_u32(uint32_t v) {
   return v;
 }
 
-constexpr int PACK_THREADS = 256;
-constexpr int PACK_ROWS_PER_THREAD = 4;
+// Block maximum of a per-thread value (bit patterns of |x|, which order like
+// the magnitudes); every thread gets the result.
+template <int THREADS>
+__device__ inline uint32_t block_max_u32(uint32_t v, uint32_t* sh) {
+  v = wave_max_u32(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = v;
+  __syncthreads();
+  uint32_t r = 0u;
+#pragma unroll
+  for (int w = 0; w < THREADS / 64; ++w) r = sh[w] > r ? sh[w] : r;
+  return r;
+}
 
-// One thread per row and channel loop; |value| maxima per channel go through
-// LDS and one global atomicMax per block and channel (order-independent).
+constexpr int PACK_THREADS = 256;
+constexpr int64_t PACK_ROWS_PER_BLOCK = PACK_THREADS;  // one row per thread per pass
+constexpr int PACK_CG = 16;                            // channels staged in LDS per record write
+// Grid cap of the sketch kernels: block b writes its per-channel maxima to
+// blockmax[b*(k+1) + t], reduced afterwards by k_qexp (no atomics).
+constexpr int SKETCH_MAX_BLOCKS = 2048;
+
+// Copy of channels [g0, g0 + gn) of rows [base, base + PACK_THREADS) from the
+// LDS stage into the row records: consecutive lanes write consecutive floats
+// of one record, so a wave's store covers whole records instead of one float
+// in each of 64 lines.
+__device__ inline void pack_records(const float (*stage)[PACK_THREADS], int64_t base, int64_t n, int g0, int gn,
+                                    uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh) {
+  for (int e = threadIdx.x; e < gn * PACK_THREADS; e += PACK_THREADS) {
+    const int r = e / gn, tt = e - r * gn;
+    const int64_t i = base + r;
+    if (i < n) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (g0 + tt)) = stage[tt][r];
+  }
+}
+
+// Channel t of the sketch: GH[t*ld_gh + i] = fp32(G[i, cols[t]] * scales[t]),
+// channel k = h.  Lanes on consecutive rows: coalesced column reads and
+// channel-major writes.  The optional row-record copy (float t of row i at
+// rec + i*ld_rec + rec_gh + 4t) goes through an LDS stage of PACK_CG channels.
 __global__ void __launch_bounds__(PACK_THREADS)
 k_pack(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float* __restrict__ h, int k,
        const int32_t* __restrict__ cols, const float* __restrict__ scales, float* __restrict__ GH, int64_t ld_gh,
-       uint32_t* __restrict__ maxbits) {
-  extern __shared__ uint32_t smax[];
-  for (int t = threadIdx.x; t <= k; t += PACK_THREADS) smax[t] = 0u;
-  __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * PACK_THREADS * PACK_ROWS_PER_THREAD + threadIdx.x;
-  for (int t = 0; t <= k; ++t) {
-    const float* src;
-    float sc = 1.0f;
-    bool zero = false;
-    if (t < k) {
-      const int col = cols[t];
-      zero = col < 0 || col >= d;  // -1 marks an all-zero sketch column
-      src = G + (int64_t)(zero ? 0 : col) * ld_g;
-      sc = scales[t];
-    } else {
-      src = h;
-    }
-    uint32_t mx = 0u;
+       uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+  __shared__ uint32_t sh[PACK_THREADS / 64];
+  __shared__ float stage[PACK_CG][PACK_THREADS];
+  __shared__ uint32_t smax[PACK_CG];
+  for (int g0 = 0; g0 <= k; g0 += PACK_CG) {
+    const int gn = (k + 1 - g0 < PACK_CG) ? k + 1 - g0 : PACK_CG;
+    uint32_t mx[PACK_CG];
 #pragma unroll
-    for (int r = 0; r < PACK_ROWS_PER_THREAD; ++r) {
-      const int64_t i = base + (int64_t)r * PACK_THREADS;
-      if (i < n) {
-        float v = zero ? 0.0f : (t < k ? src[i] * sc : src[i]);
-        GH[i * ld_gh + t] = v;
-        const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
-        mx = a > mx ? a : mx;
+    for (int tt = 0; tt < PACK_CG; ++tt) mx[tt] = 0u;
+    for (int64_t base = (int64_t)blockIdx.x * PACK_ROWS_PER_BLOCK; base < n;
+         base += (int64_t)gridDim.x * PACK_ROWS_PER_BLOCK) {
+      const int64_t i = base + threadIdx.x;
+#pragma unroll
+      for (int tt = 0; tt < PACK_CG; ++tt) {
+        const int t = g0 + tt;
+        if (tt < gn) {
+          float v = 0.0f;
+          if (i < n) {
+            if (t < k) {
+              const int col = cols[t];
+              // -1 marks an all-zero sketch column
+              v = (col < 0 || col >= d) ? 0.0f : G[(int64_t)col * ld_g + i] * scales[t];
+            } else {
+              v = h[i];
+            }
+            GH[(int64_t)t * ld_gh + i] = v;
+            const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+            mx[tt] = a > mx[tt] ? a : mx[tt];
+          }
+          stage[tt][threadIdx.x] = v;
+        }
+      }
+      if (rec) {
+        __syncthreads();
+        pack_records(stage, base, n, g0, gn, rec, ld_rec, rec_gh);
+        __syncthreads();
       }
     }
-    mx = wave_max_u32(mx);
-    if ((threadIdx.x & 63) == 0) atomicMax(&smax[t], mx);
+#pragma unroll
+    for (int tt = 0; tt < PACK_CG; ++tt) {
+      if (tt < gn) {
+        const uint32_t r = block_max_u32<PACK_THREADS>(mx[tt], sh);
+        if (threadIdx.x == 0) smax[tt] = r;
+      }
+    }
+    __syncthreads();
+    for (int tt = threadIdx.x; tt < gn; tt += PACK_THREADS) blockmax[(int64_t)blockIdx.x * (k + 1) + g0 + tt] = smax[tt];
+    __syncthreads();
   }
-  __syncthreads();
-  for (int t = threadIdx.x; t <= k; t += PACK_THREADS)
-    if (smax[t]) atomicMax(&maxbits[t], smax[t]);
 }
 
 constexpr int PROJ_THREADS = 256;
@@ -197,82 +246,88 @@ constexpr int PROJ_KT = 32;  // sketch columns per pass
 // VALU projection: one row per thread, Pi read with uniform (scalar) loads.
 __global__ void __launch_bounds__(PROJ_THREADS)
 k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k,
-          const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh, uint32_t* __restrict__ maxbits) {
-  extern __shared__ uint32_t smax[];
-  for (int t = threadIdx.x; t <= k; t += PROJ_THREADS) smax[t] = 0u;
-  __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * PROJ_THREADS + threadIdx.x;
-  const bool live = i < n;
-  const int64_t ii = live ? i : 0;
-  for (int t0 = 0; t0 < k; t0 += PROJ_KT) {
-    float acc[PROJ_KT];
+          const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh, uint8_t* __restrict__ rec,
+          int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+  __shared__ uint32_t sh[PROJ_THREADS / 64];
+  for (int t0 = 0; t0 <= k; t0 += PROJ_KT) {
+    const int kt = (k + 1 - t0 < PROJ_KT) ? k + 1 - t0 : PROJ_KT;  // channel k (h) rides in the last pass
+    uint32_t mx[PROJ_KT];
 #pragma unroll
-    for (int t = 0; t < PROJ_KT; ++t) acc[t] = 0.0f;
-    const int kt = (k - t0 < PROJ_KT) ? k - t0 : PROJ_KT;
-    for (int j = 0; j < d; ++j) {
-      const float g = G[(int64_t)j * ld_g + ii];
-      const float* pr = Pi + (int64_t)j * k + t0;
+    for (int t = 0; t < PROJ_KT; ++t) mx[t] = 0u;
+    for (int64_t i0 = (int64_t)blockIdx.x * PROJ_THREADS; i0 < n; i0 += (int64_t)gridDim.x * PROJ_THREADS) {
+      const int64_t i = i0 + threadIdx.x;
+      const bool live = i < n;
+      const int64_t ii = live ? i : 0;
+      float acc[PROJ_KT];
 #pragma unroll
-      for (int t = 0; t < PROJ_KT; ++t)
-        if (t < kt) acc[t] = fmaf(g, pr[t], acc[t]);
+      for (int t = 0; t < PROJ_KT; ++t) acc[t] = 0.0f;
+      for (int j = 0; j < d; ++j) {
+        const float g = G[(int64_t)j * ld_g + ii];
+        const float* pr = Pi + (int64_t)j * k + t0;
+#pragma unroll
+        for (int t = 0; t < PROJ_KT; ++t)
+          if (t < kt && t0 + t < k) acc[t] = fmaf(g, pr[t], acc[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < PROJ_KT; ++t) {
+        if (t < kt && live) {
+          const float v = (t0 + t < k) ? acc[t] : h[i];
+          GH[(int64_t)(t0 + t) * ld_gh + i] = v;
+          if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (t0 + t)) = v;
+          const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+          mx[t] = a > mx[t] ? a : mx[t];
+        }
+      }
     }
 #pragma unroll
     for (int t = 0; t < PROJ_KT; ++t) {
       if (t < kt) {
-        uint32_t a = 0u;
-        if (live) {
-          GH[i * ld_gh + t0 + t] = acc[t];
-          a = __float_as_uint(acc[t]) & 0x7fffffffu;
-        }
-        a = wave_max_u32(a);
-        if ((threadIdx.x & 63) == 0) atomicMax(&smax[t0 + t], a);
+        const uint32_t r = block_max_u32<PROJ_THREADS>(mx[t], sh);
+        if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + t] = r;
       }
     }
   }
-  uint32_t a = 0u;
-  if (live) {
-    const float hv = h[i];
-    GH[i * ld_gh + k] = hv;
-    a = __float_as_uint(hv) & 0x7fffffffu;
-  }
-  a = wave_max_u32(a);
-  if ((threadIdx.x & 63) == 0) atomicMax(&smax[k], a);
-  __syncthreads();
-  for (int t = threadIdx.x; t <= k; t += PROJ_THREADS)
-    if (smax[t]) atomicMax(&maxbits[t], smax[t]);
 }
 
-__global__ void k_zero_u32(uint32_t* p, int cnt) {
-  for (int i = threadIdx.x; i < cnt; i += blockDim.x) p[i] = 0u;
-}
-
-// Max |GH[:, t]| over all rows for a caller-supplied GH.
+// Per-block max |GH[t*ld_gh + i]| for a caller-supplied channel-major GH.
 __global__ void __launch_bounds__(256)
-k_maxabs(const float* __restrict__ GH, int64_t n, int64_t ld_gh, int c, uint32_t* __restrict__ maxbits) {
-  extern __shared__ uint32_t smax[];
-  for (int t = threadIdx.x; t < c; t += 256) smax[t] = 0u;
-  __syncthreads();
+k_maxabs(const float* __restrict__ GH, int64_t n, int64_t ld_gh, int c, uint32_t* __restrict__ blockmax) {
+  __shared__ uint32_t sh[4];
   const int64_t stride = (int64_t)gridDim.x * 256;
   for (int t = 0; t < c; ++t) {
     uint32_t mx = 0u;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) {
-      const uint32_t a = __float_as_uint(GH[i * ld_gh + t]) & 0x7fffffffu;
+      const uint32_t a = __float_as_uint(GH[(int64_t)t * ld_gh + i]) & 0x7fffffffu;
       mx = a > mx ? a : mx;
     }
-    mx = wave_max_u32(mx);
-    if ((threadIdx.x & 63) == 0) atomicMax(&smax[t], mx);
+    mx = block_max_u32<256>(mx, sh);
+    if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * c + t] = mx;
   }
-  __syncthreads();
-  for (int t = threadIdx.x; t < c; t += 256)
-    if (smax[t]) atomicMax(&maxbits[t], smax[t]);
 }
 
+// One block per channel: max over the blocks' maxima, then
 // qexp[t] = (QBITS-1) - floor(log2(max)), 0 for an all-zero channel.
-__global__ void k_qexp(const uint32_t* __restrict__ maxbits, int c, int32_t* __restrict__ qexp) {
-  for (int t = threadIdx.x; t < c; t += blockDim.x) {
-    const float mx = __uint_as_float(maxbits[t]);
-    qexp[t] = (mx > 0.0f) ? (QBITS - 1) - ilogbf(mx) : 0;
+__global__ void __launch_bounds__(256)
+k_qexp(const uint32_t* __restrict__ blockmax, int nblocks, int c, int32_t* __restrict__ qexp) {
+  __shared__ uint32_t sh[4];
+  const int t = blockIdx.x;
+  uint32_t mx = 0u;
+  for (int b = threadIdx.x; b < nblocks; b += 256) {
+    const uint32_t v = blockmax[(int64_t)b * c + t];
+    mx = v > mx ? v : mx;
   }
+  mx = block_max_u32<256>(mx, sh);
+  if (threadIdx.x == 0) {
+    const float m = __uint_as_float(mx);
+    qexp[t] = (m > 0.0f) ? (QBITS - 1) - ilogbf(m) : 0;
+  }
+}
+
+int sketch_blocks(int64_t n, int64_t rows_per_block) {
+  int64_t b = (n + rows_per_block - 1) / rows_per_block;
+  if (b < 1) b = 1;
+  if (b > SKETCH_MAX_BLOCKS) b = SKETCH_MAX_BLOCKS;
+  return (int)b;
 }
 
 int norm_parts(int64_t n) {
@@ -284,16 +339,20 @@ int norm_parts(int64_t n) {
 
 }  // namespace
 
-// Workspace: [norm partials d*P][norm2 d][prefix d][maxbits k+1]
+// Workspace: [norm partials d*P][norm2 d][prefix d][block maxima SKETCH_MAX_BLOCKS*(k+1)]
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k) {
   (void)kind;
   const int P = norm_parts(n);
-  return align256((int64_t)d * P * 8) + align256((int64_t)d * 8) * 2 + align256((int64_t)(k + 1) * 4);
+  return align256((int64_t)d * P * 8) + align256((int64_t)d * 8) * 2 +
+         align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4);
 }
 
+int64_t hist_exponents_ws_bytes(int32_t k) { return align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4); }
+
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                      const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                      double* norm2, int32_t* qexp, void* ws, hipStream_t st) {
+                      const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
+                      int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
+                      hipStream_t st) {
   const int P = norm_parts(n);
   char* w = static_cast<char*>(ws);
   double* part = reinterpret_cast<double*>(w);
@@ -302,39 +361,33 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
   w += align256((int64_t)d * 8);
   double* C = reinterpret_cast<double*>(w);
   w += align256((int64_t)d * 8);
-  uint32_t* maxbits = reinterpret_cast<uint32_t*>(w);
-  const size_t smax_bytes = (size_t)(k + 1) * 4;
+  uint32_t* blockmax = reinterpret_cast<uint32_t*>(w);
 
+  int nb;
   if (kind == SB_SKETCH_RANDOM_PROJECTION) {
-    hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, maxbits, k + 1);
-    const int64_t blocks = (n + PROJ_THREADS - 1) / PROJ_THREADS;
-    hipLaunchKernelGGL(k_project, dim3((unsigned)blocks), dim3(PROJ_THREADS), smax_bytes, st, G, n, d, ld_g, Pi, k,
-                       h, GH, ld_gh, maxbits);
+    nb = sketch_blocks(n, PROJ_THREADS);
+    hipLaunchKernelGGL(k_project, dim3(nb), dim3(PROJ_THREADS), 0, st, G, n, d, ld_g, Pi, k, h, GH, ld_gh, rec,
+                       ld_rec, rec_gh, blockmax);
   } else {
     int64_t chunk = (n + P - 1) / P;
     chunk = (chunk + 3) & ~int64_t(3);
     hipLaunchKernelGGL(k_colnorm_partial, dim3(P, d), dim3(NORM_THREADS), 0, st, G, n, ld_g, P, chunk, part);
     hipLaunchKernelGGL(k_colnorm_final, dim3((d + 3) / 4), dim3(256), 0, st, part, d, P, n2, norm2);
-    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, n2, d, k, u, cols, scales, C, maxbits);
-    const int64_t rows_per_block = (int64_t)PACK_THREADS * PACK_ROWS_PER_THREAD;
-    const int64_t blocks = (n + rows_per_block - 1) / rows_per_block;
-    hipLaunchKernelGGL(k_pack, dim3((unsigned)blocks), dim3(PACK_THREADS), smax_bytes, st, G, n, ld_g, d, h, k, cols,
-                       scales, GH, ld_gh, maxbits);
+    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, n2, d, k, u, cols, scales, C);
+    nb = sketch_blocks(n, 4 * PACK_ROWS_PER_BLOCK);
+    hipLaunchKernelGGL(k_pack, dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, k, cols, scales, GH, ld_gh,
+                       rec, ld_rec, rec_gh, blockmax);
   }
-  hipLaunchKernelGGL(k_qexp, dim3(1), dim3(256), 0, st, maxbits, k + 1, qexp);
+  hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
   return check_launch("sb_sketch");
 }
 
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
                               hipStream_t st) {
-  uint32_t* maxbits = static_cast<uint32_t*>(ws);
-  hipLaunchKernelGGL(k_zero_u32, dim3(1), dim3(256), 0, st, maxbits, k + 1);
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 2048) blocks = 2048;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_maxabs, dim3((unsigned)blocks), dim3(256), (size_t)(k + 1) * 4, st, GH, n, ld_gh, k + 1,
-                     maxbits);
-  hipLaunchKernelGGL(k_qexp, dim3(1), dim3(256), 0, st, maxbits, k + 1, qexp);
+  uint32_t* blockmax = static_cast<uint32_t*>(ws);
+  const int nb = sketch_blocks(n, 256);
+  hipLaunchKernelGGL(k_maxabs, dim3(nb), dim3(256), 0, st, GH, n, ld_gh, k + 1, blockmax);
+  hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
   return check_launch("sb_hist_exponents");
 }
 

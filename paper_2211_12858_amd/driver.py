@@ -1,19 +1,21 @@
 """Device-side driver: torch allocates the buffers, libsketchboost computes.
 
-``SplitSearch`` holds one binned dataset resident in HBM in the two layouts
-the kernels read:
+``SplitSearch`` holds one binned dataset resident in HBM in the three
+layouts the kernels read (built on the device by ``sb_layout_bins`` from
+the row-major bins):
 
-* row records for the histogram kernel: row i occupies ``rec_stride`` bytes,
-  its m bin bytes first and, when ``interleave`` is set, its k+1 sketch
-  floats after them (at an 8-byte aligned offset).  With 100 features and
-  k = 5 each row is exactly one 128-byte cache line, so gathering the rows
-  of a node fetches nothing it does not use.  Otherwise the sketch lives in
-  its own compact (n, k+1) array;
-* a column-major copy (feature-major, ``bins_cm[f, i]``) for the partition,
-  which then reads one contiguous run of one feature column per node.
+* quad-major words ``bins4[q, i]`` (features 4q..4q+3 of row i): the
+  histogram kernel's lanes take consecutive rows and read contiguous words;
+* column-major bytes ``bins_cm[f, i]``: the partition reads one run of the
+  split feature's column per node;
+* row records ``rec[i]`` of ``ld_rec`` bytes (one 128-byte line for 100
+  features and k = 5): the row's bins and, after each sketch, its k+1
+  sketch values; the histograms of the deeper levels read one record per
+  row.
 
-``step()`` runs one tree: sketch (once per tree) and the depth-wise level
-loop, entirely on the device.  No computation happens in Python.
+The sketch itself lives channel-major in ``GH[t, i]``.  ``step()`` runs one
+tree: the sketch (once per tree) and the depth-wise level loop, entirely on
+the device.  No computation happens in Python.
 """
 import numpy as np
 import torch
@@ -31,34 +33,37 @@ def workspace(nbytes, device):
     return t
 
 
+def record_stride(m, c):
+    """Bytes per row record: bins, then c floats; a power of two up to 128
+    bytes (so that no record straddles a 128-byte line), else a multiple of 128."""
+    need = _round_up(m, 4) + 4 * c
+    if need <= 128:
+        s = 16
+        while s < need:
+            s *= 2
+        return s
+    return _round_up(need, 128)
+
+
 class SplitSearch:
-    def __init__(self, bins, n_bins, k, depth, lam=1.0, min_child_weight=0.0, device="cuda", interleave=True):
+    def __init__(self, bins, n_bins, k, depth, lam=1.0, min_child_weight=0.0, device="cuda", ld_rec=None):
         bins = np.ascontiguousarray(bins, dtype=np.uint8)
         self.n, self.m = bins.shape
         self.n_bins, self.k, self.c, self.depth = n_bins, k, k + 1, depth
         self.lam, self.mcw = float(lam), float(min_child_weight)
-        self.device = torch.device(device)
+        self.device = dev = torch.device(device)
         n, m, c = self.n, self.m, self.c
-        self.ld_bins = _round_up(m, 4)
-        if interleave:
-            self.gh_offset = _round_up(self.ld_bins, 8)
-            self.rec_stride = _round_up(self.gh_offset + 4 * c, 128)
-        else:
-            self.gh_offset = None
-            self.rec_stride = self.ld_bins
-        rec = np.zeros((n, self.rec_stride), dtype=np.uint8)
-        rec[:, :m] = bins
-        self.rec = torch.from_numpy(rec).to(self.device)
-        self.bins_cm = torch.from_numpy(np.ascontiguousarray(bins.T)).to(self.device)
-        if interleave:
-            self.GH = None
-            self.gh_ptr = self.rec.data_ptr() + self.gh_offset
-            self.ld_gh = self.rec_stride // 4
-        else:
-            self.GH = torch.zeros((n, c), dtype=torch.float32, device=self.device)
-            self.gh_ptr = self.GH.data_ptr()
-            self.ld_gh = c
-        dev = self.device
+        self.nq = (m + 3) // 4
+        self.rec_gh = _round_up(m, 4)
+        self.ld_rec = record_stride(m, c) if ld_rec is None else ld_rec
+        self.bins4 = torch.empty((self.nq, n), dtype=torch.int32, device=dev)
+        self.bins_cm = torch.empty((m, n), dtype=torch.uint8, device=dev)
+        self.rec = torch.zeros((n, self.ld_rec), dtype=torch.uint8, device=dev)
+        rm = torch.from_numpy(bins).to(dev)
+        L.sb_layout_bins(rm, n, m, m, self.bins4, n, self.bins_cm, n, self.rec, self.ld_rec)
+        torch.cuda.synchronize(dev)
+        del rm
+        self.GH = torch.zeros((c, n), dtype=torch.float32, device=dev)
         self.qexp = torch.zeros(c, dtype=torch.int32, device=dev)
         self.cols = torch.zeros(k, dtype=torch.int32, device=dev)
         self.scales = torch.zeros(k, dtype=torch.float32, device=dev)
@@ -84,13 +89,14 @@ class SplitSearch:
             self._ws_sketch = workspace(need, self.device)
         if self.norm2 is None or self.norm2.numel() != d:
             self.norm2 = torch.zeros(d, dtype=torch.float64, device=self.device)
-        L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.gh_ptr, self.ld_gh, self.cols, self.scales,
-                    self.norm2, self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
+        L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, n, self.rec, self.ld_rec, self.rec_gh, self.cols,
+                    self.scales, self.norm2, self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
 
     # ------------------------------------------------------------ tree
     def grow(self, stream=None):
-        L.sb_grow_tree(self.rec, self.rec_stride, self.bins_cm, self.n, self.n, self.m, self.n_bins, self.gh_ptr,
-                       self.ld_gh, self.k, self.qexp, self.depth, self.lam, self.mcw, self.tree_feature,
+        n = self.n
+        L.sb_grow_tree(self.bins4, n, self.bins_cm, n, self.rec, self.ld_rec, self.rec_gh, n, self.m, self.n_bins,
+                       self.GH, n, self.k, self.qexp, self.depth, self.lam, self.mcw, self.tree_feature,
                        self.tree_bin, self.tree_score, self.row_idx, self.leaf_off, self.ws_tree,
                        self.ws_tree_bytes, stream)
 
@@ -100,10 +106,12 @@ class SplitSearch:
 
     # ------------------------------------------------------------ readback
     def gh(self):
-        """The sketch records as an (n, k+1) float32 host array."""
-        if self.GH is not None:
-            return self.GH.cpu().numpy()
-        raw = self.rec[:, self.gh_offset:self.gh_offset + 4 * self.c].contiguous()
+        """The sketch as an (n, k+1) float32 host array."""
+        return np.ascontiguousarray(self.GH.cpu().numpy().T)
+
+    def rec_gh_values(self):
+        """The sketch copy inside the row records, as an (n, k+1) float32 host array."""
+        raw = self.rec[:, self.rec_gh:self.rec_gh + 4 * self.c].contiguous()
         return raw.view(torch.float32).cpu().numpy().reshape(self.n, self.c)
 
     def tree(self):

@@ -26,11 +26,24 @@ def sync():
     torch.cuda.synchronize()
 
 
-def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None):
+def quad_major(bins):
+    """Host copy of the quad-major layout: word q of row i holds features 4q..4q+3."""
+    n, m = bins.shape
+    nq = (m + 3) // 4
+    pad = np.zeros((n, 4 * nq), dtype=np.uint8)
+    pad[:, :m] = bins
+    return np.ascontiguousarray(pad.view("<u4").reshape(n, nq).T).view(np.int32)
+
+
+def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None, rec_stride=None, rec_gh=None):
+    """Returns (GH as (n, k+1), cols, scales, norm2, qexp[, GH copy read back from the records])."""
     d, n = G_T.shape
-    ld_gh = k + 1 if ld_gh is None else ld_gh
+    ld_gh = n if ld_gh is None else ld_gh
     Gd, hd = up(G_T), up(h)
-    GH = torch.zeros((n, ld_gh), dtype=torch.float32, device=DEV)
+    GH = torch.zeros((k + 1, ld_gh), dtype=torch.float32, device=DEV)
+    rec = None
+    if rec_stride is not None:
+        rec = torch.zeros((n, rec_stride), dtype=torch.uint8, device=DEV)
     cols = torch.full((k,), -7, dtype=torch.int32, device=DEV)
     scales = torch.zeros(k, dtype=torch.float32, device=DEV)
     norm2 = torch.zeros(d, dtype=torch.float64, device=DEV)
@@ -38,10 +51,15 @@ def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None):
     ws = workspace(L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=n, d=d, k=k), DEV)
     ud = up(u, torch.float64) if u is not None else None
     Pid = up(Pi, torch.float32) if Pi is not None else None
-    L.sb_sketch(L.KIND[kind], Gd, n, d, n, hd, k, ud, Pid, GH, ld_gh, cols, scales, norm2, qexp, ws, ws.numel())
+    L.sb_sketch(L.KIND[kind], Gd, n, d, n, hd, k, ud, Pid, GH, ld_gh, rec, rec_stride or 0, rec_gh or 0, cols, scales,
+                norm2, qexp, ws, ws.numel())
     sync()
-    return (GH[:, :k + 1].cpu().numpy(), cols.cpu().numpy(), scales.cpu().numpy(), norm2.cpu().numpy(),
-            qexp.cpu().numpy())
+    out = (np.ascontiguousarray(GH[:, :n].cpu().numpy().T), cols.cpu().numpy(), scales.cpu().numpy(),
+           norm2.cpu().numpy(), qexp.cpu().numpy())
+    if rec is not None:
+        raw = rec[:, rec_gh:rec_gh + 4 * (k + 1)].contiguous().view(torch.float32).cpu().numpy()
+        out = out + (raw.reshape(n, k + 1),)
+    return out
 
 
 def qexp_rule(GH):
@@ -53,20 +71,38 @@ def qexp_rule(GH):
     return np.array(out, dtype=np.int32)
 
 
-def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, ld_bins=None, H=None):
+def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None, ld_pad=0, ld_rec=None):
+    """Histograms through the C ABI; GH is an (n, k+1) host array.
+
+    Without row_idx the data go up as quad-major bins and a channel-major
+    sketch (leading dimension n + ld_pad); with row_idx as row records of
+    ld_rec bytes (default: the smallest multiple of 16 that holds them).
+    """
     n, m = bins.shape
     c = GH.shape[1]
     k = c - 1
-    ld_bins = (m + 3) // 4 * 4 if ld_bins is None else ld_bins
-    bpad = np.zeros((n, ld_bins), dtype=np.uint8)
-    bpad[:, :m] = bins
     n_nodes = len(node_off) - 1
     n_build = n_nodes if build_list is None else len(build_list)
     ws = workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=n_bins, k=k,
                                         n_nodes=max(n_nodes, n_build)), DEV)
     if H is None:
         H = torch.full((n_nodes, m, n_bins, c), float("nan"), dtype=torch.float64, device=DEV)
-    L.sb_build_histograms(up(bpad), n, m, ld_bins, n_bins, up(GH, torch.float32), c, k, up(qexp, torch.int32),
+    b4 = gh = rec = None
+    ld = n + ld_pad
+    rec_gh = 0
+    if row_idx is None:
+        qm = quad_major(bins)
+        b4 = np.zeros((qm.shape[0], ld), dtype=np.int32)
+        b4[:, :n] = qm
+        gh = np.zeros((c, ld), dtype=np.float32)
+        gh[:, :n] = GH.T
+        b4, gh = up(b4), up(gh)
+    else:
+        if ld_rec is None:
+            ld_rec = ((m + 3) // 4 * 4 + 4 * c + 15) // 16 * 16
+        rec_np, rec_gh = make_records(bins, GH, ld_rec)
+        rec = up(rec_np)
+    L.sb_build_histograms(b4, ld, rec, ld_rec or 0, rec_gh, n, m, n_bins, gh, ld, k, up(qexp, torch.int32),
                           None if row_idx is None else up(row_idx, torch.int32), up(node_off, torch.int32), n_nodes,
                           None if build_list is None else up(build_list, torch.int32), n_build, H, ws, ws.numel())
     sync()
@@ -116,3 +152,14 @@ def run_partition(bins, row_in, node_off, bf, bb):
                         bl_out, ws, ws.numel())
     sync()
     return row_out.cpu().numpy(), off_out.cpu().numpy(), bl_out.cpu().numpy()
+
+
+def make_records(bins, GH, ld_rec):
+    """Host row records: bins in bytes 0..m-1, the k+1 floats at byte round_up(m, 4)."""
+    n, m = bins.shape
+    c = GH.shape[1]
+    rec_gh = (m + 3) // 4 * 4
+    rec = np.zeros((n, ld_rec), dtype=np.uint8)
+    rec[:, :m] = bins
+    rec[:, rec_gh:rec_gh + 4 * c] = np.ascontiguousarray(GH, dtype=np.float32).view(np.uint8).reshape(n, 4 * c)
+    return rec, rec_gh

@@ -34,7 +34,8 @@ def header_functions():
 def test_header_declares_the_boundary():
     fns = header_functions()
     for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
-                 "sb_partition_rows", "sb_grow_tree", "sb_last_error", "sb_abi_version", "sb_workspace_bytes"):
+                 "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_last_error",
+                 "sb_abi_version", "sb_workspace_bytes"):
         assert name in fns
 
 
@@ -48,7 +49,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_error_text(L):
-    assert L.sb_abi_version() == 1
+    assert L.sb_abi_version() == 2
     assert isinstance(L.sb_last_error(), str)
 
 
@@ -56,7 +57,7 @@ def test_workspace_bytes(L):
     assert L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=1000, d=20, k=5) > 0
     assert L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=1000, m=100, n_bins=256, k=5, n_nodes=16) > 0
     assert L.sb_workspace_bytes(L.SB_CALL_SCORE_SPLITS, m=100, n_nodes=32) >= 32 * 100 * 12
-    assert L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=10_000, n_nodes=8) >= 10_000
+    assert L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=10_000, n_nodes=8) >= 10_000 // 8  # one flag bit per row
     assert L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10_000, m=10, n_bins=256, k=5, depth=3) > 0
     with pytest.raises(L.SBError):
         L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10, m=10, n_bins=256, k=5, depth=13)
@@ -77,8 +78,8 @@ F = FAKE
 
 
 def sketch_args(**kw):
-    a = dict(kind=0, G=F, n=100, d=10, ld_g=100, h=F, k=3, u=F, Pi=F, GH=F, ld_gh=4, cols=F, scales=F, norm2=F,
-             qexp=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a = dict(kind=0, G=F, n=100, d=10, ld_g=100, h=F, k=3, u=F, Pi=F, GH=F, ld_gh=100, rec=None, ld_rec=0, rec_gh=0,
+             cols=F, scales=F, norm2=F, qexp=F, ws=F, ws_bytes=1 << 30, stream=0)
     a.update(kw)
     return list(a.values())
 
@@ -88,12 +89,15 @@ def sketch_args(**kw):
     (dict(G=None), 1),
     (dict(n=0), 1),
     (dict(k=0), 1),
-    (dict(k=11, ld_gh=12), 1),       # top outputs needs k <= d
+    (dict(k=11), 1),                 # top outputs needs k <= d
     (dict(ld_g=99), 2),
-    (dict(ld_gh=3), 2),
+    (dict(ld_gh=99), 2),             # channel-major GH needs ld_gh >= n
     (dict(kind=1, u=None), 1),
     (dict(kind=2, Pi=None), 1),
-    (dict(kind=3, k=4, ld_gh=5), 1), # identity needs k == d
+    (dict(kind=3, k=4), 1),          # identity needs k == d
+    (dict(rec=F, ld_rec=24, rec_gh=0), 2),   # record stride not a multiple of 16
+    (dict(rec=F, ld_rec=16, rec_gh=4), 2),   # k+1 floats do not fit after rec_gh
+    (dict(rec=F + 4, ld_rec=32, rec_gh=0), 2),  # misaligned records
     (dict(ws_bytes=16), 1),
     (dict(ws=F + 8), 2),             # misaligned workspace
     (dict(ws=None), 1),
@@ -104,27 +108,30 @@ def test_sketch_rejects(L, kw, code):
 
 
 def hist_args(**kw):
-    a = dict(bins=F, n=1000, m=10, ld_bins=12, n_bins=256, GH=F, ld_gh=6, k=5, qexp=F, row_idx=None, node_off=F,
-             n_nodes=2, build_list=F, n_build=1, H=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a = dict(bins4=F, ld4=1000, rec=None, ld_rec=0, rec_gh=0, n=1000, m=10, n_bins=256, GH=F, ld_gh=1000, k=5, qexp=F,
+             row_idx=None, node_off=F, n_nodes=2, build_list=F, n_build=1, H=F, ws=F, ws_bytes=1 << 30, stream=0)
     a.update(kw)
     return list(a.values())
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(bins=None), 1),
+    (dict(bins4=None), 1),
     (dict(H=None), 1),
     (dict(n=0), 1),
     (dict(m=0), 1),
     (dict(n_bins=1), 1),
     (dict(n_bins=257), 1),
     (dict(k=0), 1),
-    (dict(ld_bins=10), 2),           # not a multiple of 4
-    (dict(ld_bins=8), 2),            # < m
-    (dict(bins=F + 2), 2),           # misaligned base
-    (dict(ld_gh=5), 2),
+    (dict(ld4=999), 2),              # < n
+    (dict(bins4=F + 2), 2),          # misaligned base
+    (dict(ld_gh=999), 2),
+    (dict(GH=None), 1),
+    (dict(row_idx=F), 1),            # rows through row_idx need the records
+    (dict(row_idx=F, rec=F, ld_rec=64, rec_gh=8), 2),   # bins overlap the sketch floats
+    (dict(row_idx=F, rec=F, ld_rec=40, rec_gh=12), 2),  # stride not a multiple of 16
     (dict(n_nodes=0), 1),
     (dict(n_build=3), 1),            # more than n_nodes
-    (dict(k=100, ld_gh=101), 3),     # LDS budget exceeded
+    (dict(k=100), 3),                # LDS budget exceeded
     (dict(ws_bytes=100), 1),
 ])
 def test_build_histograms_rejects(L, kw, code):
@@ -177,19 +184,44 @@ def test_partition_rejects(L, kw, code):
     assert _code(L.sb_partition_rows, *part_args(**kw)) == code
 
 
-def grow_args(**kw):
-    a = dict(bins=F, ld_bins=12, bins_cm=F, ld_cm=1000, n=1000, m=10, n_bins=256, GH=F, ld_gh=6, k=5, qexp=F,
-             depth=3, lam=1.0, mcw=0.0, tf=F, tb=F, ts=F, rows=F, leaf=F, ws=F, ws_bytes=1 << 34, stream=0)
+def layout_args(**kw):
+    a = dict(bins=F, n=1000, m=10, ld_bins=10, bins4=F, ld4=1000, bins_cm=None, ld_cm=0, rec=None, ld_rec=0,
+             stream=0)
     a.update(kw)
     return list(a.values())
 
 
 @pytest.mark.parametrize("kw,code", [
     (dict(bins=None), 1),
+    (dict(n=0), 1),
+    (dict(ld_bins=9), 2),
+    (dict(ld4=999), 2),
+    (dict(bins_cm=F, ld_cm=10), 2),
+    (dict(rec=F, ld_rec=24), 2),
+    (dict(rec=F, ld_rec=8), 2),
+])
+def test_layout_rejects(L, kw, code):
+    assert _code(L.sb_layout_bins, *layout_args(**kw)) == code
+
+
+def grow_args(**kw):
+    a = dict(bins4=F, ld4=1000, bins_cm=F, ld_cm=1000, rec=F, ld_rec=64, rec_gh=12, n=1000, m=10, n_bins=256, GH=F,
+             ld_gh=1000, k=5, qexp=F, depth=3, lam=1.0, mcw=0.0, tf=F, tb=F, ts=F, rows=F, leaf=F, ws=F,
+             ws_bytes=1 << 34, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bins4=None), 1),
+    (dict(rec=None), 1),
     (dict(depth=0), 1),
     (dict(depth=13), 1),
     (dict(ld_cm=10), 2),
-    (dict(ld_bins=11), 2),
+    (dict(ld4=999), 2),
+    (dict(ld_gh=999), 2),
+    (dict(rec_gh=8), 2),
+    (dict(ld_rec=32), 2),
     (dict(lam=-1.0), 1),
     (dict(ws_bytes=1000), 1),
 ])

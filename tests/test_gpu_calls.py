@@ -52,13 +52,47 @@ def test_sketch_random_sampling_zero_gradients():
     assert not GH_g[:, :k].any() and np.all(GH_g[:, k] == 1.0)
 
 
-def test_sketch_interleaved_records():
-    # GH written into 32-float records (the 128-byte row-record layout)
-    case = small_case(2049, 1, 2, 12, seed=9, k=5)
-    GH_g, cols_g, _, _, _ = gu.run_sketch("top_outputs", case.G_T, case.h, 5, ld_gh=32)
-    GH_o, cols_o, _, _ = oracle.sketch("top_outputs", case.G, case.h, 5)
+@pytest.mark.parametrize("kind,k,stride,gh_at", [("top_outputs", 5, 128, 100), ("identity", 12, 64, 8),
+                                                 ("random_projection", 3, 32, 16)])
+def test_sketch_row_records(kind, k, stride, gh_at):
+    # the same k+1 values, bit for bit, inside the row records (float t at byte gh_at + 4t)
+    d = 12
+    case = small_case(2049, 1, 2, d, seed=9, k=k)
+    out = gu.run_sketch(kind, case.G_T, case.h, k, Pi=case.Pi, u=case.u, rec_stride=stride, rec_gh=gh_at)
+    GH_g, rec_vals = out[0], out[5]
+    assert np.array_equal(rec_vals.view(np.uint32), GH_g.view(np.uint32))
+    if kind != "random_projection":
+        GH_o, _, _, _ = oracle.sketch(kind, case.G, case.h, k)
+        assert np.array_equal(GH_g.view(np.uint32), GH_o.view(np.uint32))
+
+
+def test_sketch_padded_leading_dimension():
+    case = small_case(3001, 1, 2, 9, seed=10, k=4)
+    GH_g, cols_g, _, _, _ = gu.run_sketch("top_outputs", case.G_T, case.h, 4, ld_gh=3001 + 77)
+    GH_o, cols_o, _, _ = oracle.sketch("top_outputs", case.G, case.h, 4)
     assert np.array_equal(cols_g, cols_o)
     assert np.array_equal(GH_g.view(np.uint32), GH_o.view(np.uint32))
+
+
+# ---------------------------------------------------------------- layouts
+@pytest.mark.parametrize("n,m,ld_rec,seed", [(1, 1, 16, 0), (1000, 7, 16, 1), (4099, 100, 128, 2), (777, 33, 48, 3)])
+def test_layout_bins(n, m, ld_rec, seed):
+    import torch
+    from paper_2211_12858_amd import _lib as L
+    rng = np.random.default_rng(seed)
+    bins = rng.integers(0, 256, (n, m), dtype=np.uint8)
+    ld4, ld_cm = n + 5, n + 3
+    nq = (m + 3) // 4
+    b4 = torch.full((nq, ld4), -1, dtype=torch.int32, device=gu.DEV)
+    cm = torch.full((m, ld_cm), 7, dtype=torch.uint8, device=gu.DEV)
+    rec = torch.full((n, ld_rec), 9, dtype=torch.uint8, device=gu.DEV)
+    L.sb_layout_bins(gu.up(bins), n, m, m, b4, ld4, cm, ld_cm, rec, ld_rec)
+    gu.sync()
+    assert np.array_equal(b4.cpu().numpy()[:, :n], gu.quad_major(bins))
+    assert (b4.cpu().numpy()[:, n:] == -1).all()
+    assert np.array_equal(cm.cpu().numpy()[:, :n], bins.T)
+    r = rec.cpu().numpy()
+    assert np.array_equal(r[:, :m], bins) and (r[:, m:] == 9).all()
 
 
 @pytest.mark.parametrize("n,d,k,seed", [(5000, 40, 5, 0), (20001, 200, 20, 1), (777, 3, 8, 2)])
@@ -104,6 +138,7 @@ HIST_CASES = [
     (9000, 13, 256, 20, 16, True, 5),       # k=20 (21 channels)
     (12000, 31, 256, 10, 32, True, 6),      # k=10, many nodes, some empty
     (5000, 3, 7, 2, 2, False, 7),           # odd bins, m not a multiple of 4
+    (7001, 100, 256, 5, 1, False, 8),       # five slices, root read straight from the data
 ]
 
 
@@ -121,7 +156,11 @@ def test_histograms(n, m, B, k, n_nodes, build, seed):
             build_list = np.array([0], dtype=np.int32)
     else:
         build_list = None
-    Hg = gu.run_hist(case.bins, GH, qexp, B, rows, off, build_list).cpu().numpy()
+    if seed == 8:  # positions are the rows (no row_idx), leading dimension padded
+        rows = np.arange(n, dtype=np.int32)
+        Hg = gu.run_hist(case.bins, GH, qexp, B, None, off, build_list, ld_pad=19).cpu().numpy()
+    else:
+        Hg = gu.run_hist(case.bins, GH, qexp, B, rows, off, build_list).cpu().numpy()
     todo = range(n_nodes) if build_list is None else build_list
     chan_max = np.abs(GH.astype(np.float64)).max(axis=0)
     ones = np.ones((n, 1), dtype=np.float32)

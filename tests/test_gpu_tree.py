@@ -19,9 +19,9 @@ import gpu_util as gu  # noqa: E402
 from paper_2211_12858_amd.driver import SplitSearch  # noqa: E402
 
 
-def grow_on_device(inp, kind, k, depth, lam=1.0, mcw=0.0, interleave=True, n_bins=None):
+def grow_on_device(inp, kind, k, depth, lam=1.0, mcw=0.0, ld_rec=None, n_bins=None):
     n_bins = inp.wl.n_bins if n_bins is None else n_bins
-    ss = SplitSearch(inp.bins, n_bins, k, depth, lam, mcw, device=gu.DEV, interleave=interleave)
+    ss = SplitSearch(inp.bins, n_bins, k, depth, lam, mcw, device=gu.DEV, ld_rec=ld_rec)
     G_T = gu.up(inp.G_T)
     h = gu.up(inp.h)
     u = gu.up(inp.u[:k], torch.float64)
@@ -31,11 +31,12 @@ def grow_on_device(inp, kind, k, depth, lam=1.0, mcw=0.0, interleave=True, n_bin
     return ss
 
 
-def check_tree(inp, kind, k, depth, lam=1.0, mcw=0.0, interleave=True, n_bins=None):
+def check_tree(inp, kind, k, depth, lam=1.0, mcw=0.0, ld_rec=None, n_bins=None):
     n_bins = inp.wl.n_bins if n_bins is None else n_bins
-    ss = grow_on_device(inp, kind, k, depth, lam, mcw, interleave, n_bins)
+    ss = grow_on_device(inp, kind, k, depth, lam, mcw, ld_rec, n_bins)
     dev = ss.tree()
     GH_dev = ss.gh()
+    assert np.array_equal(ss.rec_gh_values().view(np.uint32), GH_dev.view(np.uint32))
     GH_o, cols, scales, _ = oracle.sketch(kind, inp.G, inp.h, k, u=inp.u[:k], Pi=inp.Pi)
     if kind != "random_projection":
         assert np.array_equal(ss.cols.cpu().numpy(), cols)
@@ -89,9 +90,10 @@ def test_tree_multilabel_top10_reduced():
     check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth)
 
 
-def test_tree_separate_gh_layout():
+def test_tree_wide_row_records():
+    # records of 256 bytes (two lines per row) instead of the default 128
     wl = workload("mc200k_top5", n=50_000)
-    check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth, interleave=False)
+    check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth, ld_rec=256)
 
 
 @pytest.mark.parametrize("n,m,B,d,depth", [(1, 1, 2, 2, 3), (7, 2, 2, 3, 4), (300, 5, 3, 2, 5), (4099, 9, 16, 4, 7)])
