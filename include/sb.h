@@ -192,8 +192,8 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
 /*
  * sb_build_histograms -- per-node histograms of one tree level (Section 3.4).
  *
- * For every built node j, feature f, bin b and channel t <= k:
- *   H[((j*m + f)*n_bins + b)*(k+1) + t] = sum over the rows r of node j whose
+ * For every built node j, feature f, channel t <= k and bin b:
+ *   H[((j*m + f)*(k+1) + t)*n_bins + b] = sum over the rows r of node j whose
  *       feature f has bin b of channel t of r's sketch,
  * accumulated exactly in fixed point (see sb_hist_exponents) and written as
  * fp64.  Nodes not in the build list are left untouched.
@@ -210,7 +210,7 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  * k, qexp   sketch columns and the exponents from sb_sketch.
  * node_off  n_nodes+1 offsets.
  * build_list  n_build node ids to build (NULL = every node; n_build ignored).
- * H         out: [n_nodes][m][n_bins][k+1] fp64.
+ * H         out: [n_nodes][m][k+1][n_bins] fp64.
  */
 int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t rec_gh,
                             int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
@@ -225,7 +225,7 @@ int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* r
  *   H_child[c ^ 1] = H_parent[p] - H_child[c]   (all m*n_bins*(k+1) cells).
  * Exact, because histograms are fixed-point sums stored in fp64.  Entries of
  * build_list that are not 2p or 2p+1 leave that pair untouched.
- * H_parent: [n_parents][m][n_bins][k+1]; H_child: [2*n_parents][...], updated
+ * H_parent: [n_parents][m][k+1][n_bins]; H_child: [2*n_parents][...], updated
  * in place.
  */
 int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t n_parents, int32_t m,
@@ -241,7 +241,7 @@ int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t 
  * candidate maximises S; ties go to the lower f, then the lower b.  Scores
  * are evaluated in fp64.  A node without a valid candidate gets
  * (-1, -1, -inf).
- * H: [n_nodes][m][n_bins][k+1] fp64.  lambda > 0, min_child_weight >= 0.
+ * H: [n_nodes][m][k+1][n_bins] fp64.  lambda > 0, min_child_weight >= 0.
  * best_feature, best_bin, best_score: out, n_nodes entries each.
  */
 int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins, int32_t k, double lambda,
@@ -273,8 +273,9 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
  *
  * Runs, for level l = 0..depth-1: histograms (all rows at l = 0, read from
  * bins4 and GH; from l = 1 on, the smaller child of each pair, read from the
- * row records), sibling subtraction, scoring and partition, entirely on the
- * device with no host synchronisation.
+ * row records), sibling subtraction (fused into the histogram reduction),
+ * scoring and partition, entirely on the device with no host
+ * synchronisation.
  * bins4 / bins_cm / rec hold the same binned features in the three layouts;
  * GH (channel-major) and the sketch inside rec come from one sb_sketch call;
  * qexp from the same call.

@@ -61,7 +61,7 @@ int32_t check_hist_shape(const char* call, int64_t n, int32_t m, int32_t n_bins,
 }
 
 struct GrowLayout {
-  int64_t H0, H1, rows_tmp, offs, blists, call, total;
+  int64_t H0, H1, rows_tmp, offs, blists, pre, call, total;
 };
 
 GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth) {
@@ -90,6 +90,8 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   p += level_offs;
   L.blists = p;
   p += align256((int64_t(1) << depth) * 4);
+  L.pre = p;
+  p += align256((maxn + 1) * 8);
   L.call = p;
   p += call;
   L.total = p;
@@ -104,10 +106,13 @@ int32_t check_rec(const char* call, const void* rec, int64_t ld_rec, int64_t rec
   return SB_OK;
 }
 
-__global__ void k_root_offsets(int32_t* off, int32_t n) {
+// Level 0: one node of all n rows, and its histogram prefix.
+__global__ void k_root_offsets(int32_t* off, int64_t* pre, int32_t n) {
   if (threadIdx.x == 0) {
     off[0] = 0;
     off[1] = n;
+    pre[0] = 0;
+    pre[1] = n;
   }
 }
 
@@ -369,8 +374,8 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   int32_t* rows_tmp = reinterpret_cast<int32_t*>(w + G.rows_tmp);
   int32_t* offs = reinterpret_cast<int32_t*>(w + G.offs);
   int32_t* blists = reinterpret_cast<int32_t*>(w + G.blists);
+  int64_t* pre = reinterpret_cast<int64_t*>(w + G.pre);
   void* cws = w + G.call;
-  const int64_t cpn = (int64_t)m * n_bins * (k + 1);
 
   // level l node offsets start at offs + (2^l - 1) + l (2^l + 1 entries), its
   // build list at blists + 2^(l-1) - 1
@@ -380,20 +385,21 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     return ((depth - l) % 2 == 0) ? row_idx_out : rows_tmp;
   };
 
-  hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), (int32_t)n);
+  hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), pre, (int32_t)n);
   for (int l = 0; l < depth; ++l) {
     const int32_t nn = 1 << l;
     double* Hcur = Hbuf[l & 1];
     const int32_t* row_in = l == 0 ? nullptr : level_rows(l);
     const int32_t* off_l = level_off(l);
+    // the prefix of the built nodes' sizes comes from the previous level's
+    // partition (from k_root_offsets at the root), and the reduce writes the
+    // siblings by subtraction from the previous level
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l,
-                                   1, nullptr, 1, Hcur, cws, st);
+                                   1, nullptr, 1, Hcur, cws, st, pre, nullptr);
     } else {
-      const int32_t* bl = level_build(l);
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l,
-                                   nn, bl, nn / 2, Hcur, cws, st);
-      if (!rc) rc = launch_subtract(Hbuf[(l - 1) & 1], Hcur, nn / 2, cpn, bl, st);
+                                   nn, level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1]);
     }
     if (rc) return rc;
     const int64_t base = (int64_t(1) << l) - 1;
@@ -402,7 +408,8 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     if (rc) return rc;
     const bool last = l == depth - 1;
     rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,
-                          level_rows(l + 1), last ? leaf_off_out : level_off(l + 1), level_build(l + 1), cws, st);
+                          level_rows(l + 1), last ? leaf_off_out : level_off(l + 1), level_build(l + 1), cws, st,
+                          last ? nullptr : pre);
     if (rc) return rc;
   }
   return check_launch(call);

@@ -71,7 +71,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
                                 int32_t k, const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
-                                const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st);
+                                const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
+                                const int64_t* pre_given = nullptr, const double* H_parent = nullptr);
 int32_t launch_subtract(const double* Hp, double* Hc, int32_t n_parents, int64_t cells_per_node,
                         const int32_t* build_list, hipStream_t st);
 
@@ -82,7 +83,8 @@ int32_t launch_score(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes);
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
-                         int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st);
+                         int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,
+                         int64_t* next_pre = nullptr);
 
 // ---------------------------------------------------------------- profiling
 // Event pairs around histogram-kernel launches while profiling is on (per thread).

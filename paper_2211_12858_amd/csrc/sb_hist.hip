@@ -81,6 +81,7 @@ struct HistArgs {
   int64_t* pre;
   int64_t* partial;
   double* H;
+  const double* Hp;  // parent level, for the fused sibling subtraction (may be null)
   int64_t n;
   int32_t m, n_bins, c, pairs, n_nodes, n_build;
   int32_t nq, f, slices, rows_wave, cells, q, cpt, steps_per_window;
@@ -205,6 +206,29 @@ struct RowRef {
   bool on;
 };
 
+// N consecutive words from a 4-byte aligned address, in 16- and 8-byte loads
+// (the memory system accepts multi-dword loads at dword alignment).
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint32_t u32x2_a4 __attribute__((ext_vector_type(2), aligned(4)));
+template <int N>
+__device__ inline void load_run(const uint32_t* p, uint32_t* out) {
+#pragma unroll
+  for (int i = 0; i + 4 <= N; i += 4) {
+    const u32x4_a4 v = *reinterpret_cast<const u32x4_a4*>(p + i);
+    out[i] = v.x;
+    out[i + 1] = v.y;
+    out[i + 2] = v.z;
+    out[i + 3] = v.w;
+  }
+  constexpr int R = N & 3;
+  if constexpr (R >= 2) {
+    const u32x2_a4 v = *reinterpret_cast<const u32x2_a4*>(p + (N - R));
+    out[N - R] = v.x;
+    out[N - R + 1] = v.y;
+  }
+  if constexpr (R & 1) out[N - 1] = p[N - 1];
+}
+
 // EXACT: CMAX channels and NQMAX quads exactly (no per-element tests, so the
 // load path has no branches and the compiler can count outstanding loads).
 // Lanes without a row load row 0 and never use the data.  FROM_REC: the row
@@ -217,13 +241,22 @@ __device__ inline void load_row(const HistArgs& a, RowRef ref, int f0, int nq, i
   if constexpr (FROM_REC) {
     const uint8_t* r = a.rec + row * a.ld_rec;
     const uint32_t* wp = reinterpret_cast<const uint32_t*>(r) + (f0 >> 2);
+    const uint32_t* gp = reinterpret_cast<const uint32_t*>(r + a.rec_gh);
+    if constexpr (EXACT) {
+      // both runs lie in the row's record: a few wide loads instead of one per word
+      load_run<NQMAX>(wp, d.word);
+      uint32_t gw[CMAX];
+      load_run<CMAX>(gp, gw);
 #pragma unroll
-    for (int qq = 0; qq < NQMAX; ++qq)
-      if (EXACT || qq < nq) d.word[qq] = wp[qq];
-    const float* ghr = reinterpret_cast<const float*>(r + a.rec_gh);
+      for (int t = 0; t < CMAX; ++t) d.g[t] = __uint_as_float(gw[t]);
+    } else {
 #pragma unroll
-    for (int t = 0; t < CMAX; ++t)
-      if (EXACT || t < c) d.g[t] = ghr[t];
+      for (int qq = 0; qq < NQMAX; ++qq)
+        if (qq < nq) d.word[qq] = wp[qq];
+#pragma unroll
+      for (int t = 0; t < CMAX; ++t)
+        if (t < c) d.g[t] = __uint_as_float(gp[t]);
+    }
   } else {
     const uint32_t* wp = a.bins4 + (int64_t)(f0 >> 2) * a.ld4 + row;
 #pragma unroll
@@ -417,9 +450,11 @@ k_hist(HistArgs a) {
 
 __device__ inline int64_t group_of(int64_t x, int64_t T, int64_t Q) { return ((x + 1) * Q - 1) / T; }
 
-// H[node][f][b][t] = sum of the partials of the row groups that covered the
+// H[node][f][t][b] = sum of the partials of the row groups that covered the
 // node.  Partial channel cell e = 2 * e64 + half, with 64-bit LDS cell e64
 // laid out [channel pair][feature in slice][bin] and t = 2 * pair + half.
+// With the parent level given (Hp), the built node j of pair p also yields
+// its sibling: H[j ^ 1] = Hp[p] - H[j], exact in fixed point.
 __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   const int p = blockIdx.y, s = blockIdx.z;
@@ -445,7 +480,11 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
         sum += a.partial[((int64_t)s * a.slots + q + p) * a.cells + e];
     }
   }
-  a.H[(((int64_t)j * a.m + f) * a.n_bins + bin) * a.c + t] = ldexp((double)sum, -a.qexp[t]);
+  const int64_t cpn = (int64_t)a.m * a.c * a.n_bins;
+  const int64_t idx = ((int64_t)f * a.c + t) * a.n_bins + bin;
+  const double v = ldexp((double)sum, -a.qexp[t]);
+  a.H[(int64_t)j * cpn + idx] = v;
+  if (a.Hp && (j == 2 * p || j == 2 * p + 1)) a.H[(int64_t)(j ^ 1) * cpn + idx] = a.Hp[(int64_t)p * cpn + idx] - v;
 }
 
 __global__ void __launch_bounds__(256)
@@ -467,7 +506,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
                                 int32_t k, const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
-                                const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st) {
+                                const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
+                                const int64_t* pre_given, const double* H_parent) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build);
   HistArgs a{};
   a.bins4 = bins4;
@@ -482,9 +522,10 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.node_off = node_off;
   a.build_list = build_list;
   char* w = static_cast<char*>(ws);
-  a.pre = reinterpret_cast<int64_t*>(w);
+  a.pre = pre_given ? const_cast<int64_t*>(pre_given) : reinterpret_cast<int64_t*>(w);
   a.partial = reinterpret_cast<int64_t*>(w + align256((int64_t)(n_build + 1) * 8));
   a.H = H;
+  a.Hp = H_parent;
   a.n = n;
   a.m = m;
   a.n_bins = n_bins;
@@ -504,7 +545,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.slots = pl.slots;
   if (rows_step > WINDOW_ROWS) return fail(SB_E_UNSUPPORTED, "histogram step exceeds the fixed-point window");
 
-  hipLaunchKernelGGL(k_hist_plan, dim3(1), dim3(1024), 0, st, a);
+  if (!pre_given) hipLaunchKernelGGL(k_hist_plan, dim3(1), dim3(1024), 0, st, a);
   const int grid = pl.q_pad * pl.slices;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;

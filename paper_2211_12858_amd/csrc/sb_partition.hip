@@ -39,6 +39,7 @@ struct PartArgs {
   int32_t* row_out;
   int32_t* off_out;
   int32_t* build_out;
+  int64_t* next_pre;    // may be null: prefix of the built children's sizes, for the next level's histograms
   uint64_t* masks;      // n_tiles * PT_MASKS
   int32_t* tile_cnt;    // n_tiles
   int32_t* tile_off;    // n_tiles + 1 entries (last = total)
@@ -175,6 +176,17 @@ __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
     a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
   }
   if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
+  if (a.next_pre) {
+    const int64_t total_built = block_excl_scan(
+        a.n_nodes,
+        [&](int j) -> int64_t {
+          int64_t size;
+          const int64_t nl = node_left(a, j, &size);
+          return nl <= size - nl ? nl : size - nl;
+        },
+        [&](int j, int64_t pre) { a.next_pre[j] = pre; }, sh);
+    if (threadIdx.x == 0) a.next_pre[a.n_nodes] = total_built;
+  }
 }
 
 __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
@@ -232,7 +244,8 @@ int64_t partition_ws_bytes(int64_t n, int32_t n_nodes) {
 
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
-                         int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st) {
+                         int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,
+                         int64_t* next_pre) {
   const int64_t tiles = (n + PT_TILE - 1) / PT_TILE;
   PartArgs a{};
   a.bins_cm = bins_cm;
@@ -244,6 +257,7 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.row_out = row_out;
   a.off_out = off_out;
   a.build_out = build_out;
+  a.next_pre = next_pre;
   char* w = static_cast<char*>(ws);
   a.masks = reinterpret_cast<uint64_t*>(w);
   w += align256(tiles * PT_MASKS * 8);

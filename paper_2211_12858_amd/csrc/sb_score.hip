@@ -3,10 +3,12 @@
 //
 // k_score_feature: one wave per (node, feature).  Each lane owns a run of
 //   consecutive bins; a per-lane prefix plus a wave scan (shuffles) gives
-//   the inclusive prefix over bins of every channel.  Histogram values are
-//   fixed-point sums stored in fp64, so these prefix sums are exact.  The
-//   lane then scores its thresholds and the wave keeps the best (score
-//   descending, bin ascending).
+//   the inclusive prefix over bins of every channel.  H is laid out
+//   [node][feature][channel][bin], so a wave reads each channel's bins as
+//   one contiguous run.  Histogram values are fixed-point sums stored in
+//   fp64, so these prefix sums are exact.  The lane then scores its
+//   thresholds and the wave keeps the best (score descending, bin
+//   ascending).
 // k_score_node: one wave per node picks the best feature (score descending,
 //   feature ascending).  Fixed reduction order: results do not depend on
 //   timing.
@@ -42,7 +44,7 @@ k_score_feature(const double* __restrict__ H, int n_nodes, int m, int B, int k, 
   if (f >= m) return;
   const int c = k + 1;
   const int bpl = (B + 63) / 64;
-  const double* Hf = H + ((int64_t)j * m + f) * B * c;
+  const double* Hf = H + ((int64_t)j * m + f) * c * B;
   const int b0 = lane * bpl;
 
   // hessian channel
@@ -51,7 +53,7 @@ k_score_feature(const double* __restrict__ H, int n_nodes, int m, int B, int k, 
 #pragma unroll
   for (int i = 0; i < MAX_BPL; ++i) {
     const int b = b0 + i;
-    if (i < bpl && b < B) run += Hf[(int64_t)b * c + k];
+    if (i < bpl && b < B) run += Hf[(int64_t)k * B + b];
     hl[i] = run;
     sl[i] = 0.0;
     sr[i] = 0.0;
@@ -68,7 +70,7 @@ k_score_feature(const double* __restrict__ H, int n_nodes, int m, int B, int k, 
 #pragma unroll
     for (int i = 0; i < MAX_BPL; ++i) {
       const int b = b0 + i;
-      if (i < bpl && b < B) r += Hf[(int64_t)b * c + t];
+      if (i < bpl && b < B) r += Hf[(int64_t)t * B + b];
       gl[i] = r;
     }
     const double in = wave_incl_scan(r);

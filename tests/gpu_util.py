@@ -72,7 +72,7 @@ def qexp_rule(GH):
 
 
 def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None, ld_pad=0, ld_rec=None):
-    """Histograms through the C ABI; GH is an (n, k+1) host array.
+    """Histograms through the C ABI (device layout [node][feature][channel][bin]); GH is an (n, k+1) host array.
 
     Without row_idx the data go up as quad-major bins and a channel-major
     sketch (leading dimension n + ld_pad); with row_idx as row records of
@@ -86,7 +86,7 @@ def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None,
     ws = workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=n_bins, k=k,
                                         n_nodes=max(n_nodes, n_build)), DEV)
     if H is None:
-        H = torch.full((n_nodes, m, n_bins, c), float("nan"), dtype=torch.float64, device=DEV)
+        H = torch.full((n_nodes, m, c, n_bins), float("nan"), dtype=torch.float64, device=DEV)
     b4 = gh = rec = None
     ld = n + ld_pad
     rec_gh = 0
@@ -109,6 +109,11 @@ def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None,
     return H
 
 
+def host_layout(H):
+    """Device histograms [node][feature][channel][bin] as [node][feature][bin][channel] (the oracle's layout)."""
+    return np.ascontiguousarray(np.swapaxes(np.asarray(H), -1, -2))
+
+
 def hist_tolerance_ok(Hg, Ho, counts, qexp, mass, chan_max):
     """Check a device histogram against the oracle's.
 
@@ -128,8 +133,9 @@ def hist_tolerance_ok(Hg, Ho, counts, qexp, mass, chan_max):
 
 
 def run_score(H_np, n_bins, k, lam=1.0, mcw=0.0):
+    """H_np in the oracle's layout [node][feature][bin][channel]."""
     n_nodes, m = H_np.shape[:2]
-    Hd = up(H_np, torch.float64)
+    Hd = up(host_layout(H_np), torch.float64)
     bf = torch.zeros(n_nodes, dtype=torch.int32, device=DEV)
     bb = torch.zeros(n_nodes, dtype=torch.int32, device=DEV)
     bs = torch.zeros(n_nodes, dtype=torch.float64, device=DEV)

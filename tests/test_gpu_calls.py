@@ -158,9 +158,9 @@ def test_histograms(n, m, B, k, n_nodes, build, seed):
         build_list = None
     if seed == 8:  # positions are the rows (no row_idx), leading dimension padded
         rows = np.arange(n, dtype=np.int32)
-        Hg = gu.run_hist(case.bins, GH, qexp, B, None, off, build_list, ld_pad=19).cpu().numpy()
+        Hg = gu.host_layout(gu.run_hist(case.bins, GH, qexp, B, None, off, build_list, ld_pad=19).cpu().numpy())
     else:
-        Hg = gu.run_hist(case.bins, GH, qexp, B, rows, off, build_list).cpu().numpy()
+        Hg = gu.host_layout(gu.run_hist(case.bins, GH, qexp, B, rows, off, build_list).cpu().numpy())
     todo = range(n_nodes) if build_list is None else build_list
     chan_max = np.abs(GH.astype(np.float64)).max(axis=0)
     ones = np.ones((n, 1), dtype=np.float32)
