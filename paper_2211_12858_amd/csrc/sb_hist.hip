@@ -139,13 +139,12 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
   if (threadIdx.x == 1023) a.pre[a.n_build] = part[1023];
 }
 
-// Thread t owns the contiguous 64-bit cells [t*H, t*H + H), H =
-// HIST_MAX_CELLS_PER_THREAD / 2, read as 128-bit words; cell j carries the
-// channel cells 2j (low half) and 2j+1 (high half) of the thread's totals.
-// The LDS always holds H cells per thread (cells past the plan's count stay
-// zero), so the reads need no bounds tests.  Cells are folded 4 at a time
-// with compiler barriers in between, which bounds the registers the reads
-// hold on top of the 2*MAXC registers of totals.
+// Thread t owns the 64-bit cells j = t + HIST_THREADS * i, i < H (H =
+// HIST_MAX_CELLS_PER_THREAD / 2): consecutive threads own consecutive cells,
+// so the fold's 64-bit LDS reads and the final partial writes are contiguous
+// per wave.  Cell i of the thread carries its channel totals 2i (low half)
+// and 2i+1 (high half).  The LDS always holds H cells per thread (cells past
+// the plan's count stay zero), so the reads need no bounds tests.
 //
 // A cell holds S = Hi * 2^32 + Lo (mod 2^64), Hi and Lo the exact running
 // channel sums, and the totals hold the sums as of the previous read, so
@@ -154,24 +153,23 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
 // arithmetic high word of D - dLo.
 __device__ inline void fold_cells(const uint64_t* lds64, int64_t* tot) {
   constexpr int H = HIST_MAX_CELLS_PER_THREAD / 2;
-  static_assert(H % 4 == 0, "fold reads 4 cells at a time");
-  const uint4* src = reinterpret_cast<const uint4*>(lds64 + threadIdx.x * H);
 #pragma unroll
-  for (int j0 = 0; j0 < H; j0 += 4) {
+  for (int i0 = 0; i0 < H; i0 += 4) {
     asm volatile("" ::: "memory");
-    const uint4 x = src[j0 / 2];
-    const uint4 y = src[j0 / 2 + 1];
-    const uint64_t cur[4] = {(uint64_t)x.x | ((uint64_t)x.y << 32), (uint64_t)x.z | ((uint64_t)x.w << 32),
-                             (uint64_t)y.x | ((uint64_t)y.y << 32), (uint64_t)y.z | ((uint64_t)y.w << 32)};
+    uint64_t cur[4];
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int i = 2 * (j0 + jj);
-      const uint64_t last = ((uint64_t)tot[i + 1] << 32) + (uint64_t)tot[i];
-      const uint64_t d = cur[jj] - last;
-      const int64_t dlo = (int64_t)(int32_t)(uint32_t)d;
-      const int64_t dhi = (int64_t)(d - (uint64_t)dlo) >> 32;
-      tot[i] += dlo;
-      tot[i + 1] += dhi;
+    for (int ii = 0; ii < 4; ++ii) cur[ii] = (i0 + ii < H) ? lds64[threadIdx.x + HIST_THREADS * (i0 + ii)] : 0;
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      if (i0 + ii < H) {
+        const int i = 2 * (i0 + ii);
+        const uint64_t last = ((uint64_t)tot[i + 1] << 32) + (uint64_t)tot[i];
+        const uint64_t d = cur[ii] - last;
+        const int64_t dlo = (int64_t)(int32_t)(uint32_t)d;
+        const int64_t dhi = (int64_t)(d - (uint64_t)dlo) >> 32;
+        tot[i] += dlo;
+        tot[i + 1] += dhi;
+      }
     }
   }
   asm volatile("" ::: "memory");
@@ -382,7 +380,6 @@ template <int CMAX, int NQMAX, bool EXACT>
 __global__ void __launch_bounds__(HIST_THREADS)
 k_hist(HistArgs a) {
   extern __shared__ uint64_t lds64[];
-  int32_t* lds = reinterpret_cast<int32_t*>(lds64);
   const int b = blockIdx.x;
   const int xcd = b & 7, g = b >> 3;
   const int q = (g / a.slices) * 8 + xcd;
@@ -417,7 +414,7 @@ k_hist(HistArgs a) {
   int64_t tot[HIST_MAX_CELLS_PER_THREAD];
 #pragma unroll
   for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) tot[jj] = 0;
-  for (int e = tid; e < HIST_THREADS * HIST_MAX_CELLS_PER_THREAD; e += HIST_THREADS) lds[e] = 0;
+  for (int i = 0; i < HIST_MAX_CELLS_PER_THREAD / 2; ++i) lds64[tid + HIST_THREADS * i] = 0;
   __syncthreads();
 
   int64_t v = v0;
@@ -433,13 +430,18 @@ k_hist(HistArgs a) {
     // end of this node's part: final fold, write the partial, reset
     __syncthreads();
     fold_cells(lds64, tot);
+    // partial channel cells 2j, 2j+1 of 64-bit cell j, one 16-byte store per cell
     int64_t* dst = a.partial + ((int64_t)s * a.slots + q + p) * a.cells;
 #pragma unroll
-    for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) {
-      const int e = tid * HIST_MAX_CELLS_PER_THREAD + jj;
-      if (e < a.cells) dst[e] = tot[jj];
-      lds[e] = 0;
-      tot[jj] = 0;
+    for (int i = 0; i < HIST_MAX_CELLS_PER_THREAD / 2; ++i) {
+      const int j64 = tid + HIST_THREADS * i;
+      if (2 * j64 < a.cells) {
+        const longlong2 v2 = make_longlong2(tot[2 * i], tot[2 * i + 1]);
+        reinterpret_cast<longlong2*>(dst)[j64] = v2;
+      }
+      lds64[j64] = 0;
+      tot[2 * i] = 0;
+      tot[2 * i + 1] = 0;
     }
     __syncthreads();
     v = vend;
@@ -475,9 +477,20 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   int64_t sum = 0;
   if (hi > lo) {
     const int64_t qlo = group_of(lo, T, a.q), qhi = group_of(hi - 1, T, a.q);
-    for (int64_t q = qlo; q <= qhi; ++q) {
-      if (q * T / a.q < (q + 1) * T / a.q)
-        sum += a.partial[((int64_t)s * a.slots + q + p) * a.cells + e];
+    const int64_t* src = a.partial + ((int64_t)s * a.slots + p) * a.cells + e;
+    if (T >= a.q) {
+      // every row group holds at least one position: independent loads, four sums
+      int64_t acc[4] = {0, 0, 0, 0};
+      int64_t q = qlo;
+      for (; q + 4 <= qhi + 1; q += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[u] += src[(q + u) * a.cells];
+      }
+      for (; q <= qhi; ++q) acc[0] += src[q * a.cells];
+      sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    } else {
+      for (int64_t q = qlo; q <= qhi; ++q)
+        if (q * T / a.q < (q + 1) * T / a.q) sum += src[q * a.cells];
     }
   }
   const int64_t cpn = (int64_t)a.m * a.c * a.n_bins;

@@ -66,28 +66,49 @@ __device__ inline int find_node(const PartArgs& a, int64_t i) {
 
 __device__ inline int32_t popc64(uint64_t x) { return __popcll(x); }
 
+// Each thread handles the positions t0 + tid + 256*it, it < 16.  The row
+// indices of all 16 positions are loaded first, then their bins, so each
+// thread keeps 16 independent loads in flight instead of a chain of 16
+// dependent pairs.  Node offsets and splits come from LDS.
 __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   __shared__ int32_t wsum[PT_THREADS / 64];
   const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
-  int64_t i = t0 + threadIdx.x;
-  int j = find_node(a, i);
+  int64_t row[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    const int64_t ic = i < a.n ? i : a.n - 1;
+    row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
+  }
+  // node of each position (positions grow with it) and its split
+  int32_t f_of[PT_ITERS], b_of[PT_ITERS];
+  int j = find_node(a, t0 + threadIdx.x);
   int64_t jend = off_at(a, j + 1);
-  int cnt = 0;
-#pragma unroll 4
-  for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
-    bool left = false;
-    if (i < a.n && i >= first && i < last) {
-      while (i >= jend && j < a.n_nodes - 1) {
-        ++j;
-        jend = off_at(a, j + 1);
-      }
-      int64_t row = a.row_in ? (int64_t)a.row_in[i] : i;
-      row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
-      const int32_t f = a.best_f[j];
-      left = (f < 0 || f >= a.m) ? true : (int32_t)a.bins_cm[(int64_t)f * a.ld_cm + row] <= a.best_b[j];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    while (i >= jend && j < a.n_nodes - 1) {
+      ++j;
+      jend = off_at(a, j + 1);
     }
+    const int32_t f = a.best_f[j];
+    const bool live = i < a.n && i >= first && i < last;
+    f_of[it] = (!live) ? -2 : ((f < 0 || f >= a.m) ? -1 : f);
+    b_of[it] = a.best_b[j];
+  }
+  uint32_t bin[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t r = row[it] < 0 ? 0 : (row[it] >= a.n ? a.n - 1 : row[it]);
+    bin[it] = f_of[it] >= 0 ? a.bins_cm[(int64_t)f_of[it] * a.ld_cm + r] : 0u;
+  }
+  int cnt = 0;
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    // terminal node (f = -1): every row goes left; positions outside the nodes (-2) are not flagged
+    const bool left = f_of[it] == -1 || (f_of[it] >= 0 && (int32_t)bin[it] <= b_of[it]);
     const uint64_t mask = __ballot(left);
     if (lane == 0) {
       a.masks[(int64_t)blockIdx.x * PT_MASKS + it * (PT_THREADS / 64) + wave] = mask;
@@ -104,31 +125,37 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
 }
 
 // Exclusive scan over v(0..N-1) by one 1024-thread block; out(i, prefix) is
-// called for every i, and the total is returned to every thread.
+// called for every i, and the total is returned to every thread.  Each
+// thread scans a contiguous run of per = ceil(N/1024) values; the per-thread
+// totals are scanned with wave shuffles and one pass over the 16 wave totals.
 template <typename V, typename O>
 __device__ int64_t block_excl_scan(int N, V v, O out, int64_t* sh) {
   const int per = (N + 1023) / 1024;
   const int p0 = threadIdx.x * per;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int64_t local = 0;
   for (int i = 0; i < per; ++i)
     if (p0 + i < N) local += v(p0 + i);
-  __syncthreads();
-  sh[threadIdx.x] = local;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    int64_t x = threadIdx.x >= off ? sh[threadIdx.x - off] : 0;
-    __syncthreads();
-    sh[threadIdx.x] += x;
-    __syncthreads();
+  int64_t incl = local;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
   }
-  int64_t run = threadIdx.x ? sh[threadIdx.x - 1] : 0;
+  __syncthreads();  // sh may still be read by a previous scan
+  if (lane == 63) sh[wave] = incl;
+  __syncthreads();
+  int64_t wbase = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    const int64_t x = sh[w];
+    if (w < wave) wbase += x;
+    total += x;
+  }
+  int64_t run = wbase + incl - local;
   for (int i = 0; i < per; ++i)
     if (p0 + i < N) {
       out(p0 + i, run);
       run += v(p0 + i);
     }
-  const int64_t total = sh[1023];
-  __syncthreads();
   return total;
 }
 
@@ -142,28 +169,30 @@ __device__ inline int64_t node_left(const PartArgs& a, int j, int64_t* size_out)
 }
 
 __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
-  __shared__ int64_t sh[1024];
+  __shared__ int64_t sh[16];
   // 1. tile offsets
   const int64_t total = block_excl_scan(
       a.n_tiles, [&](int t) -> int64_t { return a.tile_cnt[t]; },
       [&](int t, int64_t pre) { a.tile_off[t] = (int32_t)pre; }, sh);
   if (threadIdx.x == 0) a.tile_off[a.n_tiles] = (int32_t)total;
   __syncthreads();
-  // 2. Lb_j = left rows before each node boundary
-  for (int j = threadIdx.x; j <= a.n_nodes; j += 1024) {
-    const int64_t x = off_at(a, j);
-    const int64_t t = x / PT_TILE;
-    int64_t lb;
-    if (t >= a.n_tiles) {
-      lb = total;
-    } else {
-      const int w = (int)(x - t * PT_TILE);
-      const uint64_t* mk = a.masks + t * PT_MASKS;
-      lb = a.tile_off[t];
-      for (int q = 0; q < (w >> 6); ++q) lb += popc64(mk[q]);
-      if (w & 63) lb += popc64(mk[w >> 6] & ((uint64_t(1) << (w & 63)) - 1));
+  // 2. Lb_j = left rows before each node boundary: one wave per boundary,
+  // lane q counts the flags of ballot q of the boundary's tile
+  {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int j = wave; j <= a.n_nodes; j += 16) {
+      const int64_t x = off_at(a, j);
+      const int64_t t = x / PT_TILE;
+      int64_t c = 0;
+      if (t < a.n_tiles) {
+        const int w = (int)(x - t * PT_TILE);
+        const uint64_t mq = a.masks[t * PT_MASKS + lane];
+        if (lane < (w >> 6)) c = popc64(mq);
+        else if (lane == (w >> 6) && (w & 63)) c = popc64(mq & ((uint64_t(1) << (w & 63)) - 1));
+      }
+      for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
+      if (lane == 0) a.Lb[j] = (int32_t)(t < a.n_tiles ? a.tile_off[t] + c : total);
     }
-    a.Lb[j] = (int32_t)lb;
   }
   __syncthreads();
   // 3. children and build list
@@ -194,14 +223,24 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
   __shared__ int32_t pre[PT_MASKS];
   const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (threadIdx.x < PT_MASKS) mk[threadIdx.x] = a.masks[(int64_t)blockIdx.x * PT_MASKS + threadIdx.x];
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t r = a.tile_off[blockIdx.x];
-    for (int q = 0; q < PT_MASKS; ++q) {
-      pre[q] = r;
-      r += popc64(mk[q]);
+  int64_t row[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    const int64_t ic = i < a.n ? i : a.n - 1;
+    row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
+  }
+  // ballots of the tile and their exclusive prefix, by the first wave
+  if (wave == 0) {
+    const uint64_t m = a.masks[(int64_t)blockIdx.x * PT_MASKS + lane];
+    const int32_t c = popc64(m);
+    int32_t incl = c;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
     }
+    mk[lane] = m;
+    pre[lane] = a.tile_off[blockIdx.x] + incl - c;
   }
   __syncthreads();
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
@@ -210,7 +249,7 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
   int j = find_node(a, i);
   int64_t jstart = off_at(a, j), jend = off_at(a, j + 1);
   int64_t lbj = a.Lb[j], nleft = (int64_t)a.Lb[j + 1] - lbj;
-#pragma unroll 4
+#pragma unroll
   for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
@@ -224,12 +263,11 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
       const uint64_t m = mk[q];
       const bool left = (m >> lane) & 1u;
       const int64_t L = (int64_t)pre[q] + popc64(m & below);
-      int64_t row = a.row_in ? (int64_t)a.row_in[i] : i;
-      row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
+      const int64_t rw = row[it] < 0 ? 0 : (row[it] >= a.n ? a.n - 1 : row[it]);
       const int64_t lrel = L - lbj;
       int64_t dest = left ? jstart + lrel : jstart + nleft + (i - jstart) - lrel;
       dest = dest < 0 ? 0 : (dest >= a.n ? a.n - 1 : dest);
-      a.row_out[dest] = (int32_t)row;
+      a.row_out[dest] = (int32_t)rw;
     }
   }
 }
