@@ -240,53 +240,103 @@ k_pack(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float*
   }
 }
 
-constexpr int PROJ_THREADS = 256;
-constexpr int PROJ_KT = 32;  // sketch columns per pass
+constexpr int PROJ_THREADS = 1024;
+constexpr int PROJ_KT = 32;               // sketch columns per pass
+constexpr int PROJ_JU = 16;               // G loads in flight per thread
+constexpr int PROJ_LDS_FLOATS = 32768;    // 128 KB: the Pi block staged per pass
 
-// VALU projection: one row per thread, Pi read with uniform (scalar) loads.
+// Random Projections (Section 3.3), HBM-bound on the read of G: one row per
+// thread, PROJ_JU columns of G loaded ahead, and the pass's block of Pi
+// (rows j0..j0+jc, columns t0..t0+KT) staged in LDS and read by broadcast.
+// Each output is an fp32 fmaf chain over j in increasing order.  Columns
+// past k are padded with zeros in LDS and never written.
+template <int KT>
 __global__ void __launch_bounds__(PROJ_THREADS)
-k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k,
-          const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh, uint8_t* __restrict__ rec,
-          int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k, int t0,
+          float* __restrict__ GH, int64_t ld_gh, uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh,
+          uint32_t* __restrict__ blockmax) {
+  extern __shared__ float sPi[];  // [jc][KT]
   __shared__ uint32_t sh[PROJ_THREADS / 64];
-  for (int t0 = 0; t0 <= k; t0 += PROJ_KT) {
-    const int kt = (k + 1 - t0 < PROJ_KT) ? k + 1 - t0 : PROJ_KT;  // channel k (h) rides in the last pass
-    uint32_t mx[PROJ_KT];
+  const int kt = (k - t0 < KT) ? k - t0 : KT;
+  const int jcap = PROJ_LDS_FLOATS / KT;
+  uint32_t mx[KT];
 #pragma unroll
-    for (int t = 0; t < PROJ_KT; ++t) mx[t] = 0u;
-    for (int64_t i0 = (int64_t)blockIdx.x * PROJ_THREADS; i0 < n; i0 += (int64_t)gridDim.x * PROJ_THREADS) {
-      const int64_t i = i0 + threadIdx.x;
-      const bool live = i < n;
-      const int64_t ii = live ? i : 0;
-      float acc[PROJ_KT];
+  for (int t = 0; t < KT; ++t) mx[t] = 0u;
+  for (int64_t base = (int64_t)blockIdx.x * PROJ_THREADS; base < n; base += (int64_t)gridDim.x * PROJ_THREADS) {
+    const int64_t i = base + threadIdx.x;
+    const bool live = i < n;
+    const int64_t ii = live ? i : n - 1;
+    float acc[KT];
 #pragma unroll
-      for (int t = 0; t < PROJ_KT; ++t) acc[t] = 0.0f;
-      for (int j = 0; j < d; ++j) {
-        const float g = G[(int64_t)j * ld_g + ii];
-        const float* pr = Pi + (int64_t)j * k + t0;
-#pragma unroll
-        for (int t = 0; t < PROJ_KT; ++t)
-          if (t < kt && t0 + t < k) acc[t] = fmaf(g, pr[t], acc[t]);
+    for (int t = 0; t < KT; ++t) acc[t] = 0.0f;
+    for (int j0 = 0; j0 < d; j0 += jcap) {
+      const int jc = (d - j0 < jcap) ? d - j0 : jcap;
+      __syncthreads();
+      for (int e = threadIdx.x; e < jc * KT; e += PROJ_THREADS) {
+        const int jj = e / KT, t = e - jj * KT;
+        sPi[e] = (t < kt) ? Pi[(int64_t)(j0 + jj) * k + t0 + t] : 0.0f;
       }
+      __syncthreads();
+      for (int jb = 0; jb < jc; jb += PROJ_JU) {
+        float g[PROJ_JU];
 #pragma unroll
-      for (int t = 0; t < PROJ_KT; ++t) {
-        if (t < kt && live) {
-          const float v = (t0 + t < k) ? acc[t] : h[i];
-          GH[(int64_t)(t0 + t) * ld_gh + i] = v;
-          if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (t0 + t)) = v;
-          const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+        for (int u = 0; u < PROJ_JU; ++u) {
+          const int j = j0 + jb + u;
+          g[u] = (jb + u < jc) ? G[(int64_t)j * ld_g + ii] : 0.0f;
+        }
+#pragma unroll
+        for (int u = 0; u < PROJ_JU; ++u) {
+          if (jb + u < jc) {
+            const float4* pr = reinterpret_cast<const float4*>(sPi + (jb + u) * KT);
+#pragma unroll
+            for (int t4 = 0; t4 < KT / 4; ++t4) {
+              const float4 p4 = pr[t4];
+              acc[4 * t4] = fmaf(g[u], p4.x, acc[4 * t4]);
+              acc[4 * t4 + 1] = fmaf(g[u], p4.y, acc[4 * t4 + 1]);
+              acc[4 * t4 + 2] = fmaf(g[u], p4.z, acc[4 * t4 + 2]);
+              acc[4 * t4 + 3] = fmaf(g[u], p4.w, acc[4 * t4 + 3]);
+            }
+          }
+        }
+      }
+    }
+    if (live) {
+#pragma unroll
+      for (int t = 0; t < KT; ++t) {
+        if (t < kt) {
+          GH[(int64_t)(t0 + t) * ld_gh + i] = acc[t];
+          if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (t0 + t)) = acc[t];
+          const uint32_t a = __float_as_uint(acc[t]) & 0x7fffffffu;
           mx[t] = a > mx[t] ? a : mx[t];
         }
       }
     }
+  }
 #pragma unroll
-    for (int t = 0; t < PROJ_KT; ++t) {
-      if (t < kt) {
-        const uint32_t r = block_max_u32<PROJ_THREADS>(mx[t], sh);
-        if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + t] = r;
-      }
+  for (int t = 0; t < KT; ++t) {
+    if (t < kt) {
+      const uint32_t r = block_max_u32<PROJ_THREADS>(mx[t], sh);
+      if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + t] = r;
     }
   }
+}
+
+// The hessian channel of a projected sketch: GH[k*ld_gh + i] = h[i] (and the
+// record copy), with its per-block maximum.
+__global__ void __launch_bounds__(256)
+k_project_h(const float* __restrict__ h, int64_t n, int k, float* __restrict__ GH, int64_t ld_gh,
+            uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+  __shared__ uint32_t sh[4];
+  uint32_t mx = 0u;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    const float v = h[i];
+    GH[(int64_t)k * ld_gh + i] = v;
+    if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * k) = v;
+    const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
+    mx = a > mx ? a : mx;
+  }
+  mx = block_max_u32<256>(mx, sh);
+  if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = mx;
 }
 
 // Per-block max |GH[t*ld_gh + i]| for a caller-supplied channel-major GH.
@@ -365,9 +415,24 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
 
   int nb;
   if (kind == SB_SKETCH_RANDOM_PROJECTION) {
+    // one grid for every pass, so that block b's maxima of all channels sit in row b
     nb = sketch_blocks(n, PROJ_THREADS);
-    hipLaunchKernelGGL(k_project, dim3(nb), dim3(PROJ_THREADS), 0, st, G, n, d, ld_g, Pi, k, h, GH, ld_gh, rec,
-                       ld_rec, rec_gh, blockmax);
+    for (int t0 = 0; t0 < k; t0 += PROJ_KT) {
+      const int kt = (k - t0 < PROJ_KT) ? k - t0 : PROJ_KT;
+      const int KT = (kt + 3) / 4 * 4;
+      const int jc = (d < PROJ_LDS_FLOATS / KT) ? d : PROJ_LDS_FLOATS / KT;
+      const size_t lds = (size_t)jc * KT * 4;
+#define SB_PROJ(K)                                                                                               \
+  case K:                                                                                                        \
+    hipLaunchKernelGGL((k_project<K>), dim3(nb), dim3(PROJ_THREADS), lds, st, G, n, d, ld_g, Pi, k, t0, GH, ld_gh, \
+                       rec, ld_rec, rec_gh, blockmax);                                                           \
+    break;
+      switch (KT) {
+        SB_PROJ(4) SB_PROJ(8) SB_PROJ(12) SB_PROJ(16) SB_PROJ(20) SB_PROJ(24) SB_PROJ(28) SB_PROJ(32)
+      }
+#undef SB_PROJ
+    }
+    hipLaunchKernelGGL(k_project_h, dim3(nb), dim3(256), 0, st, h, n, k, GH, ld_gh, rec, ld_rec, rec_gh, blockmax);
   } else {
     int64_t chunk = (n + P - 1) / P;
     chunk = (chunk + 3) & ~int64_t(3);
