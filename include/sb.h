@@ -49,17 +49,16 @@
  * - COLUMN-MAJOR BINS (bins_cm, ld_cm): the bin of (row i, feature f) is the
  *   byte bins_cm[f*ld_cm + i], ld_cm >= n.  The partition reads it: the rows
  *   of a node are read in one run of the split feature's column.
- * - ROW RECORDS (rec, ld_rec, rec_gh): row i owns the ld_rec bytes at
- *   rec + i*ld_rec; its m bins are bytes 0..m-1 and, once sb_sketch has
- *   written the sketch into the records, channel t of its sketch is the
- *   float at byte rec_gh + 4t.  Requirements: 16-byte aligned base,
- *   ld_rec % 16 == 0, rec_gh % 4 == 0, rec_gh >= m, rec_gh + 4(k+1) <= ld_rec.
+ * - ROW RECORDS (rec, ld_rec): row i's m bins are the bytes rec[i*ld_rec ..
+ *   i*ld_rec + m-1]; ld_rec >= m, ld_rec % 16 == 0, 16-byte aligned base.
  *   The histograms of the deeper levels read it through row indices: one
- *   row is one contiguous record (exactly one 128-byte line for m = 100,
- *   k = 5).
- * - CHANNEL-MAJOR SKETCH (GH, ld_gh): channel t of row i is GH[t*ld_gh + i],
- *   ld_gh >= n.  Channels 0..k-1 are the sketch columns, channel k is the
- *   hessian weight h.
+ *   row is one contiguous record (one 128-byte line for m <= 128 with
+ *   ld_rec = 128).
+ * - ROW-MAJOR SKETCH (GH, ld_gh): channel t of row i is GH[i*ld_gh + t],
+ *   ld_gh >= k+1 floats, 16-byte aligned base.  Channels 0..k-1 are the
+ *   sketch columns, channel k is the hessian weight h.  With ld_gh a multiple
+ *   of 8 every row fills whole 32-byte sectors, which sb_sketch writes in
+ *   full (floats k+1 .. ld_gh-1 are written as 0).
  * sb_layout_bins() builds the three bin layouts from a row-major matrix.
  */
 #ifndef SB_H_
@@ -155,14 +154,10 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
  * u       RANDOM_SAMPLING only: k uniforms in [0, 1) (fp64, device).  The
  *         random numbers are an input so that results are reproducible.
  * Pi      RANDOM_PROJECTION only: d x k, row-major (Pi[j*k + t]), fp32.
- * GH      out: channel-major sketch, ld_gh >= n:
- *         GH[t*ld_gh + i] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
- *         fp32 multiply; the projection sum for RANDOM_PROJECTION) and
- *         GH[k*ld_gh + i] = h[i].
- * rec, ld_rec, rec_gh  optional (rec may be NULL): the same k+1 values are
- *         also written into the row records (float t of row i at byte
- *         i*ld_rec + rec_gh + 4t), where the histograms of the deeper levels
- *         read them.
+ * GH      out: row-major sketch, ld_gh >= k+1 floats per row, 16-byte aligned:
+ *         GH[i*ld_gh + t] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
+ *         fp32 multiply; the projection sum for RANDOM_PROJECTION),
+ *         GH[i*ld_gh + k] = h[i], and GH[i*ld_gh + t] = 0 for k < t < ld_gh.
  * cols, scales  out (not RANDOM_PROJECTION): k entries each.
  * norm2   out: d fp64 squared column norms; required for TOP_OUTPUTS and
  *         RANDOM_SAMPLING, optional (may be NULL) for IDENTITY, ignored for
@@ -171,14 +166,13 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
  *         sb_build_histograms (same rule as sb_hist_exponents).
  */
 int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                  const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
-                  int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
-                  int64_t ws_bytes, void* stream);
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream);
 
 /*
- * sb_hist_exponents -- fixed-point exponents for a given GH (channel-major).
+ * sb_hist_exponents -- fixed-point exponents for a given GH (row-major).
  *
- * For channel t (t <= k) with M_t = max_i |GH[t*ld_gh + i]|:
+ * For channel t (t <= k) with M_t = max_i |GH[i*ld_gh + t]|:
  *   qexp[t] = 18 - floor(log2(M_t))   (qexp[t] = 0 if M_t == 0),
  * so every value maps to an integer rint(v * 2^qexp[t]) of magnitude <= 2^19.
  * sb_build_histograms accumulates those integers exactly and reports sums
@@ -198,22 +192,22 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  * accumulated exactly in fixed point (see sb_hist_exponents) and written as
  * fp64.  Nodes not in the build list are left untouched.
  *
- * The rows are read from one of two sources:
+ * The bins come from one of two sources, the sketch always from GH
+ * (row-major, ld_gh >= k+1, 16-byte aligned, n rows):
  * row_idx == NULL: node j's rows are the positions node_off[j] ..
- *           node_off[j+1] of the arrays bins4 (quad-major, ld4 >= n, 4-byte
- *           aligned) and GH (channel-major, ld_gh >= n); every load is
- *           coalesced.  rec may be NULL.
+ *           node_off[j+1]; their bins are read from bins4 (quad-major,
+ *           ld4 >= n, 4-byte aligned).  Every load covers contiguous rows.
+ *           rec may be NULL.
  * row_idx != NULL: node j's rows are row_idx[node_off[j] .. node_off[j+1]),
- *           each < n, read from their row records (rec, ld_rec, rec_gh; the
- *           sketch must have been written into them by sb_sketch): one record
- *           per row.  bins4 and GH may be NULL.
+ *           each < n; their bins are read from the row records (rec,
+ *           ld_rec): one record per row.  bins4 may be NULL.
  * k, qexp   sketch columns and the exponents from sb_sketch.
  * node_off  n_nodes+1 offsets.
  * build_list  n_build node ids to build (NULL = every node; n_build ignored).
  * H         out: [n_nodes][m][k+1][n_bins] fp64.
  */
-int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t rec_gh,
-                            int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
+                            int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
                             const int32_t* qexp, const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                             const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
                             void* stream);
@@ -271,14 +265,13 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
 /*
  * sb_grow_tree -- the whole level loop for one tree (depth-wise growth).
  *
- * Runs, for level l = 0..depth-1: histograms (all rows at l = 0, read from
- * bins4 and GH; from l = 1 on, the smaller child of each pair, read from the
- * row records), sibling subtraction (fused into the histogram reduction),
+ * Runs, for level l = 0..depth-1: histograms (all rows at l = 0, bins read
+ * from bins4; from l = 1 on, the smaller child of each pair, bins read from
+ * the row records), sibling subtraction (fused into the histogram reduction),
  * scoring and partition, entirely on the device with no host
  * synchronisation.
  * bins4 / bins_cm / rec hold the same binned features in the three layouts;
- * GH (channel-major) and the sketch inside rec come from one sb_sketch call;
- * qexp from the same call.
+ * GH (row-major) and qexp come from sb_sketch.
  * tree_feature, tree_bin, tree_score: out, 2^depth - 1 entries in level
  *   order (node j of level l at index 2^l - 1 + j).
  * row_idx_out: out, n rows grouped by leaf; leaf_off_out: out, 2^depth + 1
@@ -287,8 +280,8 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
  * 1 <= depth <= 12.
  */
 int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm, int64_t ld_cm, const uint8_t* rec,
-                     int64_t ld_rec, int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH,
-                     int64_t ld_gh, int32_t k, const int32_t* qexp, int32_t depth, double lambda,
+                     int64_t ld_rec, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
+                     int32_t k, const int32_t* qexp, int32_t depth, double lambda,
                      double min_child_weight, int32_t* tree_feature, int32_t* tree_bin, double* tree_score,
                      int32_t* row_idx_out, int32_t* leaf_off_out, void* ws, int64_t ws_bytes, void* stream);
 

@@ -62,16 +62,15 @@ _PROTOS = {
     "sb_abi_version": (_I32, []),
     "sb_workspace_bytes": (_I64, [_I32, _I64, _I32, _I32, _I32, _I32, _I32, _I32]),
     "sb_layout_bins": (_I32, [_P, _I64, _I32, _I64, _P, _I64, _P, _I64, _P, _I64, _P]),
-    "sb_sketch": (_I32, [_I32, _P, _I64, _I32, _I64, _P, _I32, _P, _P, _P, _I64, _P, _I64, _I64, _P, _P, _P, _P, _P,
-                         _I64, _P]),
+    "sb_sketch": (_I32, [_I32, _P, _I64, _I32, _I64, _P, _I32, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _I64, _P]),
     "sb_hist_exponents": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I64, _P]),
-    "sb_build_histograms": (_I32, [_P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _I32,
-                                   _P, _I32, _P, _P, _I64, _P]),
+    "sb_build_histograms": (_I32, [_P, _I64, _P, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _P, _P, _I32, _P,
+                                   _I32, _P, _P, _I64, _P]),
     "sb_subtract_histograms": (_I32, [_P, _P, _I32, _I32, _I32, _I32, _P, _P]),
     "sb_score_splits": (_I32, [_P, _I32, _I32, _I32, _I32, _F64, _F64, _P, _P, _P, _P, _I64, _P]),
     "sb_partition_rows": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _I64, _P]),
-    "sb_grow_tree": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _I32, _F64,
-                            _F64, _P, _P, _P, _P, _P, _P, _I64, _P]),
+    "sb_grow_tree": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _I32, _F64, _F64,
+                            _P, _P, _P, _P, _P, _P, _I64, _P]),
 }
 
 _PROTOS["sb_profile_begin"] = (_I32, [])
@@ -139,23 +138,21 @@ def sb_layout_bins(bins, n, m, ld_bins, bins4, ld4, bins_cm, ld_cm, rec, ld_rec,
                                         ld_rec, _stream(stream)))
 
 
-def sb_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, rec, ld_rec, rec_gh, cols, scales, norm2, qexp, ws,
-              ws_bytes, stream=None):
+def sb_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws, ws_bytes, stream=None):
     return _check(load().sb_sketch(kind, _ptr(G), n, d, ld_g, _ptr(h), k, _ptr(u), _ptr(Pi), _ptr(GH), ld_gh,
-                                   _ptr(rec), ld_rec, rec_gh, _ptr(cols), _ptr(scales), _ptr(norm2), _ptr(qexp),
-                                   _ptr(ws), ws_bytes, _stream(stream)))
+                                   _ptr(cols), _ptr(scales), _ptr(norm2), _ptr(qexp), _ptr(ws), ws_bytes,
+                                   _stream(stream)))
 
 
 def sb_hist_exponents(GH, n, ld_gh, k, qexp, ws, ws_bytes, stream=None):
     return _check(load().sb_hist_exponents(_ptr(GH), n, ld_gh, k, _ptr(qexp), _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def sb_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off,
-                        n_nodes, build_list, n_build, H, ws, ws_bytes, stream=None):
-    return _check(load().sb_build_histograms(_ptr(bins4), ld4, _ptr(rec), ld_rec, rec_gh, n, m, n_bins, _ptr(GH),
-                                             ld_gh, k, _ptr(qexp), _ptr(row_idx), _ptr(node_off), n_nodes,
-                                             _ptr(build_list), n_build, _ptr(H), _ptr(ws), ws_bytes,
-                                             _stream(stream)))
+def sb_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
+                        build_list, n_build, H, ws, ws_bytes, stream=None):
+    return _check(load().sb_build_histograms(_ptr(bins4), ld4, _ptr(rec), ld_rec, n, m, n_bins, _ptr(GH), ld_gh, k,
+                                             _ptr(qexp), _ptr(row_idx), _ptr(node_off), n_nodes, _ptr(build_list),
+                                             n_build, _ptr(H), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def sb_subtract_histograms(H_parent, H_child, n_parents, m, n_bins, k, build_list, stream=None):
@@ -177,10 +174,10 @@ def sb_partition_rows(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, be
                                            _stream(stream)))
 
 
-def sb_grow_tree(bins4, ld4, bins_cm, ld_cm, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, depth, lam,
+def sb_grow_tree(bins4, ld4, bins_cm, ld_cm, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, depth, lam,
                  min_child_weight, tree_feature, tree_bin, tree_score, row_idx_out, leaf_off_out, ws, ws_bytes,
                  stream=None):
-    return _check(load().sb_grow_tree(_ptr(bins4), ld4, _ptr(bins_cm), ld_cm, _ptr(rec), ld_rec, rec_gh, n, m, n_bins,
+    return _check(load().sb_grow_tree(_ptr(bins4), ld4, _ptr(bins_cm), ld_cm, _ptr(rec), ld_rec, n, m, n_bins,
                                       _ptr(GH), ld_gh, k, _ptr(qexp), depth, lam, min_child_weight,
                                       _ptr(tree_feature), _ptr(tree_bin), _ptr(tree_score), _ptr(row_idx_out),
                                       _ptr(leaf_off_out), _ptr(ws), ws_bytes, _stream(stream)))

@@ -98,11 +98,16 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   return L;
 }
 
-int32_t check_rec(const char* call, const void* rec, int64_t ld_rec, int64_t rec_gh, int32_t m, int32_t k) {
-  if (!aligned(rec, 16) || ld_rec % 16 != 0 || rec_gh % 4 != 0 || rec_gh < m || rec_gh + 4ll * (k + 1) > ld_rec)
-    return fail(SB_E_SHAPE, std::string(call) +
-                                ": row records need a 16-byte aligned base, ld_rec % 16 == 0, rec_gh % 4 == 0, "
-                                "rec_gh >= m and rec_gh + 4(k+1) <= ld_rec");
+int32_t check_rec(const char* call, const void* rec, int64_t ld_rec, int32_t m) {
+  if (!aligned(rec, 16) || ld_rec % 16 != 0 || ld_rec < m)
+    return fail(SB_E_SHAPE, std::string(call) + ": row records need a 16-byte aligned base, ld_rec % 16 == 0 and "
+                                                "ld_rec >= m");
+  return SB_OK;
+}
+
+int32_t check_gh(const char* call, const void* GH, int64_t ld_gh, int32_t k) {
+  if (!aligned(GH, 16) || ld_gh < k + 1)
+    return fail(SB_E_SHAPE, std::string(call) + ": GH needs a 16-byte aligned base and ld_gh >= k + 1 (row-major)");
   return SB_OK;
 }
 
@@ -209,9 +214,8 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
 }
 
 int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                  const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
-                  int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
-                  int64_t ws_bytes, void* stream) {
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
   if (kind < SB_SKETCH_TOP_OUTPUTS || kind > SB_SKETCH_IDENTITY)
     return fail(SB_E_UNSUPPORTED, "sb_sketch: unknown sketch kind " + std::to_string(kind));
   if (!G || !h || !GH || !qexp) return fail(SB_E_ARG, "sb_sketch: G, h, GH and qexp must not be NULL");
@@ -219,9 +223,8 @@ int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld
   if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_sketch: d must be in [1, 65535]");
   if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_sketch: k must be in [1, 255]");
   if (ld_g < n) return fail(SB_E_SHAPE, "sb_sketch: ld_g must be >= n");
-  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_sketch: ld_gh must be >= n (GH is channel-major)");
-  if (rec) {
-    const int32_t rr = check_rec("sb_sketch", rec, ld_rec, rec_gh, 0, k);
+  {
+    const int32_t rr = check_gh("sb_sketch", GH, ld_gh, k);
     if (rr) return rr;
   }
   switch (kind) {
@@ -243,8 +246,8 @@ int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld
   }
   int32_t rc = need_ws(ws, ws_bytes, sketch_ws_bytes(kind, n, d, k), "sb_sketch");
   if (rc) return rc;
-  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, rec, ld_rec, rec_gh, cols, scales, norm2, qexp,
-                       ws, static_cast<hipStream_t>(stream));
+  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws,
+                       static_cast<hipStream_t>(stream));
 }
 
 int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
@@ -252,30 +255,32 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
   if (!GH || !qexp) return fail(SB_E_ARG, "sb_hist_exponents: GH and qexp must not be NULL");
   if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_hist_exponents: n must be in [1, 2^31)");
   if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_hist_exponents: k must be in [1, 255]");
-  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_hist_exponents: ld_gh must be >= n (GH is channel-major)");
+  if (ld_gh < k + 1) return fail(SB_E_SHAPE, "sb_hist_exponents: ld_gh must be >= k + 1 (GH is row-major)");
   int32_t rc = need_ws(ws, ws_bytes, hist_exponents_ws_bytes(k), "sb_hist_exponents");
   if (rc) return rc;
   return launch_hist_exponents(GH, n, ld_gh, k, qexp, ws, static_cast<hipStream_t>(stream));
 }
 
-int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t rec_gh,
-                            int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
+                            int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
                             const int32_t* qexp, const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                             const int32_t* build_list, int32_t n_build, double* H, void* ws, int64_t ws_bytes,
                             void* stream) {
   const char* call = "sb_build_histograms";
-  if (!qexp || !node_off || !H) return fail(SB_E_ARG, "sb_build_histograms: qexp, node_off and H must not be NULL");
+  if (!GH || !qexp || !node_off || !H)
+    return fail(SB_E_ARG, "sb_build_histograms: GH, qexp, node_off and H must not be NULL");
   int32_t rc = check_hist_shape(call, n, m, n_bins, k);
+  if (rc) return rc;
+  rc = check_gh(call, GH, ld_gh, k);
   if (rc) return rc;
   if (row_idx) {
     if (!rec) return fail(SB_E_ARG, "sb_build_histograms: rows through row_idx are read from rec, which is NULL");
-    rc = check_rec(call, rec, ld_rec, rec_gh, m, k);
+    rc = check_rec(call, rec, ld_rec, m);
     if (rc) return rc;
   } else {
-    if (!bins4 || !GH) return fail(SB_E_ARG, "sb_build_histograms: without row_idx, bins4 and GH must not be NULL");
+    if (!bins4) return fail(SB_E_ARG, "sb_build_histograms: without row_idx, bins4 must not be NULL");
     if (ld4 < n || !aligned(bins4, 4))
       return fail(SB_E_SHAPE, "sb_build_histograms: bins4 needs ld4 >= n and a 4-byte aligned base");
-    if (ld_gh < n) return fail(SB_E_SHAPE, "sb_build_histograms: ld_gh must be >= n (GH is channel-major)");
   }
   if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, "sb_build_histograms: n_nodes must be in [1, 2^20]");
   if (build_list == nullptr) n_build = n_nodes;
@@ -285,8 +290,8 @@ int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* r
     return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) cells exceed the LDS budget");
   rc = need_ws(ws, ws_bytes, hist_ws_bytes(m, n_bins, k, n_build), call);
   if (rc) return rc;
-  return launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off,
-                                 n_nodes, build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
+  return launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
+                                 build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
 }
 
 int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t n_parents, int32_t m,
@@ -342,8 +347,8 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
 }
 
 int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm, int64_t ld_cm, const uint8_t* rec,
-                     int64_t ld_rec, int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH,
-                     int64_t ld_gh, int32_t k, const int32_t* qexp, int32_t depth, double lambda,
+                     int64_t ld_rec, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
+                     int32_t k, const int32_t* qexp, int32_t depth, double lambda,
                      double min_child_weight, int32_t* tree_feature, int32_t* tree_bin, double* tree_score,
                      int32_t* row_idx_out, int32_t* leaf_off_out, void* ws, int64_t ws_bytes, void* stream) {
   const char* call = "sb_grow_tree";
@@ -356,9 +361,10 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   if (ld4 < n || !aligned(bins4, 4))
     return fail(SB_E_SHAPE, "sb_grow_tree: bins4 needs ld4 >= n and a 4-byte aligned base");
   if (ld_cm < n) return fail(SB_E_SHAPE, "sb_grow_tree: ld_cm must be >= n");
-  rc = check_rec(call, rec, ld_rec, rec_gh, m, k);
+  rc = check_rec(call, rec, ld_rec, m);
   if (rc) return rc;
-  if (ld_gh < n) return fail(SB_E_SHAPE, "sb_grow_tree: ld_gh must be >= n (GH is channel-major)");
+  rc = check_gh(call, GH, ld_gh, k);
+  if (rc) return rc;
   if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_grow_tree: lambda must be > 0");
   if (!(min_child_weight >= 0.0) || !std::isfinite(min_child_weight))
     return fail(SB_E_ARG, "sb_grow_tree: min_child_weight must be >= 0");
@@ -395,11 +401,11 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     // partition (from k_root_offsets at the root), and the reduce writes the
     // siblings by subtraction from the previous level
     if (l == 0) {
-      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l,
-                                   1, nullptr, 1, Hcur, cws, st, pre, nullptr);
+      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
+                                   nullptr, 1, Hcur, cws, st, pre, nullptr);
     } else {
-      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, rec_gh, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l,
-                                   nn, level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1]);
+      rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
+                                   level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1]);
     }
     if (rc) return rc;
     const int64_t base = (int64_t(1) << l) - 1;

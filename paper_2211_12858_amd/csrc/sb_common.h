@@ -59,17 +59,16 @@ int32_t launch_layout(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins
                       uint8_t* bins_cm, int64_t ld_cm, uint8_t* rec, int64_t ld_rec, hipStream_t st);
 
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                      const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
-                      int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
-                      hipStream_t st);
+                      const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                      double* norm2, int32_t* qexp, void* ws, hipStream_t st);
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k);
 int64_t hist_exponents_ws_bytes(int32_t k);
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
                               hipStream_t st);
 
-int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec,
-                                int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
-                                int32_t k, const int32_t* qexp,
+int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
+                                int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+                                const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
                                 const int64_t* pre_given = nullptr, const double* H_parent = nullptr);

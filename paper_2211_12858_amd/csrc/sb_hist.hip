@@ -21,9 +21,10 @@
 //    independent of the grid and of the order of the atomics) and writes the
 //    fp64 histogram.  Sums of fixed-point values are exact in fp64, which
 //    makes sibling subtraction exact as well.
-// Rows come either as positions of contiguous data (quad-major bins and a
-// channel-major sketch: every load is 256 contiguous bytes per wave) or
-// through row indices from the row records (one record line per row).
+// Rows come either as positions of contiguous data (quad-major bins: 256
+// contiguous bytes per wave and word) or through row indices from the row
+// records (one record line per row); the sketch is read from its row-major
+// records (whole 32-byte sectors) in both cases.
 // Workgroups that share a row range but own different slices are placed on
 // the same XCD (dispatch is round-robin over the 8 XCDs by block index) so
 // the rows they all read stay in that XCD's L2.
@@ -73,7 +74,7 @@ struct HistArgs {
   const float* GH;
   int64_t ld_gh;
   const uint8_t* rec;
-  int64_t ld_rec, rec_gh;
+  int64_t ld_rec;
   const int32_t* qexp;
   const int32_t* row_idx;
   const int32_t* node_off;
@@ -229,41 +230,38 @@ __device__ inline void load_run(const uint32_t* p, uint32_t* out) {
 
 // EXACT: CMAX channels and NQMAX quads exactly (no per-element tests, so the
 // load path has no branches and the compiler can count outstanding loads).
-// Lanes without a row load row 0 and never use the data.  FROM_REC: the row
-// is read from its record (bins at byte 0, sketch at byte rec_gh), else from
-// the quad-major bins and the channel-major sketch.
+// Lanes without a row load row 0 and never use the data.  FROM_REC: the bins
+// are read from the row's record, else from the quad-major bins; the sketch
+// values always come from the row's row-major GH record.
 template <int CMAX, int NQMAX, bool EXACT, bool FROM_REC>
 __device__ inline void load_row(const HistArgs& a, RowRef ref, int f0, int nq, int c, RowData<CMAX, NQMAX>& d) {
   int64_t row = ref.on ? (int64_t)ref.raw : 0;
   row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
+  const uint32_t* gp = reinterpret_cast<const uint32_t*>(a.GH + row * a.ld_gh);
   if constexpr (FROM_REC) {
-    const uint8_t* r = a.rec + row * a.ld_rec;
-    const uint32_t* wp = reinterpret_cast<const uint32_t*>(r) + (f0 >> 2);
-    const uint32_t* gp = reinterpret_cast<const uint32_t*>(r + a.rec_gh);
+    const uint32_t* wp = reinterpret_cast<const uint32_t*>(a.rec + row * a.ld_rec) + (f0 >> 2);
     if constexpr (EXACT) {
-      // both runs lie in the row's record: a few wide loads instead of one per word
       load_run<NQMAX>(wp, d.word);
-      uint32_t gw[CMAX];
-      load_run<CMAX>(gp, gw);
-#pragma unroll
-      for (int t = 0; t < CMAX; ++t) d.g[t] = __uint_as_float(gw[t]);
     } else {
 #pragma unroll
       for (int qq = 0; qq < NQMAX; ++qq)
         if (qq < nq) d.word[qq] = wp[qq];
-#pragma unroll
-      for (int t = 0; t < CMAX; ++t)
-        if (t < c) d.g[t] = __uint_as_float(gp[t]);
     }
   } else {
     const uint32_t* wp = a.bins4 + (int64_t)(f0 >> 2) * a.ld4 + row;
 #pragma unroll
     for (int qq = 0; qq < NQMAX; ++qq)
       if (EXACT || qq < nq) d.word[qq] = wp[(int64_t)qq * a.ld4];
-    const float* ghr = a.GH + row;
+  }
+  if constexpr (EXACT) {
+    uint32_t gw[CMAX];
+    load_run<CMAX>(gp, gw);
+#pragma unroll
+    for (int t = 0; t < CMAX; ++t) d.g[t] = __uint_as_float(gw[t]);
+  } else {
 #pragma unroll
     for (int t = 0; t < CMAX; ++t)
-      if (EXACT || t < c) d.g[t] = ghr[(int64_t)t * a.ld_gh];
+      if (t < c) d.g[t] = __uint_as_float(gp[t]);
   }
 }
 
@@ -515,9 +513,9 @@ k_subtract(const double* __restrict__ Hp, double* __restrict__ Hc, int64_t cpn, 
 
 }  // namespace
 
-int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec,
-                                int64_t rec_gh, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,
-                                int32_t k, const int32_t* qexp,
+int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
+                                int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
+                                const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
                                 const int64_t* pre_given, const double* H_parent) {
@@ -527,7 +525,6 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.ld4 = ld4;
   a.rec = rec;
   a.ld_rec = ld_rec;
-  a.rec_gh = rec_gh;
   a.GH = GH;
   a.ld_gh = ld_gh;
   a.qexp = qexp;

@@ -5,10 +5,10 @@
 //       p_j proportional to it).
 //   k_select   : Top Outputs ranks, Random Sampling inverse-CDF draws from
 //       given uniforms, identity.
-//   k_pack     : GH[t, i] = fp32(G[i, col_t] * scale_t), GH[k, i] = h_i
-//       (channel-major, optionally also into the row records), plus per-block
-//       maxima of |value| for the fixed-point histogram exponents.
-//   k_project  : GH[0:k, i] = (G Pi)[i, :] (Section 3.3), fp32 accumulation.
+//   k_pack     : GH[i, t] = fp32(G[i, col_t] * scale_t), GH[i, k] = h_i
+//       (row-major, rows written whole), plus per-block maxima of |value|
+//       for the fixed-point histogram exponents.
+//   k_project  : GH[i, 0:k] = (G Pi)[i, :] (Section 3.3), fp32 accumulation.
 //   k_qexp     : per-channel maximum over the blocks and the exponents.
 //
 // G is column-major, so every kernel reads whole columns with lanes on
@@ -52,10 +52,24 @@ k_colnorm_partial(const float* __restrict__ G, int64_t n, int64_t ld, int parts,
   if (i0 >= i1) {
     // empty chunk: contributes zero
   } else if ((((uintptr_t)(col + i0)) & 15) == 0) {
+    // four 16-byte loads in flight per thread; fixed summation order
     const int64_t nv = (i1 - i0) >> 2;
     const float4* v4 = reinterpret_cast<const float4*>(col + i0);
-    for (int64_t q = threadIdx.x; q < nv; q += NORM_THREADS) {
-      float4 x = v4[q];
+    int64_t q = threadIdx.x;
+    for (; q + 3 * NORM_THREADS < nv; q += 4 * NORM_THREADS) {
+      float4 x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = v4[q + u * NORM_THREADS];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        acc += (double)x[u].x * x[u].x;
+        acc += (double)x[u].y * x[u].y;
+        acc += (double)x[u].z * x[u].z;
+        acc += (double)x[u].w * x[u].w;
+      }
+    }
+    for (; q < nv; q += NORM_THREADS) {
+      const float4 x = v4[q];
       acc += (double)x.x * x.x;
       acc += (double)x.y * x.y;
       acc += (double)x.z * x.z;
@@ -164,79 +178,70 @@ __device__ inline uint32_t block_max_u32(uint32_t v, uint32_t* sh) {
 
 constexpr int PACK_THREADS = 256;
 constexpr int64_t PACK_ROWS_PER_BLOCK = PACK_THREADS;  // one row per thread per pass
-constexpr int PACK_CG = 16;                            // channels staged in LDS per record write
+constexpr int PACK_CG = 16;                            // floats of a row written per pass
 // Grid cap of the sketch kernels: block b writes its per-channel maxima to
 // blockmax[b*(k+1) + t], reduced afterwards by k_qexp (no atomics).
 constexpr int SKETCH_MAX_BLOCKS = 2048;
 
-// Copy of channels [g0, g0 + gn) of rows [base, base + PACK_THREADS) from the
-// LDS stage into the row records: consecutive lanes write consecutive floats
-// of one record, so a wave's store covers whole records instead of one float
-// in each of 64 lines.
-__device__ inline void pack_records(const float (*stage)[PACK_THREADS], int64_t base, int64_t n, int g0, int gn,
-                                    uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh) {
-  for (int e = threadIdx.x; e < gn * PACK_THREADS; e += PACK_THREADS) {
-    const int r = e / gn, tt = e - r * gn;
-    const int64_t i = base + r;
-    if (i < n) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (g0 + tt)) = stage[tt][r];
+// The floats g0..g0+gn-1 of row i, 16-byte stores when the row allows (every
+// row of a multiple-of-4 stride starts 16-byte aligned).
+__device__ inline void store_row_run(float* dst, const float* v, int gn, bool vec4) {
+  if (vec4 && (gn & 3) == 0) {
+#pragma unroll
+    for (int t4 = 0; t4 < PACK_CG / 4; ++t4)
+      if (4 * t4 < gn)
+        reinterpret_cast<float4*>(dst)[t4] = make_float4(v[4 * t4], v[4 * t4 + 1], v[4 * t4 + 2], v[4 * t4 + 3]);
+  } else {
+#pragma unroll
+    for (int tt = 0; tt < PACK_CG; ++tt)
+      if (tt < gn) dst[tt] = v[tt];
   }
 }
 
-// Channel t of the sketch: GH[t*ld_gh + i] = fp32(G[i, cols[t]] * scales[t]),
-// channel k = h.  Lanes on consecutive rows: coalesced column reads and
-// channel-major writes.  The optional row-record copy (float t of row i at
-// rec + i*ld_rec + rec_gh + 4t) goes through an LDS stage of PACK_CG channels.
+// Row-major sketch: GH[i*ld_gh + t] = fp32(G[i, cols[t]] * scales[t]) for
+// t < k, h_i for t = k, 0 after that.  One row per thread: the column reads
+// are coalesced across the wave and every row is written whole (with
+// ld_gh % 8 == 0, whole 32-byte sectors, so no partial-sector writes).
 __global__ void __launch_bounds__(PACK_THREADS)
 k_pack(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float* __restrict__ h, int k,
        const int32_t* __restrict__ cols, const float* __restrict__ scales, float* __restrict__ GH, int64_t ld_gh,
-       uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+       uint32_t* __restrict__ blockmax) {
   __shared__ uint32_t sh[PACK_THREADS / 64];
-  __shared__ float stage[PACK_CG][PACK_THREADS];
-  __shared__ uint32_t smax[PACK_CG];
-  for (int g0 = 0; g0 <= k; g0 += PACK_CG) {
-    const int gn = (k + 1 - g0 < PACK_CG) ? k + 1 - g0 : PACK_CG;
+  const bool vec4 = (ld_gh & 3) == 0;
+  for (int g0 = 0; g0 < ld_gh; g0 += PACK_CG) {
+    const int gn = (ld_gh - g0 < PACK_CG) ? (int)(ld_gh - g0) : PACK_CG;
     uint32_t mx[PACK_CG];
 #pragma unroll
     for (int tt = 0; tt < PACK_CG; ++tt) mx[tt] = 0u;
     for (int64_t base = (int64_t)blockIdx.x * PACK_ROWS_PER_BLOCK; base < n;
          base += (int64_t)gridDim.x * PACK_ROWS_PER_BLOCK) {
       const int64_t i = base + threadIdx.x;
+      if (i >= n) continue;
+      float v[PACK_CG];
 #pragma unroll
       for (int tt = 0; tt < PACK_CG; ++tt) {
         const int t = g0 + tt;
-        if (tt < gn) {
-          float v = 0.0f;
-          if (i < n) {
-            if (t < k) {
-              const int col = cols[t];
-              // -1 marks an all-zero sketch column
-              v = (col < 0 || col >= d) ? 0.0f : G[(int64_t)col * ld_g + i] * scales[t];
-            } else {
-              v = h[i];
-            }
-            GH[(int64_t)t * ld_gh + i] = v;
-            const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
-            mx[tt] = a > mx[tt] ? a : mx[tt];
-          }
-          stage[tt][threadIdx.x] = v;
+        float x = 0.0f;
+        if (tt < gn && t < k) {
+          const int col = cols[t];
+          // -1 marks an all-zero sketch column
+          x = (col < 0 || col >= d) ? 0.0f : G[(int64_t)col * ld_g + i] * scales[t];
+        } else if (tt < gn && t == k) {
+          x = h[i];
         }
+        v[tt] = x;
+        const uint32_t a = __float_as_uint(x) & 0x7fffffffu;
+        mx[tt] = a > mx[tt] ? a : mx[tt];
       }
-      if (rec) {
-        __syncthreads();
-        pack_records(stage, base, n, g0, gn, rec, ld_rec, rec_gh);
-        __syncthreads();
-      }
+      store_row_run(GH + i * ld_gh + g0, v, gn, vec4);
     }
 #pragma unroll
     for (int tt = 0; tt < PACK_CG; ++tt) {
-      if (tt < gn) {
+      if (tt < gn && g0 + tt <= k) {
         const uint32_t r = block_max_u32<PACK_THREADS>(mx[tt], sh);
-        if (threadIdx.x == 0) smax[tt] = r;
+        if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + g0 + tt] = r;
       }
     }
-    __syncthreads();
-    for (int tt = threadIdx.x; tt < gn; tt += PACK_THREADS) blockmax[(int64_t)blockIdx.x * (k + 1) + g0 + tt] = smax[tt];
-    __syncthreads();
   }
 }
 
@@ -253,8 +258,7 @@ constexpr int PROJ_LDS_FLOATS = 32768;    // 128 KB: the Pi block staged per pas
 template <int KT>
 __global__ void __launch_bounds__(PROJ_THREADS)
 k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k, int t0,
-          float* __restrict__ GH, int64_t ld_gh, uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh,
-          uint32_t* __restrict__ blockmax) {
+          float* __restrict__ GH, int64_t ld_gh, uint32_t* __restrict__ blockmax) {
   extern __shared__ float sPi[];  // [jc][KT]
   __shared__ uint32_t sh[PROJ_THREADS / 64];
   const int kt = (k - t0 < KT) ? k - t0 : KT;
@@ -304,8 +308,7 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
 #pragma unroll
       for (int t = 0; t < KT; ++t) {
         if (t < kt) {
-          GH[(int64_t)(t0 + t) * ld_gh + i] = acc[t];
-          if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * (t0 + t)) = acc[t];
+          GH[i * ld_gh + t0 + t] = acc[t];
           const uint32_t a = __float_as_uint(acc[t]) & 0x7fffffffu;
           mx[t] = a > mx[t] ? a : mx[t];
         }
@@ -321,17 +324,17 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
   }
 }
 
-// The hessian channel of a projected sketch: GH[k*ld_gh + i] = h[i] (and the
-// record copy), with its per-block maximum.
+// The hessian channel of a projected sketch, GH[i*ld_gh + k] = h[i], and the
+// zero padding of the row after it, with the channel's per-block maximum.
 __global__ void __launch_bounds__(256)
 k_project_h(const float* __restrict__ h, int64_t n, int k, float* __restrict__ GH, int64_t ld_gh,
-            uint8_t* __restrict__ rec, int64_t ld_rec, int64_t rec_gh, uint32_t* __restrict__ blockmax) {
+            uint32_t* __restrict__ blockmax) {
   __shared__ uint32_t sh[4];
   uint32_t mx = 0u;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
     const float v = h[i];
-    GH[(int64_t)k * ld_gh + i] = v;
-    if (rec) *reinterpret_cast<float*>(rec + i * ld_rec + rec_gh + 4 * k) = v;
+    GH[i * ld_gh + k] = v;
+    for (int64_t t = k + 1; t < ld_gh; ++t) GH[i * ld_gh + t] = 0.0f;
     const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
     mx = a > mx ? a : mx;
   }
@@ -339,19 +342,32 @@ k_project_h(const float* __restrict__ h, int64_t n, int k, float* __restrict__ G
   if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = mx;
 }
 
-// Per-block max |GH[t*ld_gh + i]| for a caller-supplied channel-major GH.
+// Per-block max |GH[i*ld_gh + t]| for a caller-supplied row-major GH: one
+// row per thread, PACK_CG channels per pass.
 __global__ void __launch_bounds__(256)
 k_maxabs(const float* __restrict__ GH, int64_t n, int64_t ld_gh, int c, uint32_t* __restrict__ blockmax) {
   __shared__ uint32_t sh[4];
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  for (int t = 0; t < c; ++t) {
-    uint32_t mx = 0u;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += stride) {
-      const uint32_t a = __float_as_uint(GH[(int64_t)t * ld_gh + i]) & 0x7fffffffu;
-      mx = a > mx ? a : mx;
+  for (int g0 = 0; g0 < c; g0 += PACK_CG) {
+    const int gn = (c - g0 < PACK_CG) ? c - g0 : PACK_CG;
+    uint32_t mx[PACK_CG];
+#pragma unroll
+    for (int tt = 0; tt < PACK_CG; ++tt) mx[tt] = 0u;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+#pragma unroll
+      for (int tt = 0; tt < PACK_CG; ++tt) {
+        if (tt < gn) {
+          const uint32_t a = __float_as_uint(GH[i * ld_gh + g0 + tt]) & 0x7fffffffu;
+          mx[tt] = a > mx[tt] ? a : mx[tt];
+        }
+      }
     }
-    mx = block_max_u32<256>(mx, sh);
-    if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * c + t] = mx;
+#pragma unroll
+    for (int tt = 0; tt < PACK_CG; ++tt) {
+      if (tt < gn) {
+        const uint32_t r = block_max_u32<256>(mx[tt], sh);
+        if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * c + g0 + tt] = r;
+      }
+    }
   }
 }
 
@@ -400,9 +416,8 @@ int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k) {
 int64_t hist_exponents_ws_bytes(int32_t k) { return align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4); }
 
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                      const double* u, const float* Pi, float* GH, int64_t ld_gh, uint8_t* rec, int64_t ld_rec,
-                      int64_t rec_gh, int32_t* cols, float* scales, double* norm2, int32_t* qexp, void* ws,
-                      hipStream_t st) {
+                      const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                      double* norm2, int32_t* qexp, void* ws, hipStream_t st) {
   const int P = norm_parts(n);
   char* w = static_cast<char*>(ws);
   double* part = reinterpret_cast<double*>(w);
@@ -425,14 +440,14 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
 #define SB_PROJ(K)                                                                                               \
   case K:                                                                                                        \
     hipLaunchKernelGGL((k_project<K>), dim3(nb), dim3(PROJ_THREADS), lds, st, G, n, d, ld_g, Pi, k, t0, GH, ld_gh, \
-                       rec, ld_rec, rec_gh, blockmax);                                                           \
+                       blockmax);                                                                                \
     break;
       switch (KT) {
         SB_PROJ(4) SB_PROJ(8) SB_PROJ(12) SB_PROJ(16) SB_PROJ(20) SB_PROJ(24) SB_PROJ(28) SB_PROJ(32)
       }
 #undef SB_PROJ
     }
-    hipLaunchKernelGGL(k_project_h, dim3(nb), dim3(256), 0, st, h, n, k, GH, ld_gh, rec, ld_rec, rec_gh, blockmax);
+    hipLaunchKernelGGL(k_project_h, dim3(nb), dim3(256), 0, st, h, n, k, GH, ld_gh, blockmax);
   } else {
     int64_t chunk = (n + P - 1) / P;
     chunk = (chunk + 3) & ~int64_t(3);
@@ -441,7 +456,7 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
     hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, n2, d, k, u, cols, scales, C);
     nb = sketch_blocks(n, 4 * PACK_ROWS_PER_BLOCK);
     hipLaunchKernelGGL(k_pack, dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, k, cols, scales, GH, ld_gh,
-                       rec, ld_rec, rec_gh, blockmax);
+                       blockmax);
   }
   hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
   return check_launch("sb_sketch");

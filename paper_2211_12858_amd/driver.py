@@ -8,12 +8,12 @@ the row-major bins):
   histogram kernel's lanes take consecutive rows and read contiguous words;
 * column-major bytes ``bins_cm[f, i]``: the partition reads one run of the
   split feature's column per node;
-* row records ``rec[i]`` of ``ld_rec`` bytes (one 128-byte line for 100
-  features and k = 5): the row's bins and, after each sketch, its k+1
-  sketch values; the histograms of the deeper levels read one record per
+* row records ``rec[i]`` of ``ld_rec`` bytes (one 128-byte line for up to
+  128 features): the histograms of the deeper levels read one record per
   row.
 
-The sketch itself lives channel-major in ``GH[t, i]``.  ``step()`` runs one
+The sketch lives row-major in ``GH[i, t]``, each row padded to a multiple of
+8 floats so that it fills whole 32-byte sectors.  ``step()`` runs one
 tree: the sketch (once per tree) and the depth-wise level loop, entirely on
 the device.  No computation happens in Python.
 """
@@ -33,10 +33,10 @@ def workspace(nbytes, device):
     return t
 
 
-def record_stride(m, c):
-    """Bytes per row record: bins, then c floats; a power of two up to 128
-    bytes (so that no record straddles a 128-byte line), else a multiple of 128."""
-    need = _round_up(m, 4) + 4 * c
+def record_stride(m):
+    """Bytes per row record: a power of two up to 128 bytes (so that no
+    record straddles a 128-byte line), else a multiple of 128."""
+    need = _round_up(m, 16)
     if need <= 128:
         s = 16
         while s < need:
@@ -54,8 +54,8 @@ class SplitSearch:
         self.device = dev = torch.device(device)
         n, m, c = self.n, self.m, self.c
         self.nq = (m + 3) // 4
-        self.rec_gh = _round_up(m, 4)
-        self.ld_rec = record_stride(m, c) if ld_rec is None else ld_rec
+        self.ld_rec = record_stride(m) if ld_rec is None else ld_rec
+        self.ld_gh = _round_up(c, 8)
         self.bins4 = torch.empty((self.nq, n), dtype=torch.int32, device=dev)
         self.bins_cm = torch.empty((m, n), dtype=torch.uint8, device=dev)
         self.rec = torch.zeros((n, self.ld_rec), dtype=torch.uint8, device=dev)
@@ -63,7 +63,7 @@ class SplitSearch:
         L.sb_layout_bins(rm, n, m, m, self.bins4, n, self.bins_cm, n, self.rec, self.ld_rec)
         torch.cuda.synchronize(dev)
         del rm
-        self.GH = torch.zeros((c, n), dtype=torch.float32, device=dev)
+        self.GH = torch.zeros((n, self.ld_gh), dtype=torch.float32, device=dev)
         self.qexp = torch.zeros(c, dtype=torch.int32, device=dev)
         self.cols = torch.zeros(k, dtype=torch.int32, device=dev)
         self.scales = torch.zeros(k, dtype=torch.float32, device=dev)
@@ -89,14 +89,14 @@ class SplitSearch:
             self._ws_sketch = workspace(need, self.device)
         if self.norm2 is None or self.norm2.numel() != d:
             self.norm2 = torch.zeros(d, dtype=torch.float64, device=self.device)
-        L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, n, self.rec, self.ld_rec, self.rec_gh, self.cols,
-                    self.scales, self.norm2, self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
+        L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, self.ld_gh, self.cols, self.scales, self.norm2,
+                    self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
 
     # ------------------------------------------------------------ tree
     def grow(self, stream=None):
         n = self.n
-        L.sb_grow_tree(self.bins4, n, self.bins_cm, n, self.rec, self.ld_rec, self.rec_gh, n, self.m, self.n_bins,
-                       self.GH, n, self.k, self.qexp, self.depth, self.lam, self.mcw, self.tree_feature,
+        L.sb_grow_tree(self.bins4, n, self.bins_cm, n, self.rec, self.ld_rec, n, self.m, self.n_bins, self.GH,
+                       self.ld_gh, self.k, self.qexp, self.depth, self.lam, self.mcw, self.tree_feature,
                        self.tree_bin, self.tree_score, self.row_idx, self.leaf_off, self.ws_tree,
                        self.ws_tree_bytes, stream)
 
@@ -107,12 +107,11 @@ class SplitSearch:
     # ------------------------------------------------------------ readback
     def gh(self):
         """The sketch as an (n, k+1) float32 host array."""
-        return np.ascontiguousarray(self.GH.cpu().numpy().T)
+        return np.ascontiguousarray(self.GH[:, :self.c].cpu().numpy())
 
-    def rec_gh_values(self):
-        """The sketch copy inside the row records, as an (n, k+1) float32 host array."""
-        raw = self.rec[:, self.rec_gh:self.rec_gh + 4 * self.c].contiguous()
-        return raw.view(torch.float32).cpu().numpy().reshape(self.n, self.c)
+    def gh_padding(self):
+        """The padding floats of the sketch rows (written as 0)."""
+        return self.GH[:, self.c:].cpu().numpy()
 
     def tree(self):
         """Host copies of the tree arrays, split per level."""

@@ -35,15 +35,12 @@ def quad_major(bins):
     return np.ascontiguousarray(pad.view("<u4").reshape(n, nq).T).view(np.int32)
 
 
-def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None, rec_stride=None, rec_gh=None):
-    """Returns (GH as (n, k+1), cols, scales, norm2, qexp[, GH copy read back from the records])."""
+def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None):
+    """Returns (GH as (n, k+1), cols, scales, norm2, qexp, the padding floats of the rows)."""
     d, n = G_T.shape
-    ld_gh = n if ld_gh is None else ld_gh
+    ld_gh = (k + 1 + 7) // 8 * 8 if ld_gh is None else ld_gh
     Gd, hd = up(G_T), up(h)
-    GH = torch.zeros((k + 1, ld_gh), dtype=torch.float32, device=DEV)
-    rec = None
-    if rec_stride is not None:
-        rec = torch.zeros((n, rec_stride), dtype=torch.uint8, device=DEV)
+    GH = torch.full((n, ld_gh), float("nan"), dtype=torch.float32, device=DEV)
     cols = torch.full((k,), -7, dtype=torch.int32, device=DEV)
     scales = torch.zeros(k, dtype=torch.float32, device=DEV)
     norm2 = torch.zeros(d, dtype=torch.float64, device=DEV)
@@ -51,15 +48,11 @@ def run_sketch(kind, G_T, h, k, u=None, Pi=None, ld_gh=None, rec_stride=None, re
     ws = workspace(L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=n, d=d, k=k), DEV)
     ud = up(u, torch.float64) if u is not None else None
     Pid = up(Pi, torch.float32) if Pi is not None else None
-    L.sb_sketch(L.KIND[kind], Gd, n, d, n, hd, k, ud, Pid, GH, ld_gh, rec, rec_stride or 0, rec_gh or 0, cols, scales,
-                norm2, qexp, ws, ws.numel())
+    L.sb_sketch(L.KIND[kind], Gd, n, d, n, hd, k, ud, Pid, GH, ld_gh, cols, scales, norm2, qexp, ws, ws.numel())
     sync()
-    out = (np.ascontiguousarray(GH[:, :n].cpu().numpy().T), cols.cpu().numpy(), scales.cpu().numpy(),
-           norm2.cpu().numpy(), qexp.cpu().numpy())
-    if rec is not None:
-        raw = rec[:, rec_gh:rec_gh + 4 * (k + 1)].contiguous().view(torch.float32).cpu().numpy()
-        out = out + (raw.reshape(n, k + 1),)
-    return out
+    g = GH.cpu().numpy()
+    return (np.ascontiguousarray(g[:, :k + 1]), cols.cpu().numpy(), scales.cpu().numpy(), norm2.cpu().numpy(),
+            qexp.cpu().numpy(), g[:, k + 1:])
 
 
 def qexp_rule(GH):
@@ -71,12 +64,13 @@ def qexp_rule(GH):
     return np.array(out, dtype=np.int32)
 
 
-def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None, ld_pad=0, ld_rec=None):
-    """Histograms through the C ABI (device layout [node][feature][channel][bin]); GH is an (n, k+1) host array.
+def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None, ld_pad=0, ld_rec=None, ld_gh=None):
+    """Histograms through the C ABI (device layout [node][feature][channel][bin]).
 
-    Without row_idx the data go up as quad-major bins and a channel-major
-    sketch (leading dimension n + ld_pad); with row_idx as row records of
-    ld_rec bytes (default: the smallest multiple of 16 that holds them).
+    GH is an (n, k+1) host array, uploaded row-major with ld_gh floats per
+    row (default: k+1 rounded up to 8).  Without row_idx the bins go up
+    quad-major (leading dimension n + ld_pad); with row_idx as row records of
+    ld_rec bytes (default: m rounded up to 16).
     """
     n, m = bins.shape
     c = GH.shape[1]
@@ -87,22 +81,21 @@ def run_hist(bins, GH, qexp, n_bins, row_idx, node_off, build_list=None, H=None,
                                         n_nodes=max(n_nodes, n_build)), DEV)
     if H is None:
         H = torch.full((n_nodes, m, c, n_bins), float("nan"), dtype=torch.float64, device=DEV)
-    b4 = gh = rec = None
+    ld_gh = (c + 7) // 8 * 8 if ld_gh is None else ld_gh
+    gh = np.zeros((n, ld_gh), dtype=np.float32)
+    gh[:, :c] = GH
+    b4 = rec = None
     ld = n + ld_pad
-    rec_gh = 0
     if row_idx is None:
         qm = quad_major(bins)
         b4 = np.zeros((qm.shape[0], ld), dtype=np.int32)
         b4[:, :n] = qm
-        gh = np.zeros((c, ld), dtype=np.float32)
-        gh[:, :n] = GH.T
-        b4, gh = up(b4), up(gh)
+        b4 = up(b4)
     else:
         if ld_rec is None:
-            ld_rec = ((m + 3) // 4 * 4 + 4 * c + 15) // 16 * 16
-        rec_np, rec_gh = make_records(bins, GH, ld_rec)
-        rec = up(rec_np)
-    L.sb_build_histograms(b4, ld, rec, ld_rec or 0, rec_gh, n, m, n_bins, gh, ld, k, up(qexp, torch.int32),
+            ld_rec = (m + 15) // 16 * 16
+        rec = up(make_records(bins, ld_rec))
+    L.sb_build_histograms(b4, ld, rec, ld_rec or 0, n, m, n_bins, up(gh), ld_gh, k, up(qexp, torch.int32),
                           None if row_idx is None else up(row_idx, torch.int32), up(node_off, torch.int32), n_nodes,
                           None if build_list is None else up(build_list, torch.int32), n_build, H, ws, ws.numel())
     sync()
@@ -160,12 +153,9 @@ def run_partition(bins, row_in, node_off, bf, bb):
     return row_out.cpu().numpy(), off_out.cpu().numpy(), bl_out.cpu().numpy()
 
 
-def make_records(bins, GH, ld_rec):
-    """Host row records: bins in bytes 0..m-1, the k+1 floats at byte round_up(m, 4)."""
+def make_records(bins, ld_rec):
+    """Host row records: the m bins of row i in bytes 0..m-1 of record i."""
     n, m = bins.shape
-    c = GH.shape[1]
-    rec_gh = (m + 3) // 4 * 4
     rec = np.zeros((n, ld_rec), dtype=np.uint8)
     rec[:, :m] = bins
-    rec[:, rec_gh:rec_gh + 4 * c] = np.ascontiguousarray(GH, dtype=np.float32).view(np.uint8).reshape(n, 4 * c)
-    return rec, rec_gh
+    return rec

@@ -78,8 +78,8 @@ F = FAKE
 
 
 def sketch_args(**kw):
-    a = dict(kind=0, G=F, n=100, d=10, ld_g=100, h=F, k=3, u=F, Pi=F, GH=F, ld_gh=100, rec=None, ld_rec=0, rec_gh=0,
-             cols=F, scales=F, norm2=F, qexp=F, ws=F, ws_bytes=1 << 30, stream=0)
+    a = dict(kind=0, G=F, n=100, d=10, ld_g=100, h=F, k=3, u=F, Pi=F, GH=F, ld_gh=8, cols=F, scales=F, norm2=F,
+             qexp=F, ws=F, ws_bytes=1 << 30, stream=0)
     a.update(kw)
     return list(a.values())
 
@@ -89,15 +89,13 @@ def sketch_args(**kw):
     (dict(G=None), 1),
     (dict(n=0), 1),
     (dict(k=0), 1),
-    (dict(k=11), 1),                 # top outputs needs k <= d
+    (dict(k=11, ld_gh=12), 1),       # top outputs needs k <= d
     (dict(ld_g=99), 2),
-    (dict(ld_gh=99), 2),             # channel-major GH needs ld_gh >= n
+    (dict(ld_gh=3), 2),              # row-major GH needs ld_gh >= k + 1
+    (dict(GH=F + 4), 2),             # GH rows need a 16-byte aligned base
     (dict(kind=1, u=None), 1),
     (dict(kind=2, Pi=None), 1),
     (dict(kind=3, k=4), 1),          # identity needs k == d
-    (dict(rec=F, ld_rec=24, rec_gh=0), 2),   # record stride not a multiple of 16
-    (dict(rec=F, ld_rec=16, rec_gh=4), 2),   # k+1 floats do not fit after rec_gh
-    (dict(rec=F + 4, ld_rec=32, rec_gh=0), 2),  # misaligned records
     (dict(ws_bytes=16), 1),
     (dict(ws=F + 8), 2),             # misaligned workspace
     (dict(ws=None), 1),
@@ -108,7 +106,7 @@ def test_sketch_rejects(L, kw, code):
 
 
 def hist_args(**kw):
-    a = dict(bins4=F, ld4=1000, rec=None, ld_rec=0, rec_gh=0, n=1000, m=10, n_bins=256, GH=F, ld_gh=1000, k=5, qexp=F,
+    a = dict(bins4=F, ld4=1000, rec=None, ld_rec=0, n=1000, m=10, n_bins=256, GH=F, ld_gh=8, k=5, qexp=F,
              row_idx=None, node_off=F, n_nodes=2, build_list=F, n_build=1, H=F, ws=F, ws_bytes=1 << 30, stream=0)
     a.update(kw)
     return list(a.values())
@@ -124,14 +122,14 @@ def hist_args(**kw):
     (dict(k=0), 1),
     (dict(ld4=999), 2),              # < n
     (dict(bins4=F + 2), 2),          # misaligned base
-    (dict(ld_gh=999), 2),
+    (dict(ld_gh=5), 2),              # fewer floats per row than channels
     (dict(GH=None), 1),
     (dict(row_idx=F), 1),            # rows through row_idx need the records
-    (dict(row_idx=F, rec=F, ld_rec=64, rec_gh=8), 2),   # bins overlap the sketch floats
-    (dict(row_idx=F, rec=F, ld_rec=40, rec_gh=12), 2),  # stride not a multiple of 16
+    (dict(row_idx=F, rec=F, ld_rec=8), 2),     # records shorter than m
+    (dict(row_idx=F, rec=F, ld_rec=40), 2),    # stride not a multiple of 16
     (dict(n_nodes=0), 1),
     (dict(n_build=3), 1),            # more than n_nodes
-    (dict(k=100), 3),                # LDS budget exceeded
+    (dict(k=100, ld_gh=104), 3),     # LDS budget exceeded
     (dict(ws_bytes=100), 1),
 ])
 def test_build_histograms_rejects(L, kw, code):
@@ -205,8 +203,8 @@ def test_layout_rejects(L, kw, code):
 
 
 def grow_args(**kw):
-    a = dict(bins4=F, ld4=1000, bins_cm=F, ld_cm=1000, rec=F, ld_rec=64, rec_gh=12, n=1000, m=10, n_bins=256, GH=F,
-             ld_gh=1000, k=5, qexp=F, depth=3, lam=1.0, mcw=0.0, tf=F, tb=F, ts=F, rows=F, leaf=F, ws=F,
+    a = dict(bins4=F, ld4=1000, bins_cm=F, ld_cm=1000, rec=F, ld_rec=16, n=1000, m=10, n_bins=256, GH=F,
+             ld_gh=8, k=5, qexp=F, depth=3, lam=1.0, mcw=0.0, tf=F, tb=F, ts=F, rows=F, leaf=F, ws=F,
              ws_bytes=1 << 34, stream=0)
     a.update(kw)
     return list(a.values())
@@ -219,9 +217,9 @@ def grow_args(**kw):
     (dict(depth=13), 1),
     (dict(ld_cm=10), 2),
     (dict(ld4=999), 2),
-    (dict(ld_gh=999), 2),
-    (dict(rec_gh=8), 2),
-    (dict(ld_rec=32), 2),
+    (dict(ld_gh=5), 2),
+    (dict(ld_rec=8), 2),
+    (dict(ld_rec=24), 2),
     (dict(lam=-1.0), 1),
     (dict(ws_bytes=1000), 1),
 ])

@@ -53,7 +53,7 @@ def test_fullsize_sketch_bit_exact(grown):
     wl, inp, ss, tree, GH_o, cols_o = grown
     assert np.array_equal(ss.cols.cpu().numpy(), cols_o)
     assert np.array_equal(ss.gh().view(np.uint32), GH_o.view(np.uint32))
-    assert np.array_equal(ss.rec_gh_values().view(np.uint32), GH_o.view(np.uint32))
+    assert not ss.gh_padding().any()
 
 
 def test_fullsize_partition_properties(grown):
@@ -114,7 +114,7 @@ def test_fullsize_root_histograms_sampled_features(grown):
     H = torch.full((1, m, c, B), float("nan"), dtype=torch.float64, device=gu.DEV)
     ws = workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=B, k=k, n_nodes=1), gu.DEV)
     off = gu.up(np.array([0, n], dtype=np.int32))
-    L.sb_build_histograms(ss.bins4, n, None, 0, 0, n, m, B, ss.GH, n, k, ss.qexp, None, off, 1, None, 1, H, ws,
+    L.sb_build_histograms(ss.bins4, n, None, 0, n, m, B, ss.GH, ss.ld_gh, k, ss.qexp, None, off, 1, None, 1, H, ws,
                           ws.numel())
     gu.sync()
     Hg = gu.host_layout(H.cpu().numpy())[0]
