@@ -29,7 +29,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
 METRIC = "sec per tree (depth 6) + histogram-build HBM GB/s (% of peak)"
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "hist_traffic.json")
-HIST_SRC = os.path.join(HERE, "paper_2211_12858_amd", "csrc", "sb_hist.hip")
+HIST_SRCS = [os.path.join(HERE, "paper_2211_12858_amd", "csrc", f) for f in ("sb_hist.hip", "sb_common.h")]
 
 
 def log(*a):
@@ -68,13 +68,21 @@ def hist_algorithmic_bytes(leaf_off, depth, m, n_bins, c):
     return per_launch
 
 
+def hist_source_hash():
+    """sha256 over the histogram kernel's source files (the traffic record is tied to it)."""
+    h = hashlib.sha256()
+    for f in HIST_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def traffic_for_current_kernel():
     """Counter-measured HBM bytes per histogram launch, if taken on this kernel source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
         rec = json.load(open(TRAFFIC_FILE))
-        src = hashlib.sha256(open(HIST_SRC, "rb").read()).hexdigest()
+        src = hist_source_hash()
         if rec.get("kernel_source_sha256") != src:
             return None
         return rec.get("bytes_per_launch")

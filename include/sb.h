@@ -173,11 +173,11 @@ int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld
  * sb_hist_exponents -- fixed-point exponents for a given GH (row-major).
  *
  * For channel t (t <= k) with M_t = max_i |GH[i*ld_gh + t]|:
- *   qexp[t] = 18 - floor(log2(M_t))   (qexp[t] = 0 if M_t == 0),
- * so every value maps to an integer rint(v * 2^qexp[t]) of magnitude <= 2^19.
+ *   qexp[t] = 17 - floor(log2(M_t))   (qexp[t] = 0 if M_t == 0),
+ * so every value maps to an integer rint(v * 2^qexp[t]) of magnitude <= 2^18.
  * sb_build_histograms accumulates those integers exactly and reports sums
  * times 2^-qexp[t]; each element therefore contributes an error of at most
- * half a quantum, 2^-(qexp[t]+1) <= 2^-19 M_t.  Exponents must stay fixed
+ * half a quantum, 2^-(qexp[t]+1) <= 2^-18 M_t.  Exponents must stay fixed
  * for every level of a tree so that sibling subtraction is exact.
  */
 int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,

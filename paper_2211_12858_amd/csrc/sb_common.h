@@ -16,12 +16,15 @@ int32_t fail(int32_t code, const std::string& msg);
 int32_t check_launch(const char* what);
 
 // ---------------------------------------------------------------- fixed point
-// Quantised magnitudes are <= 2^QBITS (qexp = QBITS-1 - floor(log2(max|v|))).
-constexpr int QBITS = 19;
-// LDS cells are int32 running sums read back into int64 every window; the
-// change between two reads spans at most two windows, so
-// 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
-constexpr int WINDOW_ROWS = 1536;
+// Quantised magnitudes are <= 2^QBITS (qexp = QBITS-1 - floor(log2(max|v|))),
+// so each value carries an error of at most 2^-(QBITS+1) of its channel's
+// maximum magnitude.
+constexpr int QBITS = 18;
+// Each channel's LDS sum is a 32-bit running sum read back into int64 every
+// window of WINDOW_ROWS rows (4 steps of the 768-thread workgroup).  A cell
+// gets at most one value per row, and the change between two reads spans at
+// most two windows, so 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
+constexpr int WINDOW_ROWS = 3072;
 static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point window overflow");
 
 // ---------------------------------------------------------------- histogram plan

@@ -60,7 +60,7 @@ def qexp_rule(GH):
     out = []
     for t in range(GH.shape[1]):
         mx = float(np.max(np.abs(GH[:, t].astype(np.float64)))) if GH.shape[0] else 0.0
-        out.append(18 - math.frexp(mx)[1] + 1 if mx > 0 else 0)
+        out.append(17 - math.frexp(mx)[1] + 1 if mx > 0 else 0)  # 17 - floor(log2 mx)
     return np.array(out, dtype=np.int32)
 
 
