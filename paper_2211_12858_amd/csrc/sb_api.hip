@@ -61,7 +61,7 @@ int32_t check_hist_shape(const char* call, int64_t n, int32_t m, int32_t n_bins,
 }
 
 struct GrowLayout {
-  int64_t H0, H1, rows_tmp, offs, blists, pre, call, total;
+  int64_t H0, H1, rows_tmp, offs, blists, pre, feat_s, feat_b, call, total;
 };
 
 GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth) {
@@ -92,6 +92,10 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   p += align256((int64_t(1) << depth) * 4);
   L.pre = p;
   p += align256((maxn + 1) * 8);
+  L.feat_s = p;
+  p += align256(maxn * m * 8);
+  L.feat_b = p;
+  p += align256(maxn * m * 4);
   L.call = p;
   p += call;
   L.total = p;
@@ -381,6 +385,11 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   int32_t* offs = reinterpret_cast<int32_t*>(w + G.offs);
   int32_t* blists = reinterpret_cast<int32_t*>(w + G.blists);
   int64_t* pre = reinterpret_cast<int64_t*>(w + G.pre);
+  double* feat_s = reinterpret_cast<double*>(w + G.feat_s);
+  int32_t* feat_b = reinterpret_cast<int32_t*>(w + G.feat_b);
+  // the fused level end (histogram reduction, subtraction and per-feature
+  // scoring in one kernel) holds its per-bin channel sums in registers
+  const bool fused = k + 1 <= FUSED_SCORE_MAX_C;
   void* cws = w + G.call;
 
   // level l node offsets start at offs + (2^l - 1) + l (2^l + 1 entries), its
@@ -400,17 +409,22 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     // the prefix of the built nodes' sizes comes from the previous level's
     // partition (from k_root_offsets at the root), and the reduce writes the
     // siblings by subtraction from the previous level
+    const int64_t base = (int64_t(1) << l) - 1;
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
-                                   nullptr, 1, Hcur, cws, st, pre, nullptr);
+                                   nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
+                                   min_child_weight);
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
-                                   level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1]);
+                                   level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],
+                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight);
     }
     if (rc) return rc;
-    const int64_t base = (int64_t(1) << l) - 1;
-    rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
-                      tree_score + base, cws, st);
+    if (fused)
+      rc = launch_score_node(feat_s, feat_b, nn, m, tree_feature + base, tree_bin + base, tree_score + base, st);
+    else
+      rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
+                        tree_score + base, cws, st);
     if (rc) return rc;
     const bool last = l == depth - 1;
     rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,

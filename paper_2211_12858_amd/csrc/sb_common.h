@@ -74,13 +74,21 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
-                                const int64_t* pre_given = nullptr, const double* H_parent = nullptr);
+                                const int64_t* pre_given = nullptr, const double* H_parent = nullptr,
+                                double* feat_s = nullptr, int32_t* feat_b = nullptr, double lam = 0.0,
+                                double mcw = 0.0);
+// The fused level end (reduction, subtraction and per-feature scoring in one
+// kernel) stages both nodes' values of one feature in LDS: channels up to
+// this many (64 KB at 256 bins).
+constexpr int FUSED_SCORE_MAX_C = 16;
 int32_t launch_subtract(const double* Hp, double* Hc, int32_t n_parents, int64_t cells_per_node,
                         const int32_t* build_list, hipStream_t st);
 
 int64_t score_ws_bytes(int32_t n_nodes, int32_t m);
 int32_t launch_score(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins, int32_t k, double lambda,
                      double mcw, int32_t* best_f, int32_t* best_b, double* best_s, void* ws, hipStream_t st);
+int32_t launch_score_node(const double* feat_s, const int32_t* feat_b, int32_t n_nodes, int32_t m, int32_t* best_f,
+                          int32_t* best_b, double* best_s, hipStream_t st);
 
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes);
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,

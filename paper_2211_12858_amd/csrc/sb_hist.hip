@@ -511,6 +511,169 @@ k_subtract(const double* __restrict__ Hp, double* __restrict__ Hc, int64_t cpn, 
     dst[i] = src[i] - built[i];
 }
 
+constexpr int MAX_BPL_F = 4;  // bins per lane in the fused scoring (n_bins <= 256)
+
+__device__ inline bool score_better(double sa, int ia, double sb_, int ib) {
+  return sa > sb_ || (sa == sb_ && ia < ib);
+}
+
+// Fused end of a level (the level loop's path): one block per (feature f,
+// built node p), one thread per bin.  The block sums feature f's int64
+// partials of node p, writes the fp64 histogram of the built node j (and,
+// with the parent level given, of its sibling by exact subtraction), then
+// scores every threshold of f for both nodes as k_score_feature does
+// (Section 2, eq. 4: prefix sums over bins, fp64, ties to the lower bin)
+// and writes the best (score, bin) per (node, feature) for k_score_node.
+struct ScoreOut {
+  double* s;
+  int32_t* b;
+  double lam, mcw;
+};
+
+template <int PMAX>
+__global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut so) {
+  const int f = blockIdx.x, p = blockIdx.y;
+  const int32_t j = node_of(a, p);
+  if (j < 0 || j >= a.n_nodes || f >= a.m) return;
+  const int B = a.n_bins, c = a.c, k = c - 1;
+  const int s = f / a.f, fl = f - s * a.f;
+  const int FB = a.f * B;
+  const int bin = threadIdx.x;
+  const bool on = bin < B;
+  const bool sib = a.Hp && (j == 2 * p || j == 2 * p + 1);
+  const int64_t cpn = (int64_t)a.m * c * B;
+  const int64_t T = a.pre[a.n_build];
+  const int64_t lo = a.pre[p], hi = a.pre[p + 1];
+  const int64_t qlo = hi > lo ? group_of(lo, T, a.q) : 0, qhi = hi > lo ? group_of(hi - 1, T, a.q) : -1;
+  const bool dense = T >= a.q;  // every row group holds at least one position
+  // int64 channel sums of this bin over the node's row groups: the loads of
+  // four groups and every channel pair are in flight together
+  int64_t acc_lo[PMAX], acc_hi[PMAX];
+#pragma unroll
+  for (int pr = 0; pr < PMAX; ++pr) acc_lo[pr] = acc_hi[pr] = 0;
+  if (on) {
+    const int64_t e64 = (int64_t)fl * B + bin;
+    const longlong2* src = reinterpret_cast<const longlong2*>(a.partial + ((int64_t)s * a.slots + p) * a.cells) + e64;
+    const int64_t stride = a.cells / 2;  // one row group, in 16-byte cells
+    int64_t q = qlo;
+    if (dense) {
+      for (; q + 4 <= qhi + 1; q += 4) {
+        longlong2 v[4][PMAX];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int pr = 0; pr < PMAX; ++pr)
+            if (pr < a.pairs) v[u][pr] = src[(q + u) * stride + (int64_t)pr * FB];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int pr = 0; pr < PMAX; ++pr)
+            if (pr < a.pairs) {
+              acc_lo[pr] += v[u][pr].x;
+              acc_hi[pr] += v[u][pr].y;
+            }
+      }
+    }
+    for (; q <= qhi; ++q) {
+      if (dense || q * T / a.q < (q + 1) * T / a.q) {
+#pragma unroll
+        for (int pr = 0; pr < PMAX; ++pr)
+          if (pr < a.pairs) {
+            const longlong2 v = src[q * stride + (int64_t)pr * FB];
+            acc_lo[pr] += v.x;
+            acc_hi[pr] += v.y;
+          }
+      }
+    }
+  }
+  // fp64 histogram values of this bin: written to H (and the sibling by
+  // subtraction) and staged in LDS as [node][channel][bin] for the scan
+  extern __shared__ double xv[];
+#pragma unroll
+  for (int t = 0; t < 2 * PMAX; ++t) {
+    if (t < c && on) {
+      const int64_t idx = ((int64_t)f * c + t) * B + bin;
+      const double x = ldexp((double)((t & 1) ? acc_hi[t >> 1] : acc_lo[t >> 1]), -a.qexp[t]);
+      a.H[(int64_t)j * cpn + idx] = x;
+      xv[t * B + bin] = x;
+      if (sib) {
+        const double xs = a.Hp[(int64_t)p * cpn + idx] - x;
+        a.H[(int64_t)(j ^ 1) * cpn + idx] = xs;
+        xv[(c + t) * B + bin] = xs;
+      }
+    }
+  }
+  __syncthreads();
+  // one wave per node: lane l owns bins l*bpl .. l*bpl+bpl-1; per channel a
+  // lane prefix plus a wave scan gives the inclusive prefix over bins
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (wave >= (sib ? 2 : 1)) return;
+  const double* xn = xv + wave * c * B;
+  const int bpl = (B + 63) / 64;
+  const int b0 = lane * bpl;
+  double sl[MAX_BPL_F], sr[MAX_BPL_F], hl[MAX_BPL_F];
+  double th = 0.0;
+#pragma unroll
+  for (int i = 0; i < MAX_BPL_F; ++i) sl[i] = sr[i] = hl[i] = 0.0;
+  for (int t = 0; t < c; ++t) {
+    double pfx[MAX_BPL_F];
+    double r = 0.0;
+#pragma unroll
+    for (int i = 0; i < MAX_BPL_F; ++i) {
+      if (i < bpl && b0 + i < B) r += xn[t * B + b0 + i];
+      pfx[i] = r;
+    }
+    double in = r;
+    for (int off = 1; off < 64; off <<= 1) {
+      const double o = __shfl_up(in, off, 64);
+      if (lane >= off) in += o;
+    }
+    const double ex = in - r;
+    const double tot = __shfl(in, 63, 64);
+    if (t < k) {
+#pragma unroll
+      for (int i = 0; i < MAX_BPL_F; ++i) {
+        const double L = pfx[i] + ex, R = tot - L;
+        sl[i] += L * L;
+        sr[i] += R * R;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MAX_BPL_F; ++i) hl[i] = pfx[i] + ex;
+      th = tot;
+    }
+  }
+  double best_s = -INFINITY;
+  int best_b = -1;
+#pragma unroll
+  for (int i = 0; i < MAX_BPL_F; ++i) {
+    const int b = b0 + i;
+    if (i < bpl && b <= B - 2) {
+      const double HL = hl[i], HR = th - hl[i];
+      if (HL > so.mcw && HR > so.mcw) {
+        const double S = sl[i] / (HL + so.lam) + sr[i] / (HR + so.lam);
+        if (S > best_s) {
+          best_s = S;
+          best_b = b;
+        }
+      }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const double os = __shfl_xor(best_s, off, 64);
+    const int ob = __shfl_xor(best_b, off, 64);
+    if (ob >= 0 && (best_b < 0 || score_better(os, ob, best_s, best_b))) {
+      best_s = os;
+      best_b = ob;
+    }
+  }
+  if (lane == 0) {
+    const int32_t nd = wave ? (j ^ 1) : j;
+    so.s[(int64_t)nd * a.m + f] = best_s;
+    so.b[(int64_t)nd * a.m + f] = best_b;
+  }
+}
+
 }  // namespace
 
 int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
@@ -518,7 +681,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int32_t* qexp,
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
-                                const int64_t* pre_given, const double* H_parent) {
+                                const int64_t* pre_given, const double* H_parent, double* feat_s, int32_t* feat_b,
+                                double lam, double mcw) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build);
   HistArgs a{};
   a.bins4 = bins4;
@@ -585,8 +749,17 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     (void)hipEventRecord(e1, st);
     profile_record(e0, e1);
   }
-  dim3 rg((pl.cells + 255) / 256, n_build, pl.slices);
-  hipLaunchKernelGGL(k_hist_reduce, rg, dim3(256), 0, st, a);
+  if (feat_s) {
+    ScoreOut so{feat_s, feat_b, lam, mcw};
+    const dim3 g(m, n_build);
+    const size_t lds = (size_t)2 * pl.c * n_bins * 8;  // [node][channel][bin], built node and sibling
+    if (pl.pairs <= 4) hipLaunchKernelGGL((k_hist_reduce_score<4>), g, dim3(256), lds, st, a, so);
+    else if (pl.pairs <= 8) hipLaunchKernelGGL((k_hist_reduce_score<8>), g, dim3(256), lds, st, a, so);
+    else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 16 channels");
+  } else {
+    dim3 rg((pl.cells + 255) / 256, n_build, pl.slices);
+    hipLaunchKernelGGL(k_hist_reduce, rg, dim3(256), 0, st, a);
+  }
   return check_launch("sb_build_histograms");
 }
 

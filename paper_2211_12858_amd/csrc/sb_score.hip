@@ -165,4 +165,10 @@ int32_t launch_score(const double* H, int32_t n_nodes, int32_t m, int32_t n_bins
   return check_launch("sb_score_splits");
 }
 
+int32_t launch_score_node(const double* feat_s, const int32_t* feat_b, int32_t n_nodes, int32_t m, int32_t* best_f,
+                          int32_t* best_b, double* best_s, hipStream_t st) {
+  hipLaunchKernelGGL(k_score_node, dim3(n_nodes), dim3(64), 0, st, feat_s, feat_b, m, best_f, best_b, best_s);
+  return check_launch("sb_grow_tree");
+}
+
 }  // namespace sb
