@@ -21,6 +21,9 @@ Modules
             eq. 4; Section 3 S_G; Section 3.4 histogram algorithm).
 ``brute``   exact-rational brute force over every candidate split of tiny
             inputs, independent of histograms and prefix sums.
+``leaf``    leaf values of a grown tree from the full gradient matrix
+            (Section 2 "Finding the leaf values", eq. 3) and the per-leaf
+            objective they minimise.
 
 Parity status: every function is pinned by the non-GPU tests
 (``tests/test_oracle_*.py``) except the exact values of the random draws
@@ -44,3 +47,4 @@ from .split import (  # noqa: F401
     sketch_score,
 )
 from .brute import brute_best_split, brute_tree, exact_region_score  # noqa: F401
+from .leaf import leaf_rows, leaf_values, leaf_objective  # noqa: F401
