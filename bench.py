@@ -29,7 +29,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
 METRIC = "sec per tree (depth 6) + histogram-build HBM GB/s (% of peak)"
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "hist_traffic.json")
-HIST_SRCS = [os.path.join(HERE, "paper_2211_12858_amd", "csrc", f) for f in ("sb_hist.hip", "sb_common.h")]
+HIST_SRCS = [os.path.join(HERE, "paper_2211_12858_amd", "csrc", f) for f in ("sb_hist.hip", "sb_hist_plan.h")]
 
 
 def log(*a):
@@ -66,6 +66,11 @@ def hist_algorithmic_bytes(leaf_off, depth, m, n_bins, c):
             rows, nodes = int(np.minimum(left, right).sum()), len(left)
         per_launch.append(rows * (m + 4 * c) + nodes * m * n_bins * c * 4)
     return per_launch
+
+
+def leaf_algorithmic_bytes(n, d, n_leaves):
+    """Leaf values: G read once (n*d*4), the row order once (4n), the values written (n_leaves*d*8)."""
+    return n * d * 4 + 4 * n + n_leaves * d * 8
 
 
 def hist_source_hash():
@@ -197,6 +202,19 @@ def main():
     achieved = bytes_per_launch / (ms_per_launch * 1e-3) / 1e9
     traffic = traffic_for_current_kernel()
 
+    # leaf values of the last tree from the full G (eq. 3), timed on their own
+    for _ in range(2):
+        ss.leaf_values(G_T)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(K):
+        ss.leaf_values(G_T)
+    stop.record()
+    torch.cuda.synchronize()
+    leaf_ms = start.elapsed_time(stop) / K
+    leaf_bytes = leaf_algorithmic_bytes(wl.n, wl.d, 1 << wl.depth)
+    log("bench: leaf values %.3f ms per tree" % leaf_ms)
+
     sec_per_tree = total_ms / K / 1e3
     out = {
         "metric": METRIC,
@@ -229,6 +247,16 @@ def main():
             "kernel": "k_hist",
             "bytes_per_launch": bytes_per_launch,
             "ms_per_launch": ms_per_launch,
+        },
+    }
+    out["next"] = {
+        "leaf_values": {
+            "ms_per_tree": leaf_ms,
+            "bytes": leaf_bytes,
+            "GBps": leaf_bytes / (leaf_ms * 1e-3) / 1e9,
+            "frac_hbm_peak": leaf_bytes / (leaf_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "what": "sb_leaf_values over the last tree's %d leaves, full d=%d, unit hessians; not inside value"
+                    % (1 << wl.depth, wl.d),
         },
     }
     if not args.no_cpu_baseline:

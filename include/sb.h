@@ -71,7 +71,7 @@
 extern "C" {
 #endif
 
-#define SB_ABI_VERSION 2
+#define SB_ABI_VERSION 3
 
 /* Status codes. */
 enum {
@@ -97,7 +97,8 @@ enum {
   SB_CALL_SCORE_SPLITS = 2,
   SB_CALL_PARTITION_ROWS = 3,
   SB_CALL_GROW_TREE = 4,
-  SB_CALL_HIST_EXPONENTS = 5
+  SB_CALL_HIST_EXPONENTS = 5,
+  SB_CALL_LEAF_VALUES = 6
 };
 
 /* Text of the last non-OK status returned on this thread ("" if none). */
@@ -109,8 +110,9 @@ int32_t sb_abi_version(void);
 /*
  * Workspace bytes needed by one call.  Arguments not used by a call are
  * ignored (pass 0).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
- * SCORE_SPLITS, PARTITION_ROWS).  depth: tree depth (GROW_TREE).  d: output
- * dimension (SKETCH).  Returns -1 (and sets the error text) for invalid
+ * SCORE_SPLITS, PARTITION_ROWS), leaves (LEAF_VALUES).  depth: tree depth
+ * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES; the LEAF_VALUES size
+ * covers all three hessian forms).  Returns -1 (and sets the error text) for invalid
  * sizes.  sb_layout_bins and sb_subtract_histograms need no workspace.
  */
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
@@ -284,6 +286,34 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
                      int32_t k, const int32_t* qexp, int32_t depth, double lambda,
                      double min_child_weight, int32_t* tree_feature, int32_t* tree_bin, double* tree_score,
                      int32_t* row_idx_out, int32_t* leaf_off_out, void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_leaf_values -- leaf values of a grown tree from the full gradient matrix
+ * (Section 2, "Finding the leaf values", eq. 3; Section 3: the sketch only
+ * serves the structure search, leaf values use all d outputs).
+ *
+ * For leaf L (rows row_idx[leaf_off[L] .. leaf_off[L+1])) and output j:
+ *   V[L*ld_v + j] = -sum_{i in L} G[i, j] / (sum_{i in L} h_ij + lambda),
+ * the minimiser of the leaf's second-order objective with diagonal Hessians.
+ * G        n x d gradients, column-major: (i, j) at G[j*ld_g + i], ld_g >= n.
+ * hess     per-element hessians h_ij, column-major like G (hess[j*ld_hess + i],
+ *          ld_hess >= n), or NULL.
+ * h        per-row hessians h_i used for every output when hess is NULL, or
+ *          NULL: then h_ij = 1 and the denominator is the leaf's row count
+ *          plus lambda (the weight of the hessian-free score S_G).
+ * row_idx, leaf_off  the leaf segments, as sb_grow_tree writes them: row_idx
+ *          a permutation of 0..n-1, leaf_off n_leaves+1 non-decreasing offsets
+ *          from 0 to n.  1 <= n_leaves <= 4096.
+ * lambda   > 0.  Hessians must be >= 0.
+ * V        out: n_leaves x d fp64, row-major with ld_v >= d.  Empty leaves get 0.
+ * Accumulation is exact integer arithmetic per block of rows plus fp64 sums
+ * in a fixed order: results are deterministic.  Each element contributes an
+ * error of at most 2^-41 of the largest magnitude of its column within its
+ * block of 2048 rows.
+ */
+int32_t sb_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
+                       const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
+                       double lambda, double* V, int64_t ld_v, void* ws, int64_t ws_bytes, void* stream);
 
 /*
  * Kernel timing for benchmarks.  Between sb_profile_begin() and

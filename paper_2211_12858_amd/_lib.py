@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "libsketchboost.so")
 SB_OK, SB_E_ARG, SB_E_SHAPE, SB_E_UNSUPPORTED, SB_E_DEVICE = 0, 1, 2, 3, 4
 SB_SKETCH_TOP_OUTPUTS, SB_SKETCH_RANDOM_SAMPLING, SB_SKETCH_RANDOM_PROJECTION, SB_SKETCH_IDENTITY = 0, 1, 2, 3
 (SB_CALL_SKETCH, SB_CALL_BUILD_HISTOGRAMS, SB_CALL_SCORE_SPLITS, SB_CALL_PARTITION_ROWS, SB_CALL_GROW_TREE,
- SB_CALL_HIST_EXPONENTS) = range(6)
+ SB_CALL_HIST_EXPONENTS, SB_CALL_LEAF_VALUES) = range(7)
 
 KIND = {
     "top_outputs": SB_SKETCH_TOP_OUTPUTS,
@@ -40,6 +40,7 @@ SYMBOLS = (
     "sb_score_splits",
     "sb_partition_rows",
     "sb_grow_tree",
+    "sb_leaf_values",
     "sb_profile_begin",
     "sb_profile_end",
 )
@@ -73,6 +74,8 @@ _PROTOS = {
                             _P, _P, _P, _P, _P, _P, _I64, _P]),
 }
 
+_PROTOS["sb_leaf_values"] = (_I32, [_P, _I64, _I32, _I64, _P, _I64, _P, _P, _P, _I32, _F64, _P, _I64, _P, _I64,
+                                     _P])
 _PROTOS["sb_profile_begin"] = (_I32, [])
 _PROTOS["sb_profile_end"] = (_I32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)])
 
@@ -181,6 +184,13 @@ def sb_grow_tree(bins4, ld4, bins_cm, ld_cm, rec, ld_rec, n, m, n_bins, GH, ld_g
                                       _ptr(GH), ld_gh, k, _ptr(qexp), depth, lam, min_child_weight,
                                       _ptr(tree_feature), _ptr(tree_bin), _ptr(tree_score), _ptr(row_idx_out),
                                       _ptr(leaf_off_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def sb_leaf_values(G, n, d, ld_g, hess, ld_hess, h, row_idx, leaf_off, n_leaves, lam, V, ld_v, ws, ws_bytes,
+                   stream=None):
+    return _check(load().sb_leaf_values(_ptr(G), n, d, ld_g, _ptr(hess), ld_hess, _ptr(h), _ptr(row_idx),
+                                        _ptr(leaf_off), n_leaves, lam, _ptr(V), ld_v, _ptr(ws), ws_bytes,
+                                        _stream(stream)))
 
 
 def sb_profile_begin():

@@ -39,6 +39,7 @@ namespace {
 
 constexpr int64_t MAX_ROWS = (int64_t(1) << 31) - 1;
 constexpr int MAX_DEPTH = 12;
+constexpr int32_t MAX_LEAVES = 1 << MAX_DEPTH;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -194,6 +195,9 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
       if (b < 0) break;
       return b;
     }
+    case SB_CALL_LEAF_VALUES:
+      if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535 || n_nodes < 1 || n_nodes > MAX_LEAVES) break;
+      return leaf_ws_bytes(n, d, n_nodes);
     default:
       set_error("sb_workspace_bytes: unknown call id");
       return -1;
@@ -433,6 +437,24 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     if (rc) return rc;
   }
   return check_launch(call);
+}
+
+int32_t sb_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
+                       const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
+                       double lambda, double* V, int64_t ld_v, void* ws, int64_t ws_bytes, void* stream) {
+  if (!G || !row_idx || !leaf_off || !V)
+    return fail(SB_E_ARG, "sb_leaf_values: G, row_idx, leaf_off and V must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_leaf_values: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_leaf_values: d must be in [1, 65535]");
+  if (n_leaves < 1 || n_leaves > MAX_LEAVES) return fail(SB_E_ARG, "sb_leaf_values: n_leaves must be in [1, 4096]");
+  if (ld_g < n) return fail(SB_E_SHAPE, "sb_leaf_values: ld_g must be >= n");
+  if (hess && ld_hess < n) return fail(SB_E_SHAPE, "sb_leaf_values: ld_hess must be >= n");
+  if (ld_v < d) return fail(SB_E_SHAPE, "sb_leaf_values: ld_v must be >= d");
+  if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_leaf_values: lambda must be > 0");
+  const int32_t rc = need_ws(ws, ws_bytes, leaf_ws_bytes(n, d, n_leaves), "sb_leaf_values");
+  if (rc) return rc;
+  return launch_leaf_values(G, n, d, ld_g, hess, ld_hess, h, row_idx, leaf_off, n_leaves, lambda, V, ld_v, ws,
+                            static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

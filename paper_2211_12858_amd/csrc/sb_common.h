@@ -7,6 +7,7 @@
 #include <string>
 
 #include "../../include/sb.h"
+#include "sb_hist_plan.h"
 
 namespace sb {
 
@@ -14,48 +15,6 @@ namespace sb {
 void set_error(const std::string& msg);
 int32_t fail(int32_t code, const std::string& msg);
 int32_t check_launch(const char* what);
-
-// ---------------------------------------------------------------- fixed point
-// Quantised magnitudes are <= 2^QBITS (qexp = QBITS-1 - floor(log2(max|v|))),
-// so each value carries an error of at most 2^-(QBITS+1) of its channel's
-// maximum magnitude.
-constexpr int QBITS = 18;
-// Each channel's LDS sum is a 32-bit running sum read back into int64 every
-// window of WINDOW_ROWS rows (4 steps of the 768-thread workgroup).  A cell
-// gets at most one value per row, and the change between two reads spans at
-// most two windows, so 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
-constexpr int WINDOW_ROWS = 3072;
-static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point window overflow");
-
-// ---------------------------------------------------------------- histogram plan
-// One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
-// VGPRs per lane) and up to 40 channel cells per thread (20 64-bit LDS cells
-// of two channels each: 120 KB of the 160 KB LDS).  Each thread keeps the
-// int64 totals of its 40 channel cells in 80 VGPRs next to the prefetched
-// row data of the step loop; with 4 waves per SIMD (128 VGPRs) they would
-// spill to scratch.
-constexpr int HIST_THREADS = 768;
-constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
-constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
-// MI355X: 8 XCDs of 32 CUs; workgroup b is dispatched to XCD b % 8.
-constexpr int HIST_CUS_PER_XCD = 32;
-// A lane holds the bin words of up to 16 quads (64 features) of its row.
-constexpr int HIST_MAX_QUADS = 16;
-
-struct HistPlan {
-  int c;          // channels k+1
-  int pairs;      // 64-bit LDS cells per (feature, bin): ceil(c/2)
-  int nq;         // 4-feature quads per slice
-  int f;          // features per slice (4*nq)
-  int slices;     // feature slices
-  int rows_wave;  // rows one wave handles per step (64 / nq)
-  int cells;      // 2 * pairs * f * n_bins channel cells per workgroup
-  int q;          // row groups per slice
-  int q_pad;      // q rounded up to a multiple of 8 (XCD-aware mapping)
-  int64_t slots;  // partial slots per slice: q + n_build
-};
-HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
-int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
 
 // ---------------------------------------------------------------- launches (stream-ordered)
 int32_t launch_layout(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, uint32_t* bins4, int64_t ld4,
@@ -95,6 +54,11 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
                          int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,
                          int64_t* next_pre = nullptr);
+
+int64_t leaf_ws_bytes(int64_t n, int32_t d, int32_t n_leaves);
+int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
+                           const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
+                           double lambda, double* V, int64_t ld_v, void* ws, hipStream_t st);
 
 // ---------------------------------------------------------------- profiling
 // Event pairs around histogram-kernel launches while profiling is on (per thread).

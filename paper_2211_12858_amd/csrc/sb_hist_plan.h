@@ -1,0 +1,51 @@
+// Constants and work plan of the histogram kernel (fixed point, workgroup
+// shape, LDS budget, feature slicing).
+#pragma once
+
+#include <cstdint>
+
+namespace sb {
+
+// ---------------------------------------------------------------- fixed point
+// Quantised magnitudes are <= 2^QBITS (qexp = QBITS-1 - floor(log2(max|v|))),
+// so each value carries an error of at most 2^-(QBITS+1) of its channel's
+// maximum magnitude.
+constexpr int QBITS = 18;
+// Each channel's LDS sum is a 32-bit running sum read back into int64 every
+// window of WINDOW_ROWS rows (4 steps of the 768-thread workgroup).  A cell
+// gets at most one value per row, and the change between two reads spans at
+// most two windows, so 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
+constexpr int WINDOW_ROWS = 3072;
+static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point window overflow");
+
+// ---------------------------------------------------------------- histogram plan
+// One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
+// VGPRs per lane) and up to 40 channel cells per thread (20 64-bit LDS cells
+// of two channels each: 120 KB of the 160 KB LDS).  Each thread keeps the
+// int64 totals of its 40 channel cells in 80 VGPRs next to the prefetched
+// row data of the step loop; with 4 waves per SIMD (128 VGPRs) they would
+// spill to scratch.
+constexpr int HIST_THREADS = 768;
+constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
+constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
+// MI355X: 8 XCDs of 32 CUs; workgroup b is dispatched to XCD b % 8.
+constexpr int HIST_CUS_PER_XCD = 32;
+// A lane holds the bin words of up to 16 quads (64 features) of its row.
+constexpr int HIST_MAX_QUADS = 16;
+
+struct HistPlan {
+  int c;          // channels k+1
+  int pairs;      // 64-bit LDS cells per (feature, bin): ceil(c/2)
+  int nq;         // 4-feature quads per slice
+  int f;          // features per slice (4*nq)
+  int slices;     // feature slices
+  int rows_wave;  // rows one wave handles per step (64 / nq)
+  int cells;      // 2 * pairs * f * n_bins channel cells per workgroup
+  int q;          // row groups per slice
+  int q_pad;      // q rounded up to a multiple of 8 (XCD-aware mapping)
+  int64_t slots;  // partial slots per slice: q + n_build
+};
+HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
+int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
+
+}  // namespace sb

@@ -1,0 +1,330 @@
+// Leaf values from the full gradient matrix (Section 2, "Finding the leaf
+// values": with diagonal Hessians the value of leaf R is, output by output,
+// v_j = -sum_{i in R} g_ij / (sum_{i in R} h_ij + lambda), eq. 3.  Section 3:
+// the sketch serves only the search for the structure; leaf values use all d
+// outputs of G).
+//
+// A leaf's rows are scattered over the rows of G, and G is column-major, so
+// gathering a leaf's rows would fetch a whole 32-byte sector for every 4-byte
+// value.  The path streams G once, in row order, instead:
+//   k_leaf_of     writes every row's leaf id (uint16) from the leaf segments;
+//   k_leaf_accum  one block per (chunk of J channels, split of the rows).  The
+//                 lanes take consecutive rows of a column (256-byte loads per
+//                 wave) and add every value into an LDS cell (leaf, channel);
+//   k_leaf_final  sums the splits' partials per (leaf, output) in a fixed
+//                 order and divides.
+// Channels are the d gradient columns followed by the hessian columns (d of
+// them per element, or one per-row weight, or none: then the denominator is
+// the leaf's row count).
+//
+// Exact, order-free accumulation.  Per tile of LEAF_TILE rows and per
+// channel, the block takes M = max |v| over the tile, with M < 2^E, and maps
+// each v to the integer rint(v * 2^(LEAF_QL - E)), of magnitude <= 2^LEAF_QL.
+// LEAF_TILE * 2^LEAF_QL <= 2^52, so any sum of one tile's integers is an
+// integer below 2^53: the 64-bit LDS integer atomics reach the same sum in any
+// order, and that sum times 2^(E - LEAF_QL) is an exact fp64 value.  One thread
+// per cell adds it to the cell's fp64 accumulator, tile after tile, so the
+// rounding order is fixed and the result does not depend on timing.  Each
+// element is off by at most 2^(E - LEAF_QL - 1) <= M * 2^-LEAF_QL.
+#include <cmath>
+
+#include "sb_common.h"
+
+namespace sb {
+namespace {
+
+constexpr int LEAF_THREADS = 256;
+constexpr int LEAF_SPT = 8;                             // rows per thread per tile
+constexpr int LEAF_TILE = LEAF_THREADS * LEAF_SPT;      // 2048 rows
+constexpr int LEAF_QL = 41;                             // 2^11 rows * 2^41 = 2^52
+static_assert((int64_t)LEAF_TILE << LEAF_QL <= (int64_t(1) << 52), "tile sums must stay exact in fp64");
+constexpr int64_t LEAF_LDS_MAX = 64 * 1024;             // integer + fp64 cells of one block
+constexpr int LEAF_TARGET_BLOCKS = 4096;                // 16 per CU
+constexpr int LEAF_MAX_LEAVES = 4096;
+// channels per block (fewer for many leaves, so that the cells fit LEAF_LDS_MAX)
+constexpr int LEAF_JMAX = 4;
+
+struct LeafArgs {
+  const float* G;
+  int64_t ld_g;
+  int32_t d;
+  const float* hess;  // per-element hessians (column-major) or NULL
+  int64_t ld_h;
+  const float* h;     // per-row hessian or NULL
+  const void* leaf_of;  // uint8 ids for up to 256 leaves, else uint16
+  int64_t n;
+  int32_t n_leaves;
+  int32_t nch;
+  int32_t n_tiles;
+  int32_t tiles_per_split;
+  double* part;       // [leaf][nch][split]
+};
+
+__device__ inline const float* chan_ptr(const LeafArgs& a, int c) {
+  if (c < a.d) return a.G + (int64_t)c * a.ld_g;
+  if (a.hess) return a.hess + (int64_t)(c - a.d) * a.ld_h;
+  return a.h;
+}
+
+// 2^e as a double, for |e| <= 1022.
+__device__ inline double pow2(int e) { return __longlong_as_double((long long)(1023 + e) << 52); }
+
+template <typename LT>
+__global__ void __launch_bounds__(256) k_leaf_of(const int32_t* __restrict__ row_idx,
+                                                  const int32_t* __restrict__ leaf_off, int32_t n_leaves, int64_t n,
+                                                  LT* __restrict__ leaf_of) {
+  __shared__ int32_t soff[LEAF_MAX_LEAVES];
+  for (int L = threadIdx.x; L < n_leaves; L += blockDim.x) soff[L] = leaf_off[L];
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
+    // the last leaf whose segment starts at or before p (empty leaves are skipped)
+    int lo = 0, hi = n_leaves - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((int64_t)soff[mid] <= p)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    int64_t r = row_idx[p];
+    r = r < 0 ? 0 : (r >= n ? n - 1 : r);
+    leaf_of[r] = (LT)lo;
+  }
+}
+
+// rint(y) as an int64 for |y| < 2^51: adding 1.5 * 2^52 leaves the integer
+// nearest to y (ties to even) in the low mantissa bits, and the fused
+// multiply-add rounds the exact product v * scale only once.
+__device__ inline long long rint_to_ll(float v, double scale) {
+  const double t = fma((double)v, scale, 6755399441055744.0);
+  return __double_as_longlong(t) - 0x4338000000000000ll;
+}
+
+template <int J, typename LT>
+struct LeafTile {
+  float v[LEAF_SPT][J];
+  int lf[LEAF_SPT];
+};
+
+template <int J, typename LT>
+__device__ inline void leaf_load(const LeafArgs& a, const float* const (&col)[J], int t, int top,
+                                 LeafTile<J, LT>& x) {
+  // Rows past the end load row n-1 and get a negative leaf id, which drops
+  // them from the adds (they may still raise the tile maximum, which only has
+  // to bound the tile's values).  No value depends on a condition, so the
+  // compiler issues every load of the tile back to back instead of waiting
+  // for each one inside its own branch.
+  const LT* ids = static_cast<const LT*>(a.leaf_of);
+  const int64_t r0 = (int64_t)t * LEAF_TILE;
+#pragma unroll
+  for (int s = 0; s < LEAF_SPT; ++s) {
+    const int64_t row = r0 + threadIdx.x + LEAF_THREADS * s;
+    const int64_t rc = row < a.n ? row : a.n - 1;
+    const int l = (int)ids[rc];
+    x.lf[s] = (l > top ? top : l) - (row < a.n ? 0 : 0x10000);
+#pragma unroll
+    for (int j = 0; j < J; ++j) x.v[s][j] = col[j][rc];
+  }
+}
+
+// One tile: block-wide maximum per channel, quantisation, integer adds into
+// the LDS cells, then the exact fp64 conversion into the accumulators.
+template <int J, typename LT>
+__device__ inline void leaf_tile(const LeafTile<J, LT>& x, const bool (&live)[J], float (&wmax)[LEAF_THREADS / 64][J],
+                                 double (&sconv)[J], unsigned long long* icell, double* acc, int NL) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cells = NL * J;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    float mx = 0.0f;
+#pragma unroll
+    for (int s = 0; s < LEAF_SPT; ++s) mx = fmaxf(mx, fabsf(x.v[s][j]));
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    if (lane == 0) wmax[wave][j] = mx;
+  }
+  __syncthreads();
+  double sc[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    float M = wmax[0][j];
+#pragma unroll
+    for (int w = 1; w < LEAF_THREADS / 64; ++w) M = fmaxf(M, wmax[w][j]);
+    int E = 0;
+    if (M > 0.0f) (void)frexpf(M, &E);  // M = f * 2^E with f in [0.5, 1): every |v| < 2^E
+    sc[j] = M > 0.0f ? pow2(LEAF_QL - E) : 0.0;
+    if (tid == j) sconv[j] = M > 0.0f ? pow2(E - LEAF_QL) : 0.0;
+  }
+#pragma unroll
+  for (int s = 0; s < LEAF_SPT; ++s) {
+    // a row past the end adds 0 to leaf 0
+    const bool in = x.lf[s] >= 0;
+    const int l = in ? x.lf[s] : 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const long long q = rint_to_ll(x.v[s][j], sc[j]);
+      if (live[j]) atomicAdd(&icell[j * NL + l], (unsigned long long)(in ? q : 0ll));
+    }
+  }
+  __syncthreads();
+  // The next tile's adds (and its writes of wmax and sconv) start only after
+  // its first barrier, which every thread reaches after finishing this loop.
+  for (int cell = tid; cell < cells; cell += LEAF_THREADS) {
+    const long long q = (long long)icell[cell];
+    if (q != 0) {
+      acc[cell] += (double)q * sconv[cell / NL];
+      icell[cell] = 0ull;
+    }
+  }
+}
+
+template <int J, typename LT>
+__global__ void __launch_bounds__(LEAF_THREADS) k_leaf_accum(LeafArgs a) {
+  // Cells are channel-major ([J][n_leaves]): the lanes of one add instruction
+  // share the channel, so their addresses differ by leaf and spread over the
+  // LDS banks.
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ float wmax[LEAF_THREADS / 64][J];
+  __shared__ double sconv[J];
+  const int NL = a.n_leaves;
+  const int cells = NL * J;
+  unsigned long long* icell = reinterpret_cast<unsigned long long*>(smem);
+  double* acc = reinterpret_cast<double*>(smem + (size_t)cells * 8);
+  const int tid = threadIdx.x;
+  const int c0 = blockIdx.x * J;
+  const int split = blockIdx.y;
+
+  const float* col[J];
+  bool live[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    live[j] = c0 + j < a.nch;
+    col[j] = chan_ptr(a, live[j] ? c0 + j : c0);  // a channel past the last one reads the chunk's first
+  }
+  for (int cell = tid; cell < cells; cell += LEAF_THREADS) {
+    icell[cell] = 0ull;
+    acc[cell] = 0.0;
+  }
+  const int t0 = split * a.tiles_per_split;
+  const int t1 = min(a.n_tiles, t0 + a.tiles_per_split);
+  const int top = NL - 1;
+  __syncthreads();
+
+  for (int t = t0; t < t1; ++t) {
+    LeafTile<J, LT> x;
+    leaf_load(a, col, t, top, x);
+    leaf_tile(x, live, wmax, sconv, icell, acc, NL);
+  }
+  __syncthreads();
+  for (int cell = tid; cell < cells; cell += LEAF_THREADS) {
+    const int j = cell / NL, L = cell - j * NL;
+    if (c0 + j < a.nch) a.part[((int64_t)L * a.nch + c0 + j) * gridDim.y + split] = acc[cell];
+  }
+}
+
+// One wave per (leaf, output): the lanes sum the splits' partials (stored
+// split-contiguous) in a fixed lane-strided order, then a fixed butterfly
+// combines the lanes.  hmode: 0 = no hessian (row counts), 1 = per-element
+// hessian channels d..2d-1, 2 = one per-row hessian channel d.
+__global__ void __launch_bounds__(256) k_leaf_final(const double* __restrict__ part, int32_t n_splits,
+                                                    int32_t n_leaves, int32_t d, int32_t nch, int32_t hmode,
+                                                    const int32_t* __restrict__ leaf_off, double lam,
+                                                    double* __restrict__ V, int64_t ld_v) {
+  const int lane = threadIdx.x & 63;
+  const int64_t out = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (out >= (int64_t)n_leaves * d) return;
+  const int L = (int)(out / d), j = (int)(out % d);
+  const double* pg = part + ((int64_t)L * nch + j) * n_splits;
+  const double* ph = hmode == 1 ? part + ((int64_t)L * nch + d + j) * n_splits
+                                : part + ((int64_t)L * nch + d) * n_splits;
+  double gs = 0.0, hs = 0.0;
+  for (int s = lane; s < n_splits; s += 64) {
+    gs += pg[s];
+    if (hmode != 0) hs += ph[s];
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    gs += __shfl_xor(gs, off, 64);
+    hs += __shfl_xor(hs, off, 64);
+  }
+  if (lane != 0) return;
+  if (hmode == 0) hs = (double)((int64_t)leaf_off[L + 1] - (int64_t)leaf_off[L]);
+  V[(int64_t)L * ld_v + j] = -gs / (hs + lam);
+}
+
+struct LeafPlan {
+  int J, nch, n_chunks, n_tiles, tps, splits;
+  int64_t lds;
+};
+
+LeafPlan leaf_plan(int64_t n, int32_t nch, int32_t n_leaves) {
+  LeafPlan p{};
+  p.J = LEAF_JMAX;
+  while (p.J > 1 && (int64_t)n_leaves * p.J * 16 > LEAF_LDS_MAX) p.J >>= 1;
+  p.nch = nch;
+  p.n_chunks = (nch + p.J - 1) / p.J;
+  p.n_tiles = (int)((n + LEAF_TILE - 1) / LEAF_TILE);
+  int splits = (LEAF_TARGET_BLOCKS + p.n_chunks - 1) / p.n_chunks;
+  if (splits < 1) splits = 1;
+  if (splits > p.n_tiles) splits = p.n_tiles;
+  p.tps = (p.n_tiles + splits - 1) / splits;
+  p.splits = (p.n_tiles + p.tps - 1) / p.tps;
+  p.lds = (int64_t)n_leaves * p.J * 16;
+  return p;
+}
+
+int64_t leaf_ws_for(int64_t n, int32_t nch, int32_t n_leaves) {
+  const LeafPlan p = leaf_plan(n, nch, n_leaves);
+  return align256(n * 2) + align256((int64_t)p.splits * n_leaves * nch * 8);
+}
+
+template <int J, typename LT>
+void launch_accum(const LeafPlan& p, const LeafArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((k_leaf_accum<J, LT>), dim3(p.n_chunks, p.splits), dim3(LEAF_THREADS), (size_t)p.lds, st, a);
+}
+
+template <typename LT>
+void launch_leaf_kernels(const LeafPlan& p, LeafArgs a, const int32_t* row_idx, const int32_t* leaf_off, void* ids,
+                         hipStream_t st) {
+  const int64_t blocks_of = (a.n + 255) / 256;
+  hipLaunchKernelGGL(k_leaf_of<LT>, dim3((unsigned)(blocks_of < 2048 ? blocks_of : 2048)), dim3(256), 0, st, row_idx,
+                     leaf_off, a.n_leaves, a.n, static_cast<LT*>(ids));
+  a.leaf_of = ids;
+  switch (p.J) {
+    case 4: launch_accum<4, LT>(p, a, st); break;
+    case 2: launch_accum<2, LT>(p, a, st); break;
+    default: launch_accum<1, LT>(p, a, st); break;
+  }
+}
+
+}  // namespace
+
+int64_t leaf_ws_bytes(int64_t n, int32_t d, int32_t n_leaves) {
+  // the largest of the three hessian forms
+  int64_t b = leaf_ws_for(n, d, n_leaves);
+  const int64_t b1 = leaf_ws_for(n, d + 1, n_leaves);
+  const int64_t b2 = leaf_ws_for(n, 2 * d, n_leaves);
+  if (b1 > b) b = b1;
+  if (b2 > b) b = b2;
+  return b;
+}
+
+int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
+                           const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
+                           double lambda, double* V, int64_t ld_v, void* ws, hipStream_t st) {
+  const int hmode = hess ? 1 : (h ? 2 : 0);
+  const int32_t nch = d + (hmode == 1 ? d : (hmode == 2 ? 1 : 0));
+  const LeafPlan p = leaf_plan(n, nch, n_leaves);
+  char* w = static_cast<char*>(ws);
+  double* part = reinterpret_cast<double*>(w + align256(n * 2));
+  const LeafArgs a{G, ld_g, d, hess, ld_hess, h, nullptr, n, n_leaves, nch, p.n_tiles, p.tps, part};
+  if (n_leaves <= 256)
+    launch_leaf_kernels<uint8_t>(p, a, row_idx, leaf_off, w, st);
+  else
+    launch_leaf_kernels<uint16_t>(p, a, row_idx, leaf_off, w, st);
+  const int64_t outs = (int64_t)n_leaves * d;
+  hipLaunchKernelGGL(k_leaf_final, dim3((unsigned)((outs + 3) / 4)), dim3(256), 0, st, part, p.splits, n_leaves, d,
+                     nch, hmode, leaf_off, lambda, V, ld_v);
+  return check_launch("sb_leaf_values");
+}
+
+}  // namespace sb

@@ -15,7 +15,8 @@ the row-major bins):
 The sketch lives row-major in ``GH[i, t]``, each row padded to a multiple of
 8 floats so that it fills whole 32-byte sectors.  ``step()`` runs one
 tree: the sketch (once per tree) and the depth-wise level loop, entirely on
-the device.  No computation happens in Python.
+the device; ``leaf_values()`` then gives the tree's leaf values from the
+full gradient matrix.  No computation happens in Python.
 """
 import numpy as np
 import torch
@@ -77,6 +78,8 @@ class SplitSearch:
         self.ws_tree = workspace(self.ws_tree_bytes, dev)
         self._ws_sketch = None
         self.norm2 = None
+        self._ws_leaf = None
+        self.V = None
 
     # ------------------------------------------------------------ sketch
     def sketch(self, kind, G_T, h, u=None, Pi=None, stream=None):
@@ -103,6 +106,24 @@ class SplitSearch:
     def step(self, kind, G_T, h, u=None, Pi=None, stream=None):
         self.sketch(kind, G_T, h, u, Pi, stream)
         self.grow(stream)
+
+    # ------------------------------------------------------------ leaf values
+    def leaf_values(self, G_T, hess_T=None, h=None, stream=None):
+        """Leaf values of the last grown tree from the full G (eq. 3): self.V, (2^depth, d) fp64.
+
+        hess_T: (d, n) per-element hessians, or h: (n,) per-row hessians, or
+        neither (h = 1)."""
+        d, n = G_T.shape
+        assert n == self.n and G_T.is_contiguous() and G_T.dtype == torch.float32
+        n_leaves = 1 << self.depth
+        need = L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=n, d=d, n_nodes=n_leaves)
+        if self._ws_leaf is None or self._ws_leaf.numel() < need:
+            self._ws_leaf = workspace(need, self.device)
+        if self.V is None or self.V.shape != (n_leaves, d):
+            self.V = torch.zeros((n_leaves, d), dtype=torch.float64, device=self.device)
+        L.sb_leaf_values(G_T, n, d, n, hess_T, n, h, self.row_idx, self.leaf_off, n_leaves, self.lam, self.V, d,
+                         self._ws_leaf, self._ws_leaf.numel(), stream)
+        return self.V
 
     # ------------------------------------------------------------ readback
     def gh(self):

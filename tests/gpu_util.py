@@ -159,3 +159,55 @@ def make_records(bins, ld_rec):
     rec = np.zeros((n, ld_rec), dtype=np.uint8)
     rec[:, :m] = bins
     return rec
+
+
+def run_leaf(G_T, row_idx, leaf_off, lam, hess_T=None, h=None, ld_v=None, device_G=None):
+    """sb_leaf_values on host inputs (G_T, hess_T: (d, n) column-major).  Returns V (n_leaves, d)."""
+    d, n = G_T.shape if device_G is None else device_G.shape
+    n_leaves = len(leaf_off) - 1
+    ld_v = d if ld_v is None else ld_v
+    Gd = up(G_T) if device_G is None else device_G
+    Hd = up(hess_T) if hess_T is not None else None
+    hd = up(h) if h is not None else None
+    V = torch.full((n_leaves, ld_v), float("nan"), dtype=torch.float64, device=DEV)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=n, d=d, n_nodes=n_leaves), DEV)
+    L.sb_leaf_values(Gd, n, d, n, Hd, n, hd, up(np.asarray(row_idx, dtype=np.int32)),
+                     up(np.asarray(leaf_off, dtype=np.int32)), n_leaves, lam, V, ld_v, ws, ws.numel())
+    sync()
+    return V.cpu().numpy()
+
+
+LEAF_QUANTUM = 2.0 ** -41  # per-element error bound of the leaf sums, relative to the column's largest magnitude
+
+
+def leaf_value_error_ok(V, V_o, G, rows_of, lam, hess=None, h=None, col_max=None):
+    """|V - V_o| within the bound that the fixed-point accumulation and fp64 sums allow.
+
+    The numerator and denominator sums carry at most n_L * 2^-41 * M (M: the
+    column's largest magnitude over all rows) plus 1e-13 of the leaf's absolute
+    mass; the quotient adds both relative errors and one rounding.
+    col_max: the columns' largest magnitudes over all n rows, when G holds only
+    some of them.  Returns (ok, worst ratio of error to bound)."""
+    G = np.asarray(G, dtype=np.float64)
+    Mg = np.abs(G).max(axis=0) if col_max is None else np.asarray(col_max, dtype=np.float64)
+    worst = 0.0
+    for Lf, rows in enumerate(rows_of):
+        nL = rows.shape[0]
+        A = np.abs(G[rows]).sum(axis=0)
+        eg = nL * LEAF_QUANTUM * Mg + 1e-13 * A
+        if hess is not None:
+            Hh = np.asarray(hess, dtype=np.float64)
+            hs = Hh[rows].sum(axis=0)
+            eh = nL * LEAF_QUANTUM * np.abs(Hh).max(axis=0) + 1e-13 * hs
+        elif h is not None:
+            hh = np.asarray(h, dtype=np.float64)
+            hs = np.full(G.shape[1], hh[rows].sum())
+            eh = nL * LEAF_QUANTUM * np.abs(hh).max() + 1e-13 * hs
+        else:
+            hs = np.full(G.shape[1], float(nL))
+            eh = np.zeros(G.shape[1])
+        den = hs + lam
+        bound = eg / den + np.abs(V_o[Lf]) * eh / den + 4e-16 * np.abs(V_o[Lf]) + 1e-300
+        ratio = np.abs(V[Lf] - V_o[Lf]) / bound
+        worst = max(worst, float(ratio.max()))
+    return worst <= 1.0, worst

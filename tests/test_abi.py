@@ -34,7 +34,7 @@ def header_functions():
 def test_header_declares_the_boundary():
     fns = header_functions()
     for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
-                 "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_last_error",
+                 "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_leaf_values", "sb_last_error",
                  "sb_abi_version", "sb_workspace_bytes"):
         assert name in fns
 
@@ -49,7 +49,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_error_text(L):
-    assert L.sb_abi_version() == 2
+    assert L.sb_abi_version() == 3
     assert isinstance(L.sb_last_error(), str)
 
 
@@ -61,6 +61,9 @@ def test_workspace_bytes(L):
     assert L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10_000, m=10, n_bins=256, k=5, depth=3) > 0
     with pytest.raises(L.SBError):
         L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=10, m=10, n_bins=256, k=5, depth=13)
+    assert L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=10_000, d=100, n_nodes=64) >= 10_000 * 2
+    with pytest.raises(L.SBError):
+        L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=10_000, d=100, n_nodes=4097)
     with pytest.raises(L.SBError):
         L.sb_workspace_bytes(99)
     with pytest.raises(L.SBError):  # 4 features x 256 bins x 101 channels do not fit the LDS budget
@@ -225,6 +228,34 @@ def grow_args(**kw):
 ])
 def test_grow_tree_rejects(L, kw, code):
     assert _code(L.sb_grow_tree, *grow_args(**kw)) == code
+
+
+def leaf_args(**kw):
+    a = dict(G=F, n=1000, d=10, ld_g=1000, hess=None, ld_hess=0, h=None, row_idx=F, leaf_off=F, n_leaves=64,
+             lam=1.0, V=F, ld_v=10, ws=F, ws_bytes=1 << 30, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=None), 1),
+    (dict(V=None), 1),
+    (dict(row_idx=None), 1),
+    (dict(n=0), 1),
+    (dict(d=0), 1),
+    (dict(n_leaves=0), 1),
+    (dict(n_leaves=4097), 1),
+    (dict(ld_g=999), 2),
+    (dict(hess=F, ld_hess=999), 2),
+    (dict(ld_v=9), 2),
+    (dict(lam=0.0), 1),
+    (dict(lam=float("inf")), 1),
+    (dict(ws_bytes=100), 1),
+    (dict(ws=F + 8), 2),
+])
+def test_leaf_values_rejects(L, kw, code):
+    assert _code(L.sb_leaf_values, *leaf_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_leaf_values")
 
 
 def test_error_text_is_per_thread(L):

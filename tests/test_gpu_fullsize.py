@@ -129,3 +129,29 @@ def test_fullsize_root_histograms_sampled_features(grown):
         mass = oracle.node_histograms(sub, np.abs(GH_o), rows, B)[0]
         ok1, ok2, worst = gu.hist_tolerance_ok(Hg[f], Ho, counts, qexp, mass, chan_max)
         assert ok1 and ok2, (f, worst)
+
+
+def test_fullsize_leaf_values_sampled_leaves(grown):
+    # leaf values of the full-size tree from the full G (eq. 3), in the
+    # configuration bench.py times: unit hessians, all 64 leaves computed,
+    # eight leaves (the largest, the smallest non-empty, six random) checked
+    wl, inp, ss, tree, GH_o, _ = grown
+    G_T = gu.up(inp.G_T)
+    V = ss.leaf_values(G_T).cpu().numpy()
+    gu.sync()
+    off = tree["leaf_off"]
+    sizes = np.diff(off)
+    rng = np.random.default_rng(11)
+    nonempty = np.flatnonzero(sizes > 0)
+    pick = {int(np.argmax(sizes)), int(nonempty[np.argmin(sizes[nonempty])])}
+    pick |= set(int(x) for x in rng.choice(len(sizes), 6, replace=False))
+    assert np.all(V[sizes == 0] == 0)
+    G = inp.G
+    col_max = np.abs(inp.G_T).max(axis=1)
+    for Lf in sorted(pick):
+        rows = tree["row_idx"][off[Lf]:off[Lf + 1]].astype(np.int64)
+        sub_idx = np.arange(rows.size, dtype=np.int32)
+        Vo = oracle.leaf_values(G[rows], sub_idx, np.array([0, rows.size]), wl.lam)
+        ok, worst = gu.leaf_value_error_ok(V[Lf:Lf + 1], Vo, G[rows], [sub_idx.astype(np.int64)], wl.lam,
+                                           col_max=col_max)
+        assert ok, (Lf, worst)
