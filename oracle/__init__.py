@@ -24,6 +24,8 @@ Modules
 ``leaf``    leaf values of a grown tree from the full gradient matrix
             (Section 2 "Finding the leaf values", eq. 3) and the per-leaf
             objective they minimise.
+``boost``   loss derivatives (eq. 2) of softmax and sigmoid cross-entropy,
+            the prediction update and the boosting loop (Section 2).
 
 Parity status: every function is pinned by the non-GPU tests
 (``tests/test_oracle_*.py``) except the exact values of the random draws
@@ -48,3 +50,4 @@ from .split import (  # noqa: F401
 )
 from .brute import brute_best_split, brute_tree, exact_region_score  # noqa: F401
 from .leaf import leaf_rows, leaf_values, leaf_objective  # noqa: F401
+from . import boost  # noqa: F401
