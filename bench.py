@@ -73,6 +73,51 @@ def leaf_algorithmic_bytes(n, d, n_leaves):
     return n * d * 4 + 4 * n + n_leaves * d * 8
 
 
+def boost_leg(wl, inp, dev, L, warm=100, timed=100):
+    """The whole boosting step on the workload (Section 2), timed as in Appendix B.7:
+    iterations warm+1 .. warm+timed, so that set-up costs drop out.  Starts from
+    zero scores with the workload's labels; learning rate 0.01."""
+    import torch
+    from paper_2211_12858_amd.driver import Booster
+    if wl.loss != "softmax":
+        return None
+    bst = Booster(inp.bins, wl.n_bins, wl.d, "softmax", wl.kind, wl.k, wl.depth, wl.lam, lr=0.01, device=dev)
+    bst.set_target(torch.from_numpy(inp.y).to(dev))
+    Pi = torch.from_numpy(inp.Pi).to(dev)
+    rng = np.random.default_rng(wl.seed + 2000)
+    u_all = torch.from_numpy(rng.random((warm + timed, wl.k))).to(dev)
+    for s in range(warm):
+        bst.step(u=u_all[s], Pi=Pi)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for s in range(timed):
+        bst.step(u=u_all[warm + s], Pi=Pi)
+    b.record()
+    torch.cuda.synchronize()
+    it_ms = a.elapsed_time(b) / timed
+    # the gradient pass on its own (scores, labels and norms in; G, hessians out)
+    a.record()
+    for _ in range(10):
+        bst.gradients()
+    b.record()
+    torch.cuda.synchronize()
+    g_ms = a.elapsed_time(b) / 10
+    n, d = wl.n, wl.d
+    g_bytes = 3 * n * d * 4 + 4 * n  # scores read, G and hessians written, labels read
+    log("bench: boosting iteration %.3f ms (gradient pass %.3f ms)" % (it_ms, g_ms))
+    return {
+        "ms_per_iteration": it_ms,
+        "iterations": "%d-%d (the difference protocol of the synthetic experiment)" % (warm + 1, warm + timed),
+        "what": "softmax-CE gradients with column norms, sketch from those norms, tree, leaf values with the "
+                "full G and per-element hessians, score update; lr 0.01, zero initial scores",
+        "gradient_pass_ms": g_ms,
+        "gradient_pass_bytes": g_bytes,
+        "gradient_pass_GBps": g_bytes / (g_ms * 1e-3) / 1e9,
+    }
+
+
 def hist_source_hash():
     """sha256 over the histogram kernel's source files (the traffic record is tied to it)."""
     h = hashlib.sha256()
@@ -137,6 +182,7 @@ def main():
     ap.add_argument("--workload", default="mc2m_rs5")
     ap.add_argument("--cpu-sample-rows", type=int, default=800_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-boost", action="store_true", help="skip the boosting-loop leg")
     ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
     args = ap.parse_args()
 
@@ -215,6 +261,8 @@ def main():
     leaf_bytes = leaf_algorithmic_bytes(wl.n, wl.d, 1 << wl.depth)
     log("bench: leaf values %.3f ms per tree" % leaf_ms)
 
+    boost = None if args.no_boost else boost_leg(wl, inp, dev, L)
+
     sec_per_tree = total_ms / K / 1e3
     out = {
         "metric": METRIC,
@@ -259,6 +307,8 @@ def main():
                     % (1 << wl.depth, wl.d),
         },
     }
+    if boost is not None:
+        out["next"]["boosting"] = boost
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_sample_rows)

@@ -98,7 +98,15 @@ enum {
   SB_CALL_PARTITION_ROWS = 3,
   SB_CALL_GROW_TREE = 4,
   SB_CALL_HIST_EXPONENTS = 5,
-  SB_CALL_LEAF_VALUES = 6
+  SB_CALL_LEAF_VALUES = 6,
+  SB_CALL_GRADIENTS = 7,
+  SB_CALL_UPDATE_PREDICTIONS = 8
+};
+
+/* Losses of sb_gradients (the cross-entropies of the paper's experiments). */
+enum {
+  SB_LOSS_SOFTMAX_CE = 0,  /* multiclass: softmax cross-entropy, one label per row */
+  SB_LOSS_SIGMOID_BCE = 1  /* multilabel: binary cross-entropy per output, sigmoid link */
 };
 
 /* Text of the last non-OK status returned on this thread ("" if none). */
@@ -111,8 +119,9 @@ int32_t sb_abi_version(void);
  * Workspace bytes needed by one call.  Arguments not used by a call are
  * ignored (pass 0).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
  * SCORE_SPLITS, PARTITION_ROWS), leaves (LEAF_VALUES).  depth: tree depth
- * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES; the LEAF_VALUES size
- * covers all three hessian forms).  Returns -1 (and sets the error text) for invalid
+ * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES, GRADIENTS; the
+ * LEAF_VALUES size covers all three hessian forms).  UPDATE_PREDICTIONS needs
+ * only n.  Returns -1 (and sets the error text) for invalid
  * sizes.  sb_layout_bins and sb_subtract_histograms need no workspace.
  */
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
@@ -170,6 +179,18 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
 int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
                   const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
                   double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_sketch_given_norms -- sb_sketch with the squared column norms of G as an
+ * INPUT (norm2: d fp64 values, for example from sb_gradients), so that G is
+ * not read for them.  TOP_OUTPUTS and RANDOM_SAMPLING rank and draw by these
+ * values; the other kinds ignore them.  Every other argument, output and rule
+ * is that of sb_sketch; the workspace size is sb_sketch's.
+ */
+int32_t sb_sketch_given_norms(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h,
+                              int32_t k, const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols,
+                              float* scales, const double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes,
+                              void* stream);
 
 /*
  * sb_hist_exponents -- fixed-point exponents for a given GH (row-major).
@@ -314,6 +335,43 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
 int32_t sb_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
                        const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
                        double lambda, double* V, int64_t ld_v, void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_gradients -- first and second derivatives of the loss at the current
+ * predictions (Section 2, eq. 2), with the squared column norms of G that the
+ * sketch ranks and draws by (Sections 3.1, 3.2) summed in the same pass.
+ *
+ * F        n x d raw scores, column-major: (i, j) at F[j*ld_f + i], ld_f >= n.
+ * loss     SB_LOSS_SOFTMAX_CE: labels[i] in [0, d) (int32, n entries; Y
+ *            unused).  p = softmax(F_i); g_ij = p_ij - [j == labels[i]],
+ *            h_ij = p_ij (1 - p_ij) (the diagonal of the softmax Hessian).
+ *          SB_LOSS_SIGMOID_BCE: Y n x d uint8 0/1 targets, column-major with
+ *            ld_y >= n (labels unused).  s = sigmoid(F); g_ij = s_ij - Y_ij,
+ *            h_ij = s_ij (1 - s_ij).
+ * G        out: n x d fp32 gradients, column-major, ld_g >= n.
+ * hess     out (may be NULL): n x d fp32 h_ij, column-major, ld_hess >= n.
+ * h_row    out (may be NULL): n fp32 row means of h_ij (one weight per row).
+ * norm2    out (may be NULL): d fp64 values sum_i G[i, j]^2 of the stored G,
+ *          added in a fixed order (deterministic).
+ * fp32 arithmetic with the library's expf; labels outside [0, d) give a row
+ * without a target column.  F and G must not overlap.
+ */
+int32_t sb_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
+                     const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
+                     float* h_row, double* norm2, void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_update_predictions -- the model update a_t = a_{t-1} + lr * f_t
+ * (Section 2): for every row i in leaf L of the grown tree and output j,
+ *   F[j*ld_f + i] = fp32( (double)F[j*ld_f + i] + lr * V[L*ld_v + j] ),
+ * the product and the sum in fp64, rounded once.
+ * row_idx, leaf_off, n_leaves: the leaf segments as sb_grow_tree writes them
+ * (1 <= n_leaves <= 4096).  V: n_leaves x d fp64 leaf values (sb_leaf_values),
+ * ld_v >= d.  F is updated in place.
+ */
+int32_t sb_update_predictions(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                              const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                              void* ws, int64_t ws_bytes, void* stream);
 
 /*
  * Kernel timing for benchmarks.  Between sb_profile_begin() and

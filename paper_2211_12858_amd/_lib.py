@@ -18,7 +18,9 @@ LIB_PATH = os.path.join(HERE, "libsketchboost.so")
 SB_OK, SB_E_ARG, SB_E_SHAPE, SB_E_UNSUPPORTED, SB_E_DEVICE = 0, 1, 2, 3, 4
 SB_SKETCH_TOP_OUTPUTS, SB_SKETCH_RANDOM_SAMPLING, SB_SKETCH_RANDOM_PROJECTION, SB_SKETCH_IDENTITY = 0, 1, 2, 3
 (SB_CALL_SKETCH, SB_CALL_BUILD_HISTOGRAMS, SB_CALL_SCORE_SPLITS, SB_CALL_PARTITION_ROWS, SB_CALL_GROW_TREE,
- SB_CALL_HIST_EXPONENTS, SB_CALL_LEAF_VALUES) = range(7)
+ SB_CALL_HIST_EXPONENTS, SB_CALL_LEAF_VALUES, SB_CALL_GRADIENTS, SB_CALL_UPDATE_PREDICTIONS) = range(9)
+SB_LOSS_SOFTMAX_CE, SB_LOSS_SIGMOID_BCE = 0, 1
+LOSS = {"softmax": SB_LOSS_SOFTMAX_CE, "sigmoid": SB_LOSS_SIGMOID_BCE}
 
 KIND = {
     "top_outputs": SB_SKETCH_TOP_OUTPUTS,
@@ -34,6 +36,7 @@ SYMBOLS = (
     "sb_workspace_bytes",
     "sb_layout_bins",
     "sb_sketch",
+    "sb_sketch_given_norms",
     "sb_hist_exponents",
     "sb_build_histograms",
     "sb_subtract_histograms",
@@ -41,6 +44,8 @@ SYMBOLS = (
     "sb_partition_rows",
     "sb_grow_tree",
     "sb_leaf_values",
+    "sb_gradients",
+    "sb_update_predictions",
     "sb_profile_begin",
     "sb_profile_end",
 )
@@ -76,6 +81,9 @@ _PROTOS = {
 
 _PROTOS["sb_leaf_values"] = (_I32, [_P, _I64, _I32, _I64, _P, _I64, _P, _P, _P, _I32, _F64, _P, _I64, _P, _I64,
                                      _P])
+_PROTOS["sb_sketch_given_norms"] = _PROTOS["sb_sketch"]
+_PROTOS["sb_gradients"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _I64, _P])
+_PROTOS["sb_update_predictions"] = (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _I64, _F64, _P, _I64, _P])
 _PROTOS["sb_profile_begin"] = (_I32, [])
 _PROTOS["sb_profile_end"] = (_I32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)])
 
@@ -147,6 +155,13 @@ def sb_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, 
                                    _stream(stream)))
 
 
+def sb_sketch_given_norms(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws, ws_bytes,
+                          stream=None):
+    return _check(load().sb_sketch_given_norms(kind, _ptr(G), n, d, ld_g, _ptr(h), k, _ptr(u), _ptr(Pi), _ptr(GH),
+                                               ld_gh, _ptr(cols), _ptr(scales), _ptr(norm2), _ptr(qexp), _ptr(ws),
+                                               ws_bytes, _stream(stream)))
+
+
 def sb_hist_exponents(GH, n, ld_gh, k, qexp, ws, ws_bytes, stream=None):
     return _check(load().sb_hist_exponents(_ptr(GH), n, ld_gh, k, _ptr(qexp), _ptr(ws), ws_bytes, _stream(stream)))
 
@@ -191,6 +206,18 @@ def sb_leaf_values(G, n, d, ld_g, hess, ld_hess, h, row_idx, leaf_off, n_leaves,
     return _check(load().sb_leaf_values(_ptr(G), n, d, ld_g, _ptr(hess), ld_hess, _ptr(h), _ptr(row_idx),
                                         _ptr(leaf_off), n_leaves, lam, _ptr(V), ld_v, _ptr(ws), ws_bytes,
                                         _stream(stream)))
+
+
+def sb_gradients(loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, norm2, ws, ws_bytes,
+                 stream=None):
+    return _check(load().sb_gradients(loss, _ptr(F), n, d, ld_f, _ptr(labels), _ptr(Y), ld_y, _ptr(G), ld_g,
+                                      _ptr(hess), ld_hess, _ptr(h_row), _ptr(norm2), _ptr(ws), ws_bytes,
+                                      _stream(stream)))
+
+
+def sb_update_predictions(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws, ws_bytes, stream=None):
+    return _check(load().sb_update_predictions(_ptr(F), n, d, ld_f, _ptr(row_idx), _ptr(leaf_off), n_leaves, _ptr(V),
+                                               ld_v, lr, _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def sb_profile_begin():

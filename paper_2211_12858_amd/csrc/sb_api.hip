@@ -195,6 +195,12 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
       if (b < 0) break;
       return b;
     }
+    case SB_CALL_GRADIENTS:
+      if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535) break;
+      return grad_ws_bytes(n, d);
+    case SB_CALL_UPDATE_PREDICTIONS:
+      if (n < 1 || n > MAX_ROWS) break;
+      return update_ws_bytes(n);
     case SB_CALL_LEAF_VALUES:
       if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535 || n_nodes < 1 || n_nodes > MAX_LEAVES) break;
       return leaf_ws_bytes(n, d, n_nodes);
@@ -221,41 +227,68 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
                        static_cast<hipStream_t>(stream));
 }
 
-int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
-                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+int32_t check_sketch(const char* call, int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g,
+                     const float* h, int32_t k, const double* u, const float* Pi, float* GH, int64_t ld_gh,
+                     int32_t* cols, float* scales, const double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes) {
+  const std::string c(call);
   if (kind < SB_SKETCH_TOP_OUTPUTS || kind > SB_SKETCH_IDENTITY)
-    return fail(SB_E_UNSUPPORTED, "sb_sketch: unknown sketch kind " + std::to_string(kind));
-  if (!G || !h || !GH || !qexp) return fail(SB_E_ARG, "sb_sketch: G, h, GH and qexp must not be NULL");
-  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_sketch: n must be in [1, 2^31)");
-  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_sketch: d must be in [1, 65535]");
-  if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_sketch: k must be in [1, 255]");
-  if (ld_g < n) return fail(SB_E_SHAPE, "sb_sketch: ld_g must be >= n");
+    return fail(SB_E_UNSUPPORTED, c + ": unknown sketch kind " + std::to_string(kind));
+  if (!G || !h || !GH || !qexp) return fail(SB_E_ARG, c + ": G, h, GH and qexp must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, c + ": n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, c + ": d must be in [1, 65535]");
+  if (k < 1 || k > 255) return fail(SB_E_ARG, c + ": k must be in [1, 255]");
+  if (ld_g < n) return fail(SB_E_SHAPE, c + ": ld_g must be >= n");
   {
-    const int32_t rr = check_gh("sb_sketch", GH, ld_gh, k);
+    const int32_t rr = check_gh(call, GH, ld_gh, k);
     if (rr) return rr;
   }
   switch (kind) {
     case SB_SKETCH_TOP_OUTPUTS:
-      if (k > d) return fail(SB_E_ARG, "sb_sketch: top outputs needs k <= d");
-      if (!cols || !scales || !norm2) return fail(SB_E_ARG, "sb_sketch: cols, scales and norm2 must not be NULL");
+      if (k > d) return fail(SB_E_ARG, c + ": top outputs needs k <= d");
+      if (!cols || !scales || !norm2) return fail(SB_E_ARG, c + ": cols, scales and norm2 must not be NULL");
       break;
     case SB_SKETCH_RANDOM_SAMPLING:
-      if (!u) return fail(SB_E_ARG, "sb_sketch: random sampling needs k uniforms u");
-      if (!cols || !scales || !norm2) return fail(SB_E_ARG, "sb_sketch: cols, scales and norm2 must not be NULL");
+      if (!u) return fail(SB_E_ARG, c + ": random sampling needs k uniforms u");
+      if (!cols || !scales || !norm2) return fail(SB_E_ARG, c + ": cols, scales and norm2 must not be NULL");
       break;
     case SB_SKETCH_RANDOM_PROJECTION:
-      if (!Pi) return fail(SB_E_ARG, "sb_sketch: random projection needs Pi");
+      if (!Pi) return fail(SB_E_ARG, c + ": random projection needs Pi");
       break;
     case SB_SKETCH_IDENTITY:
-      if (k != d) return fail(SB_E_ARG, "sb_sketch: identity sketch needs k == d");
-      if (!cols || !scales) return fail(SB_E_ARG, "sb_sketch: cols and scales must not be NULL");
+      if (k != d) return fail(SB_E_ARG, c + ": identity sketch needs k == d");
+      if (!cols || !scales) return fail(SB_E_ARG, c + ": cols and scales must not be NULL");
       break;
   }
-  int32_t rc = need_ws(ws, ws_bytes, sketch_ws_bytes(kind, n, d, k), "sb_sketch");
+  return need_ws(ws, ws_bytes, sketch_ws_bytes(kind, n, d, k), call);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t sb_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                  const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
+                  double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
+  const int32_t rc = check_sketch("sb_sketch", kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp,
+                                  ws, ws_bytes);
   if (rc) return rc;
   return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, norm2, qexp, ws,
                        static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_sketch_given_norms(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h,
+                              int32_t k, const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols,
+                              float* scales, const double* norm2, int32_t* qexp, void* ws, int64_t ws_bytes,
+                              void* stream) {
+  const int32_t rc = check_sketch("sb_sketch_given_norms", kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales,
+                                  norm2, qexp, ws, ws_bytes);
+  if (rc) return rc;
+  return launch_sketch(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, scales, nullptr, qexp, ws,
+                       static_cast<hipStream_t>(stream), norm2);
 }
 
 int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
@@ -455,6 +488,48 @@ int32_t sb_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const
   if (rc) return rc;
   return launch_leaf_values(G, n, d, ld_g, hess, ld_hess, h, row_idx, leaf_off, n_leaves, lambda, V, ld_v, ws,
                             static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
+                     const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
+                     float* h_row, double* norm2, void* ws, int64_t ws_bytes, void* stream) {
+  if (loss != SB_LOSS_SOFTMAX_CE && loss != SB_LOSS_SIGMOID_BCE)
+    return fail(SB_E_UNSUPPORTED, "sb_gradients: unknown loss " + std::to_string(loss));
+  if (!F || !G) return fail(SB_E_ARG, "sb_gradients: F and G must not be NULL");
+  if (loss == SB_LOSS_SOFTMAX_CE && !labels) return fail(SB_E_ARG, "sb_gradients: softmax needs labels");
+  if (loss == SB_LOSS_SIGMOID_BCE && !Y) return fail(SB_E_ARG, "sb_gradients: sigmoid needs the targets Y");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_gradients: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_gradients: d must be in [1, 65535]");
+  if (ld_f < n || ld_g < n) return fail(SB_E_SHAPE, "sb_gradients: ld_f and ld_g must be >= n");
+  if (hess && ld_hess < n) return fail(SB_E_SHAPE, "sb_gradients: ld_hess must be >= n");
+  if (loss == SB_LOSS_SIGMOID_BCE && ld_y < n) return fail(SB_E_SHAPE, "sb_gradients: ld_y must be >= n");
+  {
+    const char* f0 = reinterpret_cast<const char*>(F);
+    const char* g0 = reinterpret_cast<const char*>(G);
+    const int64_t fb = ((int64_t)(d - 1) * ld_f + n) * 4, gb = ((int64_t)(d - 1) * ld_g + n) * 4;
+    if (f0 < g0 + gb && g0 < f0 + fb) return fail(SB_E_SHAPE, "sb_gradients: F and G overlap");
+  }
+  const int32_t rc = need_ws(ws, ws_bytes, norm2 ? grad_ws_bytes(n, d) : 0, "sb_gradients");
+  if (rc) return rc;
+  return launch_gradients(loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, norm2, ws,
+                          static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_update_predictions(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                              const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                              void* ws, int64_t ws_bytes, void* stream) {
+  if (!F || !row_idx || !leaf_off || !V)
+    return fail(SB_E_ARG, "sb_update_predictions: F, row_idx, leaf_off and V must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_update_predictions: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_update_predictions: d must be in [1, 65535]");
+  if (n_leaves < 1 || n_leaves > MAX_LEAVES)
+    return fail(SB_E_ARG, "sb_update_predictions: n_leaves must be in [1, 4096]");
+  if (ld_f < n) return fail(SB_E_SHAPE, "sb_update_predictions: ld_f must be >= n");
+  if (ld_v < d) return fail(SB_E_SHAPE, "sb_update_predictions: ld_v must be >= d");
+  if (!std::isfinite(lr)) return fail(SB_E_ARG, "sb_update_predictions: lr must be finite");
+  const int32_t rc = need_ws(ws, ws_bytes, update_ws_bytes(n), "sb_update_predictions");
+  if (rc) return rc;
+  return launch_update(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

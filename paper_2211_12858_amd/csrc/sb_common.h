@@ -20,9 +20,10 @@ int32_t check_launch(const char* what);
 int32_t launch_layout(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bins, uint32_t* bins4, int64_t ld4,
                       uint8_t* bins_cm, int64_t ld_cm, uint8_t* rec, int64_t ld_rec, hipStream_t st);
 
+// norm2_in: the squared column norms as an input (G is not read for them), or NULL.
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
                       const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                      double* norm2, int32_t* qexp, void* ws, hipStream_t st);
+                      double* norm2, int32_t* qexp, void* ws, hipStream_t st, const double* norm2_in = nullptr);
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k);
 int64_t hist_exponents_ws_bytes(int32_t k);
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
@@ -59,6 +60,14 @@ int64_t leaf_ws_bytes(int64_t n, int32_t d, int32_t n_leaves);
 int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,
                            const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
                            double lambda, double* V, int64_t ld_v, void* ws, hipStream_t st);
+
+int64_t grad_ws_bytes(int64_t n, int32_t d);
+int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
+                         const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
+                         float* h_row, double* norm2, void* ws, hipStream_t st);
+int64_t update_ws_bytes(int64_t n);
+int32_t launch_update(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx, const int32_t* leaf_off,
+                      int32_t n_leaves, const double* V, int64_t ld_v, double lr, void* ws, hipStream_t st);
 
 // ---------------------------------------------------------------- profiling
 // Event pairs around histogram-kernel launches while profiling is on (per thread).

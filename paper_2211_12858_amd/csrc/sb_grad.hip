@@ -1,0 +1,254 @@
+// Loss derivatives with fused column norms, and the prediction update
+// (Section 2: eq. 2 gives the first and second derivatives of the loss at the
+// current predictions; the model is updated by a_t = a_{t-1} + eps * f_t).
+//
+// k_grad: one thread per row, the rows of a block in one 256-row tile, tiles
+//   grid-strided.  The lanes of a wave take consecutive rows, so every load
+//   and store is one 256-byte run of a column of the column-major matrices.
+//   Softmax cross-entropy: a first pass over the row's scores keeps a running
+//   maximum and the sum of exp(a - max), rescaled chunk by chunk; the second
+//   pass re-reads the scores and writes g = p - onehot(y), h = p (1 - p).
+//   Sigmoid cross-entropy needs one pass: g = s - Y, h = s (1 - s).
+//   The squared column norms of the stored G (what Top Outputs and Random
+//   Sampling rank and draw by, Sections 3.1, 3.2) are summed in the same pass:
+//   each 16-column chunk of g goes through LDS, 16 threads per column add 16
+//   rows each in fp64, a fixed butterfly joins them, and one thread adds the
+//   tile's sum to the block's partial (a fixed order).  k_grad_norm_final adds
+//   the blocks' partials in a fixed order, so the norms are deterministic.
+// k_update: F[i, j] += lr * V[leaf of i, j] in fp64, rounded once to fp32.
+//   lr * V of a chunk of columns is staged in LDS; the leaf ids come from the
+//   leaf segments (k_leaf_ids, shared with the leaf values).
+#include <cmath>
+
+#include "sb_common.h"
+#include "sb_leaf_ids.h"
+
+namespace sb {
+namespace {
+
+constexpr int GRAD_THREADS = 256;
+constexpr int GRAD_JA = 8;          // columns per load batch of the softmax first pass
+constexpr int GRAD_JC = 16;         // columns per chunk of the second pass (norm staging)
+constexpr int GRAD_MAX_BLOCKS = 2048;
+constexpr int UPD_THREADS = 256;
+constexpr int UPD_LDS_DOUBLES = 8192;  // lr * V of one column chunk: at most 64 KB
+constexpr int UPD_JC = 16;             // columns per chunk at most
+constexpr int UPD_MAX_BLOCKS = 2048;
+
+struct GradArgs {
+  int loss;
+  const float* F;
+  int64_t n;
+  int32_t d;
+  int64_t ld_f;
+  const int32_t* labels;
+  const uint8_t* Y;
+  int64_t ld_y;
+  float* G;
+  int64_t ld_g;
+  float* hess;
+  int64_t ld_h;
+  float* h_row;
+  double* npart;  // [d][blocks] or NULL
+  int32_t n_tiles;
+};
+
+__global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
+  __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
+  const int tid = threadIdx.x;
+  const int d = a.d;
+  const float inv_d = 1.0f / (float)d;
+  bool first = true;
+  for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+    const int64_t row = (int64_t)tile * GRAD_THREADS + tid;
+    const bool ok = row < a.n;
+    const int64_t rc = ok ? row : a.n - 1;  // rows past the end read row n-1 and store nothing
+    float m = -INFINITY, s = 0.0f, inv = 0.0f;
+    int y = -1;
+    if (a.loss == SB_LOSS_SOFTMAX_CE) {
+      y = a.labels[rc];
+      for (int j0 = 0; j0 < d; j0 += GRAD_JA) {
+        float x[GRAD_JA];
+        // columns past d (last chunk only) repeat column d-1: a repeat of
+        // the row's own score leaves the maximum unchanged, and its exp is
+        // dropped from the sum below
+#pragma unroll
+        for (int u = 0; u < GRAD_JA; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
+        float cm = x[0];
+#pragma unroll
+        for (int u = 1; u < GRAD_JA; ++u) cm = fmaxf(cm, x[u]);
+        const float mn = fmaxf(m, cm);
+        float add = 0.0f;
+#pragma unroll
+        for (int u = 0; u < GRAD_JA; ++u) add += (j0 + u < d) ? expf(x[u] - mn) : 0.0f;
+        s = s * expf(m - mn) + add;
+        m = mn;
+      }
+      inv = 1.0f / s;
+    }
+    float hsum = 0.0f;
+    for (int j0 = 0; j0 < d; j0 += GRAD_JC) {
+      float x[GRAD_JC];
+#pragma unroll
+      for (int u = 0; u < GRAD_JC; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
+      uint8_t yb[GRAD_JC];
+      if (a.loss == SB_LOSS_SIGMOID_BCE) {
+#pragma unroll
+        for (int u = 0; u < GRAD_JC; ++u) yb[u] = a.Y[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_y + rc];
+      }
+#pragma unroll
+      for (int u = 0; u < GRAD_JC; ++u) {
+        const int j = j0 + u;
+        float g = 0.0f, hh = 0.0f;
+        if (j < d) {
+          if (a.loss == SB_LOSS_SOFTMAX_CE) {
+            const float p = expf(x[u] - m) * inv;
+            g = (j == y) ? p - 1.0f : p;
+            hh = p * (1.0f - p);
+          } else {
+            // e = exp(-|a|) never overflows, so s keeps its relative accuracy
+            // for scores far below zero (down to fp32's subnormals)
+            const float e = expf(-fabsf(x[u]));
+            const float sg = x[u] >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
+            g = sg - (float)yb[u];
+            hh = sg * (1.0f - sg);
+          }
+          if (ok) {
+            a.G[(int64_t)j * a.ld_g + row] = g;
+            if (a.hess) a.hess[(int64_t)j * a.ld_h + row] = hh;
+          }
+          hsum += hh;
+        }
+        gbuf[u][tid] = ok ? g : 0.0f;
+      }
+      if (a.npart) {
+        __syncthreads();
+        // 16 threads per column, 16 rows each; lanes c*16 .. c*16+15 share column c
+        const int c = tid >> 4, seg = tid & 15;
+        const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
+        double acc = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = src[q];
+          acc += (double)v.x * v.x;
+          acc += (double)v.y * v.y;
+          acc += (double)v.z * v.z;
+          acc += (double)v.w * v.w;
+        }
+        for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+        if (seg == 0 && j0 + c < d) {
+          double* p = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
+          *p = first ? acc : *p + acc;
+        }
+        __syncthreads();
+      }
+    }
+    if (a.h_row && ok) a.h_row[row] = hsum * inv_d;
+    first = false;
+  }
+  // a block without tiles still defines its partials
+  if (a.npart && first)
+    for (int j = tid; j < d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
+}
+
+// One wave per column: lane l adds partials l, l+64, ... in order, then a fixed butterfly.
+__global__ void __launch_bounds__(256) k_grad_norm_final(const double* __restrict__ npart, int32_t d, int32_t parts,
+                                                         double* __restrict__ norm2) {
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (j >= d) return;
+  double s = 0.0;
+  for (int p = lane; p < parts; p += 64) s += npart[(int64_t)j * parts + p];
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (lane == 0) norm2[j] = s;
+}
+
+struct UpdArgs {
+  float* F;
+  int64_t n;
+  int32_t d;
+  int64_t ld_f;
+  const void* ids;
+  int32_t n_leaves;
+  const double* V;
+  int64_t ld_v;
+  double lr;
+  int32_t jc;  // columns per chunk
+  int32_t n_tiles;
+};
+
+template <typename LT>
+__global__ void __launch_bounds__(UPD_THREADS) k_update(UpdArgs a) {
+  // lr * V of the chunk's columns, leaf-major with an odd stride (jc + 1
+  // doubles) so that lanes of different leaves fall on different banks
+  extern __shared__ double lv[];
+  const LT* ids = static_cast<const LT*>(a.ids);
+  const int top = a.n_leaves - 1;
+  const int stride = a.jc + 1;
+  for (int j0 = 0; j0 < a.d; j0 += a.jc) {
+    const int w = (a.d - j0 < a.jc) ? a.d - j0 : a.jc;
+    __syncthreads();  // the previous chunk's readers are done
+    for (int e = threadIdx.x; e < a.n_leaves * a.jc; e += UPD_THREADS) {
+      const int L = e / a.jc, u = e - L * a.jc;
+      lv[L * stride + u] = u < w ? a.lr * a.V[(int64_t)L * a.ld_v + j0 + u] : 0.0;
+    }
+    __syncthreads();
+    for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+      const int64_t row = (int64_t)tile * UPD_THREADS + threadIdx.x;
+      const bool ok = row < a.n;
+      const int64_t rc = ok ? row : a.n - 1;
+      int L = (int)ids[rc];
+      L = L > top ? top : L;
+      const double* lvL = lv + L * stride;
+      // every load of the chunk first (columns past w repeat the last one),
+      // then the sums and the stores
+      float f[UPD_JC];
+#pragma unroll
+      for (int u = 0; u < UPD_JC; ++u) f[u] = a.F[(int64_t)(j0 + (u < w ? u : w - 1)) * a.ld_f + rc];
+#pragma unroll
+      for (int u = 0; u < UPD_JC; ++u)
+        if (u < w && ok) a.F[(int64_t)(j0 + u) * a.ld_f + row] = (float)((double)f[u] + lvL[u]);
+    }
+  }
+}
+
+}  // namespace
+
+int64_t grad_ws_bytes(int64_t n, int32_t d) {
+  const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
+  const int64_t blocks = tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS;
+  return align256((int64_t)d * blocks * 8);
+}
+
+int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
+                         const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
+                         float* h_row, double* norm2, void* ws, hipStream_t st) {
+  const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
+  const int blocks = (int)(tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS);
+  double* npart = norm2 ? static_cast<double*>(ws) : nullptr;
+  const GradArgs a{loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, npart, (int32_t)tiles};
+  hipLaunchKernelGGL(k_grad, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, blocks, norm2);
+  return check_launch("sb_gradients");
+}
+
+int64_t update_ws_bytes(int64_t n) { return leaf_ids_bytes(n); }
+
+int32_t launch_update(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx, const int32_t* leaf_off,
+                      int32_t n_leaves, const double* V, int64_t ld_v, double lr, void* ws, hipStream_t st) {
+  const int64_t tiles = (n + UPD_THREADS - 1) / UPD_THREADS;
+  const int blocks = (int)(tiles < UPD_MAX_BLOCKS ? tiles : UPD_MAX_BLOCKS);
+  int jc = UPD_LDS_DOUBLES / n_leaves - 1;  // (jc + 1) doubles per leaf
+  if (jc > UPD_JC) jc = UPD_JC;
+  if (jc > d) jc = d;
+  launch_leaf_ids(row_idx, leaf_off, n_leaves, n, ws, st);
+  const UpdArgs a{F, n, d, ld_f, ws, n_leaves, V, ld_v, lr, jc, (int32_t)tiles};
+  const size_t lds = (size_t)n_leaves * (jc + 1) * 8;
+  if (n_leaves <= 256)
+    hipLaunchKernelGGL(k_update<uint8_t>, dim3(blocks), dim3(UPD_THREADS), lds, st, a);
+  else
+    hipLaunchKernelGGL(k_update<uint16_t>, dim3(blocks), dim3(UPD_THREADS), lds, st, a);
+  return check_launch("sb_update_predictions");
+}
+
+}  // namespace sb

@@ -7,7 +7,7 @@
 // A leaf's rows are scattered over the rows of G, and G is column-major, so
 // gathering a leaf's rows would fetch a whole 32-byte sector for every 4-byte
 // value.  The path streams G once, in row order, instead:
-//   k_leaf_of     writes every row's leaf id (uint16) from the leaf segments;
+//   k_leaf_ids    writes every row's leaf id from the leaf segments;
 //   k_leaf_accum  one block per (chunk of J channels, split of the rows).  The
 //                 lanes take consecutive rows of a column (256-byte loads per
 //                 wave) and add every value into an LDS cell (leaf, channel);
@@ -29,6 +29,7 @@
 #include <cmath>
 
 #include "sb_common.h"
+#include "sb_leaf_ids.h"
 
 namespace sb {
 namespace {
@@ -40,7 +41,6 @@ constexpr int LEAF_QL = 41;                             // 2^11 rows * 2^41 = 2^
 static_assert((int64_t)LEAF_TILE << LEAF_QL <= (int64_t(1) << 52), "tile sums must stay exact in fp64");
 constexpr int64_t LEAF_LDS_MAX = 64 * 1024;             // integer + fp64 cells of one block
 constexpr int LEAF_TARGET_BLOCKS = 4096;                // 16 per CU
-constexpr int LEAF_MAX_LEAVES = 4096;
 // channels per block (fewer for many leaves, so that the cells fit LEAF_LDS_MAX)
 constexpr int LEAF_JMAX = 4;
 
@@ -68,30 +68,6 @@ __device__ inline const float* chan_ptr(const LeafArgs& a, int c) {
 
 // 2^e as a double, for |e| <= 1022.
 __device__ inline double pow2(int e) { return __longlong_as_double((long long)(1023 + e) << 52); }
-
-template <typename LT>
-__global__ void __launch_bounds__(256) k_leaf_of(const int32_t* __restrict__ row_idx,
-                                                  const int32_t* __restrict__ leaf_off, int32_t n_leaves, int64_t n,
-                                                  LT* __restrict__ leaf_of) {
-  __shared__ int32_t soff[LEAF_MAX_LEAVES];
-  for (int L = threadIdx.x; L < n_leaves; L += blockDim.x) soff[L] = leaf_off[L];
-  __syncthreads();
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n; p += stride) {
-    // the last leaf whose segment starts at or before p (empty leaves are skipped)
-    int lo = 0, hi = n_leaves - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if ((int64_t)soff[mid] <= p)
-        lo = mid;
-      else
-        hi = mid - 1;
-    }
-    int64_t r = row_idx[p];
-    r = r < 0 ? 0 : (r >= n ? n - 1 : r);
-    leaf_of[r] = (LT)lo;
-  }
-}
 
 // rint(y) as an int64 for |y| < 2^51: adding 1.5 * 2^52 leaves the integer
 // nearest to y (ties to even) in the low mantissa bits, and the fused
@@ -274,7 +250,7 @@ LeafPlan leaf_plan(int64_t n, int32_t nch, int32_t n_leaves) {
 
 int64_t leaf_ws_for(int64_t n, int32_t nch, int32_t n_leaves) {
   const LeafPlan p = leaf_plan(n, nch, n_leaves);
-  return align256(n * 2) + align256((int64_t)p.splits * n_leaves * nch * 8);
+  return leaf_ids_bytes(n) + align256((int64_t)p.splits * n_leaves * nch * 8);
 }
 
 template <int J, typename LT>
@@ -285,9 +261,7 @@ void launch_accum(const LeafPlan& p, const LeafArgs& a, hipStream_t st) {
 template <typename LT>
 void launch_leaf_kernels(const LeafPlan& p, LeafArgs a, const int32_t* row_idx, const int32_t* leaf_off, void* ids,
                          hipStream_t st) {
-  const int64_t blocks_of = (a.n + 255) / 256;
-  hipLaunchKernelGGL(k_leaf_of<LT>, dim3((unsigned)(blocks_of < 2048 ? blocks_of : 2048)), dim3(256), 0, st, row_idx,
-                     leaf_off, a.n_leaves, a.n, static_cast<LT*>(ids));
+  launch_leaf_ids(row_idx, leaf_off, a.n_leaves, a.n, ids, st);
   a.leaf_of = ids;
   switch (p.J) {
     case 4: launch_accum<4, LT>(p, a, st); break;
@@ -315,7 +289,7 @@ int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, c
   const int32_t nch = d + (hmode == 1 ? d : (hmode == 2 ? 1 : 0));
   const LeafPlan p = leaf_plan(n, nch, n_leaves);
   char* w = static_cast<char*>(ws);
-  double* part = reinterpret_cast<double*>(w + align256(n * 2));
+  double* part = reinterpret_cast<double*>(w + leaf_ids_bytes(n));
   const LeafArgs a{G, ld_g, d, hess, ld_hess, h, nullptr, n, n_leaves, nch, p.n_tiles, p.tps, part};
   if (n_leaves <= 256)
     launch_leaf_kernels<uint8_t>(p, a, row_idx, leaf_off, w, st);

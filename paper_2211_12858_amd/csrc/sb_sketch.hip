@@ -417,7 +417,7 @@ int64_t hist_exponents_ws_bytes(int32_t k) { return align256((int64_t)SKETCH_MAX
 
 int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
                       const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
-                      double* norm2, int32_t* qexp, void* ws, hipStream_t st) {
+                      double* norm2, int32_t* qexp, void* ws, hipStream_t st, const double* norm2_in) {
   const int P = norm_parts(n);
   char* w = static_cast<char*>(ws);
   double* part = reinterpret_cast<double*>(w);
@@ -449,11 +449,14 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
     }
     hipLaunchKernelGGL(k_project_h, dim3(nb), dim3(256), 0, st, h, n, k, GH, ld_gh, blockmax);
   } else {
-    int64_t chunk = (n + P - 1) / P;
-    chunk = (chunk + 3) & ~int64_t(3);
-    hipLaunchKernelGGL(k_colnorm_partial, dim3(P, d), dim3(NORM_THREADS), 0, st, G, n, ld_g, P, chunk, part);
-    hipLaunchKernelGGL(k_colnorm_final, dim3((d + 3) / 4), dim3(256), 0, st, part, d, P, n2, norm2);
-    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, n2, d, k, u, cols, scales, C);
+    if (norm2_in == nullptr) {
+      int64_t chunk = (n + P - 1) / P;
+      chunk = (chunk + 3) & ~int64_t(3);
+      hipLaunchKernelGGL(k_colnorm_partial, dim3(P, d), dim3(NORM_THREADS), 0, st, G, n, ld_g, P, chunk, part);
+      hipLaunchKernelGGL(k_colnorm_final, dim3((d + 3) / 4), dim3(256), 0, st, part, d, P, n2, norm2);
+    }
+    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, norm2_in ? norm2_in : n2, d, k, u, cols, scales,
+                       C);
     nb = sketch_blocks(n, 4 * PACK_ROWS_PER_BLOCK);
     hipLaunchKernelGGL(k_pack, dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, k, cols, scales, GH, ld_gh,
                        blockmax);

@@ -82,8 +82,11 @@ class SplitSearch:
         self.V = None
 
     # ------------------------------------------------------------ sketch
-    def sketch(self, kind, G_T, h, u=None, Pi=None, stream=None):
-        """G_T: (d, n) float32 device tensor (column-major G); h: (n,) float32."""
+    def sketch(self, kind, G_T, h, u=None, Pi=None, stream=None, norm2_in=None):
+        """G_T: (d, n) float32 device tensor (column-major G); h: (n,) float32.
+
+        norm2_in: the squared column norms of G, (d,) fp64 on the device (for
+        example from sb_gradients); then G is not read for them."""
         d, n = G_T.shape
         assert n == self.n and G_T.is_contiguous() and G_T.dtype == torch.float32
         kid = L.KIND[kind]
@@ -92,8 +95,12 @@ class SplitSearch:
             self._ws_sketch = workspace(need, self.device)
         if self.norm2 is None or self.norm2.numel() != d:
             self.norm2 = torch.zeros(d, dtype=torch.float64, device=self.device)
-        L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, self.ld_gh, self.cols, self.scales, self.norm2,
-                    self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
+        if norm2_in is None:
+            L.sb_sketch(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, self.ld_gh, self.cols, self.scales, self.norm2,
+                        self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
+        else:
+            L.sb_sketch_given_norms(kid, G_T, n, d, n, h, self.k, u, Pi, self.GH, self.ld_gh, self.cols, self.scales,
+                                    norm2_in, self.qexp, self._ws_sketch, self._ws_sketch.numel(), stream)
 
     # ------------------------------------------------------------ tree
     def grow(self, stream=None):
@@ -148,3 +155,56 @@ class SplitSearch:
         out["row_idx"] = self.row_idx.cpu().numpy()
         out["leaf_off"] = self.leaf_off.cpu().numpy()
         return out
+
+
+class Booster:
+    """The boosting loop on the device (Section 2), one tree per ``step()``:
+
+    1. derivatives of the loss at the current scores F (eq. 2), with the
+       column norms of G, in one pass (``sb_gradients``);
+    2. the sketch from those norms (``sb_sketch_given_norms``), with the
+       split-search weight h = 1 for softmax (the count weight of S_G) and the
+       row mean of the hessians for sigmoid;
+    3. the tree (``sb_grow_tree``);
+    4. leaf values from the full G and the per-element hessians (eq. 3);
+    5. F += lr * f_t (``sb_update_predictions``).
+
+    F, G and the hessians are (d, n) float32 device tensors (column-major).
+    """
+
+    def __init__(self, bins, n_bins, d, loss, kind, k, depth, lam=1.0, lr=0.01, min_child_weight=0.0,
+                 device="cuda", F0=None):
+        self.ss = SplitSearch(bins, n_bins, k, depth, lam, min_child_weight, device=device)
+        dev, n = self.ss.device, self.ss.n
+        self.n, self.d, self.loss, self.kind, self.lr = n, d, loss, kind, float(lr)
+        self.F = torch.zeros((d, n), dtype=torch.float32, device=dev) if F0 is None else F0.clone()
+        self.G = torch.empty((d, n), dtype=torch.float32, device=dev)
+        self.hess = torch.empty((d, n), dtype=torch.float32, device=dev)
+        self.h_row = torch.empty(n, dtype=torch.float32, device=dev)
+        self.ones = torch.ones(n, dtype=torch.float32, device=dev)
+        self.norm2 = torch.zeros(d, dtype=torch.float64, device=dev)
+        self.ws_grad = workspace(L.sb_workspace_bytes(L.SB_CALL_GRADIENTS, n=n, d=d), dev)
+        self.ws_upd = workspace(L.sb_workspace_bytes(L.SB_CALL_UPDATE_PREDICTIONS, n=n), dev)
+        self.labels = None
+        self.Y = None
+
+    def set_target(self, target):
+        """Labels (n,) int32 for softmax, or a (d, n) uint8 0/1 matrix for sigmoid (device tensors)."""
+        if self.loss == "softmax":
+            self.labels = target
+        else:
+            self.Y = target
+
+    def gradients(self, stream=None):
+        n, d = self.n, self.d
+        L.sb_gradients(L.LOSS[self.loss], self.F, n, d, n, self.labels, self.Y, n, self.G, n, self.hess, n,
+                       self.h_row, self.norm2, self.ws_grad, self.ws_grad.numel(), stream)
+
+    def step(self, u=None, Pi=None, stream=None):
+        self.gradients(stream)
+        h = self.ones if self.loss == "softmax" else self.h_row
+        self.ss.sketch(self.kind, self.G, h, u=u, Pi=Pi, stream=stream, norm2_in=self.norm2)
+        self.ss.grow(stream)
+        V = self.ss.leaf_values(self.G, hess_T=self.hess, stream=stream)
+        L.sb_update_predictions(self.F, self.n, self.d, self.n, self.ss.row_idx, self.ss.leaf_off, V.shape[0], V,
+                                self.d, self.lr, self.ws_upd, self.ws_upd.numel(), stream)

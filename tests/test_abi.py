@@ -34,7 +34,8 @@ def header_functions():
 def test_header_declares_the_boundary():
     fns = header_functions()
     for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
-                 "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_leaf_values", "sb_last_error",
+                 "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_leaf_values", "sb_gradients",
+                 "sb_update_predictions", "sb_sketch_given_norms", "sb_last_error",
                  "sb_abi_version", "sb_workspace_bytes"):
         assert name in fns
 
@@ -256,6 +257,60 @@ def leaf_args(**kw):
 def test_leaf_values_rejects(L, kw, code):
     assert _code(L.sb_leaf_values, *leaf_args(**kw)) == code
     assert L.sb_last_error().startswith("sb_leaf_values")
+
+
+@pytest.mark.parametrize("kw,code", [(dict(kind=7), 3), (dict(norm2=None), 1), (dict(ld_gh=3), 2)])
+def test_sketch_given_norms_rejects(L, kw, code):
+    assert _code(L.sb_sketch_given_norms, *sketch_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_sketch_given_norms")
+
+
+def grad_args(**kw):
+    a = dict(loss=0, F=F, n=1000, d=10, ld_f=1000, labels=F, Y=None, ld_y=0, G=F + 10 ** 6, ld_g=1000, hess=None,
+             ld_hess=0, h_row=None, norm2=None, ws=None, ws_bytes=0, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(loss=2), 3),
+    (dict(F=None), 1),
+    (dict(labels=None), 1),
+    (dict(loss=1, labels=None), 1),          # sigmoid needs Y
+    (dict(loss=1, Y=F, ld_y=10), 2),
+    (dict(n=0), 1),
+    (dict(d=0), 1),
+    (dict(ld_f=999), 2),
+    (dict(ld_g=999), 2),
+    (dict(hess=F, ld_hess=5), 2),
+    (dict(G=F + 400), 2),                    # G overlaps F
+    (dict(norm2=F), 1),                      # norms need a workspace
+])
+def test_gradients_rejects(L, kw, code):
+    assert _code(L.sb_gradients, *grad_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_gradients")
+
+
+def upd_args(**kw):
+    a = dict(F=F, n=1000, d=10, ld_f=1000, row_idx=F, leaf_off=F, n_leaves=64, V=F, ld_v=10, lr=0.1, ws=F,
+             ws_bytes=1 << 20, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(F=None), 1),
+    (dict(V=None), 1),
+    (dict(n=0), 1),
+    (dict(n_leaves=5000), 1),
+    (dict(ld_f=10), 2),
+    (dict(ld_v=9), 2),
+    (dict(lr=float("nan")), 1),
+    (dict(ws_bytes=16), 1),
+])
+def test_update_rejects(L, kw, code):
+    assert _code(L.sb_update_predictions, *upd_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_update_predictions")
 
 
 def test_error_text_is_per_thread(L):

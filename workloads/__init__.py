@@ -97,6 +97,8 @@ class Inputs:
     u: np.ndarray         # (k,) float64 uniforms in [0, 1) for random sampling
     Pi: np.ndarray        # (d, k) float32, N(0, 1/k), for random projections
     wl: Workload
+    y: np.ndarray = None  # (n,) int32 class labels (softmax workloads)
+    Y: np.ndarray = None  # (d, n) uint8 0/1 targets, column-major (sigmoid workloads)
 
     @property
     def G(self):
@@ -149,6 +151,8 @@ def make_inputs(wl, chunk=65_536):
             list(pool.map(one_feature, range(m)))
         G_T = np.empty((d, n), dtype=np.float32)
         h = np.ones(n, dtype=np.float32)
+        labels = np.empty(n, dtype=np.int32) if wl.loss == "softmax" else None
+        Yt = np.empty((d, n), dtype=np.uint8) if wl.loss == "sigmoid" else None
         if wl.loss == "softmax":
             W = (rng.standard_normal((m, d)) / np.sqrt(m)).astype(np.float32) if X_cm is not None else None
 
@@ -160,6 +164,7 @@ def make_inputs(wl, chunk=65_536):
                 else:
                     logits = W.T @ X_cm[:, r0:r1] + g.standard_normal((d, r1 - r0), dtype=np.float32)
                     y = np.argmax(logits, axis=0)
+                labels[r0:r1] = y
                 G_T[:, r0:r1] = _softmax_grad_cols(g.standard_normal((d, r1 - r0)), y)
             list(pool.map(one_chunk, range(len(chunks))))
         elif wl.loss == "sigmoid":
@@ -167,6 +172,7 @@ def make_inputs(wl, chunk=65_536):
                 r0, r1 = chunks[ci]
                 g = np.random.default_rng([wl.seed, 4, ci])
                 y = g.random((d, r1 - r0)) < 0.05
+                Yt[:, r0:r1] = y
                 sg = 1.0 / (1.0 + np.exp(-g.standard_normal((d, r1 - r0))))
                 G_T[:, r0:r1] = (sg - y).astype(np.float32)
                 h[r0:r1] = np.mean(sg * (1.0 - sg), axis=0).astype(np.float32)
@@ -175,7 +181,17 @@ def make_inputs(wl, chunk=65_536):
             raise ValueError(wl.loss)
     u = rng.random(k)
     Pi = (rng.standard_normal((d, k)) / np.sqrt(k)).astype(np.float32)
-    return Inputs(bins=bins, G_T=G_T, h=h, u=u, Pi=Pi, wl=wl)
+    return Inputs(bins=bins, G_T=G_T, h=h, u=u, Pi=Pi, wl=wl, y=labels, Y=Yt)
+
+
+def scores_and_targets(n, d, loss, seed, scale=1.0):
+    """Raw scores F (d, n) fp32 ~ N(0, scale^2), column-major, and targets: labels (n,)
+    int32 uniform over d classes for softmax, a (d, n) uint8 Bernoulli(0.3) matrix for sigmoid."""
+    rng = np.random.default_rng([seed, 7])
+    F_T = (rng.standard_normal((d, n)) * scale).astype(np.float32)
+    if loss == "softmax":
+        return F_T, rng.integers(0, d, n).astype(np.int32)
+    return F_T, (rng.random((d, n)) < 0.3).astype(np.uint8)
 
 
 def small_case(n, m, n_bins, d, seed, h_kind="ones", k=None):
