@@ -38,6 +38,8 @@ from .sketch import (  # noqa: F401
     identity_sketch,
     materialise,
     random_projection,
+    sparse_pi_matrix,
+    sparse_projection,
     sketch,
 )
 from .split import (  # noqa: F401

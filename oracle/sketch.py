@@ -116,6 +116,31 @@ def random_projection(G, h, Pi):
     return GH
 
 
+def sparse_pi_matrix(d, k, pi_col, pi_val):
+    """The d x k matrix of a row-sparse projection: row j holds pi_val[j, q] in
+    column pi_col[j, q] for q < s (repeated columns add; columns outside
+    [0, k) hold nothing, which lets rows be padded).  fp64."""
+    pi_col = np.asarray(pi_col).reshape(d, -1)
+    pi_val = np.asarray(pi_val, dtype=np.float64).reshape(d, -1)
+    Pi = np.zeros((d, k), dtype=np.float64)
+    for j in range(d):
+        for q in range(pi_col.shape[1]):
+            c = int(pi_col[j, q])
+            if 0 <= c < k:
+                Pi[j, c] += pi_val[j, q]
+    return Pi
+
+
+def sparse_projection(G, h, k, pi_col, pi_val):
+    """Random Projections (Section 3.3) with a sparse Pi: the entries of Pi may
+    follow distributions other than the normal one (Achlioptas), and sparse
+    JL transforms (Dasgupta, Kumar and Sarlos 2010; Kane and Nelson 2014) make
+    G Pi cheaper (the end of the proof of Prop. A.5).  G_k = G Pi exactly in
+    fp64, with Pi assembled from its row-sparse form."""
+    d = np.asarray(G).shape[1]
+    return random_projection(G, h, sparse_pi_matrix(d, k, pi_col, pi_val))
+
+
 def sketch(kind, G, h, k, u=None, Pi=None):
     """Dispatch on the sketch kind; returns (GH, cols, scales, norm2).
 

@@ -194,6 +194,34 @@ def scores_and_targets(n, d, loss, seed, scale=1.0):
     return F_T, (rng.random((d, n)) < 0.3).astype(np.uint8)
 
 
+def sparse_jl_pi(d, k, s, seed):
+    """A sparse JL projection in row-sparse form: every row j of Pi (d x k) has
+    s nonzeros in distinct random columns, each +-1/sqrt(s) with a random
+    sign (Kane and Nelson's construction with s nonzeros per input
+    coordinate).  Returns pi_col (d, s) int32 and pi_val (d, s) float32."""
+    rng = np.random.default_rng([seed, 11])
+    pi_col = np.stack([rng.choice(k, size=s, replace=False) for _ in range(d)]).astype(np.int32)
+    pi_val = (rng.choice([-1.0, 1.0], size=(d, s)) / np.sqrt(s)).astype(np.float32)
+    return pi_col, pi_val
+
+
+def achlioptas_pi(d, k, seed, s_max=8):
+    """Achlioptas' sparse projection in row-sparse form: entries sqrt(3/k) * {+1, 0, -1}
+    with probabilities {1/6, 2/3, 1/6}.  Rows with more than s_max nonzeros keep
+    their first s_max columns (rare for k <= 12); shorter rows are padded with
+    column -1 and value 0."""
+    rng = np.random.default_rng([seed, 12])
+    draw = rng.choice([1.0, 0.0, -1.0], size=(d, k), p=[1 / 6, 2 / 3, 1 / 6])
+    pi_col = np.full((d, s_max), -1, dtype=np.int32)
+    pi_val = np.zeros((d, s_max), dtype=np.float32)
+    scale = np.sqrt(3.0 / k)
+    for j in range(d):
+        nz = np.flatnonzero(draw[j])[:s_max]
+        pi_col[j, :nz.size] = nz
+        pi_val[j, :nz.size] = draw[j, nz] * scale
+    return pi_col, pi_val
+
+
 def small_case(n, m, n_bins, d, seed, h_kind="ones", k=None):
     """A small random case for unit and parity tests (uniform bins, softmax-like G)."""
     rng = np.random.default_rng(seed)
