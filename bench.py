@@ -118,6 +118,56 @@ def boost_leg(wl, inp, dev, L, warm=100, timed=100):
     }
 
 
+def projection_leg(dev, L, n=2_000_000, d=1000, k=20, reps=5):
+    """Random Projections at the 2M x 1000, k = 20 shape (Section 3.3): the dense
+    Gaussian Pi against row-sparse Pi with s = 1, 2, 4, 8 entries per row (sparse
+    JL).  G is drawn on the device (the kernels' speed does not depend on its
+    values); each call reads G once (n*d*4 bytes) and writes the sketch."""
+    import torch
+    from paper_2211_12858_amd.driver import workspace
+    from workloads import sparse_jl_pi
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    G = torch.randn((d, n), device=dev, dtype=torch.float32, generator=g)
+    h = torch.ones(n, device=dev, dtype=torch.float32)
+    ld_gh = (k + 1 + 7) // 8 * 8
+    GH = torch.empty((n, ld_gh), device=dev, dtype=torch.float32)
+    qexp = torch.empty(k + 1, device=dev, dtype=torch.int32)
+    ws = workspace(L.sb_workspace_bytes(L.SB_CALL_SKETCH, n=n, d=d, k=k), dev)
+    Pi = (torch.randn((d, k), device=dev, generator=g) / k ** 0.5).float()
+    alg = n * d * 4 + n * ld_gh * 4
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out = {"shape": "n=%d, d=%d, k=%d" % (n, d, k), "bytes": alg}
+    ms = timed(lambda: L.sb_sketch(L.SB_SKETCH_RANDOM_PROJECTION, G, n, d, n, h, k, None, Pi, GH, ld_gh, None, None,
+                                   None, qexp, ws, ws.numel()))
+    out["dense_ms"] = ms
+    for s in (1, 2, 4, 8):
+        pc, pv = sparse_jl_pi(d, k, s, seed=s)
+        pcd, pvd = torch.from_numpy(pc).to(dev), torch.from_numpy(pv).to(dev)
+        out["sparse_s%d_ms" % s] = timed(lambda: L.sb_sketch_sparse_projection(G, n, d, n, h, k, s, pcd, pvd, GH, ld_gh,
+                                                                                qexp, ws, ws.numel()))
+    best = min(out["sparse_s1_ms"], out["sparse_s2_ms"])
+    out["sparse_s1_GBps"] = alg / (out["sparse_s1_ms"] * 1e-3) / 1e9
+    out["dense_GBps"] = alg / (ms * 1e-3) / 1e9
+    log("bench: projection 2M x 1000 -> 20: dense %.3f ms, sparse s=1 %.3f ms (best of s=1,2: %.3f)"
+        % (ms, out["sparse_s1_ms"], best))
+    del G, GH
+    torch.cuda.empty_cache()
+    return out
+
+
 def hist_source_hash():
     """sha256 over the histogram kernel's source files (the traffic record is tied to it)."""
     h = hashlib.sha256()
@@ -183,6 +233,7 @@ def main():
     ap.add_argument("--cpu-sample-rows", type=int, default=800_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-boost", action="store_true", help="skip the boosting-loop leg")
+    ap.add_argument("--no-projection", action="store_true", help="skip the projection leg")
     ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
     args = ap.parse_args()
 
@@ -262,6 +313,7 @@ def main():
     log("bench: leaf values %.3f ms per tree" % leaf_ms)
 
     boost = None if args.no_boost else boost_leg(wl, inp, dev, L)
+    proj = None if args.no_projection else projection_leg(dev, L)
 
     sec_per_tree = total_ms / K / 1e3
     out = {
@@ -309,6 +361,8 @@ def main():
     }
     if boost is not None:
         out["next"]["boosting"] = boost
+    if proj is not None:
+        out["next"]["projection"] = proj
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_sample_rows)

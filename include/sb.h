@@ -193,6 +193,28 @@ int32_t sb_sketch_given_norms(int32_t kind, const float* G, int64_t n, int32_t d
                               void* stream);
 
 /*
+ * sb_sketch_sparse_projection -- Random Projections (Section 3.3) with a
+ * sparse Pi.  The paper notes that the entries of Pi may follow other
+ * distributions than the normal one (Achlioptas) and that sparse JL
+ * transforms compute G Pi faster (end of the proof of Prop. A.5).
+ *
+ * Pi (d x k) is passed row-sparse: row j holds s entries, entry q of value
+ * pi_val[j*s + q] in column pi_col[j*s + q]; columns outside [0, k) hold
+ * nothing (padding), repeated columns add.  s is 1, 2, 4 or 8.
+ * GH, ld_gh, h, qexp: as sb_sketch with RANDOM_PROJECTION:
+ *   GH[i*ld_gh + t] = sum_j G[i, j] Pi[j, t] in fp32, GH[i*ld_gh + k] = h[i],
+ *   padding written as 0.
+ * Every column of G is read once.  With s = 1 the product takes 2 n d
+ * flops, added in column order; with s = 2, 4 or 8 Pi is first assembled
+ * densely in the workspace (entries of a row added in q order in fp32) and
+ * multiplied as in sb_sketch, which is faster there.
+ * Workspace: sb_workspace_bytes(SB_CALL_SKETCH, ...).
+ */
+int32_t sb_sketch_sparse_projection(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                                    int32_t s, const int32_t* pi_col, const float* pi_val, float* GH, int64_t ld_gh,
+                                    int32_t* qexp, void* ws, int64_t ws_bytes, void* stream);
+
+/*
  * sb_hist_exponents -- fixed-point exponents for a given GH (row-major).
  *
  * For channel t (t <= k) with M_t = max_i |GH[i*ld_gh + t]|:

@@ -37,6 +37,7 @@ SYMBOLS = (
     "sb_layout_bins",
     "sb_sketch",
     "sb_sketch_given_norms",
+    "sb_sketch_sparse_projection",
     "sb_hist_exponents",
     "sb_build_histograms",
     "sb_subtract_histograms",
@@ -82,6 +83,8 @@ _PROTOS = {
 _PROTOS["sb_leaf_values"] = (_I32, [_P, _I64, _I32, _I64, _P, _I64, _P, _P, _P, _I32, _F64, _P, _I64, _P, _I64,
                                      _P])
 _PROTOS["sb_sketch_given_norms"] = _PROTOS["sb_sketch"]
+_PROTOS["sb_sketch_sparse_projection"] = (_I32, [_P, _I64, _I32, _I64, _P, _I32, _I32, _P, _P, _P, _I64, _P, _P, _I64,
+                                                 _P])
 _PROTOS["sb_gradients"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _I64, _P])
 _PROTOS["sb_update_predictions"] = (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _I64, _F64, _P, _I64, _P])
 _PROTOS["sb_profile_begin"] = (_I32, [])
@@ -160,6 +163,12 @@ def sb_sketch_given_norms(kind, G, n, d, ld_g, h, k, u, Pi, GH, ld_gh, cols, sca
     return _check(load().sb_sketch_given_norms(kind, _ptr(G), n, d, ld_g, _ptr(h), k, _ptr(u), _ptr(Pi), _ptr(GH),
                                                ld_gh, _ptr(cols), _ptr(scales), _ptr(norm2), _ptr(qexp), _ptr(ws),
                                                ws_bytes, _stream(stream)))
+
+
+def sb_sketch_sparse_projection(G, n, d, ld_g, h, k, s, pi_col, pi_val, GH, ld_gh, qexp, ws, ws_bytes, stream=None):
+    return _check(load().sb_sketch_sparse_projection(_ptr(G), n, d, ld_g, _ptr(h), k, s, _ptr(pi_col), _ptr(pi_val),
+                                                     _ptr(GH), ld_gh, _ptr(qexp), _ptr(ws), ws_bytes,
+                                                     _stream(stream)))
 
 
 def sb_hist_exponents(GH, n, ld_gh, k, qexp, ws, ws_bytes, stream=None):

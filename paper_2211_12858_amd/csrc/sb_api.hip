@@ -291,6 +291,26 @@ int32_t sb_sketch_given_norms(int32_t kind, const float* G, int64_t n, int32_t d
                        static_cast<hipStream_t>(stream), norm2);
 }
 
+int32_t sb_sketch_sparse_projection(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                                    int32_t s, const int32_t* pi_col, const float* pi_val, float* GH, int64_t ld_gh,
+                                    int32_t* qexp, void* ws, int64_t ws_bytes, void* stream) {
+  const char* call = "sb_sketch_sparse_projection";
+  if (!G || !h || !pi_col || !pi_val || !GH || !qexp)
+    return fail(SB_E_ARG, "sb_sketch_sparse_projection: G, h, pi_col, pi_val, GH and qexp must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_sketch_sparse_projection: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_sketch_sparse_projection: d must be in [1, 65535]");
+  if (k < 1 || k > 255) return fail(SB_E_ARG, "sb_sketch_sparse_projection: k must be in [1, 255]");
+  if (s != 1 && s != 2 && s != 4 && s != 8)
+    return fail(SB_E_UNSUPPORTED, "sb_sketch_sparse_projection: s must be 1, 2, 4 or 8 (pad rows with column -1)");
+  if (ld_g < n) return fail(SB_E_SHAPE, "sb_sketch_sparse_projection: ld_g must be >= n");
+  int32_t rc = check_gh(call, GH, ld_gh, k);
+  if (rc) return rc;
+  rc = need_ws(ws, ws_bytes, sketch_ws_bytes(SB_SKETCH_RANDOM_PROJECTION, n, d, k), call);
+  if (rc) return rc;
+  return launch_sketch_sparse(G, n, d, ld_g, h, k, s, pi_col, pi_val, GH, ld_gh, qexp, ws,
+                              static_cast<hipStream_t>(stream));
+}
+
 int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
                           int64_t ws_bytes, void* stream) {
   if (!GH || !qexp) return fail(SB_E_ARG, "sb_hist_exponents: GH and qexp must not be NULL");

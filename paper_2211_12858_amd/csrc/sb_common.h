@@ -25,6 +25,9 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
                       const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
                       double* norm2, int32_t* qexp, void* ws, hipStream_t st, const double* norm2_in = nullptr);
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k);
+int32_t launch_sketch_sparse(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k, int32_t s,
+                             const int32_t* pi_col, const float* pi_val, float* GH, int64_t ld_gh, int32_t* qexp,
+                             void* ws, hipStream_t st);
 int64_t hist_exponents_ws_bytes(int32_t k);
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,
                               hipStream_t st);

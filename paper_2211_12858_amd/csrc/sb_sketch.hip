@@ -9,6 +9,7 @@
 //       (row-major, rows written whole), plus per-block maxima of |value|
 //       for the fixed-point histogram exponents.
 //   k_project  : GH[i, 0:k] = (G Pi)[i, :] (Section 3.3), fp32 accumulation.
+//   k_project_sparse : the same product for a row-sparse Pi (S entries per row).
 //   k_qexp     : per-channel maximum over the blocks and the exponents.
 //
 // G is column-major, so every kernel reads whole columns with lanes on
@@ -249,23 +250,57 @@ constexpr int PROJ_THREADS = 1024;
 constexpr int PROJ_KT = 32;               // sketch columns per pass
 constexpr int PROJ_JU = 16;               // G loads in flight per thread
 constexpr int PROJ_LDS_FLOATS = 32768;    // 128 KB: the Pi block staged per pass
+constexpr int SPARSE_MAX_S = 1;           // entries per row of Pi for the sparse kernel
 
 // Random Projections (Section 3.3), HBM-bound on the read of G: one row per
 // thread, PROJ_JU columns of G loaded ahead, and the pass's block of Pi
 // (rows j0..j0+jc, columns t0..t0+KT) staged in LDS and read by broadcast.
 // Each output is an fp32 fmaf chain over j in increasing order.  Columns
 // past k are padded with zeros in LDS and never written.
+// Writes one row: channels [t0, t0 + kt) from acc; on the last pass also the
+// hessian channel k and the zero padding up to ld_gh (whole row in 16-byte
+// stores when the pass covers the row from 0 and ld_gh % 4 == 0).
+template <int KT>
+__device__ inline void store_proj_row(float* __restrict__ GH, int64_t i, int64_t ld_gh, int t0, int kt, int k,
+                                      bool last, float hv, const float (&acc)[KT]) {
+  float* row = GH + i * ld_gh;
+  if (last && t0 == 0 && (ld_gh & 3) == 0 && ld_gh <= KT + 8) {
+#pragma unroll
+    for (int q = 0; q < (KT + 8) / 4; ++q) {
+      if (4 * q < ld_gh) {
+        float o[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 4 * q + r;
+          o[r] = t < k ? acc[t < KT ? t : 0] : (t == k ? hv : 0.0f);
+        }
+        *reinterpret_cast<float4*>(row + 4 * q) = make_float4(o[0], o[1], o[2], o[3]);
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int t = 0; t < KT; ++t)
+    if (t < kt) row[t0 + t] = acc[t];
+  if (last) {
+    row[k] = hv;
+    for (int64_t t = k + 1; t < ld_gh; ++t) row[t] = 0.0f;
+  }
+}
+
 template <int KT>
 __global__ void __launch_bounds__(PROJ_THREADS)
 k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k, int t0,
-          float* __restrict__ GH, int64_t ld_gh, uint32_t* __restrict__ blockmax) {
+          const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh, uint32_t* __restrict__ blockmax) {
   extern __shared__ float sPi[];  // [jc][KT]
   __shared__ uint32_t sh[PROJ_THREADS / 64];
   const int kt = (k - t0 < KT) ? k - t0 : KT;
+  const bool last = t0 + PROJ_KT >= k;
   const int jcap = PROJ_LDS_FLOATS / KT;
   uint32_t mx[KT];
 #pragma unroll
   for (int t = 0; t < KT; ++t) mx[t] = 0u;
+  uint32_t mxh = 0u;
   for (int64_t base = (int64_t)blockIdx.x * PROJ_THREADS; base < n; base += (int64_t)gridDim.x * PROJ_THREADS) {
     const int64_t i = base + threadIdx.x;
     const bool live = i < n;
@@ -305,14 +340,15 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
       }
     }
     if (live) {
+      const float hv = last ? h[i] : 0.0f;
+      store_proj_row<KT>(GH, i, ld_gh, t0, kt, k, last, hv, acc);
 #pragma unroll
       for (int t = 0; t < KT; ++t) {
-        if (t < kt) {
-          GH[i * ld_gh + t0 + t] = acc[t];
-          const uint32_t a = __float_as_uint(acc[t]) & 0x7fffffffu;
-          mx[t] = a > mx[t] ? a : mx[t];
-        }
+        const uint32_t a = __float_as_uint(acc[t]) & 0x7fffffffu;
+        mx[t] = (t < kt && a > mx[t]) ? a : mx[t];
       }
+      const uint32_t ah = __float_as_uint(hv) & 0x7fffffffu;
+      mxh = ah > mxh ? ah : mxh;
     }
   }
 #pragma unroll
@@ -322,24 +358,103 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
       if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + t] = r;
     }
   }
+  if (last) {
+    const uint32_t r = block_max_u32<PROJ_THREADS>(mxh, sh);
+    if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = r;
+  }
 }
 
 // The hessian channel of a projected sketch, GH[i*ld_gh + k] = h[i], and the
 // zero padding of the row after it, with the channel's per-block maximum.
-__global__ void __launch_bounds__(256)
-k_project_h(const float* __restrict__ h, int64_t n, int k, float* __restrict__ GH, int64_t ld_gh,
-            uint32_t* __restrict__ blockmax) {
-  __shared__ uint32_t sh[4];
-  uint32_t mx = 0u;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
-    const float v = h[i];
-    GH[i * ld_gh + k] = v;
-    for (int64_t t = k + 1; t < ld_gh; ++t) GH[i * ld_gh + t] = 0.0f;
-    const uint32_t a = __float_as_uint(v) & 0x7fffffffu;
-    mx = a > mx ? a : mx;
+// Sparse projection (Section 3.3 with a sparse Pi: Achlioptas entries, or a
+// sparse JL transform, which the proof of Prop. A.5 names as the fast form
+// of G Pi).  Pi is row-sparse: row j holds S entries (column, value).  One
+// thread per row of G; the lanes of a wave take consecutive rows, so each
+// column of G is read once, 256 contiguous bytes per wave.  The entries of a
+// row of Pi are the same for every lane, so the accumulator they add to has a
+// wave-uniform index (VGPR indexing, no scratch) and the PROJ_JU * S entries
+// of a batch arrive in a few wide scalar loads.  fp32 accumulation in the
+// order (j, q): 2 n d S flops instead of the dense 2 n d k.  The last pass
+// also writes h and the zero padding of the row.
+template <int S>
+__global__ void __launch_bounds__(PROJ_THREADS)
+k_project_sparse(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const int32_t* __restrict__ pcol,
+                 const float* __restrict__ pval, int k, int t0, const float* __restrict__ h, float* __restrict__ GH,
+                 int64_t ld_gh, uint32_t* __restrict__ blockmax) {
+  constexpr int KT = PROJ_KT;
+  __shared__ uint32_t sh[PROJ_THREADS / 64];
+  const int kt = (k - t0 < KT) ? k - t0 : KT;
+  const bool last = t0 + KT >= k;
+  uint32_t mx[KT];
+#pragma unroll
+  for (int t = 0; t < KT; ++t) mx[t] = 0u;
+  uint32_t mxh = 0u;
+  for (int64_t base = (int64_t)blockIdx.x * PROJ_THREADS; base < n; base += (int64_t)gridDim.x * PROJ_THREADS) {
+    const int64_t i = base + threadIdx.x;
+    const bool live = i < n;
+    const int64_t ii = live ? i : n - 1;
+    float acc[KT];
+#pragma unroll
+    for (int t = 0; t < KT; ++t) acc[t] = 0.0f;
+    for (int j0 = 0; j0 < d; j0 += PROJ_JU) {
+      // columns past d (last batch only) load column d-1 and add nothing
+      float g[PROJ_JU];
+#pragma unroll
+      for (int u = 0; u < PROJ_JU; ++u) g[u] = G[(int64_t)(j0 + u < d ? j0 + u : d - 1) * ld_g + ii];
+      int tc[PROJ_JU * S];
+      float vc[PROJ_JU * S];
+#pragma unroll
+      for (int e = 0; e < PROJ_JU * S; ++e) {
+        const bool in = j0 + e / S < d;
+        tc[e] = in ? pcol[(int64_t)j0 * S + e] - t0 : -1;
+        vc[e] = in ? pval[(int64_t)j0 * S + e] : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < PROJ_JU; ++u)
+#pragma unroll
+        for (int q = 0; q < S; ++q) {
+          const int t = tc[u * S + q];
+          if ((unsigned)t < (unsigned)kt) acc[t] = fmaf(g[u], vc[u * S + q], acc[t]);
+        }
+    }
+    if (live) {
+      const float hv = last ? h[i] : 0.0f;
+      store_proj_row<KT>(GH, i, ld_gh, t0, kt, k, last, hv, acc);
+#pragma unroll
+      for (int t = 0; t < KT; ++t) {
+        const uint32_t a = __float_as_uint(acc[t]) & 0x7fffffffu;
+        mx[t] = (t < kt && a > mx[t]) ? a : mx[t];
+      }
+      const uint32_t ah = __float_as_uint(hv) & 0x7fffffffu;
+      mxh = ah > mxh ? ah : mxh;
+    }
   }
-  mx = block_max_u32<256>(mx, sh);
-  if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = mx;
+#pragma unroll
+  for (int t = 0; t < KT; ++t) {
+    if (t < kt) {
+      const uint32_t r = block_max_u32<PROJ_THREADS>(mx[t], sh);
+      if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + t] = r;
+    }
+  }
+  if (last) {
+    const uint32_t r = block_max_u32<PROJ_THREADS>(mxh, sh);
+    if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = r;
+  }
+}
+
+// Dense d x k Pi from its row-sparse form: one thread per row j, entries
+// added in q order in fp32 (columns outside [0, k) are dropped).
+__global__ void __launch_bounds__(256)
+k_assemble_pi(const int32_t* __restrict__ pcol, const float* __restrict__ pval, int d, int s, int k,
+              float* __restrict__ Pi) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  float* row = Pi + (int64_t)j * k;
+  for (int t = 0; t < k; ++t) row[t] = 0.0f;
+  for (int q = 0; q < s; ++q) {
+    const int c = pcol[(int64_t)j * s + q];
+    if (c >= 0 && c < k) row[c] += pval[(int64_t)j * s + q];
+  }
 }
 
 // Per-block max |GH[i*ld_gh + t]| for a caller-supplied row-major GH: one
@@ -403,14 +518,57 @@ int norm_parts(int64_t n) {
   return (int)p;
 }
 
+// Workspace: [norm partials d*P][norm2 d][prefix d][block maxima SKETCH_MAX_BLOCKS*(k+1)]
+// [dense Pi assembled from a sparse one, d*k]
+struct SketchWs {
+  int64_t part, n2, C, blockmax, pi, total;
+};
+
+SketchWs sketch_ws_layout(int64_t n, int32_t d, int32_t k) {
+  SketchWs L{};
+  int64_t p = 0;
+  L.part = p;
+  p += align256((int64_t)d * norm_parts(n) * 8);
+  L.n2 = p;
+  p += align256((int64_t)d * 8);
+  L.C = p;
+  p += align256((int64_t)d * 8);
+  L.blockmax = p;
+  p += align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4);
+  L.pi = p;
+  p += align256((int64_t)d * k * 4);
+  L.total = p;
+  return L;
+}
+
+// G Pi for a dense Pi, PROJ_KT sketch columns per pass; returns the grid size
+// (block b's maxima of every channel sit in row b of blockmax).
+int launch_dense_projection(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
+                            const float* Pi, float* GH, int64_t ld_gh, uint32_t* blockmax, hipStream_t st) {
+  const int nb = sketch_blocks(n, PROJ_THREADS);
+  for (int t0 = 0; t0 < k; t0 += PROJ_KT) {
+    const int kt = (k - t0 < PROJ_KT) ? k - t0 : PROJ_KT;
+    const int KT = (kt + 3) / 4 * 4;
+    const int jc = (d < PROJ_LDS_FLOATS / KT) ? d : PROJ_LDS_FLOATS / KT;
+    const size_t lds = (size_t)jc * KT * 4;
+#define SB_PROJ(K)                                                                                               \
+  case K:                                                                                                        \
+    hipLaunchKernelGGL((k_project<K>), dim3(nb), dim3(PROJ_THREADS), lds, st, G, n, d, ld_g, Pi, k, t0, h, GH,   \
+                       ld_gh, blockmax);                                                                         \
+    break;
+    switch (KT) {
+      SB_PROJ(4) SB_PROJ(8) SB_PROJ(12) SB_PROJ(16) SB_PROJ(20) SB_PROJ(24) SB_PROJ(28) SB_PROJ(32)
+    }
+#undef SB_PROJ
+  }
+  return nb;
+}
+
 }  // namespace
 
-// Workspace: [norm partials d*P][norm2 d][prefix d][block maxima SKETCH_MAX_BLOCKS*(k+1)]
 int64_t sketch_ws_bytes(int32_t kind, int64_t n, int32_t d, int32_t k) {
   (void)kind;
-  const int P = norm_parts(n);
-  return align256((int64_t)d * P * 8) + align256((int64_t)d * 8) * 2 +
-         align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4);
+  return sketch_ws_layout(n, d, k).total;
 }
 
 int64_t hist_exponents_ws_bytes(int32_t k) { return align256((int64_t)SKETCH_MAX_BLOCKS * (k + 1) * 4); }
@@ -419,35 +577,16 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
                       const double* u, const float* Pi, float* GH, int64_t ld_gh, int32_t* cols, float* scales,
                       double* norm2, int32_t* qexp, void* ws, hipStream_t st, const double* norm2_in) {
   const int P = norm_parts(n);
+  const SketchWs L = sketch_ws_layout(n, d, k);
   char* w = static_cast<char*>(ws);
-  double* part = reinterpret_cast<double*>(w);
-  w += align256((int64_t)d * P * 8);
-  double* n2 = reinterpret_cast<double*>(w);
-  w += align256((int64_t)d * 8);
-  double* C = reinterpret_cast<double*>(w);
-  w += align256((int64_t)d * 8);
-  uint32_t* blockmax = reinterpret_cast<uint32_t*>(w);
+  double* part = reinterpret_cast<double*>(w + L.part);
+  double* n2 = reinterpret_cast<double*>(w + L.n2);
+  double* C = reinterpret_cast<double*>(w + L.C);
+  uint32_t* blockmax = reinterpret_cast<uint32_t*>(w + L.blockmax);
 
   int nb;
   if (kind == SB_SKETCH_RANDOM_PROJECTION) {
-    // one grid for every pass, so that block b's maxima of all channels sit in row b
-    nb = sketch_blocks(n, PROJ_THREADS);
-    for (int t0 = 0; t0 < k; t0 += PROJ_KT) {
-      const int kt = (k - t0 < PROJ_KT) ? k - t0 : PROJ_KT;
-      const int KT = (kt + 3) / 4 * 4;
-      const int jc = (d < PROJ_LDS_FLOATS / KT) ? d : PROJ_LDS_FLOATS / KT;
-      const size_t lds = (size_t)jc * KT * 4;
-#define SB_PROJ(K)                                                                                               \
-  case K:                                                                                                        \
-    hipLaunchKernelGGL((k_project<K>), dim3(nb), dim3(PROJ_THREADS), lds, st, G, n, d, ld_g, Pi, k, t0, GH, ld_gh, \
-                       blockmax);                                                                                \
-    break;
-      switch (KT) {
-        SB_PROJ(4) SB_PROJ(8) SB_PROJ(12) SB_PROJ(16) SB_PROJ(20) SB_PROJ(24) SB_PROJ(28) SB_PROJ(32)
-      }
-#undef SB_PROJ
-    }
-    hipLaunchKernelGGL(k_project_h, dim3(nb), dim3(256), 0, st, h, n, k, GH, ld_gh, blockmax);
+    nb = launch_dense_projection(G, n, d, ld_g, h, k, Pi, GH, ld_gh, blockmax, st);
   } else {
     if (norm2_in == nullptr) {
       int64_t chunk = (n + P - 1) / P;
@@ -463,6 +602,32 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
   }
   hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
   return check_launch("sb_sketch");
+}
+
+// Rows of Pi with one entry go through the sparse kernel; with more, the
+// per-entry accumulator update (a few issue slots each) costs more than the
+// dense product at k <= 32 (2M x 1000 -> 20: sparse kernel 1.70 ms at s = 1,
+// 2.34 ms at s = 2, 4.18 ms at s = 4; assembled dense Pi 2.15-2.43 ms), so
+// Pi is assembled densely first.
+int32_t launch_sketch_sparse(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k, int32_t s,
+                             const int32_t* pi_col, const float* pi_val, float* GH, int64_t ld_gh, int32_t* qexp,
+                             void* ws, hipStream_t st) {
+  const SketchWs L = sketch_ws_layout(n, d, k);
+  char* w = static_cast<char*>(ws);
+  uint32_t* blockmax = reinterpret_cast<uint32_t*>(w + L.blockmax);
+  int nb;
+  if (s <= SPARSE_MAX_S) {
+    nb = sketch_blocks(n, PROJ_THREADS);
+    for (int t0 = 0; t0 < k; t0 += PROJ_KT)
+      hipLaunchKernelGGL((k_project_sparse<SPARSE_MAX_S>), dim3(nb), dim3(PROJ_THREADS), 0, st, G, n, d, ld_g, pi_col,
+                         pi_val, k, t0, h, GH, ld_gh, blockmax);
+  } else {
+    float* Pi = reinterpret_cast<float*>(w + L.pi);
+    hipLaunchKernelGGL(k_assemble_pi, dim3((d + 255) / 256), dim3(256), 0, st, pi_col, pi_val, d, s, k, Pi);
+    nb = launch_dense_projection(G, n, d, ld_g, h, k, Pi, GH, ld_gh, blockmax, st);
+  }
+  hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
+  return check_launch("sb_sketch_sparse_projection");
 }
 
 int32_t launch_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, int32_t* qexp, void* ws,

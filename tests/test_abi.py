@@ -35,7 +35,7 @@ def test_header_declares_the_boundary():
     fns = header_functions()
     for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
                  "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_leaf_values", "sb_gradients",
-                 "sb_update_predictions", "sb_sketch_given_norms", "sb_last_error",
+                 "sb_update_predictions", "sb_sketch_given_norms", "sb_sketch_sparse_projection", "sb_last_error",
                  "sb_abi_version", "sb_workspace_bytes"):
         assert name in fns
 
@@ -263,6 +263,27 @@ def test_leaf_values_rejects(L, kw, code):
 def test_sketch_given_norms_rejects(L, kw, code):
     assert _code(L.sb_sketch_given_norms, *sketch_args(**kw)) == code
     assert L.sb_last_error().startswith("sb_sketch_given_norms")
+
+
+def sparse_args(**kw):
+    a = dict(G=F, n=100, d=10, ld_g=100, h=F, k=5, s=1, pi_col=F, pi_val=F, GH=F, ld_gh=8, qexp=F, ws=F,
+             ws_bytes=1 << 30, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=None), 1),
+    (dict(pi_col=None), 1),
+    (dict(k=0), 1),
+    (dict(s=3), 3),
+    (dict(ld_g=99), 2),
+    (dict(ld_gh=5), 2),
+    (dict(ws_bytes=16), 1),
+])
+def test_sketch_sparse_rejects(L, kw, code):
+    assert _code(L.sb_sketch_sparse_projection, *sparse_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_sketch_sparse_projection")
 
 
 def grad_args(**kw):
