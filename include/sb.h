@@ -383,6 +383,21 @@ int32_t sb_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t
                      float* h_row, double* norm2, void* ws, int64_t ws_bytes, void* stream);
 
 /*
+ * sb_leaf_values_from_loss -- sb_leaf_values with the per-element hessians
+ * of a cross-entropy formed from G and the targets instead of being read:
+ *   SB_LOSS_SOFTMAX_CE:  p = G[i, j] + [j == labels[i]],
+ *   SB_LOSS_SIGMOID_BCE: p = G[i, j] + Y[j*ld_y + i],
+ *   h_ij = p (1 - p) in fp32,
+ * which is the hessian sb_gradients writes, up to the rounding of g
+ * (|error| <= 2^-24 per element).  V and every other argument as in
+ * sb_leaf_values; workspace: sb_workspace_bytes(SB_CALL_LEAF_VALUES, ...).
+ */
+int32_t sb_leaf_values_from_loss(int32_t loss, const float* G, int64_t n, int32_t d, int64_t ld_g,
+                                 const int32_t* labels, const uint8_t* Y, int64_t ld_y, const int32_t* row_idx,
+                                 const int32_t* leaf_off, int32_t n_leaves, double lambda, double* V, int64_t ld_v,
+                                 void* ws, int64_t ws_bytes, void* stream);
+
+/*
  * sb_update_predictions -- the model update a_t = a_{t-1} + lr * f_t
  * (Section 2): for every row i in leaf L of the grown tree and output j,
  *   F[j*ld_f + i] = fp32( (double)F[j*ld_f + i] + lr * V[L*ld_v + j] ),

@@ -45,6 +45,7 @@ SYMBOLS = (
     "sb_partition_rows",
     "sb_grow_tree",
     "sb_leaf_values",
+    "sb_leaf_values_from_loss",
     "sb_gradients",
     "sb_update_predictions",
     "sb_profile_begin",
@@ -86,6 +87,8 @@ _PROTOS["sb_sketch_given_norms"] = _PROTOS["sb_sketch"]
 _PROTOS["sb_sketch_sparse_projection"] = (_I32, [_P, _I64, _I32, _I64, _P, _I32, _I32, _P, _P, _P, _I64, _P, _P, _I64,
                                                  _P])
 _PROTOS["sb_gradients"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, _I64, _P, _I64, _P, _P, _P, _I64, _P])
+_PROTOS["sb_leaf_values_from_loss"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _I32, _F64, _P,
+                                               _I64, _P, _I64, _P])
 _PROTOS["sb_update_predictions"] = (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _I64, _F64, _P, _I64, _P])
 _PROTOS["sb_profile_begin"] = (_I32, [])
 _PROTOS["sb_profile_end"] = (_I32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)])
@@ -222,6 +225,13 @@ def sb_gradients(loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h
     return _check(load().sb_gradients(loss, _ptr(F), n, d, ld_f, _ptr(labels), _ptr(Y), ld_y, _ptr(G), ld_g,
                                       _ptr(hess), ld_hess, _ptr(h_row), _ptr(norm2), _ptr(ws), ws_bytes,
                                       _stream(stream)))
+
+
+def sb_leaf_values_from_loss(loss, G, n, d, ld_g, labels, Y, ld_y, row_idx, leaf_off, n_leaves, lam, V, ld_v, ws,
+                             ws_bytes, stream=None):
+    return _check(load().sb_leaf_values_from_loss(loss, _ptr(G), n, d, ld_g, _ptr(labels), _ptr(Y), ld_y, _ptr(row_idx),
+                                                  _ptr(leaf_off), n_leaves, lam, _ptr(V), ld_v, _ptr(ws), ws_bytes,
+                                                  _stream(stream)))
 
 
 def sb_update_predictions(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws, ws_bytes, stream=None):

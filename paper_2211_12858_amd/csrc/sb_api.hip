@@ -535,6 +535,31 @@ int32_t sb_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t
                           static_cast<hipStream_t>(stream));
 }
 
+int32_t sb_leaf_values_from_loss(int32_t loss, const float* G, int64_t n, int32_t d, int64_t ld_g,
+                                 const int32_t* labels, const uint8_t* Y, int64_t ld_y, const int32_t* row_idx,
+                                 const int32_t* leaf_off, int32_t n_leaves, double lambda, double* V, int64_t ld_v,
+                                 void* ws, int64_t ws_bytes, void* stream) {
+  const char* call = "sb_leaf_values_from_loss";
+  if (loss != SB_LOSS_SOFTMAX_CE && loss != SB_LOSS_SIGMOID_BCE)
+    return fail(SB_E_UNSUPPORTED, "sb_leaf_values_from_loss: unknown loss " + std::to_string(loss));
+  if (!G || !row_idx || !leaf_off || !V)
+    return fail(SB_E_ARG, "sb_leaf_values_from_loss: G, row_idx, leaf_off and V must not be NULL");
+  if (loss == SB_LOSS_SOFTMAX_CE && !labels) return fail(SB_E_ARG, "sb_leaf_values_from_loss: softmax needs labels");
+  if (loss == SB_LOSS_SIGMOID_BCE && !Y) return fail(SB_E_ARG, "sb_leaf_values_from_loss: sigmoid needs Y");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_leaf_values_from_loss: n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_leaf_values_from_loss: d must be in [1, 65535]");
+  if (n_leaves < 1 || n_leaves > MAX_LEAVES)
+    return fail(SB_E_ARG, "sb_leaf_values_from_loss: n_leaves must be in [1, 4096]");
+  if (ld_g < n) return fail(SB_E_SHAPE, "sb_leaf_values_from_loss: ld_g must be >= n");
+  if (loss == SB_LOSS_SIGMOID_BCE && ld_y < n) return fail(SB_E_SHAPE, "sb_leaf_values_from_loss: ld_y must be >= n");
+  if (ld_v < d) return fail(SB_E_SHAPE, "sb_leaf_values_from_loss: ld_v must be >= d");
+  if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_leaf_values_from_loss: lambda must be > 0");
+  const int32_t rc = need_ws(ws, ws_bytes, leaf_ws_bytes(n, d, n_leaves), call);
+  if (rc) return rc;
+  return launch_leaf_values_from_loss(loss, G, n, d, ld_g, labels, Y, ld_y, row_idx, leaf_off, n_leaves, lambda, V,
+                                      ld_v, ws, static_cast<hipStream_t>(stream));
+}
+
 int32_t sb_update_predictions(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
                               const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
                               void* ws, int64_t ws_bytes, void* stream) {

@@ -64,6 +64,10 @@ int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, c
                            const float* h, const int32_t* row_idx, const int32_t* leaf_off, int32_t n_leaves,
                            double lambda, double* V, int64_t ld_v, void* ws, hipStream_t st);
 
+int32_t launch_leaf_values_from_loss(int32_t loss, const float* G, int64_t n, int32_t d, int64_t ld_g,
+                                     const int32_t* labels, const uint8_t* Y, int64_t ld_y, const int32_t* row_idx,
+                                     const int32_t* leaf_off, int32_t n_leaves, double lambda, double* V, int64_t ld_v,
+                                     void* ws, hipStream_t st);
 int64_t grad_ws_bytes(int64_t n, int32_t d);
 int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
                          const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,

@@ -132,6 +132,19 @@ class SplitSearch:
                          self._ws_leaf, self._ws_leaf.numel(), stream)
         return self.V
 
+    def leaf_values_from_loss(self, loss, G_T, labels=None, Y=None, stream=None):
+        """Leaf values with the cross-entropy hessians formed from G and the targets (eq. 3)."""
+        d, n = G_T.shape
+        n_leaves = 1 << self.depth
+        need = L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=n, d=d, n_nodes=n_leaves)
+        if self._ws_leaf is None or self._ws_leaf.numel() < need:
+            self._ws_leaf = workspace(need, self.device)
+        if self.V is None or self.V.shape != (n_leaves, d):
+            self.V = torch.zeros((n_leaves, d), dtype=torch.float64, device=self.device)
+        L.sb_leaf_values_from_loss(L.LOSS[loss], G_T, n, d, n, labels, Y, n, self.row_idx, self.leaf_off, n_leaves,
+                                   self.lam, self.V, d, self._ws_leaf, self._ws_leaf.numel(), stream)
+        return self.V
+
     # ------------------------------------------------------------ readback
     def gh(self):
         """The sketch as an (n, k+1) float32 host array."""
@@ -166,7 +179,9 @@ class Booster:
        split-search weight h = 1 for softmax (the count weight of S_G) and the
        row mean of the hessians for sigmoid;
     3. the tree (``sb_grow_tree``);
-    4. leaf values from the full G and the per-element hessians (eq. 3);
+    4. leaf values from the full G and the per-element hessians (eq. 3),
+       which ``sb_leaf_values_from_loss`` forms from G and the targets
+       instead of storing them;
     5. F += lr * f_t (``sb_update_predictions``).
 
     F, G and the hessians are (d, n) float32 device tensors (column-major).
@@ -179,7 +194,6 @@ class Booster:
         self.n, self.d, self.loss, self.kind, self.lr = n, d, loss, kind, float(lr)
         self.F = torch.zeros((d, n), dtype=torch.float32, device=dev) if F0 is None else F0.clone()
         self.G = torch.empty((d, n), dtype=torch.float32, device=dev)
-        self.hess = torch.empty((d, n), dtype=torch.float32, device=dev)
         self.h_row = torch.empty(n, dtype=torch.float32, device=dev)
         self.ones = torch.ones(n, dtype=torch.float32, device=dev)
         self.norm2 = torch.zeros(d, dtype=torch.float64, device=dev)
@@ -197,14 +211,15 @@ class Booster:
 
     def gradients(self, stream=None):
         n, d = self.n, self.d
-        L.sb_gradients(L.LOSS[self.loss], self.F, n, d, n, self.labels, self.Y, n, self.G, n, self.hess, n,
-                       self.h_row, self.norm2, self.ws_grad, self.ws_grad.numel(), stream)
+        L.sb_gradients(L.LOSS[self.loss], self.F, n, d, n, self.labels, self.Y, n, self.G, n, None, 0,
+                       self.h_row if self.loss == "sigmoid" else None, self.norm2, self.ws_grad,
+                       self.ws_grad.numel(), stream)
 
     def step(self, u=None, Pi=None, stream=None):
         self.gradients(stream)
         h = self.ones if self.loss == "softmax" else self.h_row
         self.ss.sketch(self.kind, self.G, h, u=u, Pi=Pi, stream=stream, norm2_in=self.norm2)
         self.ss.grow(stream)
-        V = self.ss.leaf_values(self.G, hess_T=self.hess, stream=stream)
+        V = self.ss.leaf_values_from_loss(self.loss, self.G, self.labels, self.Y, stream=stream)
         L.sb_update_predictions(self.F, self.n, self.d, self.n, self.ss.row_idx, self.ss.leaf_off, V.shape[0], V,
                                 self.d, self.lr, self.ws_upd, self.ws_upd.numel(), stream)

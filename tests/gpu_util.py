@@ -180,14 +180,16 @@ def run_leaf(G_T, row_idx, leaf_off, lam, hess_T=None, h=None, ld_v=None, device
 LEAF_QUANTUM = 2.0 ** -41  # per-element error bound of the leaf sums, relative to the column's largest magnitude
 
 
-def leaf_value_error_ok(V, V_o, G, rows_of, lam, hess=None, h=None, col_max=None):
+def leaf_value_error_ok(V, V_o, G, rows_of, lam, hess=None, h=None, col_max=None, hess_err=0.0):
     """|V - V_o| within the bound that the fixed-point accumulation and fp64 sums allow.
 
     The numerator and denominator sums carry at most n_L * 2^-41 * M (M: the
     column's largest magnitude over all rows) plus 1e-13 of the leaf's absolute
     mass; the quotient adds both relative errors and one rounding.
     col_max: the columns' largest magnitudes over all n rows, when G holds only
-    some of them.  Returns (ok, worst ratio of error to bound)."""
+    some of them.  hess_err: a per-element error of the hessians themselves
+    (formed on the device rather than read).  Returns (ok, worst ratio of
+    error to bound)."""
     G = np.asarray(G, dtype=np.float64)
     Mg = np.abs(G).max(axis=0) if col_max is None else np.asarray(col_max, dtype=np.float64)
     worst = 0.0
@@ -198,7 +200,7 @@ def leaf_value_error_ok(V, V_o, G, rows_of, lam, hess=None, h=None, col_max=None
         if hess is not None:
             Hh = np.asarray(hess, dtype=np.float64)
             hs = Hh[rows].sum(axis=0)
-            eh = nL * LEAF_QUANTUM * np.abs(Hh).max(axis=0) + 1e-13 * hs
+            eh = nL * LEAF_QUANTUM * np.abs(Hh).max(axis=0) + 1e-13 * hs + nL * hess_err
         elif h is not None:
             hh = np.asarray(h, dtype=np.float64)
             hs = np.full(G.shape[1], hh[rows].sum())

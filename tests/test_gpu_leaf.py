@@ -99,3 +99,33 @@ def test_leaf_values_of_a_grown_tree():
     gu.sync()
     tree = ss.tree()
     check(case.G_T, tree["row_idx"], tree["leaf_off"], 1.0)
+
+
+@pytest.mark.parametrize("loss", ["softmax", "sigmoid"])
+def test_leaf_values_from_loss(loss):
+    # hessians formed from G and the targets on the device; the oracle uses the
+    # fp32-rounded hessians of the same scores.  g carries at most 2^-24 of
+    # rounding, p = g + target and h = p (1 - p) one more each, and the
+    # oracle's stored h one: at most 3.5 * 2^-24 < 2^-22 per element.
+    from oracle import boost as ob
+    from workloads import scores_and_targets
+    n, d = 2 * 2048 + 901, 6
+    F_T, tgt = scores_and_targets(n, d, loss, seed=71, scale=2.0)
+    tgt_o = tgt if loss == "softmax" else tgt.T
+    G, Hd, _, _ = ob.gradients(loss, F_T.T, tgt_o)
+    row_idx, leaf_off = grouping(n, 16, seed=72, empty=(5,))
+    G_T = np.ascontiguousarray(G.T)
+    n_leaves = 16
+    V = torch.full((n_leaves, d), float("nan"), dtype=torch.float64, device=gu.DEV)
+    ws = gu.workspace(gu.L.sb_workspace_bytes(gu.L.SB_CALL_LEAF_VALUES, n=n, d=d, n_nodes=n_leaves), gu.DEV)
+    labels = gu.up(tgt) if loss == "softmax" else None
+    Y = gu.up(tgt) if loss == "sigmoid" else None
+    gu.L.sb_leaf_values_from_loss(gu.L.LOSS[loss], gu.up(G_T), n, d, n, labels, Y, n, gu.up(row_idx), gu.up(leaf_off),
+                                  n_leaves, 1.0, V, d, ws, ws.numel())
+    gu.sync()
+    Vg = V.cpu().numpy()
+    V_o = oracle.leaf_values(G, row_idx, leaf_off, 1.0, hess=Hd)
+    ok, worst = gu.leaf_value_error_ok(Vg, V_o, G, oracle.leaf_rows(row_idx, leaf_off), 1.0, hess=Hd,
+                                       hess_err=2.0 ** -22)
+    assert ok, worst
+    assert np.all(Vg[5] == 0)
