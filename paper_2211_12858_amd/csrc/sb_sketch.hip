@@ -178,7 +178,8 @@ __device__ inline uint32_t block_max_u32(uint32_t v, uint32_t* sh) {
 }
 
 constexpr int PACK_THREADS = 256;
-constexpr int64_t PACK_ROWS_PER_BLOCK = PACK_THREADS;  // one row per thread per pass
+constexpr int PACK_ROWS = 4;                           // rows per thread per pass
+constexpr int64_t PACK_ROWS_PER_BLOCK = PACK_THREADS * PACK_ROWS;
 constexpr int PACK_CG = 16;                            // floats of a row written per pass
 // Grid cap of the sketch kernels: block b writes its per-channel maxima to
 // blockmax[b*(k+1) + t], reduced afterwards by k_qexp (no atomics).
@@ -211,30 +212,55 @@ k_pack(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float*
   const bool vec4 = (ld_gh & 3) == 0;
   for (int g0 = 0; g0 < ld_gh; g0 += PACK_CG) {
     const int gn = (ld_gh - g0 < PACK_CG) ? (int)(ld_gh - g0) : PACK_CG;
+    // what channel g0 + tt holds: a column of G (col >= 0), all zeros
+    // (col == -1: padding, or a Random Sampling column of an all-zero G), or h
+    int col[PACK_CG];
+    float sc[PACK_CG];
+#pragma unroll
+    for (int tt = 0; tt < PACK_CG; ++tt) {
+      const int t = g0 + tt;
+      const int c = (tt < gn && t < k) ? cols[t] : -1;
+      col[tt] = (c >= 0 && c < d) ? c : -1;
+      sc[tt] = (tt < gn && t < k) ? scales[t] : 0.0f;
+    }
     uint32_t mx[PACK_CG];
 #pragma unroll
     for (int tt = 0; tt < PACK_CG; ++tt) mx[tt] = 0u;
     for (int64_t base = (int64_t)blockIdx.x * PACK_ROWS_PER_BLOCK; base < n;
          base += (int64_t)gridDim.x * PACK_ROWS_PER_BLOCK) {
-      const int64_t i = base + threadIdx.x;
-      if (i >= n) continue;
-      float v[PACK_CG];
+      // PACK_ROWS rows per thread, every load issued before any use; rows past
+      // the end read row n-1 and store nothing
+      float v[PACK_ROWS][PACK_CG];
 #pragma unroll
-      for (int tt = 0; tt < PACK_CG; ++tt) {
-        const int t = g0 + tt;
-        float x = 0.0f;
-        if (tt < gn && t < k) {
-          const int col = cols[t];
-          // -1 marks an all-zero sketch column
-          x = (col < 0 || col >= d) ? 0.0f : G[(int64_t)col * ld_g + i] * scales[t];
-        } else if (tt < gn && t == k) {
-          x = h[i];
+      for (int r = 0; r < PACK_ROWS; ++r) {
+        const int64_t i = base + threadIdx.x + (int64_t)r * PACK_THREADS;
+        const int64_t ic = i < n ? i : n - 1;
+#pragma unroll
+        for (int tt = 0; tt < PACK_CG; ++tt) {
+          // the branches are uniform (the same for every lane)
+          if (col[tt] >= 0)
+            v[r][tt] = G[(int64_t)col[tt] * ld_g + ic];
+          else if (g0 + tt == k)
+            v[r][tt] = h[ic];
+          else
+            v[r][tt] = 0.0f;
         }
-        v[tt] = x;
-        const uint32_t a = __float_as_uint(x) & 0x7fffffffu;
-        mx[tt] = a > mx[tt] ? a : mx[tt];
       }
-      store_row_run(GH + i * ld_gh + g0, v, gn, vec4);
+#pragma unroll
+      for (int r = 0; r < PACK_ROWS; ++r) {
+        const int64_t i = base + threadIdx.x + (int64_t)r * PACK_THREADS;
+#pragma unroll
+        for (int tt = 0; tt < PACK_CG; ++tt) {
+          const int t = g0 + tt;
+          // one fp32 multiply: bit-exact with fp32(G * scale)
+          float x = t == k ? v[r][tt] : (col[tt] >= 0 ? v[r][tt] * sc[tt] : 0.0f);
+          x = tt < gn ? x : 0.0f;
+          v[r][tt] = x;
+          const uint32_t a = __float_as_uint(x) & 0x7fffffffu;
+          if (i < n) mx[tt] = a > mx[tt] ? a : mx[tt];
+        }
+        if (i < n) store_row_run(GH + i * ld_gh + g0, v[r], gn, vec4);
+      }
     }
 #pragma unroll
     for (int tt = 0; tt < PACK_CG; ++tt) {
@@ -243,6 +269,71 @@ k_pack(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float*
         if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (k + 1) + g0 + tt] = r;
       }
     }
+  }
+}
+
+// k_pack for sketches of KC <= 15 columns whose rows fit 16 floats: the
+// column count is a template parameter, so every load of a row is issued
+// unconditionally (a column index of -1, an all-zero Random Sampling column,
+// loads column 0 and stores 0).
+template <int KC>
+__global__ void __launch_bounds__(PACK_THREADS)
+k_pack_small(const float* __restrict__ G, int64_t n, int64_t ld_g, int d, const float* __restrict__ h,
+             const int32_t* __restrict__ cols, const float* __restrict__ scales, float* __restrict__ GH,
+             int64_t ld_gh, uint32_t* __restrict__ blockmax) {
+  __shared__ uint32_t sh[PACK_THREADS / 64];
+  const bool vec4 = (ld_gh & 3) == 0;
+  const int gn = (int)ld_gh;
+  int col[KC];
+  bool ok[KC];
+  float sc[KC];
+#pragma unroll
+  for (int t = 0; t < KC; ++t) {
+    const int c = cols[t];
+    ok[t] = c >= 0 && c < d;
+    col[t] = ok[t] ? c : 0;
+    sc[t] = scales[t];
+  }
+  uint32_t mx[KC + 1];
+#pragma unroll
+  for (int t = 0; t <= KC; ++t) mx[t] = 0u;
+  for (int64_t base = (int64_t)blockIdx.x * PACK_ROWS_PER_BLOCK; base < n;
+       base += (int64_t)gridDim.x * PACK_ROWS_PER_BLOCK) {
+    float g[PACK_ROWS][KC + 1];
+#pragma unroll
+    for (int r = 0; r < PACK_ROWS; ++r) {
+      const int64_t i = base + threadIdx.x + (int64_t)r * PACK_THREADS;
+      const int64_t ic = i < n ? i : n - 1;
+#pragma unroll
+      for (int t = 0; t < KC; ++t) g[r][t] = G[(int64_t)col[t] * ld_g + ic];
+      g[r][KC] = h[ic];
+    }
+#pragma unroll
+    for (int r = 0; r < PACK_ROWS; ++r) {
+      const int64_t i = base + threadIdx.x + (int64_t)r * PACK_THREADS;
+      float v[PACK_CG];
+#pragma unroll
+      for (int tt = 0; tt < PACK_CG; ++tt) {
+        // one fp32 multiply: bit-exact with fp32(G * scale)
+        float x = 0.0f;
+        if (tt < KC) x = ok[tt] ? g[r][tt] * sc[tt] : 0.0f;
+        if (tt == KC) x = g[r][KC];
+        v[tt] = x;
+      }
+      if (i < n) {
+#pragma unroll
+        for (int t = 0; t <= KC; ++t) {
+          const uint32_t a = __float_as_uint(v[t]) & 0x7fffffffu;
+          mx[t] = a > mx[t] ? a : mx[t];
+        }
+        store_row_run(GH + i * ld_gh, v, gn, vec4);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t <= KC; ++t) {
+    const uint32_t r = block_max_u32<PACK_THREADS>(mx[t], sh);
+    if (threadIdx.x == 0) blockmax[(int64_t)blockIdx.x * (KC + 1) + t] = r;
   }
 }
 
@@ -596,9 +687,22 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
     }
     hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, norm2_in ? norm2_in : n2, d, k, u, cols, scales,
                        C);
-    nb = sketch_blocks(n, 4 * PACK_ROWS_PER_BLOCK);
-    hipLaunchKernelGGL(k_pack, dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, k, cols, scales, GH, ld_gh,
-                       blockmax);
+    nb = sketch_blocks(n, PACK_ROWS_PER_BLOCK);
+    if (k < PACK_CG && ld_gh <= PACK_CG) {
+#define SB_PACK(K)                                                                                               \
+  case K:                                                                                                        \
+    hipLaunchKernelGGL((k_pack_small<K>), dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, cols, scales, GH, \
+                       ld_gh, blockmax);                                                                         \
+    break;
+      switch (k) {
+        SB_PACK(1) SB_PACK(2) SB_PACK(3) SB_PACK(4) SB_PACK(5) SB_PACK(6) SB_PACK(7) SB_PACK(8) SB_PACK(9)
+        SB_PACK(10) SB_PACK(11) SB_PACK(12) SB_PACK(13) SB_PACK(14) SB_PACK(15)
+      }
+#undef SB_PACK
+    } else {
+      hipLaunchKernelGGL(k_pack, dim3(nb), dim3(PACK_THREADS), 0, st, G, n, ld_g, d, h, k, cols, scales, GH, ld_gh,
+                         blockmax);
+    }
   }
   hipLaunchKernelGGL(k_qexp, dim3(k + 1), dim3(256), 0, st, blockmax, nb, k + 1, qexp);
   return check_launch("sb_sketch");
