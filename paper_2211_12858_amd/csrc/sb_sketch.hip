@@ -342,6 +342,10 @@ constexpr int PROJ_KT = 32;               // sketch columns per pass
 constexpr int PROJ_JU = 16;               // G loads in flight per thread
 constexpr int PROJ_LDS_FLOATS = 32768;    // 128 KB: the Pi block staged per pass
 constexpr int SPARSE_MAX_S = 1;           // entries per row of Pi for the sparse kernel
+#ifndef SB_PROJ_MFMA_MIN_K
+#define SB_PROJ_MFMA_MIN_K 8
+#endif
+constexpr int PROJ_MFMA_MIN_K = SB_PROJ_MFMA_MIN_K;  // from this k on the dense product runs on MFMA
 
 // Random Projections (Section 3.3), HBM-bound on the read of G: one row per
 // thread, PROJ_JU columns of G loaded ahead, and the pass's block of Pi
@@ -408,11 +412,13 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
       }
       __syncthreads();
       for (int jb = 0; jb < jc; jb += PROJ_JU) {
+        // columns past the block (last batch only) repeat its last column and
+        // are skipped below: every load is issued unconditionally
         float g[PROJ_JU];
 #pragma unroll
         for (int u = 0; u < PROJ_JU; ++u) {
-          const int j = j0 + jb + u;
-          g[u] = (jb + u < jc) ? G[(int64_t)j * ld_g + ii] : 0.0f;
+          const int j = j0 + (jb + u < jc ? jb + u : jc - 1);
+          g[u] = G[(int64_t)j * ld_g + ii];
         }
 #pragma unroll
         for (int u = 0; u < PROJ_JU; ++u) {
@@ -533,6 +539,122 @@ k_project_sparse(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, co
   }
 }
 
+// Dense projection on the matrix cores: G (n x d) times Pi (d x k) with
+// v_mfma_f32_32x32x2f32, fp32 products accumulated in fp32 (MI355X's fp32
+// MFMA rate is twice its fp32 vector rate without packed instructions, so at
+// k >= 8 the product stops being bound by the VALU).  A wave computes
+// MF_MT * 32 rows x the pass's 32 output columns.  Operands:
+//   A (32 x 2): lane l holds G[row0 + l % 32, j + l / 32] -- lanes 0-31 and
+//     32-63 each read 32 consecutive rows of one column (one 128-byte line);
+//   B (2 x 32): lane l holds Pi[j + l / 32, t0 + l % 32], from a block of Pi
+//     staged in LDS (zero past d and past the pass's kt columns);
+//   D (32 x 32): register r of lane l holds row (r / 4) * 8 + (l / 32) * 4 +
+//     r % 4, column l % 32.
+// Eight 2-column steps of A are loaded before their MFMAs.  The order in
+// which the hardware adds the products is its own, so the result is checked
+// against the exact product with the dot-product error bound.
+constexpr int MF_THREADS = 256;
+constexpr int MF_JC = 256;  // columns of G per staged block of Pi (32 KB)
+constexpr int MF_KU = 8;    // 2-column steps per batch of loads
+constexpr int MF_MT = 2;    // 32-row tiles per wave
+typedef float mf_v16 __attribute__((ext_vector_type(16)));
+
+__global__ void __launch_bounds__(MF_THREADS)
+k_project_mfma(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k,
+               int t0, const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh,
+               uint32_t* __restrict__ blockmax) {
+  __shared__ float sPi[MF_JC * 32];
+  __shared__ uint32_t smax[MF_THREADS / 64][33];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int kt = (k - t0 < 32) ? k - t0 : 32;
+  const bool last = t0 + 32 >= k;
+  const int col = lane & 31, khalf = lane >> 5;
+  uint32_t mxc = 0u, mxh = 0u;
+  constexpr int64_t ROWS = (MF_THREADS / 64) * MF_MT * 32;  // rows per block per pass
+  for (int64_t base = (int64_t)blockIdx.x * ROWS; base < n; base += (int64_t)gridDim.x * ROWS) {
+    const int64_t rw = base + (int64_t)wave * MF_MT * 32;
+    int64_t rc[MF_MT];
+#pragma unroll
+    for (int mt = 0; mt < MF_MT; ++mt) {
+      const int64_t r = rw + mt * 32 + col;
+      rc[mt] = r < n ? r : n - 1;  // rows past the end read row n-1 and store nothing
+    }
+    mf_v16 acc[MF_MT];
+#pragma unroll
+    for (int mt = 0; mt < MF_MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
+    for (int j0 = 0; j0 < d; j0 += MF_JC) {
+      const int jc = (d - j0 < MF_JC) ? d - j0 : MF_JC;
+      __syncthreads();  // the previous block of Pi is no longer read
+      for (int e = threadIdx.x; e < MF_JC * 32; e += MF_THREADS) {
+        const int jj = e >> 5, c = e & 31;
+        sPi[e] = (jj < jc && c < kt) ? Pi[(int64_t)(j0 + jj) * k + t0 + c] : 0.0f;
+      }
+      __syncthreads();
+      for (int kk = 0; kk < jc; kk += 2 * MF_KU) {
+        float a[MF_KU][MF_MT];
+#pragma unroll
+        for (int u = 0; u < MF_KU; ++u) {
+          const int jj = kk + 2 * u + khalf;
+          const int64_t jg = j0 + (jj < jc ? jj : jc - 1);  // past the block: a finite value times a zero of Pi
+#pragma unroll
+          for (int mt = 0; mt < MF_MT; ++mt) a[u][mt] = G[jg * ld_g + rc[mt]];
+        }
+#pragma unroll
+        for (int u = 0; u < MF_KU; ++u) {
+          const int jj = kk + 2 * u + khalf;
+          const float b = sPi[(jj < MF_JC ? jj : MF_JC - 1) * 32 + col] * (jj < jc ? 1.0f : 0.0f);
+#pragma unroll
+          for (int mt = 0; mt < MF_MT; ++mt)
+            acc[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u][mt], b, acc[mt], 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MF_MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = rw + mt * 32 + (r / 4) * 8 + khalf * 4 + (r % 4);
+        if (row < n && col < kt) {
+          const float v = acc[mt][r];
+          GH[row * ld_gh + t0 + col] = v;
+          const uint32_t m = __float_as_uint(v) & 0x7fffffffu;
+          mxc = m > mxc ? m : mxc;
+        }
+      }
+    if (last) {
+#pragma unroll
+      for (int q = 0; q < MF_MT / 2; ++q) {
+        const int64_t row = rw + q * 64 + lane;
+        if (row < n) {
+          const float hv = h[row];
+          GH[row * ld_gh + k] = hv;
+          for (int64_t t = k + 1; t < ld_gh; ++t) GH[row * ld_gh + t] = 0.0f;
+          const uint32_t m = __float_as_uint(hv) & 0x7fffffffu;
+          mxh = m > mxh ? m : mxh;
+        }
+      }
+    }
+  }
+  // block maxima: column col's lanes are l and l + 32; then the waves
+  {
+    const uint32_t o = __shfl_xor(mxc, 32, 64);
+    mxc = o > mxc ? o : mxc;
+    mxh = wave_max_u32(mxh);
+    if (lane < 32) smax[wave][lane] = mxc;
+    if (lane == 0) smax[wave][32] = mxh;
+  }
+  __syncthreads();
+  if (threadIdx.x <= 32) {
+    uint32_t r = 0u;
+#pragma unroll
+    for (int w = 0; w < MF_THREADS / 64; ++w) r = smax[w][threadIdx.x] > r ? smax[w][threadIdx.x] : r;
+    if (threadIdx.x < kt) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + threadIdx.x] = r;
+    if (threadIdx.x == 32 && last) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = r;
+  }
+}
+
 // Dense d x k Pi from its row-sparse form: one thread per row j, entries
 // added in q order in fp32 (columns outside [0, k) are dropped).
 __global__ void __launch_bounds__(256)
@@ -636,6 +758,13 @@ SketchWs sketch_ws_layout(int64_t n, int32_t d, int32_t k) {
 // (block b's maxima of every channel sit in row b of blockmax).
 int launch_dense_projection(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
                             const float* Pi, float* GH, int64_t ld_gh, uint32_t* blockmax, hipStream_t st) {
+  if (k >= PROJ_MFMA_MIN_K) {
+    const int nb = sketch_blocks(n, (MF_THREADS / 64) * MF_MT * 32);
+    for (int t0 = 0; t0 < k; t0 += 32)
+      hipLaunchKernelGGL(k_project_mfma, dim3(nb), dim3(MF_THREADS), 0, st, G, n, d, ld_g, Pi, k, t0, h, GH, ld_gh,
+                         blockmax);
+    return nb;
+  }
   const int nb = sketch_blocks(n, PROJ_THREADS);
   for (int t0 = 0; t0 < k; t0 += PROJ_KT) {
     const int kt = (k - t0 < PROJ_KT) ? k - t0 : PROJ_KT;
