@@ -27,6 +27,11 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
+# LDS scatter-add roof of the histogram kernel: conflict-free 64-bit LDS adds
+# of two channels each retire 17.8 channel-adds per clock per CU on MI355X
+# (paper_2211_12858_amd/microbench/lds_scatter.hip, rotated mode); 256 CUs at 2.4 GHz.
+LDS_ADDS_PER_CLK_CU = 17.8
+LDS_PEAK_GADDS = LDS_ADDS_PER_CLK_CU * 256 * 2.4
 METRIC = "sec per tree (depth 6) + histogram-build HBM GB/s (% of peak)"
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "hist_traffic.json")
 HIST_SRCS = [os.path.join(HERE, "paper_2211_12858_amd", "csrc", f) for f in ("sb_hist.hip", "sb_hist_plan.h")]
@@ -66,6 +71,12 @@ def hist_algorithmic_bytes(leaf_off, depth, m, n_bins, c):
             rows, nodes = int(np.minimum(left, right).sum()), len(left)
         per_launch.append(rows * (m + 4 * c) + nodes * m * n_bins * c * 4)
     return per_launch
+
+
+def hist_rows_built(leaf_off, depth):
+    """Rows whose histograms are built at each level (all at the root, the smaller child of each pair below)."""
+    sizes = level_sizes(leaf_off, depth)
+    return [int(s.sum()) if l == 0 else int(np.minimum(s[0::2], s[1::2]).sum()) for l, s in enumerate(sizes)]
 
 
 def leaf_algorithmic_bytes(n, d, n_leaves):
@@ -289,13 +300,17 @@ def main():
 
     # algorithmic bytes of every timed histogram launch (trees are deterministic
     # in their uniforms, so replaying one reproduces its node sizes)
-    alg = []
+    alg, rows_built = [], []
     for s in range(K):
         ss.step(wl.kind, G_T, h, u=u_all[W + s], Pi=Pi)
         torch.cuda.synchronize()
         alg += hist_algorithmic_bytes(ss.leaf_off.cpu().numpy(), wl.depth, wl.m, wl.n_bins, wl.k + 1)
+        rows_built += hist_rows_built(ss.leaf_off.cpu().numpy(), wl.depth)
     assert len(alg) == launches, (len(alg), launches)
     bytes_per_launch = float(np.mean(alg))
+    adds_per_launch = float(np.mean(rows_built)) * wl.m * (wl.k + 1)
+    lds_gadds = adds_per_launch / (hist_ms / launches * 1e-3) / 1e9
+    hist_kernel = "k_hist_rot" if wl.k + 1 <= 6 else "k_hist"
     ms_per_launch = hist_ms / launches
     achieved = bytes_per_launch / (ms_per_launch * 1e-3) / 1e9
     traffic = traffic_for_current_kernel()
@@ -345,9 +360,19 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic,
-            "kernel": "k_hist",
+            "kernel": hist_kernel,
             "bytes_per_launch": bytes_per_launch,
             "ms_per_launch": ms_per_launch,
+        },
+        # the roof that binds the histogram kernel: its useful channel-adds
+        # (rows built x m features x c channels) per second against the LDS
+        # scatter-add rate measured for conflict-free 64-bit adds
+        "lds_roofline": {
+            "achieved": lds_gadds,
+            "peak": LDS_PEAK_GADDS,
+            "unit": "G channel-adds/s",
+            "frac": lds_gadds / LDS_PEAK_GADDS,
+            "adds_per_launch": adds_per_launch,
         },
     }
     out["next"] = {

@@ -30,12 +30,35 @@
 // the rows they all read stay in that XCD's L2.
 #include "sb_common.h"
 
+// Two-step prefetch in the rotated kernel (1) or one step (0): with the
+// rotated kernel's 32 register totals the deeper pipeline spills.
+#ifndef SB_HIST_ROT_DEEP
+#define SB_HIST_ROT_DEEP 0
+#endif
+#ifndef SB_HIST_ROT_OPAQUE
+#define SB_HIST_ROT_OPAQUE 0
+#endif
+
 namespace sb {
 
 HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   HistPlan p{};
   p.c = k + 1;
   p.pairs = (p.c + 1) / 2;
+  if (p.pairs <= ROT_PMAX && n_bins <= 256) {
+    p.rot = true;
+    p.nq = ROT_F / 4;
+    p.f = ROT_F;
+    p.slices = (m + ROT_F - 1) / ROT_F;
+    p.rows_wave = 64;
+    p.cells = 2 * p.pairs * p.f * n_bins;
+    int per_xcd = HIST_CUS_PER_XCD / p.slices;
+    if (per_xcd < 1) per_xcd = 1;
+    p.q = 8 * per_xcd;
+    p.q_pad = p.q;
+    p.slots = (int64_t)p.q + n_build;
+    return p;
+  }
   const int64_t quad_bytes = 4ll * n_bins * p.pairs * 8;
   int nq_max = (int)(HIST_LDS_BYTES / quad_bytes);
   const int quads_total = (m + 3) / 4;
@@ -152,14 +175,14 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
 // the change D = S - (tot_hi * 2^32 + tot_lo) is dHi * 2^32 + dLo with
 // |dLo|, |dHi| < 2^31: dLo is the sign-extended low word of D and dHi the
 // arithmetic high word of D - dLo.
+template <int H = HIST_MAX_CELLS_PER_THREAD / 2, int NT = HIST_THREADS>
 __device__ inline void fold_cells(const uint64_t* lds64, int64_t* tot) {
-  constexpr int H = HIST_MAX_CELLS_PER_THREAD / 2;
 #pragma unroll
   for (int i0 = 0; i0 < H; i0 += 4) {
     asm volatile("" ::: "memory");
     uint64_t cur[4];
 #pragma unroll
-    for (int ii = 0; ii < 4; ++ii) cur[ii] = (i0 + ii < H) ? lds64[threadIdx.x + HIST_THREADS * (i0 + ii)] : 0;
+    for (int ii = 0; ii < 4; ++ii) cur[ii] = (i0 + ii < H) ? lds64[threadIdx.x + NT * (i0 + ii)] : 0;
 #pragma unroll
     for (int ii = 0; ii < 4; ++ii) {
       if (i0 + ii < H) {
@@ -299,6 +322,162 @@ __device__ inline void add_row(uint64_t* lds64, const RowData<CMAX, NQMAX>& d, c
   }
 }
 
+// ---------------------------------------------------------------- rotated-feature order
+// With one lane per row and the whole wave on one feature, a wave's 64
+// 64-bit adds go to banks chosen by 64 random bins, and the collisions set
+// the speed (about two thirds of the LDS cycles).  The rotated variant lets
+// the feature choose the bank instead: a slice of ROT_F = 16 features keeps
+// its cells as [bin][pair][feature], so one (bin, pair) row of 16 cells fills
+// the 32 banks once and a cell's bank pair is its feature; at step i lane l
+// adds its row's values for feature (i + l) mod 16.  Each step then puts
+// exactly four lanes on every bank pair, whatever the bins.  Measured on
+// MI355X with random bins: 17.8 channel-adds/clk/CU, against 8.8 for the
+// one-feature-per-wave order.  A lane rotates its row's 16 bin bytes once
+// (by l mod 16), so that step i reads byte i.  Features past m come from
+// padding bytes (the row records hold ld_rec >= m bytes, ld_rec % 16 == 0;
+// the quad-major planes are clamped to the last one) and land in feature
+// columns that the reduction never reads.
+
+// Byte i of out = byte (i + r) mod 16 of the 16 bytes in w: whole words by
+// r / 4 in two mask stages (bitfield inserts, so that the compiler keeps the
+// words in registers instead of indexing a private array), then bytes by
+// r mod 4 (v_alignbyte_b32 takes the 4 bytes at offset r mod 4 of the 8-byte
+// pair {hi, lo}).
+__device__ inline void rotate16(const uint32_t* w, int r, uint32_t* out) {
+  const uint32_t m1 = 0u - (uint32_t)((r >> 2) & 1), m2 = 0u - (uint32_t)((r >> 3) & 1);
+  const uint32_t sb = (uint32_t)(r & 3);
+  uint32_t t[4], u[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) t[j] = (w[(j + 1) & 3] & m1) | (w[j] & ~m1);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) u[j] = (t[(j + 2) & 3] & m2) | (t[j] & ~m2);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) out[j] = __builtin_amdgcn_alignbyte(u[(j + 1) & 3], u[j], sb);
+}
+
+// The lane's row for a rotated slice: its 16 bin bytes from features f0 ..
+// f0+15 and its C channel values, all loads unconditional.  Row numbers are
+// below 2^31, so the row arithmetic is 32-bit with one 64-bit multiply-add
+// per record address.
+template <int C, bool FROM_REC>
+__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowData<C, 4>& d) {
+  const int32_t n1 = (int32_t)a.n - 1;
+  int32_t row = ref.on ? ref.raw : 0;
+  row = row < 0 ? 0 : (row > n1 ? n1 : row);
+  const uint32_t ur = (uint32_t)row;
+  const uint32_t* gp = reinterpret_cast<const uint32_t*>(
+      reinterpret_cast<const char*>(a.GH) + (uint64_t)ur * (uint32_t)(a.ld_gh * 4));
+  if constexpr (FROM_REC) {
+    load_run<4>(reinterpret_cast<const uint32_t*>(a.rec + (uint64_t)ur * (uint32_t)a.ld_rec + f0), d.word);
+  } else {
+    const int last = ((a.m + 3) >> 2) - 1;
+#pragma unroll
+    for (int qq = 0; qq < 4; ++qq) {
+      const int plane = (f0 >> 2) + qq < last ? (f0 >> 2) + qq : last;
+      d.word[qq] = (a.bins4 + (int64_t)plane * a.ld4)[ur];
+    }
+  }
+  uint32_t gw[C];
+  load_run<C>(gp, gw);
+#pragma unroll
+  for (int t = 0; t < C; ++t) d.g[t] = __uint_as_float(gw[t]);
+}
+
+typedef __attribute__((address_space(3))) unsigned long long lds_u64;
+
+// Cell (bin, pair, feature) of a rotated slice is the 64-bit LDS word
+// (bin * P + pair) * 16 + feature; offsets are 32-bit LDS byte offsets.
+template <int C>
+__device__ inline void add_row_rot(lds_u64* lds, const RowData<C, 4>& d, const int* qe, uint32_t r, uint32_t B) {
+  constexpr int P = (C + 1) / 2;
+  int32_t vq[2 * P];
+#pragma unroll
+  for (int t = 0; t < 2 * P; ++t) vq[t] = t < C ? (int32_t)rintf(ldexpf(d.g[t < C ? t : 0], qe[t < C ? t : 0])) : 0;
+  uint64_t pk[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) pk[p] = ((uint64_t)(uint32_t)vq[2 * p + 1] << 32) + (uint64_t)(int64_t)vq[2 * p];
+  uint32_t rw[4];
+  rotate16(d.word, (int)r, rw);
+#if SB_HIST_ROT_OPAQUE
+  // hide the lane's rotation from loop-invariant hoisting, so that the 16
+  // column offsets are recomputed per row instead of held in 16 registers
+  asm volatile("" : "+v"(r));
+#endif
+  // LDS byte address of cell (0, 0, 0); the cell addresses are formed as
+  // 32-bit integers (the compiler otherwise keeps 64-bit pointer sums)
+  const uint32_t base = (uint32_t)(size_t)lds;
+  const int bmax = (int)((B - 1) & 0xffu);  // B <= 256: the 8-bit mask lets the products use 24-bit multiplies
+#pragma unroll
+  for (int i = 0; i < ROT_F; ++i) {
+    int bin = (int)((rw[i >> 2] >> (8 * (i & 3))) & 0xffu);
+    bin = bin < bmax ? bin : bmax;
+    const uint32_t addr = base + (uint32_t)bin * (uint32_t)(P * ROT_F * 8) + ((r + (uint32_t)i) & (ROT_F - 1)) * 8u;
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+      __hip_atomic_fetch_add((lds_u64*)(size_t)(addr + p * ROT_F * 8), (unsigned long long)pk[p], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+}
+
+// Rows of virtual positions [v, vend) of one node for a rotated slice, as
+// run_segment, with 32-bit positions (every position and row is below 2^31,
+// so unsigned 32-bit sums of them do not wrap).
+template <int C, bool HAS_IDX>
+__device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, const int* qe, uint32_t v,
+                                       uint32_t vend, uint32_t pstart, uint32_t seg0, int wave, int lane, int f0,
+                                       uint32_t B) {
+  constexpr uint32_t rows_step = ROT_THREADS;
+  const uint32_t last_pos = seg0 + (vend - 1 - pstart);
+  const uint32_t lane_off = (uint32_t)(wave * 64 + lane);
+  const uint32_t r = (uint32_t)lane & (ROT_F - 1);
+  auto row_at = [&](uint32_t vs) -> RowRef {
+    const uint32_t vv = vs + lane_off;
+    RowRef rr;
+    rr.on = vv < vend;
+    uint32_t pos = seg0 + (vv - pstart);
+    pos = pos < last_pos ? pos : last_pos;
+    rr.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
+    return rr;
+  };
+  constexpr bool DEEP = SB_HIST_ROT_DEEP != 0;
+  RowRef r0 = row_at(v);
+  RowRef r1 = row_at(v + rows_step);
+  RowData<C, 4> d0, d1;
+  load_row_rot<C, HAS_IDX>(a, r0, f0, d0);
+  RowRef r2;
+  if constexpr (DEEP) {
+    r2 = row_at(v + 2 * rows_step);
+    load_row_rot<C, HAS_IDX>(a, r1, f0, d1);
+  }
+  int steps = 0;
+#pragma unroll 1
+  for (uint32_t vs = v; vs < vend; vs += rows_step) {
+    if constexpr (DEEP) {
+      const RowRef r3 = row_at(vs + 3 * rows_step);
+      RowData<C, 4> d2;
+      load_row_rot<C, HAS_IDX>(a, r2, f0, d2);
+      if (r0.on) add_row_rot<C>(lds, d0, qe, r, B);
+      r0 = r1;
+      d0 = d1;
+      r1 = r2;
+      d1 = d2;
+      r2 = r3;
+    } else {
+      const RowRef r2n = row_at(vs + 2 * rows_step);
+      load_row_rot<C, HAS_IDX>(a, r1, f0, d1);
+      if (r0.on) add_row_rot<C>(lds, d0, qe, r, B);
+      r0 = r1;
+      d0 = d1;
+      r1 = r2n;
+    }
+    if (++steps == a.steps_per_window) {
+      steps = 0;
+      lds_barrier();
+      fold_cells<ROT_CPT, ROT_THREADS>((const uint64_t*)lds, tot);
+    }
+  }
+}
+
 // Accumulate the lane's rows of virtual positions [v, vend) of one node
 // (segment start seg0, first virtual position pstart) into the LDS cells,
 // folding into `tot` at every window.  HAS_IDX: rows come through row_idx
@@ -311,6 +490,8 @@ template <int CMAX, int NQMAX, bool EXACT, bool HAS_IDX>
 __device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* tot, const int* qe, int64_t v,
                                    int64_t vend, int64_t pstart, int64_t seg0, int wave, int lane, int f0, int nq,
                                    int B, int FB, int c) {
+  auto load = [&](RowRef ref, RowData<CMAX, NQMAX>& d) { load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, ref, f0, nq, c, d); };
+  auto add = [&](const RowData<CMAX, NQMAX>& d) { add_row<CMAX, NQMAX, EXACT>(lds, d, qe, nq, B, FB, c); };
   const int rows_step = HIST_THREADS;
   const int64_t last_pos = seg0 + (vend - 1 - pstart);
   auto row_at = [&](int64_t vs, int64_t lim) -> RowRef {
@@ -335,11 +516,11 @@ __device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* to
   RowRef r0 = row_at(v, vend);
   RowRef r1 = row_at(v + rows_step, vend);
   RowData<CMAX, NQMAX> d0, d1;
-  load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r0, f0, nq, c, d0);
+  load(r0, d0);
   RowRef r2;
   if constexpr (DEEP) {
     r2 = row_at(v + 2 * rows_step, vend);
-    load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r1, f0, nq, c, d1);
+    load(r1, d1);
   }
   int steps = 0;
 #pragma unroll 1
@@ -347,8 +528,8 @@ __device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* to
     if constexpr (DEEP) {
       const RowRef r3 = row_at(vs + 3 * rows_step, vend);
       RowData<CMAX, NQMAX> d2;
-      load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r2, f0, nq, c, d2);
-      if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
+      load(r2, d2);
+      if (r0.on) add(d0);
       r0 = r1;
       d0 = d1;
       r1 = r2;
@@ -356,8 +537,8 @@ __device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* to
       r2 = r3;
     } else {
       const RowRef r2n = row_at(vs + 2 * rows_step, vend);
-      load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, r1, f0, nq, c, d1);
-      if (r0.on) add_row<CMAX, NQMAX, EXACT>(lds, d0, qe, nq, B, FB, c);
+      load(r1, d1);
+      if (r0.on) add(d0);
       r0 = r1;
       d0 = d1;
       r1 = r2n;
@@ -442,6 +623,98 @@ k_hist(HistArgs a) {
       tot[2 * i + 1] = 0;
     }
     __syncthreads();
+    v = vend;
+    ++p;
+    while (p < a.n_build && a.pre[p + 1] <= v) ++p;
+  }
+}
+
+// Rotated-feature kernel (c <= 6): the same work split, windows and
+// partials as k_hist, with the slice's cells in [bin][pair][feature] order.
+// Thread t owns the 64-bit cells t + ROT_THREADS * i, i < ROT_CPT.  At the
+// end of a node's part the totals go out through LDS, one pair at a time, in
+// the partial layout of k_hist ([pair][feature][bin], 16-byte channel
+// pairs), so the reduction kernels serve both.
+template <int C>
+__global__ void __launch_bounds__(ROT_THREADS)
+k_hist_rot(HistArgs a) {
+  extern __shared__ uint64_t lds64[];
+  constexpr int P = (C + 1) / 2;
+  const int b = blockIdx.x;
+  const int xcd = b & 7, g = b >> 3;
+  const int q = (g / a.slices) * 8 + xcd;
+  const int s = g % a.slices;
+  if (q >= a.q) return;
+  const int64_t T = a.pre[a.n_build];
+  const int64_t v0 = (int64_t)q * T / a.q;
+  const int64_t v1 = (int64_t)(q + 1) * T / a.q;
+  if (v0 >= v1) return;
+
+  int lo = 0, hi = a.n_build;  // pre[lo] <= v0 < pre[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (a.pre[mid] <= v0) lo = mid;
+    else hi = mid;
+  }
+  int p = lo;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int f0 = s * ROT_F;
+  const int B = a.n_bins;
+  int qe[C];
+#pragma unroll
+  for (int t = 0; t < C; ++t) qe[t] = __builtin_amdgcn_readfirstlane(a.qexp[t]);
+
+  int64_t tot[2 * ROT_CPT];
+#pragma unroll
+  for (int jj = 0; jj < 2 * ROT_CPT; ++jj) tot[jj] = 0;
+#pragma unroll
+  for (int i = 0; i < ROT_CPT; ++i) lds64[tid + ROT_THREADS * i] = 0;
+  __syncthreads();
+
+  longlong2* stage = reinterpret_cast<longlong2*>(lds64);  // [feature][B + 1] channel pairs
+  int64_t v = v0;
+  while (v < v1) {
+    const int32_t j = node_of(a, p);
+    const int64_t pstart = a.pre[p];
+    const int64_t vend = v1 < a.pre[p + 1] ? v1 : a.pre[p + 1];
+    const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
+    lds_u64* L = (lds_u64*)lds64;  // generic to LDS address space: 32-bit offsets
+    if (a.row_idx)
+      run_segment_rot<C, true>(a, L, tot, qe, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
+                               lane, f0, (uint32_t)B);
+    else
+      run_segment_rot<C, false>(a, L, tot, qe, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
+                                lane, f0, (uint32_t)B);
+    // The node-end barriers wait for LDS operations only: the partial stores
+    // take their data from registers, so nothing here waits for them.
+    lds_barrier();
+    fold_cells<ROT_CPT, ROT_THREADS>(lds64, tot);
+    lds_barrier();  // every fold read is done: the LDS becomes the staging area
+    longlong2* dst = reinterpret_cast<longlong2*>(a.partial + ((int64_t)s * a.slots + q + p) * a.cells);
+#pragma unroll 1
+    for (int pr = 0; pr < P; ++pr) {
+#pragma unroll
+      for (int i = 0; i < ROT_CPT; ++i) {
+        const int j64 = tid + ROT_THREADS * i;
+        const int row = j64 >> 4, bin = row / P, fl = j64 & (ROT_F - 1);
+        if (row - bin * P == pr && bin < B) stage[fl * (B + 1) + bin] = make_longlong2(tot[2 * i], tot[2 * i + 1]);
+      }
+      lds_barrier();
+      for (int e = tid; e < ROT_F * B; e += ROT_THREADS) {
+        const int fl = e / B, bin = e - fl * B;
+        dst[(int64_t)pr * ROT_F * B + e] = stage[fl * (B + 1) + bin];
+      }
+      lds_barrier();
+    }
+#pragma unroll
+    for (int i = 0; i < ROT_CPT; ++i) {
+      lds64[tid + ROT_THREADS * i] = 0;
+      tot[2 * i] = 0;
+      tot[2 * i + 1] = 0;
+    }
+    lds_barrier();
     v = vend;
     ++p;
     while (p < a.n_build && a.pre[p + 1] <= v) ++p;
@@ -714,7 +987,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.cells = pl.cells;
   a.q = pl.q;
   a.cpt = (pl.cells + HIST_THREADS - 1) / HIST_THREADS;
-  const int rows_step = HIST_THREADS;
+  const int rows_step = pl.rot ? ROT_THREADS : HIST_THREADS;
   a.steps_per_window = WINDOW_ROWS / rows_step > 0 ? WINDOW_ROWS / rows_step : 1;
   a.slots = pl.slots;
   if (rows_step > WINDOW_ROWS) return fail(SB_E_UNSUPPORTED, "histogram step exceeds the fixed-point window");
@@ -724,8 +997,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   hipEvent_t e0 = nullptr, e1 = nullptr;
   const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;
   if (prof) (void)hipEventRecord(e0, st);
-  const size_t lds_bytes = (size_t)HIST_LDS_BYTES;
-  const int cm = pl.c <= 4 ? 4 : pl.c <= 8 ? 8 : pl.c <= 16 ? 16 : 24;
+  const size_t lds_bytes = (size_t)(pl.rot ? ROT_CELLS * 8 : HIST_LDS_BYTES);
+  const int cm = pl.c <= 8 ? 8 : pl.c <= 16 ? 16 : 24;
   const int nm = pl.nq <= 4 ? 4 : pl.nq <= 8 ? 8 : 16;
   // exact shapes: every slice holds nq quads and there are exactly c channels
   const bool even = pl.slices * pl.nq * 4 - m < 4;
@@ -737,12 +1010,17 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   if (cm == CM && nm == NM) {                                                                        \
     hipLaunchKernelGGL((k_hist<CM, NM, false>), dim3(grid), dim3(HIST_THREADS), lds_bytes, st, a); \
   } else
-  SB_HIST_EXACT(6, 5) SB_HIST_EXACT(6, 3) SB_HIST_EXACT(6, 13) SB_HIST_EXACT(11, 2) SB_HIST_EXACT(21, 1)
-  SB_HIST_CASE(4, 4) SB_HIST_CASE(4, 8) SB_HIST_CASE(4, 16)
+#define SB_HIST_ROT(C)                                                                            \
+  if (pl.rot && pl.c == C) {                                                                      \
+    hipLaunchKernelGGL((k_hist_rot<C>), dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a);         \
+  } else
+  SB_HIST_ROT(1) SB_HIST_ROT(2) SB_HIST_ROT(3) SB_HIST_ROT(4) SB_HIST_ROT(5) SB_HIST_ROT(6)
+  SB_HIST_EXACT(11, 2) SB_HIST_EXACT(21, 1)
   SB_HIST_CASE(8, 4) SB_HIST_CASE(8, 8) SB_HIST_CASE(8, 16)
   SB_HIST_CASE(16, 4) SB_HIST_CASE(16, 8) SB_HIST_CASE(16, 16)
   SB_HIST_CASE(24, 4) SB_HIST_CASE(24, 8) SB_HIST_CASE(24, 16)
   return fail(SB_E_UNSUPPORTED, "sb_build_histograms: more than 24 channels (k > 23)");
+#undef SB_HIST_ROT
 #undef SB_HIST_EXACT
 #undef SB_HIST_CASE
   if (prof) {

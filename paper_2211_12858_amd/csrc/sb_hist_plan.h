@@ -33,7 +33,22 @@ constexpr int HIST_CUS_PER_XCD = 32;
 // A lane holds the bin words of up to 16 quads (64 features) of its row.
 constexpr int HIST_MAX_QUADS = 16;
 
+// Rotated-feature workgroups (up to 3 channel pairs, c <= 6): a slice of 16
+// features, LDS cells [bin][pair][feature] for 256 bins (12288 64-bit cells,
+// 96 KB), ROT_CPT cells per thread.
+#ifndef SB_HIST_ROT_THREADS
+#define SB_HIST_ROT_THREADS 768
+#endif
+constexpr int ROT_THREADS = SB_HIST_ROT_THREADS;
+constexpr int ROT_F = 16;
+constexpr int ROT_PMAX = 3;
+constexpr int ROT_CELLS = 256 * ROT_PMAX * ROT_F;
+constexpr int ROT_CPT = ROT_CELLS / ROT_THREADS;
+static_assert(ROT_CPT * ROT_THREADS == ROT_CELLS, "rotated cells must split evenly over the threads");
+static_assert(WINDOW_ROWS % ROT_THREADS == 0, "a fixed-point window must be a whole number of steps");
+
 struct HistPlan {
+  bool rot;       // rotated-feature kernel (c <= 6), else the row-per-lane kernel
   int c;          // channels k+1
   int pairs;      // 64-bit LDS cells per (feature, bin): ceil(c/2)
   int nq;         // 4-feature quads per slice

@@ -11,6 +11,10 @@
 //  3: ds_write_b32 (no atomic), lane = row, 6 channels
 //  4: u32 atomics, conflict-free bins (lane-distinct), lane = row
 //  5: u32 atomics, lane = row, channel stride FB+1 and feature stride B+1
+//  6: u64 atomics, rotated feature order: cells [bin][pair][16 features],
+//     lane l adds feature (i + l) mod 16 at step i (the histogram kernel's
+//     layout for up to 6 channels)
+//  7: the same cells with every lane on feature i at step i (same-feature order)
 #include <hip/hip_runtime.h>
 #include <cstdio>
 #include <cstdlib>
@@ -52,6 +56,16 @@ __global__ void __launch_bounds__(768) k(int iters, int* out) {
 #pragma unroll
         for (int t = 0; t < C / 2; ++t) atomicAdd(l64 + t * FB + f * B + bin, (unsigned long long)it);
       }
+    } else if (MODE == 6 || MODE == 7) {
+      // 16 features x 256 bins x 3 pairs = 12288 64-bit cells (96 KB)
+      unsigned long long* l64 = reinterpret_cast<unsigned long long*>(lds);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int bin = fmix(seed + it * 131u + i) & 255;
+        const int col = MODE == 6 ? ((i + lane) & 15) : i;
+#pragma unroll
+        for (int t = 0; t < C / 2; ++t) atomicAdd(l64 + bin * 48 + t * 16 + col, (unsigned long long)it);
+      }
     } else {
 #pragma unroll
       for (int f = 0; f < F; ++f) {
@@ -76,7 +90,7 @@ int main() {
   hipEvent_t e0, e1; CK(hipEventCreate(&e0)); CK(hipEventCreate(&e1));
   const int grid = 256, iters = 200;
   const size_t lds = (C * (FB + 32) + 64) * 4;  // 124 KB < 160 KB
-  for (int mode = 0; mode < 6; ++mode) {
+  for (int mode = 0; mode < 8; ++mode) {
     auto L = [&]() {
       switch (mode) {
         case 0: hipLaunchKernelGGL(k<0>, dim3(grid), dim3(768), lds, 0, iters, out); break;
@@ -85,6 +99,8 @@ int main() {
         case 3: hipLaunchKernelGGL(k<3>, dim3(grid), dim3(768), lds, 0, iters, out); break;
         case 4: hipLaunchKernelGGL(k<4>, dim3(grid), dim3(768), lds, 0, iters, out); break;
         case 5: hipLaunchKernelGGL(k<5>, dim3(grid), dim3(768), lds, 0, iters, out); break;
+        case 6: hipLaunchKernelGGL(k<6>, dim3(grid), dim3(768), lds, 0, iters, out); break;
+        case 7: hipLaunchKernelGGL(k<7>, dim3(grid), dim3(768), lds, 0, iters, out); break;
       }
     };
     L(); CK(hipGetLastError()); CK(hipDeviceSynchronize());
@@ -92,7 +108,7 @@ int main() {
     float ms; CK(hipEventElapsedTime(&ms, e0, e1));
     // channel-adds: mode 1 does 10 rows x 6 ch per wave per iteration (60 of 64 lanes)
     double rows = (double)grid * 768 * iters * (mode == 1 ? 10.0 / 64.0 : 1.0);
-    double adds = rows * F * C;
+    double adds = rows * (mode >= 6 ? 16 : F) * C;
     printf("mode %d: %.3f ms  %.2f channel-adds/clk/CU\n", mode, ms, adds / (ms * 1e-3) / (256.0 * 2.4e9));
   }
   printf("done\n");
