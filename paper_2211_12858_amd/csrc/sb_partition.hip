@@ -7,7 +7,7 @@
 //   left  row at i -> o_j + (L[i] - Lb_j)
 //   right row at i -> o_j + nleft_j + (i - o_j) - (L[i] - Lb_j),
 // which keeps the original order inside each child.
-//   k_part_flags   : per tile of 4096 positions, the flags as 64-bit wave
+//   k_part_flags   : per tile of PT_TILE positions, the flags as 64-bit wave
 //                    ballots (bit = lane = position) and the tile's left count.
 //                    Lanes take consecutive positions, so the row-index reads
 //                    are coalesced; the bin is one byte of the split feature's
@@ -24,10 +24,14 @@
 namespace sb {
 namespace {
 
+#ifndef SB_PART_ITERS
+#define SB_PART_ITERS 4
+#endif
 constexpr int PT_THREADS = 256;
-constexpr int PT_ITERS = 16;
-constexpr int PT_TILE = PT_THREADS * PT_ITERS;  // 4096 positions
-constexpr int PT_MASKS = PT_TILE / 64;          // 64 ballots per tile
+constexpr int PT_ITERS = SB_PART_ITERS;
+constexpr int PT_TILE = PT_THREADS * PT_ITERS;  // positions per tile
+constexpr int PT_MASKS = PT_TILE / 64;          // ballots per tile
+static_assert(PT_MASKS >= 1 && PT_MASKS <= 64, "a tile's ballots are counted by one wave");
 
 struct PartArgs {
   const uint8_t* bins_cm;
@@ -186,7 +190,7 @@ __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
       int64_t c = 0;
       if (t < a.n_tiles) {
         const int w = (int)(x - t * PT_TILE);
-        const uint64_t mq = a.masks[t * PT_MASKS + lane];
+        const uint64_t mq = lane < PT_MASKS ? a.masks[t * PT_MASKS + lane] : 0;
         if (lane < (w >> 6)) c = popc64(mq);
         else if (lane == (w >> 6) && (w & 63)) c = popc64(mq & ((uint64_t(1) << (w & 63)) - 1));
       }
@@ -232,15 +236,17 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
   }
   // ballots of the tile and their exclusive prefix, by the first wave
   if (wave == 0) {
-    const uint64_t m = a.masks[(int64_t)blockIdx.x * PT_MASKS + lane];
+    const uint64_t m = lane < PT_MASKS ? a.masks[(int64_t)blockIdx.x * PT_MASKS + lane] : 0;
     const int32_t c = popc64(m);
     int32_t incl = c;
     for (int off = 1; off < 64; off <<= 1) {
       const int32_t o = __shfl_up(incl, off, 64);
       if (lane >= off) incl += o;
     }
-    mk[lane] = m;
-    pre[lane] = a.tile_off[blockIdx.x] + incl - c;
+    if (lane < PT_MASKS) {
+      mk[lane] = m;
+      pre[lane] = a.tile_off[blockIdx.x] + incl - c;
+    }
   }
   __syncthreads();
   const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);

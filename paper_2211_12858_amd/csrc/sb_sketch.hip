@@ -20,7 +20,14 @@ namespace sb {
 namespace {
 
 constexpr int NORM_THREADS = 256;
-constexpr int64_t NORM_CHUNK = 16384;  // rows per partial sum
+#ifndef SB_NORM_CHUNK
+#define SB_NORM_CHUNK 16384
+#endif
+#ifndef SB_NORM_UNROLL
+#define SB_NORM_UNROLL 4
+#endif
+constexpr int64_t NORM_CHUNK = SB_NORM_CHUNK;  // rows per partial sum
+constexpr int NORM_UNROLL = SB_NORM_UNROLL;    // 16-byte loads in flight per thread
 constexpr int NORM_MAX_PARTS = 256;
 
 __device__ inline double wave_sum(double v) {
@@ -53,16 +60,16 @@ k_colnorm_partial(const float* __restrict__ G, int64_t n, int64_t ld, int parts,
   if (i0 >= i1) {
     // empty chunk: contributes zero
   } else if ((((uintptr_t)(col + i0)) & 15) == 0) {
-    // four 16-byte loads in flight per thread; fixed summation order
+    // NORM_UNROLL 16-byte loads in flight per thread; fixed summation order
     const int64_t nv = (i1 - i0) >> 2;
     const float4* v4 = reinterpret_cast<const float4*>(col + i0);
     int64_t q = threadIdx.x;
-    for (; q + 3 * NORM_THREADS < nv; q += 4 * NORM_THREADS) {
-      float4 x[4];
+    for (; q + (NORM_UNROLL - 1) * NORM_THREADS < nv; q += NORM_UNROLL * NORM_THREADS) {
+      float4 x[NORM_UNROLL];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) x[u] = v4[q + u * NORM_THREADS];
+      for (int u = 0; u < NORM_UNROLL; ++u) x[u] = v4[q + u * NORM_THREADS];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < NORM_UNROLL; ++u) {
         acc += (double)x[u].x * x[u].x;
         acc += (double)x[u].y * x[u].y;
         acc += (double)x[u].z * x[u].z;
