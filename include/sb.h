@@ -117,7 +117,8 @@ int32_t sb_abi_version(void);
 
 /*
  * Workspace bytes needed by one call.  Arguments not used by a call are
- * ignored (pass 0).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
+ * ignored (pass 0).  n: rows (every call that takes rows, BUILD_HISTOGRAMS
+ * included).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
  * SCORE_SPLITS, PARTITION_ROWS), leaves (LEAF_VALUES).  depth: tree depth
  * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES, GRADIENTS; the
  * LEAF_VALUES size covers all three hessian forms).  UPDATE_PREDICTIONS needs
@@ -250,6 +251,9 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  * node_off  n_nodes+1 offsets.
  * build_list  n_build node ids to build (NULL = every node; n_build ignored).
  * H         out: [n_nodes][m][k+1][n_bins] fp64.
+ * With k+1 <= 6 channels and n_bins <= 256 the call first writes every row's
+ * quantised values (16 bytes per row) into its workspace, so the workspace
+ * grows with n: sb_workspace_bytes(SB_CALL_BUILD_HISTOGRAMS, n, ...).
  */
 int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
                             int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,

@@ -62,14 +62,14 @@ int32_t check_hist_shape(const char* call, int64_t n, int32_t m, int32_t n_bins,
 }
 
 struct GrowLayout {
-  int64_t H0, H1, rows_tmp, offs, blists, pre, feat_s, feat_b, call, total;
+  int64_t H0, H1, rows_tmp, offs, blists, pre, feat_s, feat_b, qrow, call, total;
 };
 
 GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t depth) {
   GrowLayout L{};
   const int64_t maxn = int64_t(1) << (depth - 1);
   const int64_t hbytes = align256(maxn * m * n_bins * (int64_t)(k + 1) * 8);
-  const int64_t hw = hist_ws_bytes(m, n_bins, k, (int32_t)maxn);
+  const int64_t hw = hist_ws_bytes(n, m, n_bins, k, (int32_t)maxn, false);
   if (hw < 0) {
     L.total = -1;
     return L;
@@ -97,6 +97,10 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   p += align256(maxn * m * 8);
   L.feat_b = p;
   p += align256(maxn * m * 4);
+  // quantised sketch rows of the rotated histogram kernel, written at the
+  // root and read by every level
+  L.qrow = p;
+  if (hist_plan(m, n_bins, k, 1).rot) p += align256(n * 16);
   L.call = p;
   p += call;
   L.total = p;
@@ -178,8 +182,8 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
       if (k < 1 || k > 255) break;
       return hist_exponents_ws_bytes(k);
     case SB_CALL_BUILD_HISTOGRAMS: {
-      if (m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || n_nodes < 1) break;
-      const int64_t b = hist_ws_bytes(m, n_bins, k, n_nodes);
+      if (n < 1 || n > MAX_ROWS || m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || n_nodes < 1) break;
+      const int64_t b = hist_ws_bytes(n, m, n_bins, k, n_nodes, true);
       if (b < 0) break;
       return b;
     }
@@ -349,7 +353,7 @@ int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* r
     return fail(SB_E_ARG, "sb_build_histograms: n_build must be in [1, min(n_nodes, 65535)]");
   if (hist_plan(m, n_bins, k, n_build).nq == 0)
     return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) cells exceed the LDS budget");
-  rc = need_ws(ws, ws_bytes, hist_ws_bytes(m, n_bins, k, n_build), call);
+  rc = need_ws(ws, ws_bytes, hist_ws_bytes(n, m, n_bins, k, n_build, true), call);
   if (rc) return rc;
   return launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
                                  build_list, n_build, H, ws, static_cast<hipStream_t>(stream));
@@ -444,6 +448,7 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   int64_t* pre = reinterpret_cast<int64_t*>(w + G.pre);
   double* feat_s = reinterpret_cast<double*>(w + G.feat_s);
   int32_t* feat_b = reinterpret_cast<int32_t*>(w + G.feat_b);
+  uint32_t* qrow = reinterpret_cast<uint32_t*>(w + G.qrow);
   // the fused level end (histogram reduction, subtraction and per-feature
   // scoring in one kernel) holds its per-bin channel sums in registers
   const bool fused = k + 1 <= FUSED_SCORE_MAX_C;
@@ -470,11 +475,11 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
                                    nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
-                                   min_child_weight);
+                                   min_child_weight, qrow, false);
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
                                    level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],
-                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight);
+                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight, qrow, true);
     }
     if (rc) return rc;
     if (fused)

@@ -83,10 +83,12 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
 }
 
 // Workspace: [pre: n_build+1 int64][partials: slices * slots * cells int64]
-int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
+// [quantised rows: n * 16 bytes, rotated kernel and quant_rows only]
+int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows) {
   HistPlan p = hist_plan(m, n_bins, k, n_build);
   if (p.nq == 0) return -1;
-  return align256((int64_t)(n_build + 1) * 8) + align256((int64_t)p.slices * p.slots * p.cells * 8);
+  const int64_t q = (p.rot && quant_rows) ? align256(n * 16) : 0;
+  return align256((int64_t)(n_build + 1) * 8) + align256((int64_t)p.slices * p.slots * p.cells * 8) + q;
 }
 
 namespace {
@@ -99,6 +101,7 @@ struct HistArgs {
   const uint8_t* rec;
   int64_t ld_rec;
   const int32_t* qexp;
+  const uint32_t* qrow;  // rotated kernel: quantised sketch rows, 4 words per row
   const int32_t* row_idx;
   const int32_t* node_off;
   const int32_t* build_list;
@@ -355,18 +358,32 @@ __device__ inline void rotate16(const uint32_t* w, int r, uint32_t* out) {
   for (int j = 0; j < 4; ++j) out[j] = __builtin_amdgcn_alignbyte(u[(j + 1) & 3], u[j], sb);
 }
 
+// A row of a rotated slice: the slice's 16 bin bytes and the row's quantised
+// channel values (one 16-byte word of 21-bit fields).
+struct RowRot {
+  uint32_t word[4];
+  uint32_t q[4];
+};
+
+typedef uint32_t u32x4_a16 __attribute__((ext_vector_type(4), aligned(16)));
+
 // The lane's row for a rotated slice: its 16 bin bytes from features f0 ..
-// f0+15 and its C channel values, all loads unconditional.  Row numbers are
+// f0+15 and its quantised values, all loads unconditional.  Row numbers are
 // below 2^31, so the row arithmetic is 32-bit with one 64-bit multiply-add
 // per record address.
-template <int C, bool FROM_REC>
-__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowData<C, 4>& d) {
+template <bool FROM_REC>
+__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowRot& d) {
   const int32_t n1 = (int32_t)a.n - 1;
   int32_t row = ref.on ? ref.raw : 0;
   row = row < 0 ? 0 : (row > n1 ? n1 : row);
   const uint32_t ur = (uint32_t)row;
-  const uint32_t* gp = reinterpret_cast<const uint32_t*>(
-      reinterpret_cast<const char*>(a.GH) + (uint64_t)ur * (uint32_t)(a.ld_gh * 4));
+  {
+    const u32x4_a16 v = *reinterpret_cast<const u32x4_a16*>(a.qrow + (uint64_t)ur * 4u);
+    d.q[0] = v.x;
+    d.q[1] = v.y;
+    d.q[2] = v.z;
+    d.q[3] = v.w;
+  }
   if constexpr (FROM_REC) {
     load_run<4>(reinterpret_cast<const uint32_t*>(a.rec + (uint64_t)ur * (uint32_t)a.ld_rec + f0), d.word);
   } else {
@@ -377,10 +394,46 @@ __device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowDa
       d.word[qq] = (a.bins4 + (int64_t)plane * a.ld4)[ur];
     }
   }
-  uint32_t gw[C];
-  load_run<C>(gp, gw);
+}
+
+// Channel value t of a quantised row: the sign-extended 21-bit field t.
+__device__ inline int32_t qfield(const uint32_t* q, int t) {
+  const uint32_t lo = q[(t / 3) * 2], hi = q[(t / 3) * 2 + 1];
+  const int f = t % 3;
+  uint32_t x;
+  if (f == 0) x = lo << 11;                                    // bits 0-20
+  else if (f == 1) x = ((lo >> QFIELD_BITS) | (hi << 11)) << 11;  // bits 21-41
+  else x = hi << 1;                                            // bits 42-62
+  return (int32_t)x >> 11;
+}
+
+// Quantised sketch rows for the rotated kernel: channel t of row i becomes
+// rint(GH[i, t] * 2^qexp[t]), the same fp32 operations that define the
+// histogram's fixed point, packed into the 21-bit fields of one 16-byte word.
+template <int C>
+__global__ void __launch_bounds__(256)
+k_quant_rows(const float* __restrict__ GH, int64_t ld_gh, int64_t n, const int32_t* __restrict__ qexp,
+             uint32_t* __restrict__ qrow) {
+  int qe[C];
 #pragma unroll
-  for (int t = 0; t < C; ++t) d.g[t] = __uint_as_float(gw[t]);
+  for (int t = 0; t < C; ++t) qe[t] = __builtin_amdgcn_readfirstlane(qexp[t]);
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  uint32_t gw[C];
+  load_run<C>(reinterpret_cast<const uint32_t*>(GH + i * ld_gh), gw);
+  uint64_t half[2] = {0, 0};
+  constexpr uint64_t M = (uint64_t(1) << QFIELD_BITS) - 1;
+#pragma unroll
+  for (int t = 0; t < C; ++t) {
+    const int32_t v = (int32_t)rintf(ldexpf(__uint_as_float(gw[t]), qe[t]));
+    half[t / 3] |= ((uint64_t)(uint32_t)v & M) << (QFIELD_BITS * (t % 3));
+  }
+  u32x4_a16 o;
+  o.x = (uint32_t)half[0];
+  o.y = (uint32_t)(half[0] >> 32);
+  o.z = (uint32_t)half[1];
+  o.w = (uint32_t)(half[1] >> 32);
+  *reinterpret_cast<u32x4_a16*>(qrow + i * 4) = o;
 }
 
 typedef __attribute__((address_space(3))) unsigned long long lds_u64;
@@ -388,11 +441,11 @@ typedef __attribute__((address_space(3))) unsigned long long lds_u64;
 // Cell (bin, pair, feature) of a rotated slice is the 64-bit LDS word
 // (bin * P + pair) * 16 + feature; offsets are 32-bit LDS byte offsets.
 template <int C>
-__device__ inline void add_row_rot(lds_u64* lds, const RowData<C, 4>& d, const int* qe, uint32_t r, uint32_t B) {
+__device__ inline void add_row_rot(lds_u64* lds, const RowRot& d, uint32_t r, uint32_t B) {
   constexpr int P = (C + 1) / 2;
   int32_t vq[2 * P];
 #pragma unroll
-  for (int t = 0; t < 2 * P; ++t) vq[t] = t < C ? (int32_t)rintf(ldexpf(d.g[t < C ? t : 0], qe[t < C ? t : 0])) : 0;
+  for (int t = 0; t < 2 * P; ++t) vq[t] = t < C ? qfield(d.q, t) : 0;
   uint64_t pk[P];
 #pragma unroll
   for (int p = 0; p < P; ++p) pk[p] = ((uint64_t)(uint32_t)vq[2 * p + 1] << 32) + (uint64_t)(int64_t)vq[2 * p];
@@ -423,7 +476,7 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowData<C, 4>& d, const i
 // run_segment, with 32-bit positions (every position and row is below 2^31,
 // so unsigned 32-bit sums of them do not wrap).
 template <int C, bool HAS_IDX>
-__device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, const int* qe, uint32_t v,
+__device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, uint32_t v,
                                        uint32_t vend, uint32_t pstart, uint32_t seg0, int wave, int lane, int f0,
                                        uint32_t B) {
   constexpr uint32_t rows_step = ROT_THREADS;
@@ -442,21 +495,21 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
   constexpr bool DEEP = SB_HIST_ROT_DEEP != 0;
   RowRef r0 = row_at(v);
   RowRef r1 = row_at(v + rows_step);
-  RowData<C, 4> d0, d1;
-  load_row_rot<C, HAS_IDX>(a, r0, f0, d0);
+  RowRot d0, d1;
+  load_row_rot<HAS_IDX>(a, r0, f0, d0);
   RowRef r2;
   if constexpr (DEEP) {
     r2 = row_at(v + 2 * rows_step);
-    load_row_rot<C, HAS_IDX>(a, r1, f0, d1);
+    load_row_rot<HAS_IDX>(a, r1, f0, d1);
   }
   int steps = 0;
 #pragma unroll 1
   for (uint32_t vs = v; vs < vend; vs += rows_step) {
     if constexpr (DEEP) {
       const RowRef r3 = row_at(vs + 3 * rows_step);
-      RowData<C, 4> d2;
-      load_row_rot<C, HAS_IDX>(a, r2, f0, d2);
-      if (r0.on) add_row_rot<C>(lds, d0, qe, r, B);
+      RowRot d2;
+      load_row_rot<HAS_IDX>(a, r2, f0, d2);
+      if (r0.on) add_row_rot<C>(lds, d0, r, B);
       r0 = r1;
       d0 = d1;
       r1 = r2;
@@ -464,8 +517,8 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
       r2 = r3;
     } else {
       const RowRef r2n = row_at(vs + 2 * rows_step);
-      load_row_rot<C, HAS_IDX>(a, r1, f0, d1);
-      if (r0.on) add_row_rot<C>(lds, d0, qe, r, B);
+      load_row_rot<HAS_IDX>(a, r1, f0, d1);
+      if (r0.on) add_row_rot<C>(lds, d0, r, B);
       r0 = r1;
       d0 = d1;
       r1 = r2n;
@@ -662,9 +715,6 @@ k_hist_rot(HistArgs a) {
   const int wave = tid >> 6, lane = tid & 63;
   const int f0 = s * ROT_F;
   const int B = a.n_bins;
-  int qe[C];
-#pragma unroll
-  for (int t = 0; t < C; ++t) qe[t] = __builtin_amdgcn_readfirstlane(a.qexp[t]);
 
   int64_t tot[2 * ROT_CPT];
 #pragma unroll
@@ -682,10 +732,10 @@ k_hist_rot(HistArgs a) {
     const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
     lds_u64* L = (lds_u64*)lds64;  // generic to LDS address space: 32-bit offsets
     if (a.row_idx)
-      run_segment_rot<C, true>(a, L, tot, qe, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
+      run_segment_rot<C, true>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
                                lane, f0, (uint32_t)B);
     else
-      run_segment_rot<C, false>(a, L, tot, qe, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
+      run_segment_rot<C, false>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
                                 lane, f0, (uint32_t)B);
     // The node-end barriers wait for LDS operations only: the partial stores
     // take their data from registers, so nothing here waits for them.
@@ -955,7 +1005,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
                                 const int64_t* pre_given, const double* H_parent, double* feat_s, int32_t* feat_b,
-                                double lam, double mcw) {
+                                double lam, double mcw, uint32_t* qrow, bool qrow_ready) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build);
   HistArgs a{};
   a.bins4 = bins4;
@@ -971,6 +1021,22 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   char* w = static_cast<char*>(ws);
   a.pre = pre_given ? const_cast<int64_t*>(pre_given) : reinterpret_cast<int64_t*>(w);
   a.partial = reinterpret_cast<int64_t*>(w + align256((int64_t)(n_build + 1) * 8));
+  if (pl.rot) {
+    // the quantised rows live in the caller's buffer (kept across a tree's
+    // levels) or else at the end of this call's workspace
+    if (!qrow)
+      qrow = reinterpret_cast<uint32_t*>(w + align256((int64_t)(n_build + 1) * 8) +
+                                         align256((int64_t)pl.slices * pl.slots * pl.cells * 8));
+    a.qrow = qrow;
+    if (!qrow_ready) {
+      const unsigned qb = (unsigned)((n + 255) / 256);
+#define SB_QUANT(C) \
+  if (pl.c == C) hipLaunchKernelGGL((k_quant_rows<C>), dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow); else
+      SB_QUANT(1) SB_QUANT(2) SB_QUANT(3) SB_QUANT(4) SB_QUANT(5) SB_QUANT(6)
+      return fail(SB_E_UNSUPPORTED, "sb_build_histograms: quantised rows hold at most 6 channels");
+#undef SB_QUANT
+    }
+  }
   a.H = H;
   a.Hp = H_parent;
   a.n = n;

@@ -17,6 +17,13 @@ constexpr int QBITS = 18;
 // most two windows, so 2 * WINDOW_ROWS * 2^QBITS must stay below 2^31.
 constexpr int WINDOW_ROWS = 3072;
 static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point window overflow");
+// The rotated kernel reads each row's quantised values, not its fp32 sketch:
+// up to 6 channels as QFIELD_BITS-bit two's-complement fields of one 16-byte
+// word (channels 0-2 in bits 0-62 of the low 64 bits, 3-5 in the high 64
+// bits), written once per sketch, so that a row's values are one 16-byte load.
+constexpr int QFIELD_BITS = 21;
+constexpr int QROW_MAX_C = 6;
+static_assert(QBITS + 2 <= QFIELD_BITS, "a quantised value of magnitude <= 2^QBITS and its sign must fit a field");
 
 // ---------------------------------------------------------------- histogram plan
 // One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
@@ -61,6 +68,8 @@ struct HistPlan {
   int64_t slots;  // partial slots per slice: q + n_build
 };
 HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
-int64_t hist_ws_bytes(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
+// Workspace of one histogram launch; quant_rows adds the n quantised sketch
+// rows of the rotated kernel (16 bytes each).
+int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows);
 
 }  // namespace sb

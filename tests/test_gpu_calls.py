@@ -149,6 +149,33 @@ def test_histograms(n, m, B, k, n_nodes, build, seed):
         assert np.isnan(Hg[others]).all()
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("gathered", [False, True])
+def test_histograms_quantised_extremes(k, gathered):
+    # values whose fixed-point images reach the largest magnitude, 2^18
+    # (1 - 2^-24 with exponent 18), mixed with both signs of small values, on
+    # every channel count the 16-byte quantised rows hold (c = 2 .. 6)
+    rng = np.random.default_rng(100 + k)
+    n, m, B = 3001, 9, 16
+    c = k + 1
+    top = np.float32(1.0) - np.float32(2.0 ** -24)
+    pool = np.array([top, -top, top / 2, -top / 2, 2.0 ** -19, -(2.0 ** -19), 0.0, 3e-5, -7e-6], dtype=np.float32)
+    GH = pool[rng.integers(0, len(pool), size=(n, c))]
+    GH[0, :] = top
+    GH[1, :] = -top
+    bins = rng.integers(0, B, size=(n, m), dtype=np.uint8)
+    qexp = gu.qexp_rule(GH)
+    assert (qexp == 18).all()
+    rows = np.sort(rng.permutation(n)[: n - 500]).astype(np.int32) if gathered else np.arange(n, dtype=np.int32)
+    off = np.array([0, len(rows)], dtype=np.int32)
+    Hg = gu.host_layout(gu.run_hist(bins, GH, qexp, B, rows if gathered else None, off).cpu().numpy())
+    Ho = oracle.node_histograms(bins, GH, rows, B)
+    counts = oracle.node_histograms(bins, np.ones((n, 1), dtype=np.float32), rows, B)[..., 0]
+    mass = oracle.node_histograms(bins, np.abs(GH), rows, B)
+    ok1, ok2, worst = gu.hist_tolerance_ok(Hg[0], Ho, counts, qexp, mass, np.abs(GH.astype(np.float64)).max(axis=0))
+    assert ok1 and ok2, worst
+
+
 def test_histograms_identity_row_order_and_determinism():
     case = small_case(50000, 20, 256, 5, seed=11)
     GH = oracle.materialise(case.G, case.h, *oracle.identity_sketch(5))
