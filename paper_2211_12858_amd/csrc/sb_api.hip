@@ -475,11 +475,12 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
                                    nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
-                                   min_child_weight, qrow, false);
+                                   min_child_weight, qrow, false, depth > 1);
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
                                    level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],
-                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight, qrow, true);
+                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight, qrow, true,
+                                   l < depth - 1);
     }
     if (rc) return rc;
     if (fused)

@@ -41,7 +41,7 @@
 
 namespace sb {
 
-HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
+HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool thin_ok) {
   HistPlan p{};
   p.c = k + 1;
   p.pairs = (p.c + 1) / 2;
@@ -49,14 +49,46 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
     p.rot = true;
     p.nq = ROT_F / 4;
     p.f = ROT_F;
-    p.slices = (m + ROT_F - 1) / ROT_F;
     p.rows_wave = 64;
     p.cells = 2 * p.pairs * p.f * n_bins;
-    int per_xcd = HIST_CUS_PER_XCD / p.slices;
-    if (per_xcd < 1) per_xcd = 1;
-    p.q = 8 * per_xcd;
+    p.slices_full = m / ROT_F;
+    const int r = m % ROT_F;
+    p.f_thin = 0;
+    if (r) {
+      int ft = 1;
+      while (ft < r) ft <<= 1;
+      if (ft == ROT_F || !thin_ok) ++p.slices_full;  // a padded slice of 16
+      else p.f_thin = ft;
+    }
+    p.slices = p.slices_full + (p.f_thin ? 1 : 0);
+    const int S = p.slices_full, cus = HIST_CUS_PER_XCD;
+    if (!p.f_thin) {
+      p.a_full = cus / S > 0 ? cus / S : 1;
+      p.b_thin = 0;
+    } else if (S == 0) {
+      p.a_full = 0;
+      p.b_thin = cus;
+    } else {
+      // per-workgroup work of a full slice is ROT_F rows-steps per row of its
+      // group, of the thin slice f_thin: minimise the larger of the two
+      int best_a = 1;
+      double best = 1e30;
+      for (int aa = 1; aa * S < cus || aa == 1; ++aa) {
+        const int bb = cus - aa * S > 0 ? cus - aa * S : 1;
+        const double cost = fmax((double)ROT_F / aa, (double)p.f_thin / bb);
+        if (cost < best) {
+          best = cost;
+          best_a = aa;
+        }
+      }
+      p.a_full = best_a;
+      p.b_thin = cus - best_a * S > 0 ? cus - best_a * S : 1;
+    }
+    p.q = 8 * p.a_full;
+    p.q_thin = 8 * p.b_thin;
     p.q_pad = p.q;
-    p.slots = (int64_t)p.q + n_build;
+    p.slots = (int64_t)(p.q > p.q_thin ? p.q : p.q_thin) + n_build;
+    p.grid = 8 * (p.a_full * S + p.b_thin);
     return p;
   }
   const int64_t quad_bytes = 4ll * n_bins * p.pairs * 8;
@@ -79,16 +111,23 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build) {
   p.q = 8 * per_xcd;
   p.q_pad = p.q;
   p.slots = (int64_t)p.q + n_build;
+  p.slices_full = p.slices;
+  p.f_thin = p.b_thin = p.q_thin = 0;
+  p.a_full = per_xcd;
+  p.grid = p.q_pad * p.slices;
   return p;
 }
 
 // Workspace: [pre: n_build+1 int64][partials: slices * slots * cells int64]
 // [quantised rows: n * 16 bytes, rotated kernel and quant_rows only]
 int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows) {
-  HistPlan p = hist_plan(m, n_bins, k, n_build);
+  HistPlan p = hist_plan(m, n_bins, k, n_build, false);
   if (p.nq == 0) return -1;
+  const HistPlan pt = hist_plan(m, n_bins, k, n_build, true);  // rows read straight from the data
+  int64_t part = (int64_t)p.slices * p.slots * p.cells;
+  if ((int64_t)pt.slices * pt.slots * pt.cells > part) part = (int64_t)pt.slices * pt.slots * pt.cells;
   const int64_t q = (p.rot && quant_rows) ? align256(n * 16) : 0;
-  return align256((int64_t)(n_build + 1) * 8) + align256((int64_t)p.slices * p.slots * p.cells * 8) + q;
+  return align256((int64_t)(n_build + 1) * 8) + align256(part * 8) + q;
 }
 
 namespace {
@@ -109,11 +148,18 @@ struct HistArgs {
   int64_t* partial;
   double* H;
   const double* Hp;  // parent level, for the fused sibling subtraction (may be null)
+  bool store_h;      // fused level end: write H (skipped at a tree's last level, whose H has no reader)
   int64_t n;
   int32_t m, n_bins, c, pairs, n_nodes, n_build;
   int32_t nq, f, slices, rows_wave, cells, q, cpt, steps_per_window;
   int64_t slots;
+  int32_t slices_full, f_thin, a_full, b_thin, q_thin;  // rotated kernel plan (see HistPlan)
 };
+
+// Row groups of slice s (the thin slice has its own count).
+__device__ inline int32_t groups_of(const HistArgs& a, int s) {
+  return (a.f_thin && s >= a.slices_full) ? a.q_thin : a.q;
+}
 
 __device__ inline int32_t clamp_i32(int64_t v, int64_t lo, int64_t hi) {
   return (int32_t)(v < lo ? lo : (v > hi ? hi : v));
@@ -358,10 +404,13 @@ __device__ inline void rotate16(const uint32_t* w, int r, uint32_t* out) {
   for (int j = 0; j < 4; ++j) out[j] = __builtin_amdgcn_alignbyte(u[(j + 1) & 3], u[j], sb);
 }
 
-// A row of a rotated slice: the slice's 16 bin bytes and the row's quantised
-// channel values (one 16-byte word of 21-bit fields).
+// A row of a rotated slice of FT features: the slice's bin bytes (FT of
+// them, in NW words) and the row's quantised channel values (one 16-byte
+// word of 21-bit fields).
+template <int FT>
 struct RowRot {
-  uint32_t word[4];
+  static constexpr int NW = (FT + 3) / 4;
+  uint32_t word[NW];
   uint32_t q[4];
 };
 
@@ -371,8 +420,9 @@ typedef uint32_t u32x4_a16 __attribute__((ext_vector_type(4), aligned(16)));
 // f0+15 and its quantised values, all loads unconditional.  Row numbers are
 // below 2^31, so the row arithmetic is 32-bit with one 64-bit multiply-add
 // per record address.
-template <bool FROM_REC>
-__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowRot& d) {
+template <int FT, bool FROM_REC>
+__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowRot<FT>& d) {
+  constexpr int NW = RowRot<FT>::NW;
   const int32_t n1 = (int32_t)a.n - 1;
   int32_t row = ref.on ? ref.raw : 0;
   row = row < 0 ? 0 : (row > n1 ? n1 : row);
@@ -385,11 +435,13 @@ __device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowRo
     d.q[3] = v.w;
   }
   if constexpr (FROM_REC) {
-    load_run<4>(reinterpret_cast<const uint32_t*>(a.rec + (uint64_t)ur * (uint32_t)a.ld_rec + f0), d.word);
+    // f0 is a multiple of 16 and ld_rec % 16 == 0: the slice's bytes are
+    // 16-byte aligned (4- or 8-byte loads for a thin slice)
+    load_run<NW>(reinterpret_cast<const uint32_t*>(a.rec + (uint64_t)ur * (uint32_t)a.ld_rec + f0), d.word);
   } else {
     const int last = ((a.m + 3) >> 2) - 1;
 #pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
+    for (int qq = 0; qq < NW; ++qq) {
       const int plane = (f0 >> 2) + qq < last ? (f0 >> 2) + qq : last;
       d.word[qq] = (a.bins4 + (int64_t)plane * a.ld4)[ur];
     }
@@ -438,10 +490,15 @@ k_quant_rows(const float* __restrict__ GH, int64_t ld_gh, int64_t n, const int32
 
 typedef __attribute__((address_space(3))) unsigned long long lds_u64;
 
-// Cell (bin, pair, feature) of a rotated slice is the 64-bit LDS word
-// (bin * P + pair) * 16 + feature; offsets are 32-bit LDS byte offsets.
-template <int C>
-__device__ inline void add_row_rot(lds_u64* lds, const RowRot& d, uint32_t r, uint32_t B) {
+// Cell (bin, pair, slot) of a rotated slice is the 64-bit LDS word
+// (bin * P + pair) * 16 + slot; offsets are 32-bit LDS byte offsets.  In a
+// slice of 16 features the slot is the feature.  A thin slice of FT < 16
+// features keeps R = 16 / FT copies: lane l adds into copy (l / FT) mod R,
+// slot feature + FT * copy, and at step i handles feature (i + l) mod FT.
+// Any 16 consecutive lanes then cover the 16 slots once, so every step puts
+// four lanes on each bank pair, as in a full slice.
+template <int C, int FT>
+__device__ inline void add_row_rot(lds_u64* lds, const RowRot<FT>& d, uint32_t r, uint32_t slot0, uint32_t B) {
   constexpr int P = (C + 1) / 2;
   int32_t vq[2 * P];
 #pragma unroll
@@ -449,6 +506,28 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot& d, uint32_t r, ui
   uint64_t pk[P];
 #pragma unroll
   for (int p = 0; p < P; ++p) pk[p] = ((uint64_t)(uint32_t)vq[2 * p + 1] << 32) + (uint64_t)(int64_t)vq[2 * p];
+  // LDS byte address of cell (0, 0, 0); the cell addresses are formed as
+  // 32-bit integers (the compiler otherwise keeps 64-bit pointer sums)
+  const uint32_t base = (uint32_t)(size_t)lds;
+  const int bmax = (int)((B - 1) & 0xffu);  // B <= 256: the 8-bit mask lets the products use 24-bit multiplies
+  if constexpr (FT < ROT_F) {
+#pragma unroll
+    for (int i = 0; i < FT; ++i) {
+      const uint32_t fi = (r + (uint32_t)i) & (FT - 1);  // this step's feature
+      // the word is chosen by a bit mask (a select or a per-lane index into
+      // d.word is turned into scratch-memory indexing by the compiler)
+      const uint32_t sel = FT > 4 ? 0u - ((fi >> 2) & 1u) : 0u;
+      const uint32_t w = d.word[0] ^ ((d.word[0] ^ d.word[RowRot<FT>::NW - 1]) & sel);
+      int bin = (int)((w >> (8 * (fi & 3))) & 0xffu);
+      bin = bin < bmax ? bin : bmax;
+      const uint32_t addr = base + (uint32_t)bin * (uint32_t)(P * ROT_F * 8) + (slot0 + fi) * 8u;
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+        __hip_atomic_fetch_add((lds_u64*)(size_t)(addr + p * ROT_F * 8), (unsigned long long)pk[p], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
+    return;
+  }
   uint32_t rw[4];
   rotate16(d.word, (int)r, rw);
 #if SB_HIST_ROT_OPAQUE
@@ -456,10 +535,6 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot& d, uint32_t r, ui
   // column offsets are recomputed per row instead of held in 16 registers
   asm volatile("" : "+v"(r));
 #endif
-  // LDS byte address of cell (0, 0, 0); the cell addresses are formed as
-  // 32-bit integers (the compiler otherwise keeps 64-bit pointer sums)
-  const uint32_t base = (uint32_t)(size_t)lds;
-  const int bmax = (int)((B - 1) & 0xffu);  // B <= 256: the 8-bit mask lets the products use 24-bit multiplies
 #pragma unroll
   for (int i = 0; i < ROT_F; ++i) {
     int bin = (int)((rw[i >> 2] >> (8 * (i & 3))) & 0xffu);
@@ -475,14 +550,15 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot& d, uint32_t r, ui
 // Rows of virtual positions [v, vend) of one node for a rotated slice, as
 // run_segment, with 32-bit positions (every position and row is below 2^31,
 // so unsigned 32-bit sums of them do not wrap).
-template <int C, bool HAS_IDX>
+template <int C, int FT, bool HAS_IDX>
 __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, uint32_t v,
                                        uint32_t vend, uint32_t pstart, uint32_t seg0, int wave, int lane, int f0,
                                        uint32_t B) {
   constexpr uint32_t rows_step = ROT_THREADS;
   const uint32_t last_pos = seg0 + (vend - 1 - pstart);
   const uint32_t lane_off = (uint32_t)(wave * 64 + lane);
-  const uint32_t r = (uint32_t)lane & (ROT_F - 1);
+  const uint32_t r = (uint32_t)lane & (FT - 1);
+  const uint32_t slot0 = FT < ROT_F ? (((uint32_t)lane / FT) & (ROT_F / FT - 1)) * FT : 0u;
   auto row_at = [&](uint32_t vs) -> RowRef {
     const uint32_t vv = vs + lane_off;
     RowRef rr;
@@ -495,21 +571,21 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
   constexpr bool DEEP = SB_HIST_ROT_DEEP != 0;
   RowRef r0 = row_at(v);
   RowRef r1 = row_at(v + rows_step);
-  RowRot d0, d1;
-  load_row_rot<HAS_IDX>(a, r0, f0, d0);
+  RowRot<FT> d0, d1;
+  load_row_rot<FT, HAS_IDX>(a, r0, f0, d0);
   RowRef r2;
   if constexpr (DEEP) {
     r2 = row_at(v + 2 * rows_step);
-    load_row_rot<HAS_IDX>(a, r1, f0, d1);
+    load_row_rot<FT, HAS_IDX>(a, r1, f0, d1);
   }
   int steps = 0;
 #pragma unroll 1
   for (uint32_t vs = v; vs < vend; vs += rows_step) {
     if constexpr (DEEP) {
       const RowRef r3 = row_at(vs + 3 * rows_step);
-      RowRot d2;
-      load_row_rot<HAS_IDX>(a, r2, f0, d2);
-      if (r0.on) add_row_rot<C>(lds, d0, r, B);
+      RowRot<FT> d2;
+      load_row_rot<FT, HAS_IDX>(a, r2, f0, d2);
+      if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
       r0 = r1;
       d0 = d1;
       r1 = r2;
@@ -517,8 +593,8 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
       r2 = r3;
     } else {
       const RowRef r2n = row_at(vs + 2 * rows_step);
-      load_row_rot<HAS_IDX>(a, r1, f0, d1);
-      if (r0.on) add_row_rot<C>(lds, d0, r, B);
+      load_row_rot<FT, HAS_IDX>(a, r1, f0, d1);
+      if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
       r0 = r1;
       d0 = d1;
       r1 = r2n;
@@ -688,19 +764,15 @@ k_hist(HistArgs a) {
 // end of a node's part the totals go out through LDS, one pair at a time, in
 // the partial layout of k_hist ([pair][feature][bin], 16-byte channel
 // pairs), so the reduction kernels serve both.
-template <int C>
-__global__ void __launch_bounds__(ROT_THREADS)
-k_hist_rot(HistArgs a) {
-  extern __shared__ uint64_t lds64[];
+// Slice s of FT features (16, or a thin slice's f_thin), row group q of
+// qn: the rows of virtual positions [q T / qn, (q+1) T / qn).
+template <int C, int FT>
+__device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds64, int s, int q, int qn) {
   constexpr int P = (C + 1) / 2;
-  const int b = blockIdx.x;
-  const int xcd = b & 7, g = b >> 3;
-  const int q = (g / a.slices) * 8 + xcd;
-  const int s = g % a.slices;
-  if (q >= a.q) return;
+  constexpr int R = ROT_F / FT;  // copies of each cell in the slice
   const int64_t T = a.pre[a.n_build];
-  const int64_t v0 = (int64_t)q * T / a.q;
-  const int64_t v1 = (int64_t)(q + 1) * T / a.q;
+  const int64_t v0 = (int64_t)q * T / qn;
+  const int64_t v1 = (int64_t)(q + 1) * T / qn;
   if (v0 >= v1) return;
 
   int lo = 0, hi = a.n_build;  // pre[lo] <= v0 < pre[hi]
@@ -723,7 +795,7 @@ k_hist_rot(HistArgs a) {
   for (int i = 0; i < ROT_CPT; ++i) lds64[tid + ROT_THREADS * i] = 0;
   __syncthreads();
 
-  longlong2* stage = reinterpret_cast<longlong2*>(lds64);  // [feature][B + 1] channel pairs
+  longlong2* stage = reinterpret_cast<longlong2*>(lds64);  // [slot][B + 1] channel pairs
   int64_t v = v0;
   while (v < v1) {
     const int32_t j = node_of(a, p);
@@ -732,11 +804,11 @@ k_hist_rot(HistArgs a) {
     const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
     lds_u64* L = (lds_u64*)lds64;  // generic to LDS address space: 32-bit offsets
     if (a.row_idx)
-      run_segment_rot<C, true>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
-                               lane, f0, (uint32_t)B);
+      run_segment_rot<C, FT, true>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
+                                   lane, f0, (uint32_t)B);
     else
-      run_segment_rot<C, false>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
-                                lane, f0, (uint32_t)B);
+      run_segment_rot<C, FT, false>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0,
+                                    wave, lane, f0, (uint32_t)B);
     // The node-end barriers wait for LDS operations only: the partial stores
     // take their data from registers, so nothing here waits for them.
     lds_barrier();
@@ -752,9 +824,17 @@ k_hist_rot(HistArgs a) {
         if (row - bin * P == pr && bin < B) stage[fl * (B + 1) + bin] = make_longlong2(tot[2 * i], tot[2 * i + 1]);
       }
       lds_barrier();
-      for (int e = tid; e < ROT_F * B; e += ROT_THREADS) {
+      // features 0 .. FT-1 of the slice; a thin slice adds its R copies
+      for (int e = tid; e < FT * B; e += ROT_THREADS) {
         const int fl = e / B, bin = e - fl * B;
-        dst[(int64_t)pr * ROT_F * B + e] = stage[fl * (B + 1) + bin];
+        longlong2 x = stage[fl * (B + 1) + bin];
+#pragma unroll
+        for (int rc = 1; rc < R; ++rc) {
+          const longlong2 y = stage[(fl + FT * rc) * (B + 1) + bin];
+          x.x += y.x;
+          x.y += y.y;
+        }
+        dst[(int64_t)pr * ROT_F * B + e] = x;
       }
       lds_barrier();
     }
@@ -768,6 +848,38 @@ k_hist_rot(HistArgs a) {
     v = vend;
     ++p;
     while (p < a.n_build && a.pre[p + 1] <= v) ++p;
+  }
+}
+
+// Rotated-feature kernel (c <= 6): the same windows and partials as k_hist,
+// with the slice's cells in [bin][pair][slot] order.  Thread t owns the
+// 64-bit cells t + ROT_THREADS * i, i < ROT_CPT.  At the end of a node's part
+// the totals go out through LDS, one pair at a time, in the partial layout
+// of k_hist ([pair][feature][bin], 16-byte channel pairs), so the reduction
+// kernels serve both.  Workgroup b runs on XCD b % 8; on each XCD the first
+// a_full * slices_full workgroups take the full slices of a_full row groups
+// (so the slices of a row group share the XCD's L2) and the next b_thin the
+// thin slice.
+template <int C>
+__global__ void __launch_bounds__(ROT_THREADS)
+k_hist_rot(HistArgs a) {
+  extern __shared__ uint64_t lds64[];
+  const int b = blockIdx.x;
+  const int xcd = b & 7, g = b >> 3;
+  const int nfull = a.a_full * a.slices_full;
+  if (g < nfull) {
+    const int q = (g / a.slices_full) * 8 + xcd;
+    if (q < a.q) hist_rot_group<C, ROT_F>(a, lds64, g % a.slices_full, q, a.q);
+    return;
+  }
+  const int q = (g - nfull) * 8 + xcd;
+  if (!a.f_thin || q >= a.q_thin) return;
+  const int s = a.slices_full;
+  switch (a.f_thin) {
+    case 1: hist_rot_group<C, 1>(a, lds64, s, q, a.q_thin); break;
+    case 2: hist_rot_group<C, 2>(a, lds64, s, q, a.q_thin); break;
+    case 4: hist_rot_group<C, 4>(a, lds64, s, q, a.q_thin); break;
+    default: hist_rot_group<C, 8>(a, lds64, s, q, a.q_thin); break;
   }
 }
 
@@ -797,9 +909,10 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   const int64_t lo = a.pre[p], hi = a.pre[p + 1];
   int64_t sum = 0;
   if (hi > lo) {
-    const int64_t qlo = group_of(lo, T, a.q), qhi = group_of(hi - 1, T, a.q);
+    const int32_t qn = groups_of(a, s);
+    const int64_t qlo = group_of(lo, T, qn), qhi = group_of(hi - 1, T, qn);
     const int64_t* src = a.partial + ((int64_t)s * a.slots + p) * a.cells + e;
-    if (T >= a.q) {
+    if (T >= qn) {
       // every row group holds at least one position: independent loads, four sums
       int64_t acc[4] = {0, 0, 0, 0};
       int64_t q = qlo;
@@ -811,7 +924,7 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
       sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     } else {
       for (int64_t q = qlo; q <= qhi; ++q)
-        if (q * T / a.q < (q + 1) * T / a.q) sum += src[q * a.cells];
+        if (q * T / qn < (q + 1) * T / qn) sum += src[q * a.cells];
     }
   }
   const int64_t cpn = (int64_t)a.m * a.c * a.n_bins;
@@ -867,8 +980,9 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
   const int64_t cpn = (int64_t)a.m * c * B;
   const int64_t T = a.pre[a.n_build];
   const int64_t lo = a.pre[p], hi = a.pre[p + 1];
-  const int64_t qlo = hi > lo ? group_of(lo, T, a.q) : 0, qhi = hi > lo ? group_of(hi - 1, T, a.q) : -1;
-  const bool dense = T >= a.q;  // every row group holds at least one position
+  const int32_t qn = groups_of(a, s);
+  const int64_t qlo = hi > lo ? group_of(lo, T, qn) : 0, qhi = hi > lo ? group_of(hi - 1, T, qn) : -1;
+  const bool dense = T >= qn;  // every row group holds at least one position
   // int64 channel sums of this bin over the node's row groups: the loads of
   // four groups and every channel pair are in flight together
   int64_t acc_lo[PMAX], acc_hi[PMAX];
@@ -898,7 +1012,7 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
       }
     }
     for (; q <= qhi; ++q) {
-      if (dense || q * T / a.q < (q + 1) * T / a.q) {
+      if (dense || q * T / qn < (q + 1) * T / qn) {
 #pragma unroll
         for (int pr = 0; pr < PMAX; ++pr)
           if (pr < a.pairs) {
@@ -917,11 +1031,11 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
     if (t < c && on) {
       const int64_t idx = ((int64_t)f * c + t) * B + bin;
       const double x = ldexp((double)((t & 1) ? acc_hi[t >> 1] : acc_lo[t >> 1]), -a.qexp[t]);
-      a.H[(int64_t)j * cpn + idx] = x;
+      if (a.store_h) a.H[(int64_t)j * cpn + idx] = x;
       xv[t * B + bin] = x;
       if (sib) {
         const double xs = a.Hp[(int64_t)p * cpn + idx] - x;
-        a.H[(int64_t)(j ^ 1) * cpn + idx] = xs;
+        if (a.store_h) a.H[(int64_t)(j ^ 1) * cpn + idx] = xs;
         xv[(c + t) * B + bin] = xs;
       }
     }
@@ -1005,8 +1119,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
                                 const int64_t* pre_given, const double* H_parent, double* feat_s, int32_t* feat_b,
-                                double lam, double mcw, uint32_t* qrow, bool qrow_ready) {
-  const HistPlan pl = hist_plan(m, n_bins, k, n_build);
+                                double lam, double mcw, uint32_t* qrow, bool qrow_ready, bool store_h) {
+  const HistPlan pl = hist_plan(m, n_bins, k, n_build, row_idx == nullptr);
   HistArgs a{};
   a.bins4 = bins4;
   a.ld4 = ld4;
@@ -1039,6 +1153,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   }
   a.H = H;
   a.Hp = H_parent;
+  a.store_h = store_h;
   a.n = n;
   a.m = m;
   a.n_bins = n_bins;
@@ -1052,6 +1167,11 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.rows_wave = pl.rows_wave;
   a.cells = pl.cells;
   a.q = pl.q;
+  a.slices_full = pl.slices_full;
+  a.f_thin = pl.f_thin;
+  a.a_full = pl.a_full;
+  a.b_thin = pl.b_thin;
+  a.q_thin = pl.q_thin;
   a.cpt = (pl.cells + HIST_THREADS - 1) / HIST_THREADS;
   const int rows_step = pl.rot ? ROT_THREADS : HIST_THREADS;
   a.steps_per_window = WINDOW_ROWS / rows_step > 0 ? WINDOW_ROWS / rows_step : 1;
@@ -1059,7 +1179,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   if (rows_step > WINDOW_ROWS) return fail(SB_E_UNSUPPORTED, "histogram step exceeds the fixed-point window");
 
   if (!pre_given) hipLaunchKernelGGL(k_hist_plan, dim3(1), dim3(1024), 0, st, a);
-  const int grid = pl.q_pad * pl.slices;
+  const int grid = pl.grid;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;
   if (prof) (void)hipEventRecord(e0, st);

@@ -63,11 +63,23 @@ struct HistPlan {
   int slices;     // feature slices
   int rows_wave;  // rows one wave handles per step (64 / nq)
   int cells;      // 2 * pairs * f * n_bins channel cells per workgroup
-  int q;          // row groups per slice
+  int q;          // row groups per (full) slice
   int q_pad;      // q rounded up to a multiple of 8 (XCD-aware mapping)
-  int64_t slots;  // partial slots per slice: q + n_build
+  int64_t slots;  // partial slots per slice: max(q, q_thin) + n_build
+  // Rotated kernel: the first slices_full slices hold 16 features each; when
+  // m is not a multiple of 16 the rest go to one thin slice of f_thin
+  // features (a power of two below 16), whose workgroups keep 16 / f_thin
+  // copies of each cell so that its adds stay conflict-free while a row
+  // costs f_thin steps instead of 16.  Per XCD: a_full row groups of every
+  // full slice and b_thin row groups of the thin slice (q = 8 a_full,
+  // q_thin = 8 b_thin), chosen to even out the work of its 32 CUs.  Only for
+  // rows read straight from the data (the root): rows gathered through row
+  // indices are cheaper to read when the slices of a row group share an XCD,
+  // so there the last slice is a padded slice of 16 like the others.
+  int slices_full, f_thin, a_full, b_thin, q_thin;
+  int grid;       // histogram workgroups
 };
-HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build);
+HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool thin_ok = false);
 // Workspace of one histogram launch; quant_rows adds the n quantised sketch
 // rows of the rotated kernel (16 bytes each).
 int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows);

@@ -112,6 +112,10 @@ HIST_CASES = [
     (12000, 31, 256, 10, 32, True, 6),      # k=10, many nodes, some empty
     (5000, 3, 7, 2, 2, False, 7),           # odd bins, m not a multiple of 4
     (7001, 100, 256, 5, 1, False, 8),       # five slices, root read straight from the data
+    (20011, 24, 256, 5, 4, True, 9),        # a 16-feature slice and a thin slice of 8 (two cell copies)
+    (6000, 7, 32, 3, 2, False, 10),         # only a thin slice of 8 features, root
+    (9001, 40, 256, 4, 8, True, 11),        # two full slices and a thin slice of 8, odd channel count
+    (4000, 2, 256, 5, 1, False, 12),        # thin slice of 2 features (eight copies)
 ]
 
 
