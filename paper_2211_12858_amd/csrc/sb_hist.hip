@@ -993,23 +993,49 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
     const longlong2* src = reinterpret_cast<const longlong2*>(a.partial + ((int64_t)s * a.slots + p) * a.cells) + e64;
     const int64_t stride = a.cells / 2;  // one row group, in 16-byte cells
     int64_t q = qlo;
-    if (dense) {
-      for (; q + 4 <= qhi + 1; q += 4) {
-        longlong2 v[4][PMAX];
+    if (dense && q + 4 <= qhi + 1) {
+      // batches of four row groups, every channel pair, double-buffered: the
+      // next batch's loads are issued before this batch is added, so a node
+      // of many row groups waits for about one memory latency, not one per
+      // batch.  The loads are unconditional (pairs past the last repeat it
+      // and are dropped), so the compiler issues them all before any wait.
+      auto load4 = [&](int64_t q0, longlong2 (&v)[4][PMAX]) {
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
           for (int pr = 0; pr < PMAX; ++pr)
-            if (pr < a.pairs) v[u][pr] = src[(q + u) * stride + (int64_t)pr * FB];
+            v[u][pr] = src[(q0 + u) * stride + (int64_t)(pr < a.pairs ? pr : a.pairs - 1) * FB];
+      };
+      auto add4 = [&](const longlong2 (&v)[4][PMAX]) {
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int pr = 0; pr < PMAX; ++pr)
-            if (pr < a.pairs) {
-              acc_lo[pr] += v[u][pr].x;
-              acc_hi[pr] += v[u][pr].y;
-            }
+          for (int pr = 0; pr < PMAX; ++pr) {
+            acc_lo[pr] += pr < a.pairs ? v[u][pr].x : 0;
+            acc_hi[pr] += pr < a.pairs ? v[u][pr].y : 0;
+          }
+      };
+      longlong2 va[4][PMAX];
+      load4(q, va);
+      q += 4;
+      if constexpr (PMAX <= 4) {
+        longlong2 vb[4][PMAX];
+        for (; q + 4 <= qhi + 1; q += 4) {
+          load4(q, vb);
+          add4(va);
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int pr = 0; pr < PMAX; ++pr) va[u][pr] = vb[u][pr];
+        }
+      } else {
+        // wide channel counts: one buffer (registers)
+        for (; q + 4 <= qhi + 1; q += 4) {
+          add4(va);
+          load4(q, va);
+        }
       }
+      add4(va);
     }
     for (; q <= qhi; ++q) {
       if (dense || q * T / qn < (q + 1) * T / qn) {
@@ -1217,7 +1243,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     ScoreOut so{feat_s, feat_b, lam, mcw};
     const dim3 g(m, n_build);
     const size_t lds = (size_t)2 * pl.c * n_bins * 8;  // [node][channel][bin], built node and sibling
-    if (pl.pairs <= 4) hipLaunchKernelGGL((k_hist_reduce_score<4>), g, dim3(256), lds, st, a, so);
+    if (pl.pairs <= 3) hipLaunchKernelGGL((k_hist_reduce_score<3>), g, dim3(256), lds, st, a, so);
+    else if (pl.pairs <= 4) hipLaunchKernelGGL((k_hist_reduce_score<4>), g, dim3(256), lds, st, a, so);
     else if (pl.pairs <= 8) hipLaunchKernelGGL((k_hist_reduce_score<8>), g, dim3(256), lds, st, a, so);
     else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 16 channels");
   } else {
