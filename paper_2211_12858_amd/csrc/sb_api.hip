@@ -462,7 +462,10 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     return ((depth - l) % 2 == 0) ? row_idx_out : rows_tmp;
   };
 
-  hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), pre, (int32_t)n);
+  // the root's offsets and prefix {0, n}: written by the kernel that
+  // quantises the sketch rows when the rotated histogram kernel runs
+  const bool quant_root = hist_plan(m, n_bins, k, 1).rot;
+  if (!quant_root) hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), pre, (int32_t)n);
   for (int l = 0; l < depth; ++l) {
     const int32_t nn = 1 << l;
     double* Hcur = Hbuf[l & 1];
@@ -475,7 +478,8 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
                                    nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
-                                   min_child_weight, qrow, false, depth > 1);
+                                   min_child_weight, qrow, false, depth > 1,
+                                   quant_root ? const_cast<int32_t*>(off_l) : nullptr);
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
                                    level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],

@@ -40,7 +40,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int64_t* pre_given = nullptr, const double* H_parent = nullptr,
                                 double* feat_s = nullptr, int32_t* feat_b = nullptr, double lam = 0.0,
                                 double mcw = 0.0, uint32_t* qrow = nullptr, bool qrow_ready = false,
-                                bool store_h = true);
+                                bool store_h = true, int32_t* root_off = nullptr);
 // The fused level end (reduction, subtraction and per-feature scoring in one
 // kernel) stages both nodes' values of one feature in LDS: channels up to
 // this many (64 KB at 256 bins).

@@ -462,10 +462,18 @@ __device__ inline int32_t qfield(const uint32_t* q, int t) {
 // Quantised sketch rows for the rotated kernel: channel t of row i becomes
 // rint(GH[i, t] * 2^qexp[t]), the same fp32 operations that define the
 // histogram's fixed point, packed into the 21-bit fields of one 16-byte word.
+// With root_off given (a tree's first level), the first thread also writes
+// the root's node offsets {0, n} and built-size prefix {0, n}.
 template <int C>
 __global__ void __launch_bounds__(256)
 k_quant_rows(const float* __restrict__ GH, int64_t ld_gh, int64_t n, const int32_t* __restrict__ qexp,
-             uint32_t* __restrict__ qrow) {
+             uint32_t* __restrict__ qrow, int32_t* root_off, int64_t* root_pre) {
+  if (root_off && blockIdx.x == 0 && threadIdx.x == 0) {
+    root_off[0] = 0;
+    root_off[1] = (int32_t)n;
+    root_pre[0] = 0;
+    root_pre[1] = n;
+  }
   int qe[C];
 #pragma unroll
   for (int t = 0; t < C; ++t) qe[t] = __builtin_amdgcn_readfirstlane(qexp[t]);
@@ -1145,7 +1153,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 const int32_t* row_idx, const int32_t* node_off, int32_t n_nodes,
                                 const int32_t* build_list, int32_t n_build, double* H, void* ws, hipStream_t st,
                                 const int64_t* pre_given, const double* H_parent, double* feat_s, int32_t* feat_b,
-                                double lam, double mcw, uint32_t* qrow, bool qrow_ready, bool store_h) {
+                                double lam, double mcw, uint32_t* qrow, bool qrow_ready, bool store_h,
+                                int32_t* root_off) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build, row_idx == nullptr);
   HistArgs a{};
   a.bins4 = bins4;
@@ -1171,7 +1180,10 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     if (!qrow_ready) {
       const unsigned qb = (unsigned)((n + 255) / 256);
 #define SB_QUANT(C) \
-  if (pl.c == C) hipLaunchKernelGGL((k_quant_rows<C>), dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow); else
+  if (pl.c == C)                                                                                            \
+    hipLaunchKernelGGL((k_quant_rows<C>), dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off,  \
+                       const_cast<int64_t*>(pre_given));                                                    \
+  else
       SB_QUANT(1) SB_QUANT(2) SB_QUANT(3) SB_QUANT(4) SB_QUANT(5) SB_QUANT(6)
       return fail(SB_E_UNSUPPORTED, "sb_build_histograms: quantised rows hold at most 6 channels");
 #undef SB_QUANT

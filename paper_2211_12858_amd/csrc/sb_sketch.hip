@@ -24,7 +24,7 @@ constexpr int NORM_THREADS = 256;
 #define SB_NORM_CHUNK 16384
 #endif
 #ifndef SB_NORM_UNROLL
-#define SB_NORM_UNROLL 4
+#define SB_NORM_UNROLL 8
 #endif
 constexpr int64_t NORM_CHUNK = SB_NORM_CHUNK;  // rows per partial sum
 constexpr int NORM_UNROLL = SB_NORM_UNROLL;    // 16-byte loads in flight per thread
