@@ -100,7 +100,10 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   // quantised sketch rows of the rotated histogram kernel, written at the
   // root and read by every level
   L.qrow = p;
-  if (hist_plan(m, n_bins, k, 1).rot) p += align256(n * 16);
+  {
+    const HistPlan hp = hist_plan(m, n_bins, k, 1);
+    if (hp.rot) p += align256(n * 16 * hp.cg);
+  }
   L.call = p;
   p += call;
   L.total = p;

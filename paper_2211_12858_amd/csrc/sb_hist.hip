@@ -45,8 +45,9 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
   HistPlan p{};
   p.c = k + 1;
   p.pairs = (p.c + 1) / 2;
-  if (p.pairs <= ROT_PMAX && n_bins <= 256) {
+  if (p.c <= ROT_MAX_C && n_bins <= 256) {
     p.rot = true;
+    p.cg = (p.c + QROW_MAX_C - 1) / QROW_MAX_C;
     p.nq = ROT_F / 4;
     p.f = ROT_F;
     p.rows_wave = 64;
@@ -62,19 +63,20 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
     }
     p.slices = p.slices_full + (p.f_thin ? 1 : 0);
     const int S = p.slices_full, cus = HIST_CUS_PER_XCD;
+    const int uf = S * p.cg, ut = p.cg;  // workgroups per full / thin row group
     if (!p.f_thin) {
-      p.a_full = cus / S > 0 ? cus / S : 1;
+      p.a_full = cus / uf > 0 ? cus / uf : 1;
       p.b_thin = 0;
     } else if (S == 0) {
       p.a_full = 0;
-      p.b_thin = cus;
+      p.b_thin = cus / ut > 0 ? cus / ut : 1;
     } else {
       // per-workgroup work of a full slice is ROT_F rows-steps per row of its
       // group, of the thin slice f_thin: minimise the larger of the two
       int best_a = 1;
       double best = 1e30;
-      for (int aa = 1; aa * S < cus || aa == 1; ++aa) {
-        const int bb = cus - aa * S > 0 ? cus - aa * S : 1;
+      for (int aa = 1; aa * uf < cus || aa == 1; ++aa) {
+        const int bb = (cus - aa * uf) / ut > 0 ? (cus - aa * uf) / ut : 1;
         const double cost = fmax((double)ROT_F / aa, (double)p.f_thin / bb);
         if (cost < best) {
           best = cost;
@@ -82,13 +84,13 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
         }
       }
       p.a_full = best_a;
-      p.b_thin = cus - best_a * S > 0 ? cus - best_a * S : 1;
+      p.b_thin = (cus - best_a * uf) / ut > 0 ? (cus - best_a * uf) / ut : 1;
     }
     p.q = 8 * p.a_full;
     p.q_thin = 8 * p.b_thin;
     p.q_pad = p.q;
     p.slots = (int64_t)(p.q > p.q_thin ? p.q : p.q_thin) + n_build;
-    p.grid = 8 * (p.a_full * S + p.b_thin);
+    p.grid = 8 * (p.a_full * uf + p.b_thin * ut);
     return p;
   }
   const int64_t quad_bytes = 4ll * n_bins * p.pairs * 8;
@@ -113,6 +115,7 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
   p.slots = (int64_t)p.q + n_build;
   p.slices_full = p.slices;
   p.f_thin = p.b_thin = p.q_thin = 0;
+  p.cg = 1;
   p.a_full = per_xcd;
   p.grid = p.q_pad * p.slices;
   return p;
@@ -126,7 +129,7 @@ int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n
   const HistPlan pt = hist_plan(m, n_bins, k, n_build, true);  // rows read straight from the data
   int64_t part = (int64_t)p.slices * p.slots * p.cells;
   if ((int64_t)pt.slices * pt.slots * pt.cells > part) part = (int64_t)pt.slices * pt.slots * pt.cells;
-  const int64_t q = (p.rot && quant_rows) ? align256(n * 16) : 0;
+  const int64_t q = (p.rot && quant_rows) ? align256(n * 16 * p.cg) : 0;
   return align256((int64_t)(n_build + 1) * 8) + align256(part * 8) + q;
 }
 
@@ -140,7 +143,7 @@ struct HistArgs {
   const uint8_t* rec;
   int64_t ld_rec;
   const int32_t* qexp;
-  const uint32_t* qrow;  // rotated kernel: quantised sketch rows, 4 words per row
+  const uint32_t* qrow;  // rotated kernel: quantised sketch rows, 4 * cg words per row
   const int32_t* row_idx;
   const int32_t* node_off;
   const int32_t* build_list;
@@ -153,7 +156,7 @@ struct HistArgs {
   int32_t m, n_bins, c, pairs, n_nodes, n_build;
   int32_t nq, f, slices, rows_wave, cells, q, cpt, steps_per_window;
   int64_t slots;
-  int32_t slices_full, f_thin, a_full, b_thin, q_thin;  // rotated kernel plan (see HistPlan)
+  int32_t slices_full, f_thin, a_full, b_thin, q_thin, cg;  // rotated kernel plan (see HistPlan)
 };
 
 // Row groups of slice s (the thin slice has its own count).
@@ -421,14 +424,15 @@ typedef uint32_t u32x4_a16 __attribute__((ext_vector_type(4), aligned(16)));
 // below 2^31, so the row arithmetic is 32-bit with one 64-bit multiply-add
 // per record address.
 template <int FT, bool FROM_REC>
-__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, RowRot<FT>& d) {
+__device__ inline void load_row_rot(const HistArgs& a, RowRef ref, int f0, const uint32_t* qbase, uint32_t qstride,
+                                    RowRot<FT>& d) {
   constexpr int NW = RowRot<FT>::NW;
   const int32_t n1 = (int32_t)a.n - 1;
   int32_t row = ref.on ? ref.raw : 0;
   row = row < 0 ? 0 : (row > n1 ? n1 : row);
   const uint32_t ur = (uint32_t)row;
   {
-    const u32x4_a16 v = *reinterpret_cast<const u32x4_a16*>(a.qrow + (uint64_t)ur * 4u);
+    const u32x4_a16 v = *reinterpret_cast<const u32x4_a16*>(qbase + (uint64_t)ur * qstride);
     d.q[0] = v.x;
     d.q[1] = v.y;
     d.q[2] = v.z;
@@ -496,6 +500,59 @@ k_quant_rows(const float* __restrict__ GH, int64_t ld_gh, int64_t n, const int32
   *reinterpret_cast<u32x4_a16*>(qrow + i * 4) = o;
 }
 
+// The same for 6 < c <= 6 CG channels: CG words per row, word g holding
+// channels 6g .. 6g + 5 (zero past c).  The row's c values come in 16-byte
+// loads (dword-aligned), the last partial group of four as single loads.
+template <int CG>
+__global__ void __launch_bounds__(256)
+k_quant_rows_wide(const float* __restrict__ GH, int64_t ld_gh, int64_t n, int c, const int32_t* __restrict__ qexp,
+                  uint32_t* __restrict__ qrow, int32_t* root_off, int64_t* root_pre) {
+  constexpr int CM = QROW_MAX_C * CG;
+  if (root_off && blockIdx.x == 0 && threadIdx.x == 0) {
+    root_off[0] = 0;
+    root_off[1] = (int32_t)n;
+    root_pre[0] = 0;
+    root_pre[1] = n;
+  }
+  int qe[CM];
+#pragma unroll
+  for (int t = 0; t < CM; ++t) qe[t] = t < c ? __builtin_amdgcn_readfirstlane(qexp[t]) : 0;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(GH + i * ld_gh);
+  uint32_t w[CM];
+#pragma unroll
+  for (int j = 0; j < CM; j += 4) {
+    if (j + 3 < c) {
+      const u32x4_a4 v = *reinterpret_cast<const u32x4_a4*>(p + j);
+      w[j] = v.x;
+      w[j + 1] = v.y;
+      w[j + 2] = v.z;
+      w[j + 3] = v.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[j + e] = j + e < c ? p[j + e] : 0u;
+    }
+  }
+  constexpr uint64_t M = (uint64_t(1) << QFIELD_BITS) - 1;
+#pragma unroll
+  for (int g = 0; g < CG; ++g) {
+    uint64_t half[2] = {0, 0};
+#pragma unroll
+    for (int jj = 0; jj < QROW_MAX_C; ++jj) {
+      const int t = QROW_MAX_C * g + jj;
+      const int32_t v = t < c ? (int32_t)rintf(ldexpf(__uint_as_float(w[t]), qe[t])) : 0;
+      half[jj / 3] |= ((uint64_t)(uint32_t)v & M) << (QFIELD_BITS * (jj % 3));
+    }
+    u32x4_a16 o;
+    o.x = (uint32_t)half[0];
+    o.y = (uint32_t)(half[0] >> 32);
+    o.z = (uint32_t)half[1];
+    o.w = (uint32_t)(half[1] >> 32);
+    *reinterpret_cast<u32x4_a16*>(qrow + (i * CG + g) * 4) = o;
+  }
+}
+
 typedef __attribute__((address_space(3))) unsigned long long lds_u64;
 
 // Cell (bin, pair, slot) of a rotated slice is the 64-bit LDS word
@@ -561,7 +618,10 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot<FT>& d, uint32_t r
 template <int C, int FT, bool HAS_IDX>
 __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, uint32_t v,
                                        uint32_t vend, uint32_t pstart, uint32_t seg0, int wave, int lane, int f0,
-                                       uint32_t B) {
+                                       uint32_t B, int grp) {
+  // this workgroup's word of each quantised row (channel group grp)
+  const uint32_t* qbase = a.qrow + 4 * grp;
+  const uint32_t qstride = 4u * (uint32_t)a.cg;
   constexpr uint32_t rows_step = ROT_THREADS;
   const uint32_t last_pos = seg0 + (vend - 1 - pstart);
   const uint32_t lane_off = (uint32_t)(wave * 64 + lane);
@@ -580,11 +640,11 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
   RowRef r0 = row_at(v);
   RowRef r1 = row_at(v + rows_step);
   RowRot<FT> d0, d1;
-  load_row_rot<FT, HAS_IDX>(a, r0, f0, d0);
+  load_row_rot<FT, HAS_IDX>(a, r0, f0, qbase, qstride, d0);
   RowRef r2;
   if constexpr (DEEP) {
     r2 = row_at(v + 2 * rows_step);
-    load_row_rot<FT, HAS_IDX>(a, r1, f0, d1);
+    load_row_rot<FT, HAS_IDX>(a, r1, f0, qbase, qstride, d1);
   }
   int steps = 0;
 #pragma unroll 1
@@ -592,7 +652,7 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
     if constexpr (DEEP) {
       const RowRef r3 = row_at(vs + 3 * rows_step);
       RowRot<FT> d2;
-      load_row_rot<FT, HAS_IDX>(a, r2, f0, d2);
+      load_row_rot<FT, HAS_IDX>(a, r2, f0, qbase, qstride, d2);
       if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
       r0 = r1;
       d0 = d1;
@@ -601,7 +661,7 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
       r2 = r3;
     } else {
       const RowRef r2n = row_at(vs + 2 * rows_step);
-      load_row_rot<FT, HAS_IDX>(a, r1, f0, d1);
+      load_row_rot<FT, HAS_IDX>(a, r1, f0, qbase, qstride, d1);
       if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
       r0 = r1;
       d0 = d1;
@@ -775,7 +835,7 @@ k_hist(HistArgs a) {
 // Slice s of FT features (16, or a thin slice's f_thin), row group q of
 // qn: the rows of virtual positions [q T / qn, (q+1) T / qn).
 template <int C, int FT>
-__device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds64, int s, int q, int qn) {
+__device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds64, int s, int grp, int q, int qn) {
   constexpr int P = (C + 1) / 2;
   constexpr int R = ROT_F / FT;  // copies of each cell in the slice
   const int64_t T = a.pre[a.n_build];
@@ -813,18 +873,20 @@ __device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds6
     lds_u64* L = (lds_u64*)lds64;  // generic to LDS address space: 32-bit offsets
     if (a.row_idx)
       run_segment_rot<C, FT, true>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0, wave,
-                                   lane, f0, (uint32_t)B);
+                                   lane, f0, (uint32_t)B, grp);
     else
       run_segment_rot<C, FT, false>(a, L, tot, (uint32_t)v, (uint32_t)vend, (uint32_t)pstart, (uint32_t)seg0,
-                                    wave, lane, f0, (uint32_t)B);
+                                    wave, lane, f0, (uint32_t)B, grp);
     // The node-end barriers wait for LDS operations only: the partial stores
     // take their data from registers, so nothing here waits for them.
     lds_barrier();
     fold_cells<ROT_CPT, ROT_THREADS>(lds64, tot);
     lds_barrier();  // every fold read is done: the LDS becomes the staging area
     longlong2* dst = reinterpret_cast<longlong2*>(a.partial + ((int64_t)s * a.slots + q + p) * a.cells);
+    // this channel group's pairs are pairs 3 grp .. 3 grp + P - 1 of the
+    // slot; pairs past the last (a short final group) are not written
 #pragma unroll 1
-    for (int pr = 0; pr < P; ++pr) {
+    for (int pr = 0; pr < P && ROT_PMAX * grp + pr < a.pairs; ++pr) {
 #pragma unroll
       for (int i = 0; i < ROT_CPT; ++i) {
         const int j64 = tid + ROT_THREADS * i;
@@ -842,7 +904,7 @@ __device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds6
           x.x += y.x;
           x.y += y.y;
         }
-        dst[(int64_t)pr * ROT_F * B + e] = x;
+        dst[(int64_t)(ROT_PMAX * grp + pr) * ROT_F * B + e] = x;
       }
       lds_barrier();
     }
@@ -874,20 +936,23 @@ k_hist_rot(HistArgs a) {
   extern __shared__ uint64_t lds64[];
   const int b = blockIdx.x;
   const int xcd = b & 7, g = b >> 3;
-  const int nfull = a.a_full * a.slices_full;
+  const int uf = a.slices_full * a.cg;  // workgroups per full row group: (slice, channel group)
+  const int nfull = a.a_full * uf;
   if (g < nfull) {
-    const int q = (g / a.slices_full) * 8 + xcd;
-    if (q < a.q) hist_rot_group<C, ROT_F>(a, lds64, g % a.slices_full, q, a.q);
+    const int q = (g / uf) * 8 + xcd;
+    const int u = g % uf;
+    if (q < a.q) hist_rot_group<C, ROT_F>(a, lds64, u / a.cg, u % a.cg, q, a.q);
     return;
   }
-  const int q = (g - nfull) * 8 + xcd;
+  const int t = g - nfull;
+  const int q = (t / a.cg) * 8 + xcd, grp = t % a.cg;
   if (!a.f_thin || q >= a.q_thin) return;
   const int s = a.slices_full;
   switch (a.f_thin) {
-    case 1: hist_rot_group<C, 1>(a, lds64, s, q, a.q_thin); break;
-    case 2: hist_rot_group<C, 2>(a, lds64, s, q, a.q_thin); break;
-    case 4: hist_rot_group<C, 4>(a, lds64, s, q, a.q_thin); break;
-    default: hist_rot_group<C, 8>(a, lds64, s, q, a.q_thin); break;
+    case 1: hist_rot_group<C, 1>(a, lds64, s, grp, q, a.q_thin); break;
+    case 2: hist_rot_group<C, 2>(a, lds64, s, grp, q, a.q_thin); break;
+    case 4: hist_rot_group<C, 4>(a, lds64, s, grp, q, a.q_thin); break;
+    default: hist_rot_group<C, 8>(a, lds64, s, grp, q, a.q_thin); break;
   }
 }
 
@@ -1174,8 +1239,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     // the quantised rows live in the caller's buffer (kept across a tree's
     // levels) or else at the end of this call's workspace
     if (!qrow)
-      qrow = reinterpret_cast<uint32_t*>(w + align256((int64_t)(n_build + 1) * 8) +
-                                         align256((int64_t)pl.slices * pl.slots * pl.cells * 8));
+      qrow = reinterpret_cast<uint32_t*>(w + hist_ws_bytes(n, m, n_bins, k, n_build, false));
     a.qrow = qrow;
     if (!qrow_ready) {
       const unsigned qb = (unsigned)((n + 255) / 256);
@@ -1185,7 +1249,15 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                        const_cast<int64_t*>(pre_given));                                                    \
   else
       SB_QUANT(1) SB_QUANT(2) SB_QUANT(3) SB_QUANT(4) SB_QUANT(5) SB_QUANT(6)
-      return fail(SB_E_UNSUPPORTED, "sb_build_histograms: quantised rows hold at most 6 channels");
+      if (pl.cg == 2)
+        hipLaunchKernelGGL(k_quant_rows_wide<2>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
+                           const_cast<int64_t*>(pre_given));
+      else if (pl.cg == 3)
+        hipLaunchKernelGGL(k_quant_rows_wide<3>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
+                           const_cast<int64_t*>(pre_given));
+      else
+        hipLaunchKernelGGL(k_quant_rows_wide<4>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
+                           const_cast<int64_t*>(pre_given));
 #undef SB_QUANT
     }
   }
@@ -1210,6 +1282,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.a_full = pl.a_full;
   a.b_thin = pl.b_thin;
   a.q_thin = pl.q_thin;
+  a.cg = pl.cg;
   a.cpt = (pl.cells + HIST_THREADS - 1) / HIST_THREADS;
   const int rows_step = pl.rot ? ROT_THREADS : HIST_THREADS;
   a.steps_per_window = WINDOW_ROWS / rows_step > 0 ? WINDOW_ROWS / rows_step : 1;
@@ -1239,6 +1312,10 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     hipLaunchKernelGGL((k_hist_rot<C>), dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a);         \
   } else
   SB_HIST_ROT(1) SB_HIST_ROT(2) SB_HIST_ROT(3) SB_HIST_ROT(4) SB_HIST_ROT(5) SB_HIST_ROT(6)
+  if (pl.rot && pl.c > QROW_MAX_C) {
+    // channel groups of six (three pairs) each
+    hipLaunchKernelGGL((k_hist_rot<QROW_MAX_C>), dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a);
+  } else
   SB_HIST_EXACT(11, 2) SB_HIST_EXACT(21, 1)
   SB_HIST_CASE(8, 4) SB_HIST_CASE(8, 8) SB_HIST_CASE(8, 16)
   SB_HIST_CASE(16, 4) SB_HIST_CASE(16, 8) SB_HIST_CASE(16, 16)

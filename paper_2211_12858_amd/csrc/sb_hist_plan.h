@@ -23,6 +23,9 @@ static_assert(2ll * WINDOW_ROWS * (1ll << QBITS) < (1ll << 31), "fixed-point win
 // bits), written once per sketch, so that a row's values are one 16-byte load.
 constexpr int QFIELD_BITS = 21;
 constexpr int QROW_MAX_C = 6;
+// More channels take several such words per row, one per channel group of
+// six; each group gets workgroups of its own (up to ROT_MAX_C channels).
+constexpr int ROT_MAX_C = 24;
 static_assert(QBITS + 2 <= QFIELD_BITS, "a quantised value of magnitude <= 2^QBITS and its sign must fit a field");
 
 // ---------------------------------------------------------------- histogram plan
@@ -77,6 +80,10 @@ struct HistPlan {
   // indices are cheaper to read when the slices of a row group share an XCD,
   // so there the last slice is a padded slice of 16 like the others.
   int slices_full, f_thin, a_full, b_thin, q_thin;
+  // Rotated kernel with c > 6 channels: cg = ceil(c / 6) channel groups of
+  // at most three pairs; every (slice, channel group) of a row group is one
+  // workgroup, and all groups of a slice write the same partial slots.
+  int cg;
   int grid;       // histogram workgroups
 };
 HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool thin_ok = false);
