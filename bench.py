@@ -188,14 +188,14 @@ def hist_source_hash():
     return h.hexdigest()
 
 
-def traffic_for_current_kernel():
-    """Counter-measured HBM bytes per histogram launch, if taken on this kernel source."""
+def traffic_for_current_kernel(wl_name):
+    """Counter-measured HBM bytes per histogram launch, if taken on this kernel source and workload."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
         rec = json.load(open(TRAFFIC_FILE))
         src = hist_source_hash()
-        if rec.get("kernel_source_sha256") != src:
+        if rec.get("kernel_source_sha256") != src or rec.get("workload") != wl_name:
             return None
         return rec.get("bytes_per_launch")
     except (OSError, ValueError):
@@ -316,10 +316,10 @@ def main():
     bytes_per_launch = float(np.mean(alg))
     adds_per_launch = float(np.mean(rows_built)) * wl.m * (wl.k + 1)
     lds_gadds = adds_per_launch / (hist_ms / launches * 1e-3) / 1e9
-    hist_kernel = "k_hist_rot" if wl.k + 1 <= 6 else "k_hist"
+    hist_kernel = "k_hist_rot" if wl.k + 1 <= 24 else "k_hist"
     ms_per_launch = hist_ms / launches
     achieved = bytes_per_launch / (ms_per_launch * 1e-3) / 1e9
-    traffic = traffic_for_current_kernel()
+    traffic = traffic_for_current_kernel(wl.name)
 
     # leaf values of the last tree from the full G (eq. 3), timed on their own
     for _ in range(2):
