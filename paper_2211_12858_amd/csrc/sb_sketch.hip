@@ -109,6 +109,8 @@ k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __res
 }
 
 // One block.
+constexpr int SELECT_LDS_D = 4096;  // Random Sampling prefix sums held in LDS up to this d
+
 __global__ void __launch_bounds__(1024)
 k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __restrict__ u,
          int32_t* __restrict__ cols, float* __restrict__ scales, double* __restrict__ C) {
@@ -132,14 +134,25 @@ k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __
       }
     }
   } else if (kind == SB_SKETCH_RANDOM_SAMPLING) {
+    // the prefix sums are formed sequentially (the order the draws are
+    // defined with); up to SELECT_LDS_D norms they live in LDS, so the
+    // sum and the searches wait on LDS instead of global memory
+    __shared__ double sC[SELECT_LDS_D];
+    const bool in_lds = d <= SELECT_LDS_D;
+    double* Cw = in_lds ? sC : C;
+    if (in_lds) {
+      for (int j = threadIdx.x; j < d; j += blockDim.x) sC[j] = n2[j];
+      __syncthreads();
+    }
     if (threadIdx.x == 0) {
       double acc = 0.0;
       for (int j = 0; j < d; ++j) {
-        acc = acc + n2[j];
-        C[j] = acc;
+        acc = acc + (in_lds ? sC[j] : n2[j]);
+        Cw[j] = acc;
       }
     }
     __syncthreads();
+    C = Cw;
     const double total = C[d - 1];
     for (int t = threadIdx.x; t < k; t += blockDim.x) {
       if (!(total > 0.0)) {
