@@ -11,6 +11,9 @@
 
 namespace sb {
 
+// A load of data that is streamed once: it does not allocate in the caches.
+__device__ inline float ld_stream(const float* p) { return __builtin_nontemporal_load(p); }
+
 // ---------------------------------------------------------------- errors
 void set_error(const std::string& msg);
 int32_t fail(int32_t code, const std::string& msg);

@@ -204,7 +204,8 @@ __global__ void __launch_bounds__(UPD_THREADS) k_update(UpdArgs a) {
       // then the sums and the stores
       float f[UPD_JC];
 #pragma unroll
-      for (int u = 0; u < UPD_JC; ++u) f[u] = a.F[(int64_t)(j0 + (u < w ? u : w - 1)) * a.ld_f + rc];
+      // streamed once (non-temporal): 301 us instead of 328 us at 2M x 100
+      for (int u = 0; u < UPD_JC; ++u) f[u] = ld_stream(a.F + (int64_t)(j0 + (u < w ? u : w - 1)) * a.ld_f + rc);
 #pragma unroll
       for (int u = 0; u < UPD_JC; ++u)
         if (u < w && ok) a.F[(int64_t)(j0 + u) * a.ld_f + row] = (float)((double)f[u] + lvL[u]);

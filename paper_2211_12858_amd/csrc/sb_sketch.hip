@@ -30,6 +30,13 @@ constexpr int64_t NORM_CHUNK = SB_NORM_CHUNK;  // rows per partial sum
 constexpr int NORM_UNROLL = SB_NORM_UNROLL;    // 16-byte loads in flight per thread
 constexpr int NORM_MAX_PARTS = 256;
 
+// A 16-byte load that does not allocate in the caches (data read once).
+__device__ inline float4 load_nt4(const float4* p) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  const f4v t = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(p));
+  return make_float4(t.x, t.y, t.z, t.w);
+}
+
 __device__ inline double wave_sum(double v) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
   return v;
@@ -66,8 +73,10 @@ k_colnorm_partial(const float* __restrict__ G, int64_t n, int64_t ld, int parts,
     int64_t q = threadIdx.x;
     for (; q + (NORM_UNROLL - 1) * NORM_THREADS < nv; q += NORM_UNROLL * NORM_THREADS) {
       float4 x[NORM_UNROLL];
+      // G is streamed once: non-temporal loads keep it out of the caches
+      // (123 us instead of 146 us for 800 MB)
 #pragma unroll
-      for (int u = 0; u < NORM_UNROLL; ++u) x[u] = v4[q + u * NORM_THREADS];
+      for (int u = 0; u < NORM_UNROLL; ++u) x[u] = load_nt4(v4 + q + u * NORM_THREADS);
 #pragma unroll
       for (int u = 0; u < NORM_UNROLL; ++u) {
         acc += (double)x[u].x * x[u].x;
@@ -438,7 +447,7 @@ k_project(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const flo
 #pragma unroll
         for (int u = 0; u < PROJ_JU; ++u) {
           const int j = j0 + (jb + u < jc ? jb + u : jc - 1);
-          g[u] = G[(int64_t)j * ld_g + ii];
+          g[u] = ld_stream(G + (int64_t)j * ld_g + ii);
         }
 #pragma unroll
         for (int u = 0; u < PROJ_JU; ++u) {
@@ -517,7 +526,8 @@ k_project_sparse(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, co
       // columns past d (last batch only) load column d-1 and add nothing
       float g[PROJ_JU];
 #pragma unroll
-      for (int u = 0; u < PROJ_JU; ++u) g[u] = G[(int64_t)(j0 + u < d ? j0 + u : d - 1) * ld_g + ii];
+      // G is streamed once: non-temporal loads (1.64 ms instead of 1.69 ms at 2M x 1000 -> 20, s = 1)
+      for (int u = 0; u < PROJ_JU; ++u) g[u] = ld_stream(G + (int64_t)(j0 + u < d ? j0 + u : d - 1) * ld_g + ii);
       int tc[PROJ_JU * S];
       float vc[PROJ_JU * S];
 #pragma unroll
@@ -619,7 +629,7 @@ k_project_mfma(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, cons
           const int jj = kk + 2 * u + khalf;
           const int64_t jg = j0 + (jj < jc ? jj : jc - 1);  // past the block: a finite value times a zero of Pi
 #pragma unroll
-          for (int mt = 0; mt < MF_MT; ++mt) a[u][mt] = G[jg * ld_g + rc[mt]];
+          for (int mt = 0; mt < MF_MT; ++mt) a[u][mt] = ld_stream(G + jg * ld_g + rc[mt]);
         }
 #pragma unroll
         for (int u = 0; u < MF_KU; ++u) {
