@@ -1110,6 +1110,27 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
       }
       add4(va);
     }
+    if (dense && q <= qhi) {
+      // the last one to three groups (all of them for a node of few groups,
+      // as at the deeper levels): one batch of unconditional loads, clamped
+      // to the node's last group and dropped past it, so they are all in
+      // flight together instead of one group per memory latency
+      longlong2 vt[4][PMAX];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int pr = 0; pr < PMAX; ++pr)
+          vt[u][pr] = src[(q + u <= qhi ? q + u : qhi) * stride + (int64_t)(pr < a.pairs ? pr : a.pairs - 1) * FB];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int pr = 0; pr < PMAX; ++pr) {
+          const bool take = q + u <= qhi && pr < a.pairs;
+          acc_lo[pr] += take ? vt[u][pr].x : 0;
+          acc_hi[pr] += take ? vt[u][pr].y : 0;
+        }
+      q = qhi + 1;
+    }
     for (; q <= qhi; ++q) {
       if (dense || q * T / qn < (q + 1) * T / qn) {
 #pragma unroll
