@@ -57,15 +57,44 @@ __device__ inline int64_t off_at(const PartArgs& a, int j) {
   return v < 0 ? 0 : (v > a.n ? a.n : v);
 }
 
+// Node table of a flags or scatter block.  With SN the level's node offsets
+// (clamped to [0, n]) and per-node values are staged in LDS once per block,
+// so the node search and the per-node reads are LDS reads rather than
+// chains of dependent global loads; levels of more than PT_LDS_NODES nodes
+// read them from global memory.
+constexpr int PT_LDS_NODES = 2048;
+template <bool SN>
+struct NodeTab {
+  const int32_t* off;
+  int64_t n;
+  __device__ int64_t at(int j) const {
+    if constexpr (SN) return off[j];
+    const int64_t v = off[j];
+    return v < 0 ? 0 : (v > n ? n : v);
+  }
+};
+
 // node owning position i: largest j in [0, n_nodes) with off[j] <= i
-__device__ inline int find_node(const PartArgs& a, int64_t i) {
-  int lo = 0, hi = a.n_nodes;  // search over off[0..n_nodes]
+template <bool SN>
+__device__ inline int find_node(const NodeTab<SN>& t, int n_nodes, int64_t i) {
+  int lo = 0, hi = n_nodes;  // search over off[0..n_nodes]
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
-    if (off_at(a, mid) <= i) lo = mid;
+    if (t.at(mid) <= i) lo = mid;
     else hi = mid;
   }
   return lo;
+}
+
+// Stage off[0..n_nodes] (clamped) into so; returns the table to search.
+template <bool SN>
+__device__ inline NodeTab<SN> stage_offsets(const PartArgs& a, int32_t* so) {
+  NodeTab<SN> t{a.off_in, a.n};
+  if constexpr (SN) {
+    for (int j = threadIdx.x; j <= a.n_nodes; j += PT_THREADS) so[j] = (int32_t)off_at(a, j);
+    t.off = so;
+  }
+  return t;
 }
 
 __device__ inline int32_t popc64(uint64_t x) { return __popcll(x); }
@@ -73,12 +102,13 @@ __device__ inline int32_t popc64(uint64_t x) { return __popcll(x); }
 // Each thread handles the positions t0 + tid + 256*it, it < 16.  The row
 // indices of all 16 positions are loaded first, then their bins, so each
 // thread keeps 16 independent loads in flight instead of a chain of 16
-// dependent pairs.  Node offsets and splits come from LDS.
+// dependent pairs.  Node offsets and splits come from the block's node table.
+template <bool SN>
 __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   __shared__ int32_t wsum[PT_THREADS / 64];
+  extern __shared__ int32_t pt_nodes[];  // SN: [off: n_nodes + 1][f: n_nodes][b: n_nodes]
   const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
   int64_t row[PT_ITERS];
 #pragma unroll
   for (int it = 0; it < PT_ITERS; ++it) {
@@ -86,21 +116,36 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
     const int64_t ic = i < a.n ? i : a.n - 1;
     row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
   }
+  const NodeTab<SN> tab = stage_offsets<SN>(a, pt_nodes);
+  const int32_t* bf = a.best_f;
+  const int32_t* bb = a.best_b;
+  if constexpr (SN) {
+    int32_t* sf = pt_nodes + a.n_nodes + 1;
+    int32_t* sb = sf + a.n_nodes;
+    for (int j = threadIdx.x; j < a.n_nodes; j += PT_THREADS) {
+      sf[j] = a.best_f[j];
+      sb[j] = a.best_b[j];
+    }
+    __syncthreads();
+    bf = sf;
+    bb = sb;
+  }
+  const int64_t first = tab.at(0), last = tab.at(a.n_nodes);
   // node of each position (positions grow with it) and its split
   int32_t f_of[PT_ITERS], b_of[PT_ITERS];
-  int j = find_node(a, t0 + threadIdx.x);
-  int64_t jend = off_at(a, j + 1);
+  int j = find_node<SN>(tab, a.n_nodes, t0 + threadIdx.x);
+  int64_t jend = tab.at(j + 1);
 #pragma unroll
   for (int it = 0; it < PT_ITERS; ++it) {
     const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
     while (i >= jend && j < a.n_nodes - 1) {
       ++j;
-      jend = off_at(a, j + 1);
+      jend = tab.at(j + 1);
     }
-    const int32_t f = a.best_f[j];
+    const int32_t f = bf[j];
     const bool live = i < a.n && i >= first && i < last;
     f_of[it] = (!live) ? -2 : ((f < 0 || f >= a.m) ? -1 : f);
-    b_of[it] = a.best_b[j];
+    b_of[it] = bb[j];
   }
   uint32_t bin[PT_ITERS];
 #pragma unroll
@@ -222,9 +267,11 @@ __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
   }
 }
 
+template <bool SN>
 __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
   __shared__ uint64_t mk[PT_MASKS];
   __shared__ int32_t pre[PT_MASKS];
+  extern __shared__ int32_t pt_nodes[];  // SN: [off: n_nodes + 1][Lb: n_nodes + 1]
   const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   int64_t row[PT_ITERS];
@@ -248,22 +295,29 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
       pre[lane] = a.tile_off[blockIdx.x] + incl - c;
     }
   }
+  const NodeTab<SN> tab = stage_offsets<SN>(a, pt_nodes);
+  const int32_t* lb = a.Lb;
+  if constexpr (SN) {
+    int32_t* sl = pt_nodes + a.n_nodes + 1;
+    for (int q = threadIdx.x; q <= a.n_nodes; q += PT_THREADS) sl[q] = a.Lb[q];
+    lb = sl;
+  }
   __syncthreads();
-  const int64_t first = off_at(a, 0), last = off_at(a, a.n_nodes);
+  const int64_t first = tab.at(0), last = tab.at(a.n_nodes);
   const uint64_t below = (uint64_t(1) << lane) - 1;
   int64_t i = t0 + threadIdx.x;
-  int j = find_node(a, i);
-  int64_t jstart = off_at(a, j), jend = off_at(a, j + 1);
-  int64_t lbj = a.Lb[j], nleft = (int64_t)a.Lb[j + 1] - lbj;
+  int j = find_node<SN>(tab, a.n_nodes, i);
+  int64_t jstart = tab.at(j), jend = tab.at(j + 1);
+  int64_t lbj = lb[j], nleft = (int64_t)lb[j + 1] - lbj;
 #pragma unroll
   for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
         ++j;
         jstart = jend;
-        jend = off_at(a, j + 1);
-        lbj = a.Lb[j];
-        nleft = (int64_t)a.Lb[j + 1] - lbj;
+        jend = tab.at(j + 1);
+        lbj = lb[j];
+        nleft = (int64_t)lb[j + 1] - lbj;
       }
       const int q = it * (PT_THREADS / 64) + wave;
       const uint64_t m = mk[q];
@@ -314,9 +368,16 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.m = m;
   a.n_nodes = n_nodes;
   a.n_tiles = (int32_t)tiles;
-  hipLaunchKernelGGL(k_part_flags, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
-  hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
-  hipLaunchKernelGGL(k_part_scatter, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
+  if (n_nodes <= PT_LDS_NODES) {
+    const size_t lf = (size_t)(3 * n_nodes + 1) * 4, ls = (size_t)(2 * n_nodes + 2) * 4;
+    hipLaunchKernelGGL(k_part_flags<true>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);
+    hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(k_part_scatter<true>, dim3((unsigned)tiles), dim3(PT_THREADS), ls, st, a);
+  } else {
+    hipLaunchKernelGGL(k_part_flags<false>, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
+    hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(k_part_scatter<false>, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
+  }
   return check_launch("sb_partition_rows");
 }
 
