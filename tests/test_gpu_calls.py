@@ -256,8 +256,10 @@ def test_score_ties_and_min_child_weight():
 
 
 # ---------------------------------------------------------------- partition
+# 2048 nodes: the largest level whose node table the flags and scatter blocks
+# stage in LDS; 3000: the same kernels reading it from global memory
 @pytest.mark.parametrize("n,m,n_nodes,seed", [(1, 1, 1, 0), (4095, 3, 1, 1), (4097, 5, 2, 2), (100003, 20, 16, 3),
-                                               (50000, 7, 64, 4)])
+                                               (50000, 7, 64, 4), (60000, 4, 2048, 5), (70001, 6, 3000, 6)])
 def test_partition_bit_exact(n, m, n_nodes, seed):
     rng = np.random.default_rng(seed)
     bins = rng.integers(0, 256, (n, m), dtype=np.uint8)
