@@ -208,21 +208,41 @@ __device__ int64_t block_excl_scan(int N, V v, O out, int64_t* sh) {
   return total;
 }
 
-// Left rows of node j, clamped to its size.
-__device__ inline int64_t node_left(const PartArgs& a, int j, int64_t* size_out) {
-  const int64_t o0 = off_at(a, j), o1 = off_at(a, j + 1);
+// Left rows of a node from its offsets and left-count bases, clamped to its size.
+__device__ inline int64_t node_left(int64_t o0, int64_t o1, int64_t lb0, int64_t lb1, int64_t* size_out) {
   const int64_t size = o1 > o0 ? o1 - o0 : 0;
-  int64_t nl = (int64_t)a.Lb[j + 1] - a.Lb[j];
+  const int64_t nl = lb1 - lb0;
   *size_out = size;
   return nl < 0 ? 0 : (nl > size ? size : nl);
 }
 
+// With SN the node offsets, the tile offsets and the left-count bases are
+// also kept in LDS, so that the block's later steps read them there instead
+// of going back to global memory (one memory latency each).
+constexpr int PB_LDS_TILES = 8192;
+template <bool SN>
 __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
   __shared__ int64_t sh[16];
+  __shared__ int32_t s_off[SN ? PT_LDS_NODES + 1 : 1], s_lb[SN ? PT_LDS_NODES + 1 : 1];
+  __shared__ int32_t s_toff[SN ? PB_LDS_TILES : 1];
+  if constexpr (SN)
+    for (int j = threadIdx.x; j <= a.n_nodes; j += 1024) s_off[j] = (int32_t)off_at(a, j);
+  auto off = [&](int j) -> int64_t {
+    if constexpr (SN) return s_off[j];
+    else return off_at(a, j);
+  };
+  auto lb = [&](int j) -> int64_t {
+    if constexpr (SN) return s_lb[j];
+    else return a.Lb[j];
+  };
   // 1. tile offsets
   const int64_t total = block_excl_scan(
       a.n_tiles, [&](int t) -> int64_t { return a.tile_cnt[t]; },
-      [&](int t, int64_t pre) { a.tile_off[t] = (int32_t)pre; }, sh);
+      [&](int t, int64_t pre) {
+        a.tile_off[t] = (int32_t)pre;
+        if constexpr (SN) s_toff[t] = (int32_t)pre;
+      },
+      sh);
   if (threadIdx.x == 0) a.tile_off[a.n_tiles] = (int32_t)total;
   __syncthreads();
   // 2. Lb_j = left rows before each node boundary: one wave per boundary,
@@ -230,7 +250,7 @@ __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
   {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int j = wave; j <= a.n_nodes; j += 16) {
-      const int64_t x = off_at(a, j);
+      const int64_t x = off(j);
       const int64_t t = x / PT_TILE;
       int64_t c = 0;
       if (t < a.n_tiles) {
@@ -239,27 +259,34 @@ __global__ void __launch_bounds__(1024) k_part_bounds(PartArgs a) {
         if (lane < (w >> 6)) c = popc64(mq);
         else if (lane == (w >> 6) && (w & 63)) c = popc64(mq & ((uint64_t(1) << (w & 63)) - 1));
       }
-      for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off, 64);
-      if (lane == 0) a.Lb[j] = (int32_t)(t < a.n_tiles ? a.tile_off[t] + c : total);
+      for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+      if (lane == 0) {
+        int64_t toff;
+        if constexpr (SN) toff = t < a.n_tiles ? s_toff[t] : 0;
+        else toff = t < a.n_tiles ? a.tile_off[t] : 0;
+        const int32_t v = (int32_t)(t < a.n_tiles ? toff + c : total);
+        a.Lb[j] = v;
+        if constexpr (SN) s_lb[j] = v;
+      }
     }
   }
   __syncthreads();
   // 3. children and build list
   for (int j = threadIdx.x; j < a.n_nodes; j += 1024) {
     int64_t size;
-    const int64_t nl = node_left(a, j, &size);
-    const int64_t o0 = off_at(a, j);
+    const int64_t o0 = off(j);
+    const int64_t nl = node_left(o0, off(j + 1), lb(j), lb(j + 1), &size);
     a.off_out[2 * j] = (int32_t)o0;
     a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
     a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
   }
-  if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off_at(a, a.n_nodes);
+  if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = (int32_t)off(a.n_nodes);
   if (a.next_pre) {
     const int64_t total_built = block_excl_scan(
         a.n_nodes,
         [&](int j) -> int64_t {
           int64_t size;
-          const int64_t nl = node_left(a, j, &size);
+          const int64_t nl = node_left(off(j), off(j + 1), lb(j), lb(j + 1), &size);
           return nl <= size - nl ? nl : size - nl;
         },
         [&](int j, int64_t pre) { a.next_pre[j] = pre; }, sh);
@@ -371,11 +398,12 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   if (n_nodes <= PT_LDS_NODES) {
     const size_t lf = (size_t)(3 * n_nodes + 1) * 4, ls = (size_t)(2 * n_nodes + 2) * 4;
     hipLaunchKernelGGL(k_part_flags<true>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);
-    hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
+    if (tiles <= PB_LDS_TILES) hipLaunchKernelGGL(k_part_bounds<true>, dim3(1), dim3(1024), 0, st, a);
+    else hipLaunchKernelGGL(k_part_bounds<false>, dim3(1), dim3(1024), 0, st, a);
     hipLaunchKernelGGL(k_part_scatter<true>, dim3((unsigned)tiles), dim3(PT_THREADS), ls, st, a);
   } else {
     hipLaunchKernelGGL(k_part_flags<false>, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
-    hipLaunchKernelGGL(k_part_bounds, dim3(1), dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(k_part_bounds<false>, dim3(1), dim3(1024), 0, st, a);
     hipLaunchKernelGGL(k_part_scatter<false>, dim3((unsigned)tiles), dim3(PT_THREADS), 0, st, a);
   }
   return check_launch("sb_partition_rows");
