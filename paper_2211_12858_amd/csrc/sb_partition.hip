@@ -19,6 +19,10 @@
 //   k_part_scatter : per tile, L[i] from the tile offset and the ballots,
 //                    then the scatter of the row indices.
 // No counter is shared between workgroups, so nothing serialises on atomics.
+// For levels of up to PT_LDS_NODES nodes, every block first copies the
+// level's node table (offsets, splits, left-count bases) into LDS, so that
+// finding a position's node is a search in LDS rather than a chain of
+// dependent global loads.
 #include "sb_common.h"
 
 namespace sb {
