@@ -27,10 +27,11 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBPS = 8000.0
-# LDS scatter-add roof of the histogram kernel: conflict-free 64-bit LDS adds
-# of two channels each retire 17.8 channel-adds per clock per CU on MI355X
-# (paper_2211_12858_amd/microbench/lds_scatter.hip, rotated mode); 256 CUs at 2.4 GHz.
-LDS_ADDS_PER_CLK_CU = 17.8
+# LDS roof of the histogram kernel: the LDS data path moves 128 bytes per
+# clock per CU; a 64-bit add carries two 32-bit channel sums, so the path
+# takes at most 128 / 4 = 32 channel-adds per clock per CU; 256 CUs at 2.4 GHz.
+LDS_BYTES_PER_CLK_CU = 128
+LDS_ADDS_PER_CLK_CU = LDS_BYTES_PER_CLK_CU // 4
 LDS_PEAK_GADDS = LDS_ADDS_PER_CLK_CU * 256 * 2.4
 METRIC = "sec per tree (depth 6) + histogram-build HBM GB/s (% of peak)"
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "hist_traffic.json")
@@ -316,7 +317,7 @@ def main():
     bytes_per_launch = float(np.mean(alg))
     adds_per_launch = float(np.mean(rows_built)) * wl.m * (wl.k + 1)
     lds_gadds = adds_per_launch / (hist_ms / launches * 1e-3) / 1e9
-    hist_kernel = "k_hist_rot" if wl.k + 1 <= 24 else "k_hist"
+    hist_kernel = "k_hist_rot"
     ms_per_launch = hist_ms / launches
     achieved = bytes_per_launch / (ms_per_launch * 1e-3) / 1e9
     traffic = traffic_for_current_kernel(wl.name)
@@ -372,7 +373,7 @@ def main():
         },
         # the roof that binds the histogram kernel: its useful channel-adds
         # (rows built x m features x c channels) per second against the LDS
-        # scatter-add rate measured for conflict-free 64-bit adds
+        # data path (128 bytes per clock per CU, 4 bytes per channel-add)
         "lds_roofline": {
             "achieved": lds_gadds,
             "peak": LDS_PEAK_GADDS,

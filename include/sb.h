@@ -36,7 +36,11 @@
  * - Calls on different streams may run concurrently if their workspaces and
  *   outputs do not overlap.  Only the error text is per-thread state.
  * - Sizes: n < 2^31 rows, m <= 65535 features, 2 <= n_bins <= 256,
- *   1 <= k <= 255 sketch columns (k+1 channels).
+ *   1 <= k <= 255 sketch columns (k+1 channels) for the sketch, scoring and
+ *   subtraction calls.  The histogram calls (sb_build_histograms,
+ *   sb_grow_tree and their sb_workspace_bytes sizes) take k <= 23 (at most
+ *   24 channels) and return SB_E_UNSUPPORTED (sizes: -1) above that.  The
+ *   paper leaves k free (Section 3); its experiments use k <= 20.
  *
  * Data layouts (device memory; the layouts are this library's choice, made
  * so that each kernel reads whole cache lines of what it needs)
@@ -251,9 +255,11 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  * node_off  n_nodes+1 offsets.
  * build_list  n_build node ids to build (NULL = every node; n_build ignored).
  * H         out: [n_nodes][m][k+1][n_bins] fp64.
- * With k+1 <= 6 channels and n_bins <= 256 the call first writes every row's
- * quantised values (16 bytes per row) into its workspace, so the workspace
- * grows with n: sb_workspace_bytes(SB_CALL_BUILD_HISTOGRAMS, n, ...).
+ * 1 <= k <= 23: more than 24 channels return SB_E_UNSUPPORTED.
+ * The call first writes every row's quantised values into its workspace,
+ * 16 * ceil((k+1)/6) bytes per row (one 16-byte word per group of six
+ * channels), so the workspace grows with n:
+ * sb_workspace_bytes(SB_CALL_BUILD_HISTOGRAMS, n, ...).
  */
 int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* rec, int64_t ld_rec, int64_t n,
                             int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh, int32_t k,
@@ -264,6 +270,10 @@ int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* r
 /*
  * sb_subtract_histograms -- sibling histograms by subtraction.
  *
+ * The paper does not use this step: its histogram algorithm (Section 3.4)
+ * builds every node.  Since a node's rows are the disjoint union of its two
+ * children's rows, every histogram cell of the parent is the sum of the
+ * children's cells, so one child follows from the parent and the other.
  * For parent p < n_parents with built child c = build_list[p] (2p or 2p+1):
  *   H_child[c ^ 1] = H_parent[p] - H_child[c]   (all m*n_bins*(k+1) cells).
  * Exact, because histograms are fixed-point sums stored in fp64.  Entries of
@@ -294,6 +304,9 @@ int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_b
 /*
  * sb_partition_rows -- split every node's rows for the next level.
  *
+ * Section 2 (finding the tree structure): the chosen split of leaf R into
+ * R_left = {x : x_f <= threshold} and R_right = R minus R_left, applied to
+ * every node of the level; the children replace the node as leaves.
  * Node j's rows (row_idx_in[node_off_in[j] .. node_off_in[j+1]), identity
  * order if row_idx_in is NULL) are split stably into left (column-major bin
  * of feature best_feature[j] <= best_bin[j]) then right, written to the same
@@ -326,7 +339,7 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
  * row_idx_out: out, n rows grouped by leaf; leaf_off_out: out, 2^depth + 1
  *   offsets of the leaves (leaf j of the last level owns
  *   row_idx_out[leaf_off_out[j] .. leaf_off_out[j+1])).
- * 1 <= depth <= 12.
+ * 1 <= depth <= 12; 1 <= k <= 23 (SB_E_UNSUPPORTED above).
  */
 int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm, int64_t ld_cm, const uint8_t* rec,
                      int64_t ld_rec, int64_t n, int32_t m, int32_t n_bins, const float* GH, int64_t ld_gh,

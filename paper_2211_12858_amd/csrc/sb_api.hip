@@ -100,10 +100,7 @@ GrowLayout grow_ws_layout(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32
   // quantised sketch rows of the rotated histogram kernel, written at the
   // root and read by every level
   L.qrow = p;
-  {
-    const HistPlan hp = hist_plan(m, n_bins, k, 1);
-    if (hp.rot) p += align256(n * 16 * hp.cg);
-  }
+  p += align256(n * 16 * hist_plan(m, n_bins, k, 1).cg);
   L.call = p;
   p += call;
   L.total = p;
@@ -121,16 +118,6 @@ int32_t check_gh(const char* call, const void* GH, int64_t ld_gh, int32_t k) {
   if (!aligned(GH, 16) || ld_gh < k + 1)
     return fail(SB_E_SHAPE, std::string(call) + ": GH needs a 16-byte aligned base and ld_gh >= k + 1 (row-major)");
   return SB_OK;
-}
-
-// Level 0: one node of all n rows, and its histogram prefix.
-__global__ void k_root_offsets(int32_t* off, int64_t* pre, int32_t n) {
-  if (threadIdx.x == 0) {
-    off[0] = 0;
-    off[1] = n;
-    pre[0] = 0;
-    pre[1] = n;
-  }
 }
 
 }  // namespace
@@ -355,7 +342,7 @@ int32_t sb_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_t* r
   if (n_build < 1 || n_build > n_nodes || n_build > 65535)
     return fail(SB_E_ARG, "sb_build_histograms: n_build must be in [1, min(n_nodes, 65535)]");
   if (hist_plan(m, n_bins, k, n_build).nq == 0)
-    return fail(SB_E_UNSUPPORTED, "sb_build_histograms: 4 features x n_bins x (k+1) cells exceed the LDS budget");
+    return fail(SB_E_UNSUPPORTED, "sb_build_histograms: at most 24 channels (k <= 23)");
   rc = need_ws(ws, ws_bytes, hist_ws_bytes(n, m, n_bins, k, n_build, true), call);
   if (rc) return rc;
   return launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_idx, node_off, n_nodes,
@@ -436,8 +423,7 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   if (!(lambda > 0.0) || !std::isfinite(lambda)) return fail(SB_E_ARG, "sb_grow_tree: lambda must be > 0");
   if (!(min_child_weight >= 0.0) || !std::isfinite(min_child_weight))
     return fail(SB_E_ARG, "sb_grow_tree: min_child_weight must be >= 0");
-  if (hist_plan(m, n_bins, k, 1).nq == 0)
-    return fail(SB_E_UNSUPPORTED, "sb_grow_tree: 4 features x n_bins x (k+1) int32 cells exceed the 160 KB LDS");
+  if (hist_plan(m, n_bins, k, 1).nq == 0) return fail(SB_E_UNSUPPORTED, "sb_grow_tree: at most 24 channels (k <= 23)");
   const GrowLayout G = grow_ws_layout(n, m, n_bins, k, depth);
   rc = need_ws(ws, ws_bytes, G.total, call);
   if (rc) return rc;
@@ -465,24 +451,21 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     return ((depth - l) % 2 == 0) ? row_idx_out : rows_tmp;
   };
 
-  // the root's offsets and prefix {0, n}: written by the kernel that
-  // quantises the sketch rows when the rotated histogram kernel runs
-  const bool quant_root = hist_plan(m, n_bins, k, 1).rot;
-  if (!quant_root) hipLaunchKernelGGL(k_root_offsets, dim3(1), dim3(64), 0, st, level_off(0), pre, (int32_t)n);
+  // the root's offsets and prefix {0, n} are written by the kernel that
+  // quantises the sketch rows
   for (int l = 0; l < depth; ++l) {
     const int32_t nn = 1 << l;
     double* Hcur = Hbuf[l & 1];
     const int32_t* row_in = l == 0 ? nullptr : level_rows(l);
     const int32_t* off_l = level_off(l);
     // the prefix of the built nodes' sizes comes from the previous level's
-    // partition (from k_root_offsets at the root), and the reduce writes the
+    // partition (from the sketch-row quantiser at the root), and the reduce writes the
     // siblings by subtraction from the previous level
     const int64_t base = (int64_t(1) << l) - 1;
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
                                    nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
-                                   min_child_weight, qrow, false, depth > 1,
-                                   quant_root ? const_cast<int32_t*>(off_l) : nullptr);
+                                   min_child_weight, qrow, false, depth > 1, const_cast<int32_t*>(off_l));
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
                                    level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],

@@ -1,43 +1,34 @@
 // Per-node histograms of one tree level (Section 3.4) and sibling subtraction.
 //
-// Design for gfx950.  The scatter-add of random bins into LDS is the roof of
-// this kernel, and it is set by LDS bank conflicts.  Measured on MI355X with
-// uniformly random bins, 768 threads and 120 KB of cells per CU:
-// ds_add_u32 retires 6.5 channel-adds/clk/CU and ds_add_u64 carrying two
-// channels 8.9 (conflict-free bins reach 14.9; ds_add_f32 only ~0.3).  So:
+// Design for gfx950.  The scatter-add of random bins into LDS bounds this
+// kernel, so every choice below serves the LDS data path:
 //  * every sketch value is quantised to an integer rint(v * 2^qexp[t]) of
-//    magnitude <= 2^QBITS;
+//    magnitude <= 2^QBITS (written once per tree as 21-bit fields of one
+//    16-byte word per row and channel group of six);
 //  * channels are packed in pairs into 64-bit LDS cells holding
 //    hi * 2^32 + lo as a two's-complement sum, one ds_add_u64 per pair;
+//  * a slice of 16 features keeps its cells as [bin][pair][feature] and lane
+//    l adds feature (i + l) mod 16 at step i, so a cell's bank pair is its
+//    feature and every instruction puts four lanes on each bank pair,
+//    whatever the bins (no bank conflicts);
 //  * each cell is a running sum modulo 2^64.  Its owner thread reads it back
 //    every window of <= WINDOW_ROWS rows, splits the change into the two
 //    channel changes (each below 2^31 in magnitude, so the split is exact)
 //    and adds them into int64 register totals;
-//  * a workgroup owns one feature slice (F features, F * n_bins cells per
-//    channel pair) and a contiguous range of the rows of the built nodes,
-//    taken in build-list order; it writes one int64 partial per node it
-//    touched;
-//  * k_hist_reduce sums the partials of each node (integer, so the result is
-//    independent of the grid and of the order of the atomics) and writes the
-//    fp64 histogram.  Sums of fixed-point values are exact in fp64, which
-//    makes sibling subtraction exact as well.
+//  * a workgroup owns one feature slice and a contiguous range of the rows of
+//    the built nodes, taken in build-list order; it writes one int64 partial
+//    per node it touched;
+//  * the reduce kernels sum the partials of each node (integers, so the
+//    result is independent of the grid) and write the fp64 histogram.  Sums
+//    of fixed-point values are exact in fp64, which makes sibling
+//    subtraction exact as well.
 // Rows come either as positions of contiguous data (quad-major bins: 256
 // contiguous bytes per wave and word) or through row indices from the row
-// records (one record line per row); the sketch is read from its row-major
-// records (whole 32-byte sectors) in both cases.
+// records (one record line per row).
 // Workgroups that share a row range but own different slices are placed on
 // the same XCD (dispatch is round-robin over the 8 XCDs by block index) so
 // the rows they all read stay in that XCD's L2.
 #include "sb_common.h"
-
-// Two-step prefetch in the rotated kernel (1) or one step (0): with the
-// rotated kernel's 32 register totals the deeper pipeline spills.
-#ifndef SB_HIST_ROT_DEEP
-#define SB_HIST_ROT_DEEP 0
-#endif
-#ifndef SB_HIST_ROT_OPAQUE
-#define SB_HIST_ROT_OPAQUE 0
-#endif
 
 namespace sb {
 
@@ -46,11 +37,9 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
   p.c = k + 1;
   p.pairs = (p.c + 1) / 2;
   if (p.c <= ROT_MAX_C && n_bins <= 256) {
-    p.rot = true;
     p.cg = (p.c + QROW_MAX_C - 1) / QROW_MAX_C;
     p.nq = ROT_F / 4;
     p.f = ROT_F;
-    p.rows_wave = 64;
     p.cells = 2 * p.pairs * p.f * n_bins;
     p.slices_full = m / ROT_F;
     const int r = m % ROT_F;
@@ -88,48 +77,22 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
     }
     p.q = 8 * p.a_full;
     p.q_thin = 8 * p.b_thin;
-    p.q_pad = p.q;
     p.slots = (int64_t)(p.q > p.q_thin ? p.q : p.q_thin) + n_build;
     p.grid = 8 * (p.a_full * uf + p.b_thin * ut);
     return p;
   }
-  const int64_t quad_bytes = 4ll * n_bins * p.pairs * 8;
-  int nq_max = (int)(HIST_LDS_BYTES / quad_bytes);
-  const int quads_total = (m + 3) / 4;
-  if (nq_max > quads_total) nq_max = quads_total;
-  if (nq_max > HIST_MAX_QUADS) nq_max = HIST_MAX_QUADS;
-  if (nq_max < 1) nq_max = 0;  // does not fit: caller rejects
-  if (nq_max == 0) return p;
-  p.slices = (quads_total + nq_max - 1) / nq_max;
-  p.nq = (quads_total + p.slices - 1) / p.slices;
-  p.f = 4 * p.nq;
-  p.rows_wave = 64;  // one lane per row; the lane covers the whole slice
-  p.cells = 2 * p.pairs * p.f * n_bins;  // channel cells, the odd channel's partner included
-  // Workgroup b runs on XCD b % 8 and a row group's slices share its XCD, so
-  // an XCD hosts (q/8) * slices workgroups; keep that within its 32 CUs (one
-  // histogram workgroup per CU) so that every workgroup starts at once.
-  int per_xcd = HIST_CUS_PER_XCD / p.slices;
-  if (per_xcd < 1) per_xcd = 1;
-  p.q = 8 * per_xcd;
-  p.q_pad = p.q;
-  p.slots = (int64_t)p.q + n_build;
-  p.slices_full = p.slices;
-  p.f_thin = p.b_thin = p.q_thin = 0;
-  p.cg = 1;
-  p.a_full = per_xcd;
-  p.grid = p.q_pad * p.slices;
-  return p;
+  return p;  // more than ROT_MAX_C channels or 256 bins: unsupported (nq = 0)
 }
 
 // Workspace: [pre: n_build+1 int64][partials: slices * slots * cells int64]
-// [quantised rows: n * 16 bytes, rotated kernel and quant_rows only]
+// [quantised rows: n * 16 * cg bytes, with quant_rows only]
 int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows) {
   HistPlan p = hist_plan(m, n_bins, k, n_build, false);
-  if (p.nq == 0) return -1;
+  if (p.nq == 0) return -1;  // unsupported shape
   const HistPlan pt = hist_plan(m, n_bins, k, n_build, true);  // rows read straight from the data
   int64_t part = (int64_t)p.slices * p.slots * p.cells;
   if ((int64_t)pt.slices * pt.slots * pt.cells > part) part = (int64_t)pt.slices * pt.slots * pt.cells;
-  const int64_t q = (p.rot && quant_rows) ? align256(n * 16 * p.cg) : 0;
+  const int64_t q = quant_rows ? align256(n * 16 * p.cg) : 0;
   return align256((int64_t)(n_build + 1) * 8) + align256(part * 8) + q;
 }
 
@@ -154,7 +117,7 @@ struct HistArgs {
   bool store_h;      // fused level end: write H (skipped at a tree's last level, whose H has no reader)
   int64_t n;
   int32_t m, n_bins, c, pairs, n_nodes, n_build;
-  int32_t nq, f, slices, rows_wave, cells, q, cpt, steps_per_window;
+  int32_t f, slices, cells, q, steps_per_window;
   int64_t slots;
   int32_t slices_full, f_thin, a_full, b_thin, q_thin, cg;  // rotated kernel plan (see HistPlan)
 };
@@ -215,19 +178,17 @@ __global__ void __launch_bounds__(1024) k_hist_plan(HistArgs a) {
   if (threadIdx.x == 1023) a.pre[a.n_build] = part[1023];
 }
 
-// Thread t owns the 64-bit cells j = t + HIST_THREADS * i, i < H (H =
-// HIST_MAX_CELLS_PER_THREAD / 2): consecutive threads own consecutive cells,
-// so the fold's 64-bit LDS reads and the final partial writes are contiguous
-// per wave.  Cell i of the thread carries its channel totals 2i (low half)
-// and 2i+1 (high half).  The LDS always holds H cells per thread (cells past
-// the plan's count stay zero), so the reads need no bounds tests.
+// Thread t owns the 64-bit cells j = t + NT * i, i < H: consecutive threads
+// own consecutive cells, so the fold's 64-bit LDS reads are contiguous per
+// wave.  Cell i of the thread carries its channel totals 2i (low half) and
+// 2i+1 (high half).
 //
 // A cell holds S = Hi * 2^32 + Lo (mod 2^64), Hi and Lo the exact running
 // channel sums, and the totals hold the sums as of the previous read, so
 // the change D = S - (tot_hi * 2^32 + tot_lo) is dHi * 2^32 + dLo with
 // |dLo|, |dHi| < 2^31: dLo is the sign-extended low word of D and dHi the
 // arithmetic high word of D - dLo.
-template <int H = HIST_MAX_CELLS_PER_THREAD / 2, int NT = HIST_THREADS>
+template <int H, int NT>
 __device__ inline void fold_cells(const uint64_t* lds64, int64_t* tot) {
 #pragma unroll
   for (int i0 = 0; i0 < H; i0 += 4) {
@@ -261,17 +222,6 @@ __device__ inline void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// One row of one lane: the slice's bins (4 per word) and the row's channel
-// values, loaded together so their latencies overlap.  Both layouts are
-// word-per-row (quad-major bins, channel-major sketch), so each of these
-// loads is one 256-byte contiguous access per wave when the wave's rows are
-// consecutive.
-template <int CMAX, int NQMAX>
-struct RowData {
-  uint32_t word[NQMAX];
-  float g[CMAX];
-};
-
 // A lane's position in a step: `raw` is the row index as loaded (not yet
 // clamped, so that issuing the load never waits for it) and `on` says whether
 // the position exists.
@@ -301,77 +251,6 @@ __device__ inline void load_run(const uint32_t* p, uint32_t* out) {
     out[N - R + 1] = v.y;
   }
   if constexpr (R & 1) out[N - 1] = p[N - 1];
-}
-
-// EXACT: CMAX channels and NQMAX quads exactly (no per-element tests, so the
-// load path has no branches and the compiler can count outstanding loads).
-// Lanes without a row load row 0 and never use the data.  FROM_REC: the bins
-// are read from the row's record, else from the quad-major bins; the sketch
-// values always come from the row's row-major GH record.
-template <int CMAX, int NQMAX, bool EXACT, bool FROM_REC>
-__device__ inline void load_row(const HistArgs& a, RowRef ref, int f0, int nq, int c, RowData<CMAX, NQMAX>& d) {
-  int64_t row = ref.on ? (int64_t)ref.raw : 0;
-  row = row < 0 ? 0 : (row >= a.n ? a.n - 1 : row);
-  const uint32_t* gp = reinterpret_cast<const uint32_t*>(a.GH + row * a.ld_gh);
-  if constexpr (FROM_REC) {
-    const uint32_t* wp = reinterpret_cast<const uint32_t*>(a.rec + row * a.ld_rec) + (f0 >> 2);
-    if constexpr (EXACT) {
-      load_run<NQMAX>(wp, d.word);
-    } else {
-#pragma unroll
-      for (int qq = 0; qq < NQMAX; ++qq)
-        if (qq < nq) d.word[qq] = wp[qq];
-    }
-  } else {
-    const uint32_t* wp = a.bins4 + (int64_t)(f0 >> 2) * a.ld4 + row;
-#pragma unroll
-    for (int qq = 0; qq < NQMAX; ++qq)
-      if (EXACT || qq < nq) d.word[qq] = wp[(int64_t)qq * a.ld4];
-  }
-  if constexpr (EXACT) {
-    uint32_t gw[CMAX];
-    load_run<CMAX>(gp, gw);
-#pragma unroll
-    for (int t = 0; t < CMAX; ++t) d.g[t] = __uint_as_float(gw[t]);
-  } else {
-#pragma unroll
-    for (int t = 0; t < CMAX; ++t)
-      if (t < c) d.g[t] = __uint_as_float(gp[t]);
-  }
-}
-
-// LDS cells are laid out [channel pair][feature in slice][bin] (64-bit): for
-// a fixed pair and feature the 64 lanes of a wave hit lds64[base + bin].  All
-// four features of a quad are accumulated; features past m (m not a multiple
-// of 4) read the padding bytes of the last word and land in cells the
-// reduction never reads.  An odd channel count pairs the last channel with a
-// zero.
-template <int CMAX, int NQMAX, bool EXACT>
-__device__ inline void add_row(uint64_t* lds64, const RowData<CMAX, NQMAX>& d, const int* qe, int nq, int B, int FB,
-                               int c) {
-  constexpr int PMAX = (CMAX + 1) / 2;
-  int32_t vq[2 * PMAX];
-#pragma unroll
-  for (int t = 0; t < 2 * PMAX; ++t)
-    vq[t] = (t < CMAX && (EXACT || t < c)) ? (int32_t)rintf(ldexpf(d.g[t < CMAX ? t : 0], qe[t < CMAX ? t : 0])) : 0;
-  uint64_t pk[PMAX];
-#pragma unroll
-  for (int p = 0; p < PMAX; ++p)
-    pk[p] = ((uint64_t)(uint32_t)vq[2 * p + 1] << 32) + (uint64_t)(int64_t)vq[2 * p];
-#pragma unroll
-  for (int qq = 0; qq < NQMAX; ++qq) {
-    if (EXACT || qq < nq) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        int bin = (int)((d.word[qq] >> (8 * u)) & 0xffu);
-        bin = bin < B ? bin : B - 1;
-        uint64_t* cell = lds64 + (4 * qq + u) * B + bin;
-#pragma unroll
-        for (int p = 0; p < PMAX; ++p)
-          if (EXACT || 2 * p < c) atomicAdd(reinterpret_cast<unsigned long long*>(cell + p * FB), pk[p]);
-      }
-    }
-  }
 }
 
 // ---------------------------------------------------------------- rotated-feature order
@@ -595,11 +474,6 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot<FT>& d, uint32_t r
   }
   uint32_t rw[4];
   rotate16(d.word, (int)r, rw);
-#if SB_HIST_ROT_OPAQUE
-  // hide the lane's rotation from loop-invariant hoisting, so that the 16
-  // column offsets are recomputed per row instead of held in 16 registers
-  asm volatile("" : "+v"(r));
-#endif
 #pragma unroll
   for (int i = 0; i < ROT_F; ++i) {
     int bin = (int)((rw[i >> 2] >> (8 * (i & 3))) & 0xffu);
@@ -612,9 +486,17 @@ __device__ inline void add_row_rot(lds_u64* lds, const RowRot<FT>& d, uint32_t r
   }
 }
 
-// Rows of virtual positions [v, vend) of one node for a rotated slice, as
-// run_segment, with 32-bit positions (every position and row is below 2^31,
-// so unsigned 32-bit sums of them do not wrap).
+// Accumulate the lane's rows of virtual positions [v, vend) of one node
+// (segment start seg0, first virtual position pstart) into the LDS cells of
+// a rotated slice, folding into `tot` at every window.  HAS_IDX: rows come
+// through row_idx and are read from their records (otherwise the position is
+// the row of the contiguous data).  Positions are 32-bit (every position and
+// row is below 2^31, so unsigned 32-bit sums of them do not wrap).  The
+// row-index load of a lane is unconditional (positions past the end are
+// clamped into the segment and marked off), so the load path has no
+// branches.  The next step's row is loaded before the current one is added,
+// so its memory latency hides behind the current step's LDS work; the
+// prefetched row stays in flight across the window folds.
 template <int C, int FT, bool HAS_IDX>
 __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t* tot, uint32_t v,
                                        uint32_t vend, uint32_t pstart, uint32_t seg0, int wave, int lane, int f0,
@@ -636,37 +518,19 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
     rr.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
     return rr;
   };
-  constexpr bool DEEP = SB_HIST_ROT_DEEP != 0;
   RowRef r0 = row_at(v);
   RowRef r1 = row_at(v + rows_step);
   RowRot<FT> d0, d1;
   load_row_rot<FT, HAS_IDX>(a, r0, f0, qbase, qstride, d0);
-  RowRef r2;
-  if constexpr (DEEP) {
-    r2 = row_at(v + 2 * rows_step);
-    load_row_rot<FT, HAS_IDX>(a, r1, f0, qbase, qstride, d1);
-  }
   int steps = 0;
 #pragma unroll 1
   for (uint32_t vs = v; vs < vend; vs += rows_step) {
-    if constexpr (DEEP) {
-      const RowRef r3 = row_at(vs + 3 * rows_step);
-      RowRot<FT> d2;
-      load_row_rot<FT, HAS_IDX>(a, r2, f0, qbase, qstride, d2);
-      if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
-      r0 = r1;
-      d0 = d1;
-      r1 = r2;
-      d1 = d2;
-      r2 = r3;
-    } else {
-      const RowRef r2n = row_at(vs + 2 * rows_step);
-      load_row_rot<FT, HAS_IDX>(a, r1, f0, qbase, qstride, d1);
-      if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
-      r0 = r1;
-      d0 = d1;
-      r1 = r2n;
-    }
+    const RowRef r2 = row_at(vs + 2 * rows_step);
+    load_row_rot<FT, HAS_IDX>(a, r1, f0, qbase, qstride, d1);
+    if (r0.on) add_row_rot<C, FT>(lds, d0, r, slot0, B);
+    r0 = r1;
+    d0 = d1;
+    r1 = r2;
     if (++steps == a.steps_per_window) {
       steps = 0;
       lds_barrier();
@@ -675,163 +539,10 @@ __device__ inline void run_segment_rot(const HistArgs& a, lds_u64* lds, int64_t*
   }
 }
 
-// Accumulate the lane's rows of virtual positions [v, vend) of one node
-// (segment start seg0, first virtual position pstart) into the LDS cells,
-// folding into `tot` at every window.  HAS_IDX: rows come through row_idx
-// and are read from their records (otherwise the position is the row of the
-// contiguous data).  The row-index load of a lane is
-// unconditional (positions past the end are clamped into the segment and
-// marked off), so the load path has no branches and the compiler's count of
-// outstanding loads stays exact.
-template <int CMAX, int NQMAX, bool EXACT, bool HAS_IDX>
-__device__ inline void run_segment(const HistArgs& a, uint64_t* lds, int64_t* tot, const int* qe, int64_t v,
-                                   int64_t vend, int64_t pstart, int64_t seg0, int wave, int lane, int f0, int nq,
-                                   int B, int FB, int c) {
-  auto load = [&](RowRef ref, RowData<CMAX, NQMAX>& d) { load_row<CMAX, NQMAX, EXACT, HAS_IDX>(a, ref, f0, nq, c, d); };
-  auto add = [&](const RowData<CMAX, NQMAX>& d) { add_row<CMAX, NQMAX, EXACT>(lds, d, qe, nq, B, FB, c); };
-  const int rows_step = HIST_THREADS;
-  const int64_t last_pos = seg0 + (vend - 1 - pstart);
-  auto row_at = [&](int64_t vs, int64_t lim) -> RowRef {
-    const int64_t vv = vs + (int64_t)wave * 64 + lane;
-    RowRef r;
-    r.on = vv < lim;
-    int64_t pos = seg0 + (vv - pstart);
-    pos = pos < last_pos ? pos : last_pos;
-    r.raw = HAS_IDX ? a.row_idx[pos] : (int32_t)pos;
-    return r;
-  };
-  // The prefetch pipeline runs through the whole segment.  With two-step
-  // prefetch (row data two steps ahead, row indices three), used when a row's
-  // data fits in 12 registers, loads stay in flight across more than one step
-  // of LDS work (the loaded memory latency is longer than one step); wider
-  // rows prefetch one step ahead to stay within the register budget.  Every
-  // steps_per_window steps all waves meet at a barrier and fold their cells;
-  // the prefetched data stays in flight across the fold.  Row indices are
-  // issued before the data loads of the same step: loads return in issue
-  // order, so waiting for an index later never waits for data behind it.
-  constexpr bool DEEP = CMAX + NQMAX <= 12;
-  RowRef r0 = row_at(v, vend);
-  RowRef r1 = row_at(v + rows_step, vend);
-  RowData<CMAX, NQMAX> d0, d1;
-  load(r0, d0);
-  RowRef r2;
-  if constexpr (DEEP) {
-    r2 = row_at(v + 2 * rows_step, vend);
-    load(r1, d1);
-  }
-  int steps = 0;
-#pragma unroll 1
-  for (int64_t vs = v; vs < vend; vs += rows_step) {
-    if constexpr (DEEP) {
-      const RowRef r3 = row_at(vs + 3 * rows_step, vend);
-      RowData<CMAX, NQMAX> d2;
-      load(r2, d2);
-      if (r0.on) add(d0);
-      r0 = r1;
-      d0 = d1;
-      r1 = r2;
-      d1 = d2;
-      r2 = r3;
-    } else {
-      const RowRef r2n = row_at(vs + 2 * rows_step, vend);
-      load(r1, d1);
-      if (r0.on) add(d0);
-      r0 = r1;
-      d0 = d1;
-      r1 = r2n;
-    }
-    if (++steps == a.steps_per_window) {
-      steps = 0;
-      lds_barrier();
-      fold_cells(lds, tot);
-    }
-  }
-}
-
-// One lane per row; each lane accumulates all F = 4*nq features of its slice
-// for its row.  Each step a wave covers 64 rows: it issues the loads of its
-// next rows and the row indices of the step after, then performs the current
-// rows' LDS atomics, so memory latency hides behind LDS work.
-template <int CMAX, int NQMAX, bool EXACT>
-__global__ void __launch_bounds__(HIST_THREADS)
-k_hist(HistArgs a) {
-  extern __shared__ uint64_t lds64[];
-  const int b = blockIdx.x;
-  const int xcd = b & 7, g = b >> 3;
-  const int q = (g / a.slices) * 8 + xcd;
-  const int s = g % a.slices;
-  if (q >= a.q) return;
-  const int64_t T = a.pre[a.n_build];
-  const int64_t v0 = (int64_t)q * T / a.q;
-  const int64_t v1 = (int64_t)(q + 1) * T / a.q;
-  if (v0 >= v1) return;
-
-  // first built node whose range holds v0: largest p with pre[p] <= v0
-  int lo = 0, hi = a.n_build;  // pre[lo] <= v0 < pre[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.pre[mid] <= v0) lo = mid;
-    else hi = mid;
-  }
-  int p = lo;
-
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
-  const int f0 = s * a.f;
-  // quads of this slice (the last slice may hold fewer; EXACT launches only
-  // when every slice holds NQMAX)
-  const int nq = EXACT ? NQMAX : ((a.m - f0 + 3) / 4 < a.nq ? (a.m - f0 + 3) / 4 : a.nq);
-  const int B = a.n_bins, c = EXACT ? CMAX : a.c;
-  const int FB = a.f * B;
-  int qe[CMAX];  // wave-uniform: kept in scalar registers
-#pragma unroll
-  for (int t = 0; t < CMAX; ++t) qe[t] = __builtin_amdgcn_readfirstlane(t < c ? a.qexp[t] : 0);
-
-  int64_t tot[HIST_MAX_CELLS_PER_THREAD];
-#pragma unroll
-  for (int jj = 0; jj < HIST_MAX_CELLS_PER_THREAD; ++jj) tot[jj] = 0;
-  for (int i = 0; i < HIST_MAX_CELLS_PER_THREAD / 2; ++i) lds64[tid + HIST_THREADS * i] = 0;
-  __syncthreads();
-
-  int64_t v = v0;
-  while (v < v1) {
-    const int32_t j = node_of(a, p);
-    const int64_t pstart = a.pre[p];
-    const int64_t vend = v1 < a.pre[p + 1] ? v1 : a.pre[p + 1];
-    const int64_t seg0 = clamp_i32(a.node_off[j], 0, a.n);
-    if (a.row_idx)
-      run_segment<CMAX, NQMAX, EXACT, true>(a, lds64, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
-    else
-      run_segment<CMAX, NQMAX, EXACT, false>(a, lds64, tot, qe, v, vend, pstart, seg0, wave, lane, f0, nq, B, FB, c);
-    // end of this node's part: final fold, write the partial, reset
-    __syncthreads();
-    fold_cells(lds64, tot);
-    // partial channel cells 2j, 2j+1 of 64-bit cell j, one 16-byte store per cell
-    int64_t* dst = a.partial + ((int64_t)s * a.slots + q + p) * a.cells;
-#pragma unroll
-    for (int i = 0; i < HIST_MAX_CELLS_PER_THREAD / 2; ++i) {
-      const int j64 = tid + HIST_THREADS * i;
-      if (2 * j64 < a.cells) {
-        const longlong2 v2 = make_longlong2(tot[2 * i], tot[2 * i + 1]);
-        reinterpret_cast<longlong2*>(dst)[j64] = v2;
-      }
-      lds64[j64] = 0;
-      tot[2 * i] = 0;
-      tot[2 * i + 1] = 0;
-    }
-    __syncthreads();
-    v = vend;
-    ++p;
-    while (p < a.n_build && a.pre[p + 1] <= v) ++p;
-  }
-}
-
-// Rotated-feature kernel (c <= 6): the same work split, windows and
-// partials as k_hist, with the slice's cells in [bin][pair][feature] order.
-// Thread t owns the 64-bit cells t + ROT_THREADS * i, i < ROT_CPT.  At the
-// end of a node's part the totals go out through LDS, one pair at a time, in
-// the partial layout of k_hist ([pair][feature][bin], 16-byte channel
-// pairs), so the reduction kernels serve both.
+// One workgroup's share of a level: the slice's cells in [bin][pair][slot]
+// order, thread t owning the 64-bit cells t + ROT_THREADS * i, i < ROT_CPT.
+// At the end of a node's part the totals go out through LDS, one pair at a
+// time, as partials laid out [pair][feature][bin] (16-byte channel pairs).
 // Slice s of FT features (16, or a thin slice's f_thin), row group q of
 // qn: the rows of virtual positions [q T / qn, (q+1) T / qn).
 template <int C, int FT>
@@ -921,15 +632,10 @@ __device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds6
   }
 }
 
-// Rotated-feature kernel (c <= 6): the same windows and partials as k_hist,
-// with the slice's cells in [bin][pair][slot] order.  Thread t owns the
-// 64-bit cells t + ROT_THREADS * i, i < ROT_CPT.  At the end of a node's part
-// the totals go out through LDS, one pair at a time, in the partial layout
-// of k_hist ([pair][feature][bin], 16-byte channel pairs), so the reduction
-// kernels serve both.  Workgroup b runs on XCD b % 8; on each XCD the first
-// a_full * slices_full workgroups take the full slices of a_full row groups
-// (so the slices of a row group share the XCD's L2) and the next b_thin the
-// thin slice.
+// The histogram kernel.  Workgroup b runs on XCD b % 8; on each XCD the
+// first a_full * slices_full * cg workgroups take the (full slice, channel
+// group) pairs of a_full row groups (so the slices of a row group share the
+// XCD's L2) and the next b_thin * cg the thin slice.
 template <int C>
 __global__ void __launch_bounds__(ROT_THREADS)
 k_hist_rot(HistArgs a) {
@@ -1242,6 +948,7 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 double lam, double mcw, uint32_t* qrow, bool qrow_ready, bool store_h,
                                 int32_t* root_off) {
   const HistPlan pl = hist_plan(m, n_bins, k, n_build, row_idx == nullptr);
+  if (pl.nq == 0) return fail(SB_E_UNSUPPORTED, "sb_build_histograms: at most 24 channels (k <= 23) and 256 bins");
   HistArgs a{};
   a.bins4 = bins4;
   a.ld4 = ld4;
@@ -1256,30 +963,28 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   char* w = static_cast<char*>(ws);
   a.pre = pre_given ? const_cast<int64_t*>(pre_given) : reinterpret_cast<int64_t*>(w);
   a.partial = reinterpret_cast<int64_t*>(w + align256((int64_t)(n_build + 1) * 8));
-  if (pl.rot) {
-    // the quantised rows live in the caller's buffer (kept across a tree's
-    // levels) or else at the end of this call's workspace
-    if (!qrow)
-      qrow = reinterpret_cast<uint32_t*>(w + hist_ws_bytes(n, m, n_bins, k, n_build, false));
-    a.qrow = qrow;
-    if (!qrow_ready) {
-      const unsigned qb = (unsigned)((n + 255) / 256);
-#define SB_QUANT(C) \
-  if (pl.c == C)                                                                                            \
-    hipLaunchKernelGGL((k_quant_rows<C>), dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off,  \
-                       const_cast<int64_t*>(pre_given));                                                    \
-  else
-      SB_QUANT(1) SB_QUANT(2) SB_QUANT(3) SB_QUANT(4) SB_QUANT(5) SB_QUANT(6)
-      if (pl.cg == 2)
-        hipLaunchKernelGGL(k_quant_rows_wide<2>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
-                           const_cast<int64_t*>(pre_given));
-      else if (pl.cg == 3)
-        hipLaunchKernelGGL(k_quant_rows_wide<3>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
-                           const_cast<int64_t*>(pre_given));
-      else
-        hipLaunchKernelGGL(k_quant_rows_wide<4>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off,
-                           const_cast<int64_t*>(pre_given));
-#undef SB_QUANT
+  // the quantised rows live in the caller's buffer (kept across a tree's
+  // levels) or else at the end of this call's workspace
+  if (!qrow) qrow = reinterpret_cast<uint32_t*>(w + hist_ws_bytes(n, m, n_bins, k, n_build, false));
+  a.qrow = qrow;
+  if (!qrow_ready) {
+    const unsigned qb = (unsigned)((n + 255) / 256);
+    int64_t* rp = const_cast<int64_t*>(pre_given);
+    switch (pl.c) {
+      case 1: hipLaunchKernelGGL(k_quant_rows<1>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      case 2: hipLaunchKernelGGL(k_quant_rows<2>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      case 3: hipLaunchKernelGGL(k_quant_rows<3>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      case 4: hipLaunchKernelGGL(k_quant_rows<4>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      case 5: hipLaunchKernelGGL(k_quant_rows<5>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      case 6: hipLaunchKernelGGL(k_quant_rows<6>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, qexp, qrow, root_off, rp); break;
+      default:
+        if (pl.cg == 2)
+          hipLaunchKernelGGL(k_quant_rows_wide<2>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off, rp);
+        else if (pl.cg == 3)
+          hipLaunchKernelGGL(k_quant_rows_wide<3>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off, rp);
+        else
+          hipLaunchKernelGGL(k_quant_rows_wide<4>, dim3(qb), dim3(256), 0, st, GH, ld_gh, n, pl.c, qexp, qrow, root_off, rp);
+        break;
     }
   }
   a.H = H;
@@ -1292,10 +997,8 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.pairs = pl.pairs;
   a.n_nodes = n_nodes;
   a.n_build = n_build;
-  a.nq = pl.nq;
   a.f = pl.f;
   a.slices = pl.slices;
-  a.rows_wave = pl.rows_wave;
   a.cells = pl.cells;
   a.q = pl.q;
   a.slices_full = pl.slices_full;
@@ -1304,47 +1007,25 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.b_thin = pl.b_thin;
   a.q_thin = pl.q_thin;
   a.cg = pl.cg;
-  a.cpt = (pl.cells + HIST_THREADS - 1) / HIST_THREADS;
-  const int rows_step = pl.rot ? ROT_THREADS : HIST_THREADS;
-  a.steps_per_window = WINDOW_ROWS / rows_step > 0 ? WINDOW_ROWS / rows_step : 1;
+  a.steps_per_window = WINDOW_ROWS / ROT_THREADS;
   a.slots = pl.slots;
-  if (rows_step > WINDOW_ROWS) return fail(SB_E_UNSUPPORTED, "histogram step exceeds the fixed-point window");
 
   if (!pre_given) hipLaunchKernelGGL(k_hist_plan, dim3(1), dim3(1024), 0, st, a);
   const int grid = pl.grid;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   const bool prof = profile_on() && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess;
   if (prof) (void)hipEventRecord(e0, st);
-  const size_t lds_bytes = (size_t)(pl.rot ? ROT_CELLS * 8 : HIST_LDS_BYTES);
-  const int cm = pl.c <= 8 ? 8 : pl.c <= 16 ? 16 : 24;
-  const int nm = pl.nq <= 4 ? 4 : pl.nq <= 8 ? 8 : 16;
-  // exact shapes: every slice holds nq quads and there are exactly c channels
-  const bool even = pl.slices * pl.nq * 4 - m < 4;
-#define SB_HIST_EXACT(C, NQ)                                                                        \
-  if (even && pl.c == C && pl.nq == NQ) {                                                           \
-    hipLaunchKernelGGL((k_hist<C, NQ, true>), dim3(grid), dim3(HIST_THREADS), lds_bytes, st, a); \
-  } else
-#define SB_HIST_CASE(CM, NM)                                                                         \
-  if (cm == CM && nm == NM) {                                                                        \
-    hipLaunchKernelGGL((k_hist<CM, NM, false>), dim3(grid), dim3(HIST_THREADS), lds_bytes, st, a); \
-  } else
-#define SB_HIST_ROT(C)                                                                            \
-  if (pl.rot && pl.c == C) {                                                                      \
-    hipLaunchKernelGGL((k_hist_rot<C>), dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a);         \
-  } else
-  SB_HIST_ROT(1) SB_HIST_ROT(2) SB_HIST_ROT(3) SB_HIST_ROT(4) SB_HIST_ROT(5) SB_HIST_ROT(6)
-  if (pl.rot && pl.c > QROW_MAX_C) {
-    // channel groups of six (three pairs) each
-    hipLaunchKernelGGL((k_hist_rot<QROW_MAX_C>), dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a);
-  } else
-  SB_HIST_EXACT(11, 2) SB_HIST_EXACT(21, 1)
-  SB_HIST_CASE(8, 4) SB_HIST_CASE(8, 8) SB_HIST_CASE(8, 16)
-  SB_HIST_CASE(16, 4) SB_HIST_CASE(16, 8) SB_HIST_CASE(16, 16)
-  SB_HIST_CASE(24, 4) SB_HIST_CASE(24, 8) SB_HIST_CASE(24, 16)
-  return fail(SB_E_UNSUPPORTED, "sb_build_histograms: more than 24 channels (k > 23)");
-#undef SB_HIST_ROT
-#undef SB_HIST_EXACT
-#undef SB_HIST_CASE
+  const size_t lds_bytes = (size_t)ROT_CELLS * 8;
+  // up to six channels: one workgroup per (slice, row group); more: channel
+  // groups of six (three pairs) each, one workgroup per (slice, group)
+  switch (pl.c) {
+    case 1: hipLaunchKernelGGL(k_hist_rot<1>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+    case 2: hipLaunchKernelGGL(k_hist_rot<2>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+    case 3: hipLaunchKernelGGL(k_hist_rot<3>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+    case 4: hipLaunchKernelGGL(k_hist_rot<4>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+    case 5: hipLaunchKernelGGL(k_hist_rot<5>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+    default: hipLaunchKernelGGL(k_hist_rot<QROW_MAX_C>, dim3(grid), dim3(ROT_THREADS), lds_bytes, st, a); break;
+  }
   if (prof) {
     (void)hipEventRecord(e1, st);
     profile_record(e0, e1);

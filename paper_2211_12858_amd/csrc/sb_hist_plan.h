@@ -29,27 +29,14 @@ constexpr int ROT_MAX_C = 24;
 static_assert(QBITS + 2 <= QFIELD_BITS, "a quantised value of magnitude <= 2^QBITS and its sign must fit a field");
 
 // ---------------------------------------------------------------- histogram plan
-// One histogram workgroup: 768 threads (12 waves, 3 per SIMD, so up to 168
-// VGPRs per lane) and up to 40 channel cells per thread (20 64-bit LDS cells
-// of two channels each: 120 KB of the 160 KB LDS).  Each thread keeps the
-// int64 totals of its 40 channel cells in 80 VGPRs next to the prefetched
-// row data of the step loop; with 4 waves per SIMD (128 VGPRs) they would
-// spill to scratch.
-constexpr int HIST_THREADS = 768;
-constexpr int HIST_MAX_CELLS_PER_THREAD = 40;
-constexpr int HIST_LDS_BYTES = HIST_MAX_CELLS_PER_THREAD * HIST_THREADS * 4;
 // MI355X: 8 XCDs of 32 CUs; workgroup b is dispatched to XCD b % 8.
 constexpr int HIST_CUS_PER_XCD = 32;
-// A lane holds the bin words of up to 16 quads (64 features) of its row.
-constexpr int HIST_MAX_QUADS = 16;
 
-// Rotated-feature workgroups (up to 3 channel pairs, c <= 6): a slice of 16
-// features, LDS cells [bin][pair][feature] for 256 bins (12288 64-bit cells,
-// 96 KB), ROT_CPT cells per thread.
-#ifndef SB_HIST_ROT_THREADS
-#define SB_HIST_ROT_THREADS 768
-#endif
-constexpr int ROT_THREADS = SB_HIST_ROT_THREADS;
+// One histogram workgroup: 768 threads (12 waves, 3 per SIMD) and the cells
+// of a slice of 16 features for up to 3 channel pairs (c <= 6), laid out
+// [bin][pair][feature] for 256 bins (12288 64-bit cells, 96 KB of the
+// 160 KB LDS), ROT_CPT cells per thread.
+constexpr int ROT_THREADS = 768;
 constexpr int ROT_F = 16;
 constexpr int ROT_PMAX = 3;
 constexpr int ROT_CELLS = 256 * ROT_PMAX * ROT_F;
@@ -58,16 +45,13 @@ static_assert(ROT_CPT * ROT_THREADS == ROT_CELLS, "rotated cells must split even
 static_assert(WINDOW_ROWS % ROT_THREADS == 0, "a fixed-point window must be a whole number of steps");
 
 struct HistPlan {
-  bool rot;       // rotated-feature kernel (c <= 6), else the row-per-lane kernel
   int c;          // channels k+1
-  int pairs;      // 64-bit LDS cells per (feature, bin): ceil(c/2)
-  int nq;         // 4-feature quads per slice
-  int f;          // features per slice (4*nq)
+  int pairs;      // channel pairs: ceil(c/2)
+  int nq;         // 4-feature quads per slice (0: the shape is not supported)
+  int f;          // features per slice (16)
   int slices;     // feature slices
-  int rows_wave;  // rows one wave handles per step (64 / nq)
-  int cells;      // 2 * pairs * f * n_bins channel cells per workgroup
-  int q;          // row groups per (full) slice
-  int q_pad;      // q rounded up to a multiple of 8 (XCD-aware mapping)
+  int cells;      // 2 * pairs * f * n_bins channel cells of a partial
+  int q;          // row groups per full slice
   int64_t slots;  // partial slots per slice: max(q, q_thin) + n_build
   // Rotated kernel: the first slices_full slices hold 16 features each; when
   // m is not a multiple of 16 the rest go to one thin slice of f_thin
@@ -86,9 +70,10 @@ struct HistPlan {
   int cg;
   int grid;       // histogram workgroups
 };
+// Plan of one histogram launch; nq == 0 when c > ROT_MAX_C or n_bins > 256.
 HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool thin_ok = false);
-// Workspace of one histogram launch; quant_rows adds the n quantised sketch
-// rows of the rotated kernel (16 bytes each).
+// Workspace of one histogram launch (-1 when unsupported); quant_rows adds
+// the n quantised sketch rows (16 * cg bytes each).
 int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows);
 
 }  // namespace sb

@@ -28,11 +28,8 @@
 namespace sb {
 namespace {
 
-#ifndef SB_PART_ITERS
-#define SB_PART_ITERS 4
-#endif
 constexpr int PT_THREADS = 256;
-constexpr int PT_ITERS = SB_PART_ITERS;
+constexpr int PT_ITERS = 4;
 constexpr int PT_TILE = PT_THREADS * PT_ITERS;  // positions per tile
 constexpr int PT_MASKS = PT_TILE / 64;          // ballots per tile
 static_assert(PT_MASKS >= 1 && PT_MASKS <= 64, "a tile's ballots are counted by one wave");
@@ -103,10 +100,10 @@ __device__ inline NodeTab<SN> stage_offsets(const PartArgs& a, int32_t* so) {
 
 __device__ inline int32_t popc64(uint64_t x) { return __popcll(x); }
 
-// Each thread handles the positions t0 + tid + 256*it, it < 16.  The row
-// indices of all 16 positions are loaded first, then their bins, so each
-// thread keeps 16 independent loads in flight instead of a chain of 16
-// dependent pairs.  Node offsets and splits come from the block's node table.
+// Each thread handles the positions t0 + tid + 256*it, it < PT_ITERS.  The
+// row indices of all its positions are loaded first, then their bins, so
+// each thread keeps PT_ITERS independent loads in flight instead of a chain
+// of dependent pairs.  Node offsets and splits come from the block's node table.
 template <bool SN>
 __global__ void __launch_bounds__(PT_THREADS) k_part_flags(PartArgs a) {
   __shared__ int32_t wsum[PT_THREADS / 64];

@@ -67,8 +67,30 @@ def test_workspace_bytes(L):
         L.sb_workspace_bytes(L.SB_CALL_LEAF_VALUES, n=10_000, d=100, n_nodes=4097)
     with pytest.raises(L.SBError):
         L.sb_workspace_bytes(99)
-    with pytest.raises(L.SBError):  # 4 features x 256 bins x 101 channels do not fit the LDS budget
+    with pytest.raises(L.SBError):  # 101 channels: more than the histogram kernels take
         L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=10, m=8, n_bins=256, k=100, n_nodes=1)
+
+
+# The histogram kernels add at most 24 channels (k <= 23).  Every wider
+# sketch is refused on the host, whatever the bin count: the sizes query
+# returns -1 and the calls return SB_E_UNSUPPORTED before any device work.
+@pytest.mark.parametrize("k,n_bins", [(24, 256), (25, 256), (26, 256), (27, 256), (28, 256), (29, 256),
+                                      (40, 64), (100, 64), (24, 2)])
+def test_histogram_calls_refuse_more_than_24_channels(L, k, n_bins):
+    for call, kw in ((L.SB_CALL_BUILD_HISTOGRAMS, dict(n_nodes=1)), (L.SB_CALL_GROW_TREE, dict(depth=3))):
+        with pytest.raises(L.SBError):
+            L.sb_workspace_bytes(call, n=1000, m=10, n_bins=n_bins, k=k, **kw)
+    ld_gh = (k + 1 + 7) // 8 * 8
+    assert _code(L.sb_build_histograms, *hist_args(k=k, n_bins=n_bins, ld_gh=ld_gh)) == 3
+    assert "24 channels" in L.sb_last_error()
+    assert _code(L.sb_grow_tree, *grow_args(k=k, n_bins=n_bins, ld_gh=ld_gh)) == 3
+    assert "24 channels" in L.sb_last_error()
+
+
+@pytest.mark.parametrize("k,n_bins", [(23, 256), (23, 64), (20, 256), (5, 256), (1, 2)])
+def test_histogram_calls_accept_up_to_24_channels(L, k, n_bins):
+    assert L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=1000, m=10, n_bins=n_bins, k=k, n_nodes=1) > 0
+    assert L.sb_workspace_bytes(L.SB_CALL_GROW_TREE, n=1000, m=10, n_bins=n_bins, k=k, depth=3) > 0
 
 
 def _code(fn, *args):
@@ -133,7 +155,8 @@ def hist_args(**kw):
     (dict(row_idx=F, rec=F, ld_rec=40), 2),    # stride not a multiple of 16
     (dict(n_nodes=0), 1),
     (dict(n_build=3), 1),            # more than n_nodes
-    (dict(k=100, ld_gh=104), 3),     # LDS budget exceeded
+    (dict(k=100, ld_gh=104), 3),     # more than 24 channels
+    (dict(k=24, ld_gh=32), 3),
     (dict(ws_bytes=100), 1),
 ])
 def test_build_histograms_rejects(L, kw, code):

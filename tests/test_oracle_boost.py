@@ -10,6 +10,8 @@ formulas the oracle implements:
   training loss at every step.
 A mutation check plants plausible mistakes and shows the pins catch each.
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -31,6 +33,26 @@ def _fd_grad_hess(loss_fn, F, target, eps=1e-4):
         g[:, j] = (lp - lm) / (2 * eps)
         h[:, j] = (lp - 2 * l0 + lm) / (eps * eps)
     return g, h
+
+
+def test_losses_hand_values():
+    """Hand values of the two cross-entropies (Section 4 uses them).
+
+    Softmax: equal scores over d classes give p = 1/d, so the loss is log d;
+    scores (log 3, 0) give p = (3/4, 1/4), so label 1 costs -log(1/4) = log 4
+    and label 0 costs log(4/3).  Sigmoid: a = 0 gives s = 1/2 (log 2 per
+    output, whatever the target); a = log 3 gives s = 3/4, so target 1 costs
+    log(4/3) and target 0 costs log 4.
+    """
+    F = np.zeros((1, 4))
+    F2 = np.array([[0.0, 0.0], [math.log(3.0), 0.0], [math.log(3.0), 0.0]])
+    got = oracle.boost.softmax_ce_loss(F2, np.array([0, 1, 0]))
+    assert got == pytest.approx([math.log(2.0), math.log(4.0), math.log(4.0 / 3.0)], rel=1e-14)
+    assert oracle.boost.softmax_ce_loss(F[:1], np.array([2]))[0] == pytest.approx(math.log(4.0), rel=1e-14)
+    Fs = np.array([[0.0, 0.0], [math.log(3.0), math.log(3.0)]])
+    Ys = np.array([[1, 0], [1, 0]], dtype=np.uint8)
+    got = oracle.boost.sigmoid_bce_loss(Fs, Ys)
+    assert got == pytest.approx([2 * math.log(2.0), math.log(4.0 / 3.0) + math.log(4.0)], rel=1e-14)
 
 
 def test_softmax_derivatives_match_finite_differences():

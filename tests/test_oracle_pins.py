@@ -42,9 +42,13 @@ def test_worked_examples(case):
             else:
                 assert valid[f, b]
                 assert S[f, b] == pytest.approx(float(Fraction(want)), rel=1e-15)
-    f, b, s1, _ = oracle.best_split(S, valid)
+    f, b, s1, s2 = oracle.best_split(S, valid)
     assert (f, b) == tuple(case["best"][:2])
     assert s1 == pytest.approx(float(Fraction(case["best"][2])), rel=1e-15)
+    if case["runner_up"] is None:
+        assert s2 == -np.inf
+    else:
+        assert s2 == pytest.approx(float(Fraction(case["runner_up"])), rel=1e-15)
     # the brute force agrees exactly with the hand values
     (bf, bb, bs), table = brute.brute_best_split(bins, GH, list(rows), case["n_bins"], 1.0)
     assert (bf, bb) == tuple(case["best"][:2]) and bs == Fraction(case["best"][2])
@@ -250,8 +254,69 @@ def test_scores_match_brute_force(seed):
     for (f, b), (s, v) in table.items():
         assert bool(valid[f, b]) == v
         assert S[f, b] == pytest.approx(float(s), rel=1e-12)
-    f, b, s1, _ = oracle.best_split(S, valid)
+    f, b, s1, s2 = oracle.best_split(S, valid)
     assert (f, b) == (bf, bb)
+    assert s2 == pytest.approx(float(brute_runner_up(table)), rel=1e-12)
+
+
+def brute_runner_up(table):
+    """Second-best valid exact score of a brute-force table (the best removed once; -inf if none)."""
+    vals = sorted((s for s, v in table.values() if v), reverse=True)
+    return vals[1] if len(vals) > 1 else -math.inf
+
+
+def _runner_up_pins_hold(best_split):
+    """The runner-up pins (hand-worked cases and exact brute force) for a given best_split."""
+    for case in json.load(open(GOLDEN))["cases"]:
+        bins = np.array(case["bins"], dtype=np.uint8)
+        GH = _gh(case["g"])
+        S, valid = oracle.split_scores(oracle.node_histograms(bins, GH, np.arange(bins.shape[0]), case["n_bins"]), 1.0)
+        s2 = best_split(S, valid)[3]
+        want = -math.inf if case["runner_up"] is None else float(Fraction(case["runner_up"]))
+        if not (s2 == want or (math.isfinite(want) and abs(s2 - want) <= 1e-15 * abs(want))):
+            return False
+    for seed in (0, 1):
+        case = small_case(40, 3, 6, 3, seed=seed, h_kind="random" if seed % 2 else "ones")
+        GH = oracle.materialise(case.G, case.h, *oracle.identity_sketch(3))
+        rows = np.arange(40)
+        S, valid = oracle.split_scores(oracle.node_histograms(case.bins, GH, rows, 6), 1.0)
+        _, table = brute.brute_best_split(case.bins, GH, list(rows), 6, 1.0)
+        if best_split(S, valid)[3] != pytest.approx(float(brute_runner_up(table)), rel=1e-12):
+            return False
+    return True
+
+
+def test_runner_up_pins_catch_planted_mistakes():
+    """Plausible mistakes in the runner-up score of best_split each fail a runner-up pin."""
+    assert _runner_up_pins_hold(oracle.best_split)
+
+    def unmasked(S, valid):           # runner-up taken over invalid candidates too
+        f, b, s1, _ = oracle.best_split(S, valid)
+        rest = S.astype(np.float64).ravel().copy()
+        if f >= 0:
+            rest[f * S.shape[1] + b] = -np.inf
+        return f, b, s1, float(rest.max()) if rest.size else -np.inf
+
+    def ties_dropped(S, valid):       # every candidate equal to the best removed, not just the best one
+        f, b, s1, _ = oracle.best_split(S, valid)
+        flat = np.where(valid, S, -np.inf).ravel()
+        rest = flat[flat < s1]
+        return f, b, s1, float(rest.max()) if rest.size else -np.inf
+
+    def same_feature_only(S, valid):  # runner-up searched within the best feature only
+        f, b, s1, _ = oracle.best_split(S, valid)
+        if f < 0:
+            return f, b, s1, -np.inf
+        row = np.where(valid[f], S[f], -np.inf).copy()
+        row[b] = -np.inf
+        return f, b, s1, float(row.max())
+
+    def best_twice(S, valid):         # the best itself reported as runner-up
+        f, b, s1, _ = oracle.best_split(S, valid)
+        return f, b, s1, s1
+
+    for bad in (unmasked, ties_dropped, same_feature_only, best_twice):
+        assert not _runner_up_pins_hold(bad), bad.__name__
 
 
 def test_partition_stable_and_terminal():
