@@ -325,6 +325,27 @@ int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t 
                           void* stream);
 
 /*
+ * sb_partition_rows_noalloc -- sb_partition_rows without a workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).
+ *
+ * Same arguments, results and checks as sb_partition_rows, minus ws and
+ * ws_bytes.  The scratch is a static device array of the library, 8 MiB per
+ * device (each GPU the library runs on holds it until the process ends),
+ * enough for n up to about 60 million rows: sizes whose workspace
+ * (sb_workspace_bytes(SB_CALL_PARTITION_ROWS, ...)) exceeds it return
+ * SB_E_UNSUPPORTED before any device work.  The call allocates nothing; its
+ * first call on a device looks up that device's copy of the array.  Every
+ * call on one GPU shares that array: calls that overlap in time on one GPU
+ * (different streams, other host threads) race and must be serialised by the
+ * caller.  Nothing in the scratch needs clearing between calls.
+ */
+int32_t sb_partition_rows_noalloc(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
+                                  const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
+                                  const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
+                                  int32_t* node_off_out, int32_t* build_list_out, void* stream);
+
+/*
  * sb_grow_tree -- the whole level loop for one tree (depth-wise growth).
  *
  * Runs, for level l = 0..depth-1: histograms (all rows at l = 0, bins read

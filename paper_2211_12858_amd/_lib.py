@@ -43,6 +43,7 @@ SYMBOLS = (
     "sb_subtract_histograms",
     "sb_score_splits",
     "sb_partition_rows",
+    "sb_partition_rows_noalloc",
     "sb_grow_tree",
     "sb_leaf_values",
     "sb_leaf_values_from_loss",
@@ -77,6 +78,7 @@ _PROTOS = {
     "sb_subtract_histograms": (_I32, [_P, _P, _I32, _I32, _I32, _I32, _P, _P]),
     "sb_score_splits": (_I32, [_P, _I32, _I32, _I32, _I32, _F64, _F64, _P, _P, _P, _P, _I64, _P]),
     "sb_partition_rows": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P, _P, _P, _P, _I64, _P]),
+    "sb_partition_rows_noalloc": (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _P, _P, _P, _P, _P]),
     "sb_grow_tree": (_I32, [_P, _I64, _P, _I64, _P, _I64, _I64, _I32, _I32, _P, _I64, _I32, _P, _I32, _F64, _F64,
                             _P, _P, _P, _P, _P, _P, _I64, _P]),
 }
@@ -202,6 +204,13 @@ def sb_partition_rows(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, be
                                            _ptr(best_feature), _ptr(best_bin), _ptr(row_idx_out),
                                            _ptr(node_off_out), _ptr(build_list_out), _ptr(ws), ws_bytes,
                                            _stream(stream)))
+
+
+def sb_partition_rows_noalloc(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature, best_bin,
+                              row_idx_out, node_off_out, build_list_out, stream=None):
+    return _check(load().sb_partition_rows_noalloc(_ptr(bins_cm), n, m, ld_cm, _ptr(row_idx_in), _ptr(node_off_in),
+                                                   n_nodes, _ptr(best_feature), _ptr(best_bin), _ptr(row_idx_out),
+                                                   _ptr(node_off_out), _ptr(build_list_out), _stream(stream)))
 
 
 def sb_grow_tree(bins4, ld4, bins_cm, ld_cm, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, depth, lam,

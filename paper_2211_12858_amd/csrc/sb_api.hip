@@ -378,24 +378,62 @@ int32_t sb_score_splits(const double* H, int32_t n_nodes, int32_t m, int32_t n_b
                       static_cast<hipStream_t>(stream));
 }
 
+}  // extern "C"
+
+namespace {
+
+int32_t check_partition(const char* call, const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
+                        const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
+                        const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
+                        int32_t* node_off_out, int32_t* build_list_out) {
+  const std::string c(call);
+  if (!bins_cm || !node_off_in || !best_feature || !best_bin || !row_idx_out || !node_off_out || !build_list_out)
+    return fail(SB_E_ARG, c + ": bins_cm, node_off_in, the splits and the outputs must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, c + ": n must be in [1, 2^31)");
+  if (m < 1) return fail(SB_E_ARG, c + ": m must be >= 1");
+  if (ld_cm < n) return fail(SB_E_SHAPE, c + ": ld_cm must be >= n");
+  if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, c + ": n_nodes must be in [1, 2^20]");
+  if (row_idx_in) {
+    const char* a0 = reinterpret_cast<const char*>(row_idx_in);
+    const char* b0 = reinterpret_cast<const char*>(row_idx_out);
+    if (a0 < b0 + n * 4 && b0 < a0 + n * 4) return fail(SB_E_SHAPE, c + ": row_idx_in and row_idx_out overlap");
+  }
+  return SB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int32_t sb_partition_rows(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
                           const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
                           const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
                           int32_t* node_off_out, int32_t* build_list_out, void* ws, int64_t ws_bytes,
                           void* stream) {
-  if (!bins_cm || !node_off_in || !best_feature || !best_bin || !row_idx_out || !node_off_out || !build_list_out)
-    return fail(SB_E_ARG, "sb_partition_rows: bins_cm, node_off_in, the splits and the outputs must not be NULL");
-  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_partition_rows: n must be in [1, 2^31)");
-  if (m < 1) return fail(SB_E_ARG, "sb_partition_rows: m must be >= 1");
-  if (ld_cm < n) return fail(SB_E_SHAPE, "sb_partition_rows: ld_cm must be >= n");
-  if (n_nodes < 1 || n_nodes > (1 << 20)) return fail(SB_E_ARG, "sb_partition_rows: n_nodes must be in [1, 2^20]");
-  if (row_idx_in) {
-    const char* a0 = reinterpret_cast<const char*>(row_idx_in);
-    const char* b0 = reinterpret_cast<const char*>(row_idx_out);
-    if (a0 < b0 + n * 4 && b0 < a0 + n * 4)
-      return fail(SB_E_SHAPE, "sb_partition_rows: row_idx_in and row_idx_out overlap");
-  }
-  int32_t rc = need_ws(ws, ws_bytes, partition_ws_bytes(n, n_nodes), "sb_partition_rows");
+  int32_t rc = check_partition("sb_partition_rows", bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes,
+                               best_feature, best_bin, row_idx_out, node_off_out, build_list_out);
+  if (rc) return rc;
+  rc = need_ws(ws, ws_bytes, partition_ws_bytes(n, n_nodes), "sb_partition_rows");
+  if (rc) return rc;
+  return launch_partition(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature, best_bin,
+                          row_idx_out, node_off_out, build_list_out, ws, static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_partition_rows_noalloc(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm,
+                                  const int32_t* row_idx_in, const int32_t* node_off_in, int32_t n_nodes,
+                                  const int32_t* best_feature, const int32_t* best_bin, int32_t* row_idx_out,
+                                  int32_t* node_off_out, int32_t* build_list_out, void* stream) {
+  const char* call = "sb_partition_rows_noalloc";
+  int32_t rc = check_partition(call, bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature,
+                               best_bin, row_idx_out, node_off_out, build_list_out);
+  if (rc) return rc;
+  const int64_t need = partition_ws_bytes(n, n_nodes);
+  if (need > PARTITION_SCRATCH_BYTES)
+    return fail(SB_E_UNSUPPORTED, std::string(call) + ": needs " + std::to_string(need) +
+                                      " bytes of scratch; the static scratch holds " +
+                                      std::to_string(PARTITION_SCRATCH_BYTES) + " (about 60 million rows)");
+  void* ws = nullptr;
+  rc = partition_scratch(&ws);
   if (rc) return rc;
   return launch_partition(bins_cm, n, m, ld_cm, row_idx_in, node_off_in, n_nodes, best_feature, best_bin,
                           row_idx_out, node_off_out, build_list_out, ws, static_cast<hipStream_t>(stream));

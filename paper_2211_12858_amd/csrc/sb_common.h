@@ -58,6 +58,10 @@ int32_t launch_score_node(const double* feat_s, const int32_t* feat_b, int32_t n
                           int32_t* best_b, double* best_s, hipStream_t st);
 
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes);
+// The static scratch of the allocation-free partition (8 MiB per device) and
+// its device address on the current device (looked up once per device).
+constexpr int64_t PARTITION_SCRATCH_BYTES = int64_t(8) << 20;
+int32_t partition_scratch(void** out);
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
                          int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,

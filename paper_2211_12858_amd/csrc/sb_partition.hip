@@ -23,10 +23,20 @@
 // level's node table (offsets, splits, left-count bases) into LDS, so that
 // finding a position's node is a search in LDS rather than a chain of
 // dependent global loads.
+#include <mutex>
+
 #include "sb_common.h"
 
 namespace sb {
 namespace {
+
+// Scratch of sb_partition_rows_noalloc: the partition's workspace as a
+// device array of the library, for callers that cannot allocate.  Each GPU
+// the library runs on holds its own copy until the process ends.  Host code
+// never passes the array's name to a kernel: it is a host-side stand-in, and
+// the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[PARTITION_SCRATCH_BYTES];
+constexpr int MAX_SCRATCH_DEVICES = 64;
 
 constexpr int PT_THREADS = 256;
 constexpr int PT_ITERS = 4;
@@ -361,6 +371,27 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
 }
 
 }  // namespace
+
+int32_t partition_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[MAX_SCRATCH_DEVICES] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+    return fail(SB_E_DEVICE, "sb_partition_rows_noalloc: no current HIP device");
+  if (dev >= MAX_SCRATCH_DEVICES)
+    return fail(SB_E_UNSUPPORTED, "sb_partition_rows_noalloc: device index " + std::to_string(dev) + " >= 64");
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SB_E_DEVICE, std::string("sb_partition_rows_noalloc: hipGetSymbolAddress failed: ") +
+                                   hipGetErrorString(e));
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return SB_OK;
+}
 
 // Workspace: [masks][tile_cnt][tile_off][Lb]
 int64_t partition_ws_bytes(int64_t n, int32_t n_nodes) {

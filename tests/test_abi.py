@@ -209,6 +209,29 @@ def test_partition_rejects(L, kw, code):
     assert _code(L.sb_partition_rows, *part_args(**kw)) == code
 
 
+def test_partition_noalloc_rejects(L):
+    """The allocation-free partition checks its arguments like sb_partition_rows and refuses sizes
+    beyond its static scratch before any device work."""
+    args = dict(bins_cm=F, n=1000, m=10, ld_cm=1000, row_idx_in=None, node_off_in=F, n_nodes=4, best_feature=F,
+                best_bin=F, row_idx_out=F, node_off_out=F, build_list_out=F, stream=0)
+
+    def call(**kw):
+        a = dict(args)
+        a.update(kw)
+        return _code(L.sb_partition_rows_noalloc, *a.values())
+
+    assert call(bins_cm=None) == 1
+    assert call(n=0) == 1
+    assert call(ld_cm=999) == 2
+    assert call(n_nodes=0) == 1
+    assert call(row_idx_in=F, row_idx_out=F + 100) == 2          # overlapping row buffers
+    n_big = (1 << 31) - 1                                          # needs ~280 MB of scratch
+    assert call(n=n_big, ld_cm=n_big) == 3
+    assert "static scratch" in L.sb_last_error()
+    assert L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=50_000_000, n_nodes=64) <= 8 << 20
+    assert L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=70_000_000, n_nodes=64) > 8 << 20
+
+
 def layout_args(**kw):
     a = dict(bins=F, n=1000, m=10, ld_bins=10, bins4=F, ld4=1000, bins_cm=None, ld_cm=0, rec=None, ld_rec=0,
              stream=0)
