@@ -203,27 +203,161 @@ def traffic_for_current_kernel(wl_name):
         return None
 
 
-def cpu_baseline(inp, wl, sample_rows):
-    """Time the oracle (as it stands) for one tree on the first sample_rows rows."""
+_POOL = {}
+
+
+def _pool_hist(task):
+    """One (node, feature range) histogram by the oracle, in a pool worker."""
     import oracle
-    ns = min(sample_rows, wl.n)
-    bins = inp.bins[:ns]
-    G = inp.G_T[:, :ns].T
-    h = inp.h[:ns]
+    j, f0, f1 = task
+    return j, f0, oracle.node_histograms(_POOL["bins"][:, f0:f1], _POOL["GH"], _POOL["segments"][j], _POOL["n_bins"])
+
+
+def oracle_tree_pooled(bins, GH, depth, lam, n_bins, min_child_weight, workers):
+    """oracle.grow_tree with its histogram step over a process pool.
+
+    Level by level, every node's histograms are computed by oracle.node_histograms
+    on feature ranges in `workers` processes (fork), then scored, chosen and
+    partitioned by the oracle's own split_scores / best_split / partition, in the
+    order of oracle.grow_tree.  Returns (features, bins, leaf segments)."""
+    import multiprocessing as mp
+    import oracle
+    n, m = bins.shape
+    step = max(1, -(-m // workers))
+    ranges = [(f0, min(m, f0 + step)) for f0 in range(0, m, step)]
+    segments = [np.arange(n, dtype=np.int64)]
+    feats, bs = [], []
+    ctx = mp.get_context("fork")
+    for _ in range(depth):
+        _POOL.update(bins=bins, GH=GH, segments=segments, n_bins=n_bins)
+        with ctx.Pool(workers) as pool:
+            parts = pool.map(_pool_hist, [(j, f0, f1) for j in range(len(segments)) for f0, f1 in ranges], chunksize=1)
+        H = [np.zeros((m, n_bins, GH.shape[1])) for _ in segments]
+        for j, f0, h in parts:
+            H[j][f0:f0 + h.shape[0]] = h
+        lf, lb, nxt = [], [], []
+        for j, rows in enumerate(segments):
+            S, valid = oracle.split_scores(H[j], lam, min_child_weight)
+            f, b, _, _ = oracle.best_split(S, valid)
+            left, right = oracle.partition(bins, rows, f, b)
+            lf.append(f)
+            lb.append(b)
+            nxt += [left, right]
+        feats.append(lf)
+        bs.append(lb)
+        segments = nxt
+    _POOL.clear()
+    return feats, bs, segments
+
+
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline_worker(path):
+    """Runs in a child process that never touches the GPU: the oracle timed on the
+    headline inputs (dumped by the parent), one tree on all rows with one thread,
+    and the same tree with the histogram step over a pool of all host cores."""
+    import oracle
+    meta = json.load(open(os.path.join(path, "meta.json")))
+    bins = np.load(os.path.join(path, "bins.npy"), mmap_mode="r")
+    G_T = np.load(os.path.join(path, "G_T.npy"), mmap_mode="r")
+    h = np.load(os.path.join(path, "h.npy"))
+    u = np.load(os.path.join(path, "u.npy"))
+    bins = np.ascontiguousarray(bins)
+    G = np.asarray(G_T).T
+    cores = len(os.sched_getaffinity(0))
     t0 = time.perf_counter()
-    GH, _, _, _ = oracle.sketch(wl.kind, G, h, wl.k, u=inp.u, Pi=inp.Pi)
-    oracle.grow_tree(bins, GH, wl.depth, wl.lam, wl.n_bins, wl.min_child_weight)
-    dt = time.perf_counter() - t0
-    scale = wl.n / ns
+    GH, _, _, _ = oracle.sketch(meta["kind"], G, h, meta["k"], u=u)
+    t_sketch = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    tree = oracle.grow_tree(bins, GH, meta["depth"], meta["lam"], meta["n_bins"], meta["mcw"])
+    t_one = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    feats, bs, segs = oracle_tree_pooled(bins, GH, meta["depth"], meta["lam"], meta["n_bins"], meta["mcw"], cores)
+    t_pool = time.perf_counter() - t0
+    same = all(list(tree["feature"][l]) == feats[l] and list(tree["bin"][l]) == bs[l] for l in range(meta["depth"]))
+    print(json.dumps({"sketch_s": t_sketch, "tree_1core_s": t_one, "tree_pool_s": t_pool, "cores": cores,
+                      "cpu_model": cpu_model(), "pool_tree_equal": bool(same)}), flush=True)
+
+
+def cpu_baseline(inp, wl):
+    """The oracle timed on this host in a child process (which never touches the GPU)."""
+    import shutil
+    import subprocess
+    import tempfile
+    path = tempfile.mkdtemp(prefix="sb_cpu_")
+    try:
+        np.save(os.path.join(path, "bins.npy"), inp.bins)
+        np.save(os.path.join(path, "G_T.npy"), inp.G_T)
+        np.save(os.path.join(path, "h.npy"), inp.h)
+        np.save(os.path.join(path, "u.npy"), inp.u)
+        json.dump({"kind": wl.kind, "k": wl.k, "depth": wl.depth, "lam": wl.lam, "n_bins": wl.n_bins,
+                   "mcw": wl.min_child_weight}, open(os.path.join(path, "meta.json"), "w"))
+        env = dict(os.environ, OMP_NUM_THREADS="1", OPENBLAS_NUM_THREADS="1", MKL_NUM_THREADS="1")
+        res = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-baseline-worker", path],
+                             capture_output=True, text=True, env=env, timeout=900)
+        if res.returncode != 0:
+            log("bench: cpu baseline worker failed: " + res.stderr[-2000:])
+            return None
+        r = json.loads(res.stdout.strip().splitlines()[-1])
+    finally:
+        shutil.rmtree(path, ignore_errors=True)
+    total_pool = r["sketch_s"] + r["tree_pool_s"]
     return {
-        "value": dt * scale,
+        "value": total_pool,
         "unit": "s/tree",
-        "cores": 1,
+        "cores": r["cores"],
         "kind": "oracle",
-        "sample": "one tree (sketch + %d levels) on the first %d of %d rows, %.2f s measured, scaled x%.1f "
-                  "(the oracle's work is linear in rows); numpy, single thread; host has %d cores"
-                  % (wl.depth, ns, wl.n, dt, scale, len(os.sched_getaffinity(0))),
+        "sample": "one whole tree (sketch + %d levels) on all %d rows of the headline workload, the oracle's "
+                  "histogram step over a process pool of %d workers (feature ranges per node), its sketch, "
+                  "scoring, choice and partition as in oracle.grow_tree; same tree as the one-thread run: %s"
+                  % (wl.depth, wl.n, r["cores"], r["pool_tree_equal"]),
+        "value_1core": r["sketch_s"] + r["tree_1core_s"],
+        "sketch_s": r["sketch_s"],
+        "cpu_model": r["cpu_model"],
     }
+
+
+def cold_mall_leg(ss, wl, G_T, h, u_all, Pi, L, trees=3):
+    """Histogram kernel with warm and with cold caches, on trees grown level by
+    level through the per-step calls (SplitSearch.grow_levelwise).  Cold: 1 GiB
+    is read and written between levels, more than the 256 MB Infinity Cache, so
+    each level's rows, records and sketch words come from HBM.  Returns the
+    histogram GB/s of both (algorithmic bytes over the kernel's event time)."""
+    import torch
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=ss.device)  # 1 GiB
+    flush.fill_(1.0)
+
+    def run(cold):
+        alg, ms = 0, 0.0
+        for t in range(trees):
+            ss.sketch(wl.kind, G_T, h, u=u_all[t], Pi=Pi)
+            L.sb_profile_begin()
+            ss.grow_levelwise(before_histograms=(lambda l: flush.mul_(1.0)) if cold else None)
+            torch.cuda.synchronize()
+            hist_ms, _ = L.sb_profile_end()
+            ms += hist_ms
+            alg += sum(hist_algorithmic_bytes(ss.leaf_off.cpu().numpy(), wl.depth, wl.m, wl.n_bins, wl.k + 1))
+        return alg / (ms * 1e-3) / 1e9, ms / trees
+
+    run(False)  # warm-up of the level-wise buffers
+    warm_gbps, warm_ms = run(False)
+    cold_gbps, cold_ms = run(True)
+    del flush
+    torch.cuda.empty_cache()
+    log("bench: histogram kernel warm %.0f GB/s (%.3f ms/tree), cold %.0f GB/s (%.3f ms/tree)"
+        % (warm_gbps, warm_ms, cold_gbps, cold_ms))
+    return {"warm_GBps": warm_gbps, "warm_ms_per_tree": warm_ms, "cold_GBps": cold_gbps,
+            "cold_ms_per_tree": cold_ms, "cold_frac_hbm_peak": cold_gbps / HBM_PEAK_GBPS,
+            "what": "trees grown level by level through sb_build_histograms / sb_subtract_histograms / "
+                    "sb_score_splits / sb_partition_rows; cold: 1 GiB streamed before every histogram launch"}
 
 
 def copy_probe(nbytes):
@@ -243,12 +377,17 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mc2m_rs5")
-    ap.add_argument("--cpu-sample-rows", type=int, default=800_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache histogram leg")
+    ap.add_argument("--cpu-baseline-worker", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--no-boost", action="store_true", help="skip the boosting-loop leg")
     ap.add_argument("--no-projection", action="store_true", help="skip the projection leg")
     ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
     args = ap.parse_args()
+    if args.cpu_baseline_worker:
+        sys.path.insert(0, HERE)
+        cpu_baseline_worker(args.cpu_baseline_worker)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -289,21 +428,27 @@ def main():
 
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
-    # the timed trees run without instrumentation: the per-launch events of
-    # the histogram profile add a pipeline drain around every histogram kernel
+    # the timed trees run without instrumentation beyond one event between
+    # trees: the per-launch events of the histogram profile add a pipeline
+    # drain around every histogram kernel
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     start.record()
     for s in range(K):
+        marks[s].record()
         ss.step(wl.kind, G_T, h, u=u_all[W + s], Pi=Pi)
+    marks[K].record()
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
+    tree_ms = np.array([marks[s].elapsed_time(marks[s + 1]) for s in range(K)])
     # the same K trees again with HIP events around every histogram launch
     L.sb_profile_begin()
     for s in range(K):
         ss.step(wl.kind, G_T, h, u=u_all[W + s], Pi=Pi)
     torch.cuda.synchronize()
     hist_ms, launches = L.sb_profile_end()
-    log("bench: %d trees in %.3f ms; histogram kernel %.3f ms over %d launches" % (K, total_ms, hist_ms, launches))
+    log("bench: %d trees in %.3f ms (median %.3f ms per tree); histogram kernel %.3f ms over %d launches"
+        % (K, total_ms, float(np.median(tree_ms)), hist_ms, launches))
 
     # algorithmic bytes of every timed histogram launch (trees are deterministic
     # in their uniforms, so replaying one reproduces its node sizes)
@@ -335,10 +480,12 @@ def main():
     leaf_bytes = leaf_algorithmic_bytes(wl.n, wl.d, 1 << wl.depth)
     log("bench: leaf values %.3f ms per tree" % leaf_ms)
 
+    cold = None if args.no_cold else cold_mall_leg(ss, wl, G_T, h, u_all, Pi, L)
     boost = None if args.no_boost else boost_leg(wl, inp, dev, L)
     proj = None if args.no_projection else projection_leg(dev, L)
 
-    sec_per_tree = total_ms / K / 1e3
+    med_ms = float(np.median(tree_ms))
+    sec_per_tree = med_ms / 1e3
     out = {
         "metric": METRIC,
         "value": sec_per_tree,
@@ -346,7 +493,7 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": total_ms / K,
+        "ms_per_step": med_ms,
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -357,6 +504,10 @@ def main():
                         "depth %d, lambda=%g" % (wl.name, wl.n, wl.m, wl.n_bins, wl.d, wl.kind.replace("_", " "),
                                                  wl.k, wl.depth, wl.lam),
         },
+        "tree_ms": {"median": med_ms, "p10": float(np.percentile(tree_ms, 10)),
+                    "p90": float(np.percentile(tree_ms, 90)), "mean": float(tree_ms.mean()),
+                    "mean_bracketed": total_ms / K, "trees": K,
+                    "what": "HIP events between consecutive trees on the stream; value is the median"},
         "hist_GBps": achieved,
         "hist_pct_peak": 100.0 * achieved / HBM_PEAK_GBPS,
         "hist_ms_per_tree": hist_ms / K,
@@ -392,13 +543,17 @@ def main():
                     % (1 << wl.depth, wl.d),
         },
     }
+    if cold is not None:
+        out["hist_cold_cache"] = cold
     if boost is not None:
         out["next"]["boosting"] = boost
     if proj is not None:
         out["next"]["projection"] = proj
     if not args.no_cpu_baseline:
-        log("bench: timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(inp, wl, args.cpu_sample_rows)
+        log("bench: timing the CPU oracle (one tree on all rows: one thread, then a pool of all cores)")
+        cb = cpu_baseline(inp, wl)
+        if cb is not None:
+            out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 

@@ -511,16 +511,20 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
                                    l < depth - 1);
     }
     if (rc) return rc;
-    if (fused)
+    // node splits: picked by the partition from the fused level end's
+    // per-feature results where it can, else by the scoring kernels first
+    const bool pick = fused && partition_picks_splits(n, nn);
+    if (fused && !pick)
       rc = launch_score_node(feat_s, feat_b, nn, m, tree_feature + base, tree_bin + base, tree_score + base, st);
-    else
+    else if (!fused)
       rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
                         tree_score + base, cws, st);
     if (rc) return rc;
     const bool last = l == depth - 1;
     rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,
                           level_rows(l + 1), last ? leaf_off_out : level_off(l + 1), level_build(l + 1), cws, st,
-                          last ? nullptr : pre);
+                          last ? nullptr : pre, pick ? feat_s : nullptr, pick ? feat_b : nullptr,
+                          pick ? tree_score + base : nullptr);
     if (rc) return rc;
   }
   return check_launch(call);

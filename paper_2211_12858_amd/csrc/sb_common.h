@@ -14,6 +14,40 @@ namespace sb {
 // A load of data that is streamed once: it does not allocate in the caches.
 __device__ inline float ld_stream(const float* p) { return __builtin_nontemporal_load(p); }
 
+// Best feature of one node from its per-feature results (score s_f, bin b_f;
+// b_f < 0: no valid threshold), by one wave: larger score first, then the
+// smaller feature.  Fixed reduction order, so every caller gets the same
+// answer.  Outputs (-1, -1, -inf) when no feature has a valid threshold.
+__device__ inline void wave_best_feature(const double* fs, const int32_t* fb, int m, int32_t* out_f, int32_t* out_b,
+                                         double* out_s) {
+  const int lane = threadIdx.x & 63;
+  double best_s = -INFINITY;
+  int best_f = -1, best_bin = -1;
+  auto better = [](double sa, int ia, double sb_, int ib) { return sa > sb_ || (sa == sb_ && ia < ib); };
+  for (int f = lane; f < m; f += 64) {
+    const int b = fb[f];
+    const double s = fs[f];
+    if (b >= 0 && (best_f < 0 || better(s, f, best_s, best_f))) {
+      best_s = s;
+      best_f = f;
+      best_bin = b;
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    const double os = __shfl_xor(best_s, off, 64);
+    const int of = __shfl_xor(best_f, off, 64);
+    const int ob = __shfl_xor(best_bin, off, 64);
+    if (of >= 0 && (best_f < 0 || better(os, of, best_s, best_f))) {
+      best_s = os;
+      best_f = of;
+      best_bin = ob;
+    }
+  }
+  *out_f = best_f;
+  *out_b = best_f >= 0 ? best_bin : -1;
+  *out_s = best_f >= 0 ? best_s : -INFINITY;
+}
+
 // ---------------------------------------------------------------- errors
 void set_error(const std::string& msg);
 int32_t fail(int32_t code, const std::string& msg);
@@ -62,10 +96,17 @@ int64_t partition_ws_bytes(int64_t n, int32_t n_nodes);
 // its device address on the current device (looked up once per device).
 constexpr int64_t PARTITION_SCRATCH_BYTES = int64_t(8) << 20;
 int32_t partition_scratch(void** out);
+// Splits come either as best_f/best_b (one per node, inputs), or, in the
+// level loop, as the fused level end's per-(node, feature) results
+// feat_s/feat_b: the partition then picks every node's best feature itself
+// and writes it to best_f/best_b/best_s (the tree's node results).  The
+// latter needs partition_picks_splits(n, n_nodes).
+bool partition_picks_splits(int64_t n, int32_t n_nodes);
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
                          int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,
-                         int64_t* next_pre = nullptr);
+                         int64_t* next_pre = nullptr, const double* feat_s = nullptr, const int32_t* feat_b = nullptr,
+                         double* best_s = nullptr);
 
 int64_t leaf_ws_bytes(int64_t n, int32_t d, int32_t n_leaves);
 int32_t launch_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* hess, int64_t ld_hess,

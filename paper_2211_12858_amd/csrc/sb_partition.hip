@@ -59,6 +59,14 @@ struct PartArgs {
   int32_t* tile_cnt;    // n_tiles
   int32_t* tile_off;    // n_tiles + 1 entries (last = total)
   int32_t* Lb;          // n_nodes + 1 entries
+  // level loop: per (node, feature) best score and bin of the fused level
+  // end; the flags kernel then picks each node's split and writes it (and
+  // its score) to best_f / best_b / best_s
+  const double* feat_s;
+  const int32_t* feat_b;
+  int32_t* out_f;
+  int32_t* out_b;
+  double* out_s;
   int64_t n;
   int32_t m, n_nodes, n_tiles;
 };
@@ -370,6 +378,298 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- two-kernel partition
+// For levels of up to PT_LDS_NODES nodes and PB_LDS_TILES tiles the level's
+// partition takes two kernels:
+//   k_part_flags_pick : the flags and tile counts of k_part_flags; in the
+//                       level loop it first picks the split of every node its
+//                       tile touches from the fused level end's per-feature
+//                       results (the argmax of k_score_node, same order), and
+//                       block b writes the split and score of the nodes
+//                       j = b (mod grid);
+//   k_part_scan_scatter : every block scans the tile counts into LDS, derives
+//                       the left-count bases Lb of the node boundaries it
+//                       needs from the ballots, and scatters its tile; block
+//                       0 also writes the child offsets, the build list and
+//                       the built-size prefix.
+// This replaces the one-block bounds kernel (and the node argmax kernel),
+// whose launches and dependent load chains dominated the small levels.
+
+// Exclusive scan over v(0..N-1) by one block of NT threads (NT / 64 waves),
+// as block_excl_scan; sh holds NT / 64 values.  Thread t owns the run
+// [t * per, (t + 1) * per) and reads each v(i) before it calls out(i, .), so
+// out may overwrite v's storage in place.
+template <int NT, typename V, typename O>
+__device__ int64_t block_scan_nt(int N, V v, O out, int64_t* sh) {
+  const int per = (N + NT - 1) / NT;
+  const int p0 = threadIdx.x * per;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int64_t local = 0;
+  for (int i = 0; i < per; ++i)
+    if (p0 + i < N) local += v(p0 + i);
+  int64_t incl = local;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  __syncthreads();
+  if (lane == 63) sh[wave] = incl;
+  __syncthreads();
+  int64_t wbase = 0, total = 0;
+  for (int w = 0; w < NT / 64; ++w) {
+    const int64_t x = sh[w];
+    if (w < wave) wbase += x;
+    total += x;
+  }
+  int64_t run = wbase + incl - local;
+  for (int i = 0; i < per; ++i)
+    if (p0 + i < N) {
+      const int64_t x = v(p0 + i);
+      out(p0 + i, run);
+      run += x;
+    }
+  return total;
+}
+
+template <bool PICK>
+__global__ void __launch_bounds__(PT_THREADS) k_part_flags_pick(PartArgs a) {
+  __shared__ int32_t wsum[PT_THREADS / 64];
+  extern __shared__ int32_t pt_nodes[];  // [off: n_nodes + 1][f: n_nodes][b: n_nodes]
+  const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int64_t row[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    const int64_t ic = i < a.n ? i : a.n - 1;
+    row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
+  }
+  const NodeTab<true> tab = stage_offsets<true>(a, pt_nodes);
+  int32_t* sf = pt_nodes + a.n_nodes + 1;
+  int32_t* sb = sf + a.n_nodes;
+  if constexpr (PICK) {
+    __syncthreads();  // offsets staged
+    // the nodes this tile touches
+    const int64_t last_pos = (t0 + PT_TILE < a.n ? t0 + PT_TILE : a.n) - 1;
+    const int ja = find_node<true>(tab, a.n_nodes, t0), jb = find_node<true>(tab, a.n_nodes, last_pos);
+    for (int j = ja + wave; j <= jb; j += PT_THREADS / 64) {
+      int32_t f, b;
+      double sc;
+      wave_best_feature(a.feat_s + (int64_t)j * a.m, a.feat_b + (int64_t)j * a.m, a.m, &f, &b, &sc);
+      if (lane == 0) {
+        sf[j] = f;
+        sb[j] = b;
+      }
+    }
+    // this block's share of the node results
+    for (int j = blockIdx.x + wave * gridDim.x; j < a.n_nodes; j += (PT_THREADS / 64) * gridDim.x) {
+      int32_t f, b;
+      double sc;
+      wave_best_feature(a.feat_s + (int64_t)j * a.m, a.feat_b + (int64_t)j * a.m, a.m, &f, &b, &sc);
+      if (lane == 0) {
+        a.out_f[j] = f;
+        a.out_b[j] = b;
+        a.out_s[j] = sc;
+      }
+    }
+  } else {
+    for (int j = threadIdx.x; j < a.n_nodes; j += PT_THREADS) {
+      sf[j] = a.best_f[j];
+      sb[j] = a.best_b[j];
+    }
+  }
+  __syncthreads();
+  const int64_t first = tab.at(0), last = tab.at(a.n_nodes);
+  int32_t f_of[PT_ITERS], b_of[PT_ITERS];
+  int j = find_node<true>(tab, a.n_nodes, t0 + threadIdx.x);
+  int64_t jend = tab.at(j + 1);
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    while (i >= jend && j < a.n_nodes - 1) {
+      ++j;
+      jend = tab.at(j + 1);
+    }
+    const int32_t f = sf[j];
+    const bool live = i < a.n && i >= first && i < last;
+    f_of[it] = (!live) ? -2 : ((f < 0 || f >= a.m) ? -1 : f);
+    b_of[it] = sb[j];
+  }
+  uint32_t bin[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t r = row[it] < 0 ? 0 : (row[it] >= a.n ? a.n - 1 : row[it]);
+    bin[it] = f_of[it] >= 0 ? a.bins_cm[(int64_t)f_of[it] * a.ld_cm + r] : 0u;
+  }
+  int cnt = 0;
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const bool left = f_of[it] == -1 || (f_of[it] >= 0 && (int32_t)bin[it] <= b_of[it]);
+    const uint64_t mask = __ballot(left);
+    if (lane == 0) {
+      a.masks[(int64_t)blockIdx.x * PT_MASKS + it * (PT_THREADS / 64) + wave] = mask;
+      cnt += popc64(mask);
+    }
+  }
+  if (lane == 0) wsum[wave] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < PT_THREADS / 64; ++w) s += wsum[w];
+    a.tile_cnt[blockIdx.x] = s;
+  }
+}
+
+__global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
+  __shared__ uint64_t mk[PT_MASKS];
+  __shared__ int32_t pre[PT_MASKS];
+  __shared__ int64_t sh[PT_THREADS / 64];
+  __shared__ int32_t span[2];
+  extern __shared__ int32_t pt_lds[];  // [toff: n_tiles][off: n_nodes + 1][lb: n_nodes + 1]
+  int32_t* s_toff = pt_lds;
+  int32_t* s_off = s_toff + a.n_tiles;
+  int32_t* s_lb = s_off + a.n_nodes + 1;
+  const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int64_t row[PT_ITERS];
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it) {
+    const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
+    const int64_t ic = i < a.n ? i : a.n - 1;
+    row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
+  }
+  for (int j = threadIdx.x; j <= a.n_nodes; j += PT_THREADS) s_off[j] = (int32_t)off_at(a, j);
+  uint64_t my_mask = 0;
+  if (wave == 0 && lane < PT_MASKS) my_mask = a.masks[(int64_t)blockIdx.x * PT_MASKS + lane];
+  // 1. exclusive prefix of the tile counts (every block its own copy): the
+  // counts are staged into LDS with eight loads in flight per thread, then
+  // each thread scans a contiguous run of them in place
+  for (int t0s = 0; t0s < a.n_tiles; t0s += 8 * PT_THREADS) {
+    int32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0s + u * PT_THREADS + threadIdx.x;
+      v[u] = t < a.n_tiles ? a.tile_cnt[t] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0s + u * PT_THREADS + threadIdx.x;
+      if (t < a.n_tiles) s_toff[t] = v[u];
+    }
+  }
+  __syncthreads();
+  const int64_t total = block_scan_nt<PT_THREADS>(
+      a.n_tiles, [&](int t) -> int64_t { return s_toff[t]; }, [&](int t, int64_t p) { s_toff[t] = (int32_t)p; }, sh);
+  __syncthreads();  // s_toff complete
+  // this tile's ballots and their prefix
+  if (wave == 0) {
+    const int32_t c = popc64(my_mask);
+    int32_t incl = c;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int32_t o = __shfl_up(incl, off, 64);
+      if (lane >= off) incl += o;
+    }
+    if (lane < PT_MASKS) {
+      mk[lane] = my_mask;
+      pre[lane] = s_toff[blockIdx.x] + incl - c;
+    }
+  }
+  __syncthreads();
+  const NodeTab<true> tab{s_off, a.n};
+  // 2. the node boundaries this block needs: all of them in block 0 (it
+  // writes the level's bounds), else those of the nodes its tile touches
+  if (threadIdx.x == 0) {
+    if (blockIdx.x == 0) {
+      span[0] = 0;
+      span[1] = a.n_nodes;
+    } else {
+      const int64_t last_pos = (t0 + PT_TILE < a.n ? t0 + PT_TILE : a.n) - 1;
+      span[0] = find_node<true>(tab, a.n_nodes, t0);
+      span[1] = find_node<true>(tab, a.n_nodes, last_pos) + 1;
+    }
+  }
+  __syncthreads();
+  const int J0 = span[0], J1 = span[1];
+  // Lb_j = left flags before position off[j]: the tile offset of its tile
+  // plus the popcounts of the ballots before it.  PT_MASKS consecutive lanes
+  // share a boundary (one ballot each) and add their counts with shuffles.
+  static_assert(PT_THREADS % PT_MASKS == 0 && 64 % PT_MASKS == 0, "a boundary's ballots share one wave");
+  const int nb = J1 - J0 + 1;
+  for (int e0 = 0; e0 < nb * PT_MASKS; e0 += PT_THREADS) {
+    const int e = e0 + threadIdx.x;
+    const int jb = J0 + e / PT_MASKS, q = e % PT_MASKS;
+    int32_t c = 0;
+    int64_t tx = 0;
+    bool in = false;
+    if (e < nb * PT_MASKS) {
+      const int64_t x = s_off[jb];
+      tx = x / PT_TILE;
+      in = tx < a.n_tiles;
+      if (in) {
+        const int w = (int)(x - tx * PT_TILE);
+        if (q < (w >> 6) || (q == (w >> 6) && (w & 63))) {
+          const uint64_t mq = a.masks[tx * PT_MASKS + q];
+          c = q < (w >> 6) ? popc64(mq) : popc64(mq & ((uint64_t(1) << (w & 63)) - 1));
+        }
+      }
+    }
+    for (int o = PT_MASKS / 2; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
+    if (e < nb * PT_MASKS && q == 0) s_lb[jb] = in ? s_toff[tx] + c : (int32_t)total;
+  }
+  __syncthreads();
+  // 3. block 0: child offsets, build list and the built-size prefix
+  if (blockIdx.x == 0) {
+    for (int j = threadIdx.x; j < a.n_nodes; j += PT_THREADS) {
+      int64_t size;
+      const int64_t o0 = s_off[j];
+      const int64_t nl = node_left(o0, s_off[j + 1], s_lb[j], s_lb[j + 1], &size);
+      a.off_out[2 * j] = (int32_t)o0;
+      a.off_out[2 * j + 1] = (int32_t)(o0 + nl);
+      a.build_out[j] = (nl <= size - nl) ? 2 * j : 2 * j + 1;
+    }
+    if (threadIdx.x == 0) a.off_out[2 * a.n_nodes] = s_off[a.n_nodes];
+    if (a.next_pre) {
+      const int64_t total_built = block_scan_nt<PT_THREADS>(
+          a.n_nodes,
+          [&](int j) -> int64_t {
+            int64_t size;
+            const int64_t nl = node_left(s_off[j], s_off[j + 1], s_lb[j], s_lb[j + 1], &size);
+            return nl <= size - nl ? nl : size - nl;
+          },
+          [&](int j, int64_t p) { a.next_pre[j] = p; }, sh);
+      if (threadIdx.x == 0) a.next_pre[a.n_nodes] = total_built;
+    }
+  }
+  // 4. scatter of the tile
+  const int64_t first = tab.at(0), last = tab.at(a.n_nodes);
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  int64_t i = t0 + threadIdx.x;
+  int j = find_node<true>(tab, a.n_nodes, i);
+  int64_t jstart = tab.at(j), jend = tab.at(j + 1);
+  int64_t lbj = s_lb[j], nleft = (int64_t)s_lb[j + 1] - lbj;
+#pragma unroll
+  for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
+    if (i < a.n && i >= first && i < last) {
+      while (i >= jend && j < a.n_nodes - 1) {
+        ++j;
+        jstart = jend;
+        jend = tab.at(j + 1);
+        lbj = s_lb[j];
+        nleft = (int64_t)s_lb[j + 1] - lbj;
+      }
+      const int q = it * (PT_THREADS / 64) + wave;
+      const uint64_t m = mk[q];
+      const bool left = (m >> lane) & 1u;
+      const int64_t L = (int64_t)pre[q] + popc64(m & below);
+      const int64_t rw = row[it] < 0 ? 0 : (row[it] >= a.n ? a.n - 1 : row[it]);
+      const int64_t lrel = L - lbj;
+      int64_t dest = left ? jstart + lrel : jstart + nleft + (i - jstart) - lrel;
+      dest = dest < 0 ? 0 : (dest >= a.n ? a.n - 1 : dest);
+      a.row_out[dest] = (int32_t)rw;
+    }
+  }
+}
+
 }  // namespace
 
 int32_t partition_scratch(void** out) {
@@ -399,10 +699,15 @@ int64_t partition_ws_bytes(int64_t n, int32_t n_nodes) {
   return align256(tiles * PT_MASKS * 8) + 2 * align256((tiles + 1) * 4) + align256((int64_t)(n_nodes + 1) * 4);
 }
 
+bool partition_picks_splits(int64_t n, int32_t n_nodes) {
+  const int64_t tiles = (n + PT_TILE - 1) / PT_TILE;
+  return n_nodes <= PT_LDS_NODES && tiles <= PB_LDS_TILES;
+}
+
 int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t ld_cm, const int32_t* row_in,
                          const int32_t* off_in, int32_t n_nodes, const int32_t* best_f, const int32_t* best_b,
                          int32_t* row_out, int32_t* off_out, int32_t* build_out, void* ws, hipStream_t st,
-                         int64_t* next_pre) {
+                         int64_t* next_pre, const double* feat_s, const int32_t* feat_b, double* best_s) {
   const int64_t tiles = (n + PT_TILE - 1) / PT_TILE;
   PartArgs a{};
   a.bins_cm = bins_cm;
@@ -427,6 +732,22 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
   a.m = m;
   a.n_nodes = n_nodes;
   a.n_tiles = (int32_t)tiles;
+  if (partition_picks_splits(n, n_nodes)) {
+    const size_t lf = (size_t)(3 * n_nodes + 1) * 4, ls = (size_t)(tiles + 2 * (n_nodes + 1)) * 4;
+    if (feat_s) {
+      a.feat_s = feat_s;
+      a.feat_b = feat_b;
+      a.out_f = const_cast<int32_t*>(best_f);
+      a.out_b = const_cast<int32_t*>(best_b);
+      a.out_s = best_s;
+      hipLaunchKernelGGL(k_part_flags_pick<true>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);
+    } else {
+      hipLaunchKernelGGL(k_part_flags_pick<false>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);
+    }
+    hipLaunchKernelGGL(k_part_scan_scatter, dim3((unsigned)tiles), dim3(PT_THREADS), ls, st, a);
+    return check_launch("sb_partition_rows");
+  }
+  if (feat_s) return fail(SB_E_UNSUPPORTED, "partition: picking splits needs <= 2048 nodes and <= 8192 tiles");
   if (n_nodes <= PT_LDS_NODES) {
     const size_t lf = (size_t)(3 * n_nodes + 1) * 4, ls = (size_t)(2 * n_nodes + 2) * 4;
     hipLaunchKernelGGL(k_part_flags<true>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);

@@ -119,32 +119,14 @@ k_score_feature(const double* __restrict__ H, int n_nodes, int m, int B, int k, 
 __global__ void __launch_bounds__(64)
 k_score_node(const double* __restrict__ ws_s, const int32_t* __restrict__ ws_b, int m, int32_t* __restrict__ bf,
              int32_t* __restrict__ bb, double* __restrict__ bs) {
-  const int j = blockIdx.x, lane = threadIdx.x;
-  double best_s = -INFINITY;
-  int best_f = -1, best_bin = -1;
-  for (int f = lane; f < m; f += 64) {
-    const int b = ws_b[(int64_t)j * m + f];
-    const double s = ws_s[(int64_t)j * m + f];
-    if (b >= 0 && (best_f < 0 || better(s, f, best_s, best_f))) {
-      best_s = s;
-      best_f = f;
-      best_bin = b;
-    }
-  }
-  for (int off = 32; off > 0; off >>= 1) {
-    const double os = __shfl_xor(best_s, off, 64);
-    const int of = __shfl_xor(best_f, off, 64);
-    const int ob = __shfl_xor(best_bin, off, 64);
-    if (of >= 0 && (best_f < 0 || better(os, of, best_s, best_f))) {
-      best_s = os;
-      best_f = of;
-      best_bin = ob;
-    }
-  }
-  if (lane == 0) {
-    bf[j] = best_f;
-    bb[j] = best_f >= 0 ? best_bin : -1;
-    bs[j] = best_f >= 0 ? best_s : -INFINITY;
+  const int j = blockIdx.x;
+  int32_t f, b;
+  double s;
+  wave_best_feature(ws_s + (int64_t)j * m, ws_b + (int64_t)j * m, m, &f, &b, &s);
+  if (threadIdx.x == 0) {
+    bf[j] = f;
+    bb[j] = b;
+    bs[j] = s;
   }
 }
 

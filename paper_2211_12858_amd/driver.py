@@ -114,6 +114,53 @@ class SplitSearch:
         self.sketch(kind, G_T, h, u, Pi, stream)
         self.grow(stream)
 
+    def grow_levelwise(self, before_histograms=None, stream=None):
+        """The same tree as grow(), through the per-step calls, level by level:
+        sb_build_histograms (the built nodes), sb_subtract_histograms (their
+        siblings), sb_score_splits and sb_partition_rows.  before_histograms(l),
+        if given, runs before level l's histogram call (bench.py streams a
+        large buffer there to take the level's data out of the caches)."""
+        n, m, B, k, c, D = self.n, self.m, self.n_bins, self.k, self.c, self.depth
+        dev = self.device
+        maxn = 1 << (D - 1)
+        if getattr(self, "_lw", None) is None:
+            cells = maxn * m * c * B
+            self._lw = {
+                "H": [torch.empty(cells, dtype=torch.float64, device=dev) for _ in range(2)],
+                "rows": [torch.empty(n, dtype=torch.int32, device=dev) for _ in range(2)],
+                "off": [torch.empty((1 << l) + 1, dtype=torch.int32, device=dev) for l in range(D + 1)],
+                "build": [torch.empty(max(1, (1 << l) // 2), dtype=torch.int32, device=dev) for l in range(D + 1)],
+                "ws_h": workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=B, k=k,
+                                                       n_nodes=maxn), dev),
+                "ws_s": workspace(L.sb_workspace_bytes(L.SB_CALL_SCORE_SPLITS, m=m, n_nodes=2 * maxn), dev),
+                "ws_p": workspace(L.sb_workspace_bytes(L.SB_CALL_PARTITION_ROWS, n=n, n_nodes=2 * maxn), dev),
+            }
+            self._lw["off"][0].copy_(torch.tensor([0, n], dtype=torch.int32))
+        w = self._lw
+        rows_in = None
+        for l in range(D):
+            nn = 1 << l
+            H, Hp = w["H"][l & 1], w["H"][(l - 1) & 1]
+            if before_histograms is not None:
+                before_histograms(l)
+            if l == 0:
+                L.sb_build_histograms(self.bins4, n, None, 0, n, m, B, self.GH, self.ld_gh, k, self.qexp, None,
+                                      w["off"][0], 1, None, 1, H, w["ws_h"], w["ws_h"].numel(), stream)
+            else:
+                L.sb_build_histograms(None, 0, self.rec, self.ld_rec, n, m, B, self.GH, self.ld_gh, k, self.qexp,
+                                      rows_in, w["off"][l], nn, w["build"][l], nn // 2, H, w["ws_h"],
+                                      w["ws_h"].numel(), stream)
+                L.sb_subtract_histograms(Hp, H, nn // 2, m, B, k, w["build"][l], stream)
+            base = nn - 1
+            tf, tb, ts = self.tree_feature[base:base + nn], self.tree_bin[base:base + nn], self.tree_score[base:base + nn]
+            L.sb_score_splits(H, nn, m, B, k, self.lam, self.mcw, tf, tb, ts, w["ws_s"], w["ws_s"].numel(), stream)
+            last = l == D - 1
+            rows_out = self.row_idx if last else w["rows"][l & 1]
+            off_out = self.leaf_off if last else w["off"][l + 1]
+            L.sb_partition_rows(self.bins_cm, n, m, n, rows_in, w["off"][l], nn, tf, tb, rows_out, off_out,
+                                w["build"][l + 1], w["ws_p"], w["ws_p"].numel(), stream)
+            rows_in = rows_out
+
     # ------------------------------------------------------------ leaf values
     def leaf_values(self, G_T, hess_T=None, h=None, stream=None):
         """Leaf values of the last grown tree from the full G (eq. 3): self.V, (2^depth, d) fp64.

@@ -126,3 +126,29 @@ def test_tree_deterministic_repeat():
             for x, y in zip(a[key], b[key]):
                 assert np.array_equal(x, y)
         assert np.array_equal(a["row_idx"], b["row_idx"])
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("mc200k_top5", {}),
+    ("mc2m_rs5", dict(n=300_000)),
+    ("ml1m_top10", dict(n=100_000, depth=7)),
+])
+def test_per_step_calls_grow_the_same_tree(name, kw):
+    """The level loop of sb_grow_tree (fused level end, splits picked by the
+    partition) against the per-step calls sb_build_histograms /
+    sb_subtract_histograms / sb_score_splits / sb_partition_rows level by level:
+    the same fixed-point sums and the same fp64 scoring, so the trees, their
+    scores and the leaf rows are identical bit for bit."""
+    wl = workload(name, **kw)
+    inp = make_inputs(wl)
+    ss = grow_on_device(inp, wl.kind, wl.k, wl.depth, wl.lam, wl.min_child_weight)
+    fused = ss.tree()
+    ss.grow_levelwise()
+    gu.sync()
+    steps = ss.tree()
+    for l in range(wl.depth):
+        assert np.array_equal(fused["feature"][l], steps["feature"][l]), l
+        assert np.array_equal(fused["bin"][l], steps["bin"][l]), l
+        assert np.array_equal(fused["score"][l].view(np.uint64), steps["score"][l].view(np.uint64)), l
+    assert np.array_equal(fused["row_idx"], steps["row_idx"])
+    assert np.array_equal(fused["leaf_off"], steps["leaf_off"])
