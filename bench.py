@@ -383,6 +383,8 @@ def main():
     ap.add_argument("--no-boost", action="store_true", help="skip the boosting-loop leg")
     ap.add_argument("--no-projection", action="store_true", help="skip the projection leg")
     ap.add_argument("--copy-probe", type=int, default=0, help="only run a plain copy of this many bytes")
+    ap.add_argument("--projection-only", action="store_true",
+                    help="only the projection leg (2M x 1000 -> 20), for profiling its kernels")
     args = ap.parse_args()
     if args.cpu_baseline_worker:
         sys.path.insert(0, HERE)
@@ -396,6 +398,13 @@ def main():
         sys.exit(2)
     if args.copy_probe:
         copy_probe(args.copy_probe)
+        return
+    if args.projection_only:
+        import torch
+        sys.path.insert(0, HERE)
+        from paper_2211_12858_amd import _lib as L
+        L.load()
+        print(json.dumps(projection_leg(torch.device("cuda:0"), L)), flush=True)
         return
 
     import torch

@@ -16,8 +16,11 @@
 //    channel changes (each below 2^31 in magnitude, so the split is exact)
 //    and adds them into int64 register totals;
 //  * a workgroup owns one feature slice and a contiguous range of the rows of
-//    the built nodes, taken in build-list order; it writes one int64 partial
-//    per node it touched;
+//    the built nodes, taken in build-list order; it writes one partial per
+//    node it touched: every channel sum as an int32 when it fits (almost
+//    always: a workgroup's sum of one bin exceeds 2^31 only past 8192 rows
+//    of full-scale values in that bin), else an escape value and the exact
+//    int64 pair in an overflow slot of the same index;
 //  * the reduce kernels sum the partials of each node (integers, so the
 //    result is independent of the grid) and write the fp64 histogram.  Sums
 //    of fixed-point values are exact in fp64, which makes sibling
@@ -84,8 +87,9 @@ HistPlan hist_plan(int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool t
   return p;  // more than ROT_MAX_C channels or 256 bins: unsupported (nq = 0)
 }
 
-// Workspace: [pre: n_build+1 int64][partials: slices * slots * cells int64]
-// [quantised rows: n * 16 * cg bytes, with quant_rows only]
+// Workspace: [pre: n_build+1 int64][partials: slices * slots * cells int32]
+// [overflow: slices * slots * cells int64][quantised rows: n * 16 * cg bytes,
+// with quant_rows only]
 int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n_build, bool quant_rows) {
   HistPlan p = hist_plan(m, n_bins, k, n_build, false);
   if (p.nq == 0) return -1;  // unsupported shape
@@ -93,10 +97,16 @@ int64_t hist_ws_bytes(int64_t n, int32_t m, int32_t n_bins, int32_t k, int32_t n
   int64_t part = (int64_t)p.slices * p.slots * p.cells;
   if ((int64_t)pt.slices * pt.slots * pt.cells > part) part = (int64_t)pt.slices * pt.slots * pt.cells;
   const int64_t q = quant_rows ? align256(n * 16 * p.cg) : 0;
-  return align256((int64_t)(n_build + 1) * 8) + align256(part * 8) + q;
+  return align256((int64_t)(n_build + 1) * 8) + align256(part * 4) + align256(part * 8) + q;
 }
 
 namespace {
+
+// Escape value of an int32 partial: the cell's exact int64 sum is in the
+// overflow slot of the same index.  INT32_MIN itself is escaped too.
+constexpr int32_t PART_ESC = INT32_MIN;
+
+__device__ inline bool fits_partial(int64_t v) { return v > (int64_t)INT32_MIN && v <= (int64_t)INT32_MAX; }
 
 struct HistArgs {
   const uint32_t* bins4;
@@ -111,7 +121,8 @@ struct HistArgs {
   const int32_t* node_off;
   const int32_t* build_list;
   int64_t* pre;
-  int64_t* partial;
+  int32_t* part32;  // partials, one int32 per channel cell (PART_ESC: see ovf)
+  int64_t* ovf;     // exact int64 partials of the escaped cells, same index
   double* H;
   const double* Hp;  // parent level, for the fused sibling subtraction (may be null)
   bool store_h;      // fused level end: write H (skipped at a tree's last level, whose H has no reader)
@@ -593,7 +604,9 @@ __device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds6
     lds_barrier();
     fold_cells<ROT_CPT, ROT_THREADS>(lds64, tot);
     lds_barrier();  // every fold read is done: the LDS becomes the staging area
-    longlong2* dst = reinterpret_cast<longlong2*>(a.partial + ((int64_t)s * a.slots + q + p) * a.cells);
+    const int64_t slot = ((int64_t)s * a.slots + q + p) * a.cells;  // channel cells
+    int2* dst = reinterpret_cast<int2*>(a.part32 + slot);
+    longlong2* dov = reinterpret_cast<longlong2*>(a.ovf + slot);
     // this channel group's pairs are pairs 3 grp .. 3 grp + P - 1 of the
     // slot; pairs past the last (a short final group) are not written
 #pragma unroll 1
@@ -615,7 +628,10 @@ __device__ __forceinline__ void hist_rot_group(const HistArgs& a, uint64_t* lds6
           x.x += y.x;
           x.y += y.y;
         }
-        dst[(int64_t)(ROT_PMAX * grp + pr) * ROT_F * B + e] = x;
+        const int64_t at = (int64_t)(ROT_PMAX * grp + pr) * ROT_F * B + e;
+        const bool fx = fits_partial(x.x), fy = fits_partial(x.y);
+        dst[at] = make_int2(fx ? (int32_t)x.x : PART_ESC, fy ? (int32_t)x.y : PART_ESC);
+        if (!(fx && fy)) dov[at] = x;
       }
       lds_barrier();
     }
@@ -690,20 +706,33 @@ __global__ void __launch_bounds__(256) k_hist_reduce(HistArgs a) {
   if (hi > lo) {
     const int32_t qn = groups_of(a, s);
     const int64_t qlo = group_of(lo, T, qn), qhi = group_of(hi - 1, T, qn);
-    const int64_t* src = a.partial + ((int64_t)s * a.slots + p) * a.cells + e;
-    if (T >= qn) {
-      // every row group holds at least one position: independent loads, four sums
-      int64_t acc[4] = {0, 0, 0, 0};
-      int64_t q = qlo;
-      for (; q + 4 <= qhi + 1; q += 4) {
+    const int64_t base = ((int64_t)s * a.slots + p) * a.cells + e;
+    const int32_t* src = a.part32 + base;
+    const int64_t* ov = a.ovf + base;
+    const bool dense = T >= qn;  // every row group holds at least one position
+    auto live = [&](int64_t q) { return q <= qhi && (dense || q * T / qn < (q + 1) * T / qn); };
+    // batches of eight row groups, loads unconditional (clamped to the last
+    // group, dropped past it); escapes are flagged, and a thread that met one
+    // sums again with the overflow slots
+    bool esc = false;
+    for (int64_t q = qlo; q <= qhi; q += 8) {
+      int32_t v[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) acc[u] += src[(q + u) * a.cells];
+      for (int u = 0; u < 8; ++u) v[u] = src[(q + u <= qhi ? q + u : qhi) * a.cells];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bool use = live(q + u);
+        sum += use ? v[u] : 0;
+        esc |= use && v[u] == PART_ESC;
       }
-      for (; q <= qhi; ++q) acc[0] += src[q * a.cells];
-      sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-    } else {
+    }
+    if (esc) {
+      sum = 0;
       for (int64_t q = qlo; q <= qhi; ++q)
-        if (q * T / qn < (q + 1) * T / qn) sum += src[q * a.cells];
+        if (live(q)) {
+          const int32_t x = src[q * a.cells];
+          sum += x == PART_ESC ? ov[q * a.cells] : (int64_t)x;
+        }
     }
   }
   const int64_t cpn = (int64_t)a.m * a.c * a.n_bins;
@@ -762,90 +791,89 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
   const int32_t qn = groups_of(a, s);
   const int64_t qlo = hi > lo ? group_of(lo, T, qn) : 0, qhi = hi > lo ? group_of(hi - 1, T, qn) : -1;
   const bool dense = T >= qn;  // every row group holds at least one position
-  // int64 channel sums of this bin over the node's row groups: the loads of
-  // four groups and every channel pair are in flight together
+  // int64 channel sums of this bin over the node's row groups, from the
+  // int32 partials.  Fast path: batches of BQ row groups and every channel
+  // pair, double-buffered (the next batch's loads are issued before this
+  // batch is added, so a node of many row groups waits for about one memory
+  // latency, not one per batch), loads unconditional (groups past the node's
+  // last and pairs past the last repeat it; the extra values are dropped),
+  // no branch on the values: escapes are only flagged.  A lane that met an
+  // escape sums its bin again with the overflow slots (rare: a workgroup's
+  // sum of one bin must pass 2^31).
   int64_t acc_lo[PMAX], acc_hi[PMAX];
 #pragma unroll
   for (int pr = 0; pr < PMAX; ++pr) acc_lo[pr] = acc_hi[pr] = 0;
-  if (on) {
+  if (on && qlo <= qhi) {
     const int64_t e64 = (int64_t)fl * B + bin;
-    const longlong2* src = reinterpret_cast<const longlong2*>(a.partial + ((int64_t)s * a.slots + p) * a.cells) + e64;
-    const int64_t stride = a.cells / 2;  // one row group, in 16-byte cells
-    int64_t q = qlo;
-    if (dense && q + 4 <= qhi + 1) {
-      // batches of four row groups, every channel pair, double-buffered: the
-      // next batch's loads are issued before this batch is added, so a node
-      // of many row groups waits for about one memory latency, not one per
-      // batch.  The loads are unconditional (pairs past the last repeat it
-      // and are dropped), so the compiler issues them all before any wait.
-      auto load4 = [&](int64_t q0, longlong2 (&v)[4][PMAX]) {
+    const int64_t base = ((int64_t)s * a.slots + p) * a.cells;
+    const int2* src = reinterpret_cast<const int2*>(a.part32 + base) + e64;
+    const longlong2* ov = reinterpret_cast<const longlong2*>(a.ovf + base) + e64;
+    const int64_t stride = a.cells / 2;  // one row group, in channel pairs
+    auto live = [&](int64_t q) { return q <= qhi && (dense || q * T / qn < (q + 1) * T / qn); };
+    bool esc = false;
+    if (dense) {
+      constexpr int BQ = PMAX <= 4 ? 8 : 4;
+      auto load = [&](int64_t q0, int2 (&v)[BQ][PMAX]) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < BQ; ++u)
 #pragma unroll
           for (int pr = 0; pr < PMAX; ++pr)
-            v[u][pr] = src[(q0 + u) * stride + (int64_t)(pr < a.pairs ? pr : a.pairs - 1) * FB];
+            v[u][pr] = src[(q0 + u <= qhi ? q0 + u : qhi) * stride + (int64_t)(pr < a.pairs ? pr : a.pairs - 1) * FB];
       };
-      auto add4 = [&](const longlong2 (&v)[4][PMAX]) {
+      auto add = [&](int64_t q0, const int2 (&v)[BQ][PMAX]) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < BQ; ++u)
 #pragma unroll
           for (int pr = 0; pr < PMAX; ++pr) {
-            acc_lo[pr] += pr < a.pairs ? v[u][pr].x : 0;
-            acc_hi[pr] += pr < a.pairs ? v[u][pr].y : 0;
+            const bool use = q0 + u <= qhi && pr < a.pairs;
+            const int2 x = v[u][pr];
+            acc_lo[pr] += use ? x.x : 0;
+            acc_hi[pr] += use ? x.y : 0;
+            esc |= use && (x.x == PART_ESC || x.y == PART_ESC);
           }
       };
-      longlong2 va[4][PMAX];
-      load4(q, va);
-      q += 4;
-      if constexpr (PMAX <= 4) {
-        longlong2 vb[4][PMAX];
-        for (; q + 4 <= qhi + 1; q += 4) {
-          load4(q, vb);
-          add4(va);
+      int2 va[BQ][PMAX], vb[BQ][PMAX];
+      int64_t q = qlo;
+      load(q, va);
+      for (; q + BQ <= qhi; q += BQ) {
+        load(q + BQ, vb);
+        add(q, va);
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < BQ; ++u)
 #pragma unroll
-            for (int pr = 0; pr < PMAX; ++pr) va[u][pr] = vb[u][pr];
-        }
-      } else {
-        // wide channel counts: one buffer (registers)
-        for (; q + 4 <= qhi + 1; q += 4) {
-          add4(va);
-          load4(q, va);
-        }
+          for (int pr = 0; pr < PMAX; ++pr) va[u][pr] = vb[u][pr];
       }
-      add4(va);
-    }
-    if (dense && q <= qhi) {
-      // the last one to three groups (all of them for a node of few groups,
-      // as at the deeper levels): one batch of unconditional loads, clamped
-      // to the node's last group and dropped past it, so they are all in
-      // flight together instead of one group per memory latency
-      longlong2 vt[4][PMAX];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int pr = 0; pr < PMAX; ++pr)
-          vt[u][pr] = src[(q + u <= qhi ? q + u : qhi) * stride + (int64_t)(pr < a.pairs ? pr : a.pairs - 1) * FB];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
+      add(q, va);
+    } else {
+      // fewer positions than row groups (tiny levels): empty groups wrote nothing
+      for (int64_t q = qlo; q <= qhi; ++q) {
+        if (!live(q)) continue;
 #pragma unroll
         for (int pr = 0; pr < PMAX; ++pr) {
-          const bool take = q + u <= qhi && pr < a.pairs;
-          acc_lo[pr] += take ? vt[u][pr].x : 0;
-          acc_hi[pr] += take ? vt[u][pr].y : 0;
+          if (pr >= a.pairs) continue;
+          const int2 x = src[q * stride + (int64_t)pr * FB];
+          acc_lo[pr] += x.x;
+          acc_hi[pr] += x.y;
+          esc |= x.x == PART_ESC || x.y == PART_ESC;
         }
-      q = qhi + 1;
+      }
     }
-    for (; q <= qhi; ++q) {
-      if (dense || q * T / qn < (q + 1) * T / qn) {
+    if (esc) {
 #pragma unroll
-        for (int pr = 0; pr < PMAX; ++pr)
-          if (pr < a.pairs) {
-            const longlong2 v = src[q * stride + (int64_t)pr * FB];
-            acc_lo[pr] += v.x;
-            acc_hi[pr] += v.y;
+      for (int pr = 0; pr < PMAX; ++pr) acc_lo[pr] = acc_hi[pr] = 0;
+      for (int64_t q = qlo; q <= qhi; ++q) {
+        if (!live(q)) continue;
+        for (int pr = 0; pr < PMAX && pr < a.pairs; ++pr) {
+          const int2 x = src[q * stride + (int64_t)pr * FB];
+          if (x.x == PART_ESC || x.y == PART_ESC) {
+            const longlong2 o = ov[q * stride + (int64_t)pr * FB];
+            acc_lo[pr] += o.x;
+            acc_hi[pr] += o.y;
+          } else {
+            acc_lo[pr] += x.x;
+            acc_hi[pr] += x.y;
           }
+        }
       }
     }
   }
@@ -962,7 +990,14 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   a.build_list = build_list;
   char* w = static_cast<char*>(ws);
   a.pre = pre_given ? const_cast<int64_t*>(pre_given) : reinterpret_cast<int64_t*>(w);
-  a.partial = reinterpret_cast<int64_t*>(w + align256((int64_t)(n_build + 1) * 8));
+  {
+    const HistPlan pt = hist_plan(m, n_bins, k, n_build, true);
+    int64_t part = (int64_t)pl.slices * pl.slots * pl.cells;
+    if ((int64_t)pt.slices * pt.slots * pt.cells > part) part = (int64_t)pt.slices * pt.slots * pt.cells;
+    char* p0 = w + align256((int64_t)(n_build + 1) * 8);
+    a.part32 = reinterpret_cast<int32_t*>(p0);
+    a.ovf = reinterpret_cast<int64_t*>(p0 + align256(part * 4));
+  }
   // the quantised rows live in the caller's buffer (kept across a tree's
   // levels) or else at the end of this call's workspace
   if (!qrow) qrow = reinterpret_cast<uint32_t*>(w + hist_ws_bytes(n, m, n_bins, k, n_build, false));

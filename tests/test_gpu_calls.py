@@ -281,3 +281,49 @@ def test_partition_bit_exact(n, m, n_nodes, seed):
     assert np.array_equal(row_g, np.concatenate(want_rows).astype(np.int32))
     assert np.array_equal(off_g, np.array(want_off, dtype=np.int32))
     assert np.array_equal(bl_g, np.array(want_bl, dtype=np.int32))
+
+
+@pytest.mark.parametrize("gathered", [False, True])
+def test_histograms_int32_partials_escape(gathered):
+    """A workgroup's partial sum of one bin leaves int32 past 8192 rows of
+    full-scale values: a constant feature puts every row of a workgroup in one
+    bin, with channels of +-(1 - 2^-24), whose
+    fixed-point images are +-2^18.  Those cells take the exact int64 overflow
+    slot; every cell must still match the oracle within the fixed-point bound.
+    With 100 features a slice has 32 (gathered) to 40 (root) row groups, so a
+    workgroup holds 12,500 to 15,000 rows."""
+    rng = np.random.default_rng(321)
+    n, m, B, k = 600_000, 100, 8, 5
+    bins = rng.integers(0, B, size=(n, m), dtype=np.uint8)
+    bins[:, 0] = 3                       # constant feature
+    bins[:, 1] = (np.arange(n) % 2).astype(np.uint8)
+    top = np.float32(1.0) - np.float32(2.0 ** -24)
+    GH = np.empty((n, k + 1), dtype=np.float32)
+    GH[:, 0] = top
+    GH[:, 1] = -top
+    GH[:, 2] = np.where(rng.random(n) < 0.5, top, -top)
+    GH[:, 3] = rng.standard_normal(n).astype(np.float32) * np.float32(0.25)
+    GH[:, 4] = np.float32(0.5)
+    GH[:, 5] = np.float32(1.0)
+    qexp = gu.qexp_rule(GH)
+    if gathered:
+        rows = np.sort(rng.permutation(n)[: n - 1000]).astype(np.int32)
+        cut = len(rows) // 3
+        off = np.array([0, cut, len(rows)], dtype=np.int32)
+        build_list = np.array([1], dtype=np.int32)
+        nodes = [1]
+    else:
+        rows = np.arange(n, dtype=np.int32)
+        off = np.array([0, n], dtype=np.int32)
+        build_list = None
+        nodes = [0]
+    Hg = gu.host_layout(gu.run_hist(bins, GH, qexp, B, rows if gathered else None, off, build_list).cpu().numpy())
+    chan_max = np.abs(GH.astype(np.float64)).max(axis=0)
+    for j in nodes:
+        node_rows = rows[off[j]:off[j + 1]]
+        Ho = oracle.node_histograms(bins, GH, node_rows, B)
+        counts = oracle.node_histograms(bins, np.ones((n, 1), dtype=np.float32), node_rows, B)[..., 0]
+        mass = oracle.node_histograms(bins, np.abs(GH), node_rows, B)
+        assert np.abs(Ho[0, 3, 0]) > 2.0 ** 14  # the constant feature's cell exceeds int32 per workgroup
+        ok1, ok2, worst = gu.hist_tolerance_ok(Hg[j], Ho, counts, qexp, mass, chan_max)
+        assert ok1 and ok2, worst

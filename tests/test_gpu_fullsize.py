@@ -155,3 +155,70 @@ def test_fullsize_leaf_values_sampled_leaves(grown):
         ok, worst = gu.leaf_value_error_ok(V[Lf:Lf + 1], Vo, G[rows], [sub_idx.astype(np.int64)], wl.lam,
                                            col_max=col_max)
         assert ok, (Lf, worst)
+
+
+def _hist_report(label, Hg, Ho, counts, qexp, mass, chan_max):
+    """Errors of one node's histograms against the oracle's: the fixed-point bound, the 1e-4 bar
+    relative to max(|H|, cell mass) with and without the channel-maximum floor, and the plain
+    relative error of the cells well above the quantisation noise."""
+    half_q = np.ldexp(1.0, -(qexp.astype(np.int64) + 1))
+    noise = counts[..., None] * half_q
+    err = np.abs(Hg - Ho)
+    fixed_ok = err <= noise + 1e-12 * mass
+    scale = np.maximum(np.abs(Ho), mass)
+    unfloored = err <= gu.TOL * scale
+    floored = err <= gu.TOL * np.maximum(scale, chan_max)
+    big = np.abs(Ho) > 1e4 * np.maximum(noise, 1e-300)
+    rel_big = float((err[big] / np.abs(Ho[big])).max()) if big.any() else 0.0
+    cells = err.size
+    print("hist %-22s cells %8d | fixed-point bound %d | 1e-4 of max(|H|, mass): %d (%.4f%%) | with the "
+          "channel-max floor: %d | max rel. error where |H| > 1e4 x noise: %.2e (%d cells)"
+          % (label, cells, int(fixed_ok.sum()), int(unfloored.sum()), 100.0 * unfloored.mean(), int(floored.sum()),
+             rel_big, int(big.sum())), flush=True)
+    return fixed_ok.all(), floored.all(), unfloored
+
+
+def test_fullsize_histograms_unfloored_report(grown):
+    """All 100 root features, and the largest and a random node of levels 3
+    and 5 built through sb_build_histograms on the tree's own rows, against
+    the oracle: every cell within the fixed-point bound and the 1e-4 bar with
+    the channel-maximum floor; the count of cells meeting 1e-4 of
+    max(|H|, cell mass) without that floor is printed (run with -s)."""
+    wl, inp, ss, tree, GH_o, _ = grown
+    n, m, B, k, c = wl.n, wl.m, wl.n_bins, wl.k, wl.k + 1
+    qexp = ss.qexp.cpu().numpy()
+    chan_max = np.abs(GH_o.astype(np.float64)).max(axis=0)
+    ones = np.ones((n, 1), dtype=np.float32)
+    absGH = np.abs(GH_o)
+    rng = np.random.default_rng(23)
+    cases = [("root", 0, 0)]
+    for level in (3, 5):
+        sizes = [node_rows(tree, wl.depth, level, j).size for j in range(1 << level)]
+        big = int(np.argmax(sizes))
+        other = int(rng.choice([j for j in range(1 << level) if j != big and sizes[j] > 0]))
+        cases += [("level %d node %d" % (level, big), level, big), ("level %d node %d" % (level, other), level, other)]
+    total, passed = 0, 0
+    for label, level, j in cases:
+        H = torch.full((1, m, c, B), float("nan"), dtype=torch.float64, device=gu.DEV)
+        ws = workspace(L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=n, m=m, n_bins=B, k=k, n_nodes=1), gu.DEV)
+        if level == 0:
+            rows = np.arange(n, dtype=np.int32)
+            off = gu.up(np.array([0, n], dtype=np.int32))
+            L.sb_build_histograms(ss.bins4, n, None, 0, n, m, B, ss.GH, ss.ld_gh, k, ss.qexp, None, off, 1, None, 1, H,
+                                  ws, ws.numel())
+        else:
+            rows = node_rows(tree, wl.depth, level, j)
+            off = gu.up(np.array([0, rows.size], dtype=np.int32))
+            L.sb_build_histograms(None, 0, ss.rec, ss.ld_rec, n, m, B, ss.GH, ss.ld_gh, k, ss.qexp,
+                                  gu.up(rows, torch.int32), off, 1, None, 1, H, ws, ws.numel())
+        gu.sync()
+        Hg = gu.host_layout(H.cpu().numpy())[0]
+        Ho = oracle.node_histograms(inp.bins, GH_o, rows, B)
+        counts = oracle.node_histograms(inp.bins, ones, rows, B)[..., 0]
+        mass = oracle.node_histograms(inp.bins, absGH, rows, B)
+        fixed_ok, floored_ok, unfloored = _hist_report(label, Hg, Ho, counts, qexp, mass, chan_max)
+        assert fixed_ok and floored_ok, label
+        total += unfloored.size
+        passed += int(unfloored.sum())
+    print("hist all sampled nodes: %d of %d cells (%.4f%%) within 1e-4 of max(|H|, mass) without the floor"
+          % (passed, total, 100.0 * passed / total), flush=True)

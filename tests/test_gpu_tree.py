@@ -152,3 +152,35 @@ def test_per_step_calls_grow_the_same_tree(name, kw):
         assert np.array_equal(fused["score"][l].view(np.uint64), steps["score"][l].view(np.uint64)), l
     assert np.array_equal(fused["row_idx"], steps["row_idx"])
     assert np.array_equal(fused["leaf_off"], steps["leaf_off"])
+
+
+def test_fused_level_end_escaped_partials():
+    """Whole trees whose partial sums leave int32 (a constant feature and
+    full-scale same-sign gradient columns, 600,000 rows): the fused level end
+    of sb_grow_tree and the per-step calls (whose histograms are checked
+    against the oracle on such data) grow the same tree bit for bit."""
+    rng = np.random.default_rng(77)
+    n, m, B, k, depth = 600_000, 100, 16, 5, 5
+    bins = rng.integers(0, B, size=(n, m), dtype=np.uint8)
+    bins[:, 0] = 7
+    top = np.float32(1.0) - np.float32(2.0 ** -24)
+    G_T = np.empty((k, n), dtype=np.float32)
+    G_T[0] = top
+    G_T[1] = -top
+    G_T[2] = np.where(bins[:, 5] < 8, top, -top)
+    G_T[3] = rng.standard_normal(n).astype(np.float32)
+    G_T[4] = np.where(bins[:, 9] < 3, np.float32(0.75), np.float32(-0.125))
+    h = np.ones(n, dtype=np.float32)
+    ss = SplitSearch(bins, B, k, depth, 1.0, 0.0, device=gu.DEV)
+    ss.step("identity", gu.up(G_T), gu.up(h))
+    gu.sync()
+    fused = ss.tree()
+    ss.grow_levelwise()
+    gu.sync()
+    steps = ss.tree()
+    for l in range(depth):
+        assert np.array_equal(fused["feature"][l], steps["feature"][l]), l
+        assert np.array_equal(fused["bin"][l], steps["bin"][l]), l
+        assert np.array_equal(fused["score"][l].view(np.uint64), steps["score"][l].view(np.uint64)), l
+    assert np.array_equal(fused["row_idx"], steps["row_idx"])
+    assert (fused["feature"][0] >= 0).all()
