@@ -53,6 +53,17 @@ struct GradArgs {
   int32_t n_tiles;
 };
 
+// Barrier for the norm staging: waits for this wave's LDS operations only.
+// A plain __syncthreads also waits for every outstanding global access,
+// here the stores of G (and the hessians) of the chunk just written.
+// 0xc07f is s_waitcnt lgkmcnt(0) in the gfx9 encoding.
+__device__ inline void lds_sync() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
   __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
   const int tid = threadIdx.x;
@@ -122,7 +133,7 @@ __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
         gbuf[u][tid] = ok ? g : 0.0f;
       }
       if (a.npart) {
-        __syncthreads();
+        lds_sync();
         // 16 threads per column, 16 rows each; lanes c*16 .. c*16+15 share column c
         const int c = tid >> 4, seg = tid & 15;
         const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
@@ -140,13 +151,94 @@ __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
           double* p = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
           *p = first ? acc : *p + acc;
         }
-        __syncthreads();
+        lds_sync();
       }
     }
     if (a.h_row && ok) a.h_row[row] = hsum * inv_d;
     first = false;
   }
   // a block without tiles still defines its partials
+  if (a.npart && first)
+    for (int j = tid; j < d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
+}
+
+// Softmax cross-entropy with the row's d <= DMAX scores held in registers:
+// F is read once.  Columns past d load column d-1 (the maximum is unchanged
+// and the sum skips them), so every load is unconditional and all of them
+// are in flight together.  The maximum is exact, the sum of exp(a - max) is
+// taken in column order and its terms are kept for p = exp(a - max) / sum,
+// then the second half as in k_grad (stores, the hessians and the
+// column-norm staging).  The grid holds as many blocks as fit on the GPU at
+// once, each looping over tiles, so no last round of blocks runs part-empty.
+template <int DMAX>
+__global__ void __launch_bounds__(GRAD_THREADS) k_grad_softmax_regs(GradArgs a) {
+  __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
+  const int tid = threadIdx.x;
+  const int d = a.d;
+  bool first = true;
+  for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
+    const int64_t row = (int64_t)tile * GRAD_THREADS + tid;
+    const bool ok = row < a.n;
+    const int64_t rc = ok ? row : a.n - 1;  // rows past the end read row n-1 and store nothing
+    const int y = a.labels[rc];
+    float x[DMAX];
+#pragma unroll
+    for (int j = 0; j < DMAX; ++j) x[j] = a.F[(int64_t)(j < d ? j : d - 1) * a.ld_f + rc];
+    float m = x[0];
+#pragma unroll
+    for (int j = 1; j < DMAX; ++j) m = fmaxf(m, x[j]);
+    // x[j] becomes exp(x[j] - max), reused for p below
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < DMAX; ++j) {
+      x[j] = expf(x[j] - m);
+      s += (j < d) ? x[j] : 0.0f;
+    }
+    const float inv = 1.0f / s;
+    float hsum = 0.0f;
+#pragma unroll
+    for (int j0 = 0; j0 < DMAX; j0 += GRAD_JC) {
+      if (j0 >= d) break;
+#pragma unroll
+      for (int u = 0; u < GRAD_JC; ++u) {
+        const int j = j0 + u;
+        float g = 0.0f;
+        if (j < d) {
+          const float p = x[j] * inv;
+          const float hh = p * (1.0f - p);
+          g = (j == y) ? p - 1.0f : p;
+          if (ok) {
+            a.G[(int64_t)j * a.ld_g + row] = g;
+            if (a.hess) a.hess[(int64_t)j * a.ld_h + row] = hh;
+          }
+          hsum += hh;
+        }
+        gbuf[u][tid] = ok ? g : 0.0f;
+      }
+      if (a.npart) {
+        lds_sync();
+        const int c = tid >> 4, seg = tid & 15;
+        const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
+        double acc = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = src[q];
+          acc += (double)v.x * v.x;
+          acc += (double)v.y * v.y;
+          acc += (double)v.z * v.z;
+          acc += (double)v.w * v.w;
+        }
+        for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+        if (seg == 0 && j0 + c < d) {
+          double* p = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
+          *p = first ? acc : *p + acc;
+        }
+        lds_sync();
+      }
+    }
+    if (a.h_row && ok) a.h_row[row] = hsum * (1.0f / (float)d);
+    first = false;
+  }
   if (a.npart && first)
     for (int j = tid; j < d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
 }
@@ -221,14 +313,39 @@ int64_t grad_ws_bytes(int64_t n, int32_t d) {
   return align256((int64_t)d * blocks * 8);
 }
 
+// Blocks of a kernel that fit on the current device at once (at least 1).
+template <typename K>
+int resident_blocks(K kernel, int threads) {
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
+    return GRAD_MAX_BLOCKS;
+  const int r = cus * per;
+  return r > 0 ? r : 1;
+}
+
 int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
                          const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
                          float* h_row, double* norm2, void* ws, hipStream_t st) {
   const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
-  const int blocks = (int)(tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS);
+  int blocks = (int)(tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS);
+  if (loss == SB_LOSS_SOFTMAX_CE && d <= 104 && d > 64) {
+    static thread_local int fit = 0;  // per-thread cache of the occupancy query
+    if (!fit) fit = resident_blocks(k_grad_softmax_regs<104>, GRAD_THREADS);
+    if (fit < blocks) blocks = fit;
+  }
   double* npart = norm2 ? static_cast<double*>(ws) : nullptr;
   const GradArgs a{loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, npart, (int32_t)tiles};
-  hipLaunchKernelGGL(k_grad, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  if (loss == SB_LOSS_SOFTMAX_CE && d <= 16)
+    hipLaunchKernelGGL(k_grad_softmax_regs<16>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 32)
+    hipLaunchKernelGGL(k_grad_softmax_regs<32>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 64)
+    hipLaunchKernelGGL(k_grad_softmax_regs<64>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 104)
+    hipLaunchKernelGGL(k_grad_softmax_regs<104>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_grad, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
   if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, blocks, norm2);
   return check_launch("sb_gradients");
 }

@@ -20,14 +20,8 @@ namespace sb {
 namespace {
 
 constexpr int NORM_THREADS = 256;
-#ifndef SB_NORM_CHUNK
-#define SB_NORM_CHUNK 16384
-#endif
-#ifndef SB_NORM_UNROLL
-#define SB_NORM_UNROLL 8
-#endif
-constexpr int64_t NORM_CHUNK = SB_NORM_CHUNK;  // rows per partial sum
-constexpr int NORM_UNROLL = SB_NORM_UNROLL;    // 16-byte loads in flight per thread
+constexpr int64_t NORM_CHUNK = 16384;  // rows per partial sum
+constexpr int NORM_UNROLL = 8;         // 16-byte loads in flight per thread
 constexpr int NORM_MAX_PARTS = 256;
 
 // A 16-byte load that does not allocate in the caches (data read once).
@@ -371,10 +365,7 @@ constexpr int PROJ_KT = 32;               // sketch columns per pass
 constexpr int PROJ_JU = 16;               // G loads in flight per thread
 constexpr int PROJ_LDS_FLOATS = 32768;    // 128 KB: the Pi block staged per pass
 constexpr int SPARSE_MAX_S = 1;           // entries per row of Pi for the sparse kernel
-#ifndef SB_PROJ_MFMA_MIN_K
-#define SB_PROJ_MFMA_MIN_K 8
-#endif
-constexpr int PROJ_MFMA_MIN_K = SB_PROJ_MFMA_MIN_K;  // from this k on the dense product runs on MFMA
+constexpr int PROJ_MFMA_MIN_K = 8;        // from this k on the dense product runs on MFMA
 
 // Random Projections (Section 3.3), HBM-bound on the read of G: one row per
 // thread, PROJ_JU columns of G loaded ahead, and the pass's block of Pi
