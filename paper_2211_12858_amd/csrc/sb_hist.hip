@@ -774,22 +774,30 @@ struct ScoreOut {
   double lam, mcw;
 };
 
-template <int PMAX>
-__global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut so) {
+// RQ threads per bin: each sums its share of the node's row groups, and the
+// shares meet in LDS (integers, so the order does not matter).  The first
+// 256 threads then carry the bin through the rest.  RQ = 4 where a node
+// spans many row groups (the first levels), else 1.
+template <int PMAX, int RQ>
+__global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, ScoreOut so) {
   const int f = blockIdx.x, p = blockIdx.y;
   const int32_t j = node_of(a, p);
   if (j < 0 || j >= a.n_nodes || f >= a.m) return;
   const int B = a.n_bins, c = a.c, k = c - 1;
   const int s = f / a.f, fl = f - s * a.f;
   const int FB = a.f * B;
-  const int bin = threadIdx.x;
+  const int bin = threadIdx.x & 255, quarter = threadIdx.x >> 8;
   const bool on = bin < B;
   const bool sib = a.Hp && (j == 2 * p || j == 2 * p + 1);
   const int64_t cpn = (int64_t)a.m * c * B;
   const int64_t T = a.pre[a.n_build];
   const int64_t lo = a.pre[p], hi = a.pre[p + 1];
   const int32_t qn = groups_of(a, s);
-  const int64_t qlo = hi > lo ? group_of(lo, T, qn) : 0, qhi = hi > lo ? group_of(hi - 1, T, qn) : -1;
+  const int64_t nlo = hi > lo ? group_of(lo, T, qn) : 0, nhi = hi > lo ? group_of(hi - 1, T, qn) : -1;
+  // this thread's quarter of the node's row groups [nlo, nhi]
+  const int64_t per = (nhi - nlo + RQ) / RQ;
+  const int64_t qlo = nlo + quarter * per;
+  const int64_t qhi = (qlo + per - 1 < nhi) ? qlo + per - 1 : nhi;
   const bool dense = T >= qn;  // every row group holds at least one position
   // int64 channel sums of this bin over the node's row groups, from the
   // int32 partials.  Fast path: batches of BQ row groups and every channel
@@ -812,7 +820,7 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
     auto live = [&](int64_t q) { return q <= qhi && (dense || q * T / qn < (q + 1) * T / qn); };
     bool esc = false;
     if (dense) {
-      constexpr int BQ = PMAX <= 4 ? 8 : 4;
+      constexpr int BQ = PMAX <= 4 ? 4 : 2;
       auto load = [&](int64_t q0, int2 (&v)[BQ][PMAX]) {
 #pragma unroll
         for (int u = 0; u < BQ; ++u)
@@ -877,12 +885,31 @@ __global__ void __launch_bounds__(256) k_hist_reduce_score(HistArgs a, ScoreOut 
       }
     }
   }
+  // the quarters meet: quarters 1..3 leave their sums in LDS, quarter 0
+  // adds them (the same LDS then stages the fp64 values for the scan)
+  extern __shared__ double xv[];
+  longlong2* part = reinterpret_cast<longlong2*>(xv);  // [quarter - 1][pair][256]
+  if (RQ > 1 && quarter > 0) {
+#pragma unroll
+    for (int pr = 0; pr < PMAX; ++pr) part[((quarter - 1) * PMAX + pr) * 256 + bin] = make_longlong2(acc_lo[pr], acc_hi[pr]);
+  }
+  if (RQ > 1) __syncthreads();
+  if (RQ > 1 && quarter == 0) {
+#pragma unroll
+    for (int qq = 0; qq < RQ - 1; ++qq)
+#pragma unroll
+      for (int pr = 0; pr < PMAX; ++pr) {
+        const longlong2 v = part[(qq * PMAX + pr) * 256 + bin];
+        acc_lo[pr] += v.x;
+        acc_hi[pr] += v.y;
+      }
+  }
+  if (RQ > 1) __syncthreads();  // the partial sums are read: the LDS becomes the scan's staging
   // fp64 histogram values of this bin: written to H (and the sibling by
   // subtraction) and staged in LDS as [node][channel][bin] for the scan
-  extern __shared__ double xv[];
 #pragma unroll
   for (int t = 0; t < 2 * PMAX; ++t) {
-    if (t < c && on) {
+    if (t < c && on && quarter == 0) {
       const int64_t idx = ((int64_t)f * c + t) * B + bin;
       const double x = ldexp((double)((t & 1) ? acc_hi[t >> 1] : acc_lo[t >> 1]), -a.qexp[t]);
       if (a.store_h) a.H[(int64_t)j * cpn + idx] = x;
@@ -1068,10 +1095,18 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   if (feat_s) {
     ScoreOut so{feat_s, feat_b, lam, mcw};
     const dim3 g(m, n_build);
-    const size_t lds = (size_t)2 * pl.c * n_bins * 8;  // [node][channel][bin], built node and sibling
-    if (pl.pairs <= 3) hipLaunchKernelGGL((k_hist_reduce_score<3>), g, dim3(256), lds, st, a, so);
-    else if (pl.pairs <= 4) hipLaunchKernelGGL((k_hist_reduce_score<4>), g, dim3(256), lds, st, a, so);
-    else if (pl.pairs <= 8) hipLaunchKernelGGL((k_hist_reduce_score<8>), g, dim3(256), lds, st, a, so);
+    // [node][channel][bin] fp64 values of the built node and its sibling, or
+    // before them the partial sums of quarters 1..3 ([quarter][pair][256])
+    const int pm = pl.pairs <= 3 ? 3 : pl.pairs <= 4 ? 4 : 8;
+    const bool wide = pl.q >= 12 * n_build;  // a node spans about q / n_build row groups
+    const int rq = wide ? 4 : 1;
+    const size_t lv = (size_t)2 * pl.c * n_bins * 8, lp = (size_t)(rq - 1) * pm * 256 * 16;
+    const size_t lds = lv > lp ? lv : lp;
+#define SB_RS(P, R) hipLaunchKernelGGL((k_hist_reduce_score<P, R>), g, dim3(256 * R), lds, st, a, so)
+    if (pm == 3) { if (wide) SB_RS(3, 4); else SB_RS(3, 1); }
+    else if (pm == 4) { if (wide) SB_RS(4, 4); else SB_RS(4, 1); }
+    else if (pl.pairs <= 8) { if (wide) SB_RS(8, 4); else SB_RS(8, 1); }
+#undef SB_RS
     else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 16 channels");
   } else {
     dim3 rg((pl.cells + 255) / 256, n_build, pl.slices);
