@@ -126,8 +126,10 @@ int32_t sb_abi_version(void);
  * SCORE_SPLITS, PARTITION_ROWS), leaves (LEAF_VALUES).  depth: tree depth
  * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES, GRADIENTS; the
  * LEAF_VALUES size covers all three hessian forms).  UPDATE_PREDICTIONS needs
- * only n.  Returns -1 (and sets the error text) for invalid
- * sizes.  sb_layout_bins and sb_subtract_histograms need no workspace.
+ * only n.  Returns -1 (and sets the error text) for sizes outside the
+ * range the call itself accepts (n < 2^31, m and d <= 65535, k <= 255,
+ * n_bins in [2, 256], nodes as documented per call).  sb_layout_bins and
+ * sb_subtract_histograms need no workspace.
  */
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
                            int32_t n_nodes, int32_t depth);

@@ -13,7 +13,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libsketchboost.so")
+# SKETCHBOOST_LIB names another build of the same library (the host-side
+# sanitizer build of the ABI tests); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("SKETCHBOOST_LIB") or os.path.join(HERE, "libsketchboost.so")
 
 SB_OK, SB_E_ARG, SB_E_SHAPE, SB_E_UNSUPPORTED, SB_E_DEVICE = 0, 1, 2, 3, 4
 SB_SKETCH_TOP_OUTPUTS, SB_SKETCH_RANDOM_SAMPLING, SB_SKETCH_RANDOM_PROJECTION, SB_SKETCH_IDENTITY = 0, 1, 2, 3

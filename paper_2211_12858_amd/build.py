@@ -51,5 +51,50 @@ def build(verbose=False):
     return LIB
 
 
+# Host-side sanitizer build: the library with AddressSanitizer and UBSan
+# on its host code (the validation layer and the launch plumbing); the
+# device code is built as usual.  Each -fsanitize applies to the host pass
+# only (-Xarch_host).  The ABI tests run against it without a GPU: every
+# call they make is refused on the host.
+SANITIZE_FLAGS = [
+    "-Xarch_host", "-fsanitize=address",
+    "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined",
+    "-Xarch_host", "-fno-omit-frame-pointer",
+]
+
+
+def build_host_sanitized(out_path, jobs=8):
+    """Build the sanitized library at out_path: one object per source, compiled in parallel, then linked."""
+    import concurrent.futures
+
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    flags = [f for f in HIPCC_FLAGS if f != "-shared"] + ["-g"] + SANITIZE_FLAGS
+    objs = [out_path + "." + os.path.basename(src) + ".o" for src in srcs]
+
+    def run(cmd):
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stderr[-4000:] + "\n")
+            raise RuntimeError("hipcc (host sanitizer build) failed with exit code %d" % res.returncode)
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as pool:
+        list(pool.map(run, [[hipcc()] + flags + ["-c", "-o", o, src] for src, o in zip(srcs, objs)]))
+    run([hipcc(), "-shared", "--offload-arch=gfx950"] + SANITIZE_FLAGS + ["-o", out_path] + objs)
+    for o in objs:
+        os.remove(o)
+    return out_path
+
+
+def sanitizer_runtime():
+    """Path of the clang AddressSanitizer runtime that the sanitized build needs preloaded."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    res = subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = res.stdout.strip()
+    return path if res.returncode == 0 and os.path.isabs(path) and os.path.exists(path) else None
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

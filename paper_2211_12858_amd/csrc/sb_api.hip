@@ -166,25 +166,29 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
                            int32_t n_nodes, int32_t depth) {
   switch (call) {
     case SB_CALL_SKETCH:
-      if (n < 1 || d < 1 || k < 1) break;
+      if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535 || k < 1 || k > 255) break;
       return sketch_ws_bytes(0, n, d, k);
     case SB_CALL_HIST_EXPONENTS:
       if (k < 1 || k > 255) break;
       return hist_exponents_ws_bytes(k);
     case SB_CALL_BUILD_HISTOGRAMS: {
-      if (n < 1 || n > MAX_ROWS || m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || n_nodes < 1) break;
+      if (n < 1 || n > MAX_ROWS || m < 1 || m > 65535 || n_bins < 2 || n_bins > 256 || k < 1 || k > 255 ||
+          n_nodes < 1 || n_nodes > (1 << 20))
+        break;
       const int64_t b = hist_ws_bytes(n, m, n_bins, k, n_nodes, true);
       if (b < 0) break;
       return b;
     }
     case SB_CALL_SCORE_SPLITS:
-      if (m < 1 || n_nodes < 1) break;
+      if (m < 1 || m > 65535 || n_nodes < 1 || n_nodes > 65535) break;
       return score_ws_bytes(n_nodes, m);
     case SB_CALL_PARTITION_ROWS:
-      if (n < 1 || n_nodes < 1) break;
+      if (n < 1 || n > MAX_ROWS || n_nodes < 1 || n_nodes > (1 << 20)) break;
       return partition_ws_bytes(n, n_nodes);
     case SB_CALL_GROW_TREE: {
-      if (n < 1 || m < 1 || n_bins < 2 || n_bins > 256 || k < 1 || depth < 1 || depth > MAX_DEPTH) break;
+      if (n < 1 || n > MAX_ROWS || m < 1 || m > 65535 || n_bins < 2 || n_bins > 256 || k < 1 || k > 255 ||
+          depth < 1 || depth > MAX_DEPTH)
+        break;
       const int64_t b = grow_ws_layout(n, m, n_bins, k, depth).total;
       if (b < 0) break;
       return b;

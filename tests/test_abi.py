@@ -71,6 +71,39 @@ def test_workspace_bytes(L):
         L.sb_workspace_bytes(L.SB_CALL_BUILD_HISTOGRAMS, n=10, m=8, n_bins=256, k=100, n_nodes=1)
 
 
+# Sizes from the valid range to the extremes of their C types, one argument
+# at a time and all together: every answer is a size or -1 with an error
+# text.  Run under UBSan (test_abi_sanitize.py) this also checks that no size
+# arithmetic overflows.
+EXTREMES = {
+    "n": [-1, 0, 1, 2**31 - 1, 2**31, 2**40, 2**62, 2**63 - 1],
+    "m": [-1, 0, 1, 2**16, 2**31 - 1, -2**31],
+    "n_bins": [-1, 0, 1, 2, 256, 257, 2**31 - 1],
+    "d": [-1, 0, 1, 2**20, 2**31 - 1],
+    "k": [-1, 0, 1, 23, 24, 255, 2**31 - 1],
+    "n_nodes": [-1, 0, 1, 4096, 4097, 2**31 - 1],
+    "depth": [-1, 0, 1, 12, 13, 2**31 - 1],
+}
+
+
+def test_workspace_bytes_at_extreme_sizes(L):
+    lib = L.load()
+    base = dict(n=1000, m=100, n_bins=256, d=100, k=5, n_nodes=16, depth=6)
+    order = ["n", "m", "n_bins", "d", "k", "n_nodes", "depth"]
+    cases = []
+    for name, values in EXTREMES.items():
+        for v in values:
+            cases.append(dict(base, **{name: v}))
+    cases.append({name: values[-1] for name, values in EXTREMES.items()})
+    cases.append({name: values[0] for name, values in EXTREMES.items()})
+    for call in range(-1, 10):
+        for kw in cases:
+            got = lib.sb_workspace_bytes(call, *[kw[o] for o in order])
+            assert got == -1 or 0 <= got < 2**62, (call, kw, got)
+            if got == -1:
+                assert L.sb_last_error(), (call, kw)
+
+
 # The histogram kernels add at most 24 channels (k <= 23).  Every wider
 # sketch is refused on the host, whatever the bin count: the sizes query
 # returns -1 and the calls return SB_E_UNSUPPORTED before any device work.
