@@ -170,77 +170,106 @@ __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
 // then the second half as in k_grad (stores, the hessians and the
 // column-norm staging).  The grid holds as many blocks as fit on the GPU at
 // once, each looping over tiles, so no last round of blocks runs part-empty.
+//
+// The column count d reaches this function opaque to the compiler, and is
+// made opaque again between the loads and the stores, so that the
+// per-column tests j < d (uniform lane masks) and column offsets are formed
+// where they are used instead of all at once and held, spilled, across a
+// phase or the tile loop.  Columns past d stay on column d-1 and store
+// column d-1's own values there (same address, same value), so the stores
+// need no branch; a full tile stores without a row guard.
+template <int DMAX, bool FULL, bool HESS>
+__device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], int64_t base, bool first,
+                                         int64_t ld_f, int64_t ld_g, int64_t ld_h, int d) {
+  const int tid = threadIdx.x;
+  const int64_t row = base + tid;
+  const bool ok = FULL || row < a.n;
+  const int loc = ok ? tid : (int)(a.n - 1 - base);  // rows past the end read row n-1 and store nothing
+  const int y = a.labels[base + loc];
+  const float* Fb = a.F + base;
+  float x[DMAX];
+#pragma unroll
+  for (int j = 0; j < DMAX; ++j) x[j] = Fb[(int64_t)(j < d ? j : d - 1) * ld_f + loc];
+  float m = x[0];
+#pragma unroll
+  for (int j = 1; j < DMAX; ++j) m = fmaxf(m, x[j]);
+  // x[j] becomes exp(x[j] - max), reused for p below
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < DMAX; ++j) {
+    x[j] = expf(x[j] - m);
+    s += (j < d) ? x[j] : 0.0f;
+  }
+  const float inv = 1.0f / s;
+  float hsum = 0.0f;
+  asm volatile("" : "+s"(d));
+  float* Gb = a.G + base;
+  float* Hb = HESS ? a.hess + base : nullptr;
+#pragma unroll
+  for (int j0 = 0; j0 < DMAX; j0 += GRAD_JC) {
+    if (j0 >= d) break;
+#pragma unroll
+    for (int u = 0; u < GRAD_JC; ++u) {
+      const int j = j0 + u;
+      const int jj = j < d ? j : d - 1;
+      const float p = x[j] * inv;
+      const float hh = p * (1.0f - p);
+      const float g = (jj == y) ? p - 1.0f : p;
+      if (ok) {
+        Gb[(int64_t)jj * ld_g + tid] = g;
+        if (HESS) Hb[(int64_t)jj * ld_h + tid] = hh;
+      }
+      hsum += (j < d) ? hh : 0.0f;
+      gbuf[u][tid] = ok ? g : 0.0f;
+    }
+    if (a.npart) {
+      lds_sync();
+      const int c = tid >> 4, seg = tid & 15;
+      const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
+      double acc = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = src[q];
+        acc += (double)v.x * v.x;
+        acc += (double)v.y * v.y;
+        acc += (double)v.z * v.z;
+        acc += (double)v.w * v.w;
+      }
+      for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+      if (seg == 0 && j0 + c < d) {
+        double* pp = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
+        *pp = first ? acc : *pp + acc;
+      }
+      lds_sync();
+    }
+  }
+  if (a.h_row && ok) a.h_row[row] = hsum * (1.0f / (float)d);
+}
+
 template <int DMAX>
 __global__ void __launch_bounds__(GRAD_THREADS) k_grad_softmax_regs(GradArgs a) {
   __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
-  const int tid = threadIdx.x;
-  const int d = a.d;
   bool first = true;
   for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
-    const int64_t row = (int64_t)tile * GRAD_THREADS + tid;
-    const bool ok = row < a.n;
-    const int64_t rc = ok ? row : a.n - 1;  // rows past the end read row n-1 and store nothing
-    const int y = a.labels[rc];
-    float x[DMAX];
-#pragma unroll
-    for (int j = 0; j < DMAX; ++j) x[j] = a.F[(int64_t)(j < d ? j : d - 1) * a.ld_f + rc];
-    float m = x[0];
-#pragma unroll
-    for (int j = 1; j < DMAX; ++j) m = fmaxf(m, x[j]);
-    // x[j] becomes exp(x[j] - max), reused for p below
-    float s = 0.0f;
-#pragma unroll
-    for (int j = 0; j < DMAX; ++j) {
-      x[j] = expf(x[j] - m);
-      s += (j < d) ? x[j] : 0.0f;
+    const int64_t ld_f = a.ld_f, ld_g = a.ld_g, ld_h = a.ld_h;
+    // d as seen by the compiler changes at every tile: the per-column tests
+    // j < d are made where they are used, not hoisted out of the tile loop
+    // as DMAX lane masks held (spilled) across it
+    int d = a.d;
+    asm volatile("" : "+s"(d));
+    const int64_t base = (int64_t)tile * GRAD_THREADS;
+    const bool full = base + GRAD_THREADS <= a.n;
+    if (a.hess) {
+      if (full) grad_softmax_tile<DMAX, true, true>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
+      else grad_softmax_tile<DMAX, false, true>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
+    } else {
+      if (full) grad_softmax_tile<DMAX, true, false>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
+      else grad_softmax_tile<DMAX, false, false>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
     }
-    const float inv = 1.0f / s;
-    float hsum = 0.0f;
-#pragma unroll
-    for (int j0 = 0; j0 < DMAX; j0 += GRAD_JC) {
-      if (j0 >= d) break;
-#pragma unroll
-      for (int u = 0; u < GRAD_JC; ++u) {
-        const int j = j0 + u;
-        float g = 0.0f;
-        if (j < d) {
-          const float p = x[j] * inv;
-          const float hh = p * (1.0f - p);
-          g = (j == y) ? p - 1.0f : p;
-          if (ok) {
-            a.G[(int64_t)j * a.ld_g + row] = g;
-            if (a.hess) a.hess[(int64_t)j * a.ld_h + row] = hh;
-          }
-          hsum += hh;
-        }
-        gbuf[u][tid] = ok ? g : 0.0f;
-      }
-      if (a.npart) {
-        lds_sync();
-        const int c = tid >> 4, seg = tid & 15;
-        const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
-        double acc = 0.0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = src[q];
-          acc += (double)v.x * v.x;
-          acc += (double)v.y * v.y;
-          acc += (double)v.z * v.z;
-          acc += (double)v.w * v.w;
-        }
-        for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-        if (seg == 0 && j0 + c < d) {
-          double* p = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
-          *p = first ? acc : *p + acc;
-        }
-        lds_sync();
-      }
-    }
-    if (a.h_row && ok) a.h_row[row] = hsum * (1.0f / (float)d);
     first = false;
   }
   if (a.npart && first)
-    for (int j = tid; j < d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
+    for (int j = threadIdx.x; j < a.d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
 }
 
 // One wave per column: lane l adds partials l, l+64, ... in order, then a fixed butterfly.
