@@ -19,10 +19,9 @@
 // follow from G and the targets (p = g + target, h = p (1 - p)), so they
 // can be formed while loading G instead of being stored and read.
 //
-// Exact, order-free accumulation.  Per tile of T rows (2048, or 1024 with
-// derived hessians) and per channel, the block takes M = max |v| over the
-// tile, with M < 2^E, and maps each v to the integer rint(v * 2^(ql - E)),
-// of magnitude <= 2^ql (ql = 41, or 42).  T * 2^ql <= 2^52, so any sum of one
+// Exact, order-free accumulation.  Per tile of T = 2048 rows and per
+// channel, the block takes M = max |v| over the tile, with M < 2^E, and maps
+// each v to the integer rint(v * 2^(ql - E)), of magnitude <= 2^ql (ql = 41).  T * 2^ql <= 2^52, so any sum of one
 // tile's integers is an integer below 2^53: the 64-bit LDS integer atomics
 // reach the same sum in any order, and that sum times 2^(E - ql) is an exact
 // fp64 value.  One thread
@@ -38,10 +37,12 @@ namespace sb {
 namespace {
 
 constexpr int LEAF_THREADS = 256;
-// Rows per thread per tile: 8 (2048-row tiles) for plain channels, 4 for
-// the derived hessians (more channels per block, so fewer rows in registers).
+// Rows per thread per tile: 8 (2048-row tiles), with plain channels and
+// with the derived hessians alike (4 rows per thread, 1024-row tiles, took
+// 368 against 290 us on 2M x 100: twice the per-tile maxima and cell
+// flushes per row).
 constexpr int LEAF_SPT = 8;
-constexpr int LEAF_SPT_DERIVED = 4;
+constexpr int LEAF_SPT_DERIVED = 8;
 // Quantum exponent for a tile of 256 * SPT rows: tile * 2^ql <= 2^52.
 constexpr int leaf_ql(int spt) { return spt == 8 ? 41 : (spt == 4 ? 42 : 40); }
 static_assert((int64_t)(LEAF_THREADS * 8) << leaf_ql(8) <= (int64_t(1) << 52), "tile sums must stay exact in fp64");
@@ -104,7 +105,11 @@ struct LeafTile {
   int lf[SPT];
 };
 
-template <int J, int SPT, typename LT>
+// DER: how the odd channels are made (0: loaded as they are; 1 softmax, 2
+// sigmoid: the hessian of the even channel's output, formed after the load).
+// With DER the two channels of an output come from one column of G, loaded
+// once.
+template <int J, int SPT, typename LT, int DER>
 __device__ inline void leaf_load(const LeafArgs& a, const float* const (&col)[J], int c0, int t, int top,
                                  LeafTile<J, SPT>& x) {
   // Rows past the end load row n-1 and get a negative leaf id, which drops
@@ -121,9 +126,9 @@ __device__ inline void leaf_load(const LeafArgs& a, const float* const (&col)[J]
     const int l = (int)ids[rc];
     x.lf[s] = (l > top ? top : l) - (row < a.n ? 0 : 0x10000);
 #pragma unroll
-    for (int j = 0; j < J; ++j) x.v[s][j] = col[j][rc];
+    for (int j = 0; j < J; ++j) x.v[s][j] = (DER && J >= 2 && (j & 1)) ? x.v[s][j - 1] : col[j][rc];
   }
-  if (a.derive) {
+  if constexpr (DER != 0) {
     // odd channel 2o+1: the hessian of output o from g = G[i, o]:
     // softmax p = g + [o == label], sigmoid s = g + Y[i, o]; h = p (1 - p).
     // Applied after every load of the tile is issued.
@@ -132,20 +137,26 @@ __device__ inline void leaf_load(const LeafArgs& a, const float* const (&col)[J]
     for (int s = 0; s < SPT; ++s) {
       const int64_t row = r0 + threadIdx.x + LEAF_THREADS * s;
       const int64_t rc = row < a.n ? row : a.n - 1;
-      const int y = a.derive == 1 ? (int)a.labels[rc] : -1;
+      const int y = DER == 1 ? (int)a.labels[rc] : -1;
 #pragma unroll
       for (int j = 0; j < J; ++j) {
         const int c = c0 + j, o = c >> 1;
-        tg[s][j] = a.derive == 1 ? (o == y ? 1.0f : 0.0f)
-                                 : (float)a.Y[(int64_t)(o < a.d ? o : a.d - 1) * a.ld_y + rc];
+        if (J >= 2 && !(j & 1)) {
+          tg[s][j] = 0.0f;  // even channel: g itself
+        } else if constexpr (DER == 1) {
+          tg[s][j] = o == y ? 1.0f : 0.0f;
+        } else {
+          tg[s][j] = (float)a.Y[(int64_t)(o < a.d ? o : a.d - 1) * a.ld_y + rc];
+        }
       }
     }
+    // c0 is a multiple of J, so for J >= 2 channel c0 + j is odd when j is
+    const bool c0_odd = (c0 & 1) != 0;
 #pragma unroll
     for (int s = 0; s < SPT; ++s)
 #pragma unroll
       for (int j = 0; j < J; ++j) {
-        const int c = c0 + j;
-        if (c & 1) {
+        if (J >= 2 ? (j & 1) != 0 : c0_odd) {
           const float p = x.v[s][j] + tg[s][j];
           x.v[s][j] = p * (1.0f - p);
         }
@@ -204,7 +215,7 @@ __device__ inline void leaf_tile(const LeafTile<J, SPT>& x, const bool (&live)[J
   }
 }
 
-template <int J, int SPT, typename LT>
+template <int J, int SPT, typename LT, int DER>
 __global__ void __launch_bounds__(LEAF_THREADS) k_leaf_accum(LeafArgs a) {
   // Cells are channel-major ([J][n_leaves]): the lanes of one add instruction
   // share the channel, so their addresses differ by leaf and spread over the
@@ -239,7 +250,7 @@ __global__ void __launch_bounds__(LEAF_THREADS) k_leaf_accum(LeafArgs a) {
 
   for (int t = t0; t < t1; ++t) {
     LeafTile<J, SPT> x;
-    leaf_load<J, SPT, LT>(a, col, c0, t, top, x);
+    leaf_load<J, SPT, LT, DER>(a, col, c0, t, top, x);
     leaf_tile(x, live, wmax, sconv, icell, acc, NL, rsh);
   }
   __syncthreads();
@@ -322,12 +333,13 @@ int64_t leaf_ws_for(int64_t n, int32_t nch, int32_t n_leaves, int jmax = LEAF_JM
 
 template <int J, typename LT>
 void launch_accum(const LeafPlan& p, const LeafArgs& a, hipStream_t st) {
-  if (p.spt == LEAF_SPT_DERIVED)
-    hipLaunchKernelGGL((k_leaf_accum<J, LEAF_SPT_DERIVED, LT>), dim3(p.n_chunks, p.splits), dim3(LEAF_THREADS),
-                       (size_t)p.lds, st, a);
+  const dim3 g(p.n_chunks, p.splits);
+  if (a.derive == 1)
+    hipLaunchKernelGGL((k_leaf_accum<J, LEAF_SPT_DERIVED, LT, 1>), g, dim3(LEAF_THREADS), (size_t)p.lds, st, a);
+  else if (a.derive == 2)
+    hipLaunchKernelGGL((k_leaf_accum<J, LEAF_SPT_DERIVED, LT, 2>), g, dim3(LEAF_THREADS), (size_t)p.lds, st, a);
   else
-    hipLaunchKernelGGL((k_leaf_accum<J, LEAF_SPT, LT>), dim3(p.n_chunks, p.splits), dim3(LEAF_THREADS),
-                       (size_t)p.lds, st, a);
+    hipLaunchKernelGGL((k_leaf_accum<J, LEAF_SPT, LT, 0>), g, dim3(LEAF_THREADS), (size_t)p.lds, st, a);
 }
 
 template <typename LT>
