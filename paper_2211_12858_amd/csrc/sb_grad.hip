@@ -64,102 +64,120 @@ __device__ inline void lds_sync() {
   asm volatile("" ::: "memory");
 }
 
+// One tile of k_grad (the loss, whether the tile is full and whether the
+// hessians are stored are template parameters, so the column loop has no
+// runtime branch).  Columns past d in the last chunk load column d-1 and
+// store column d-1's own values there (same address, same value), and d is
+// passed in opaque to the compiler, as in grad_softmax_tile below.
+template <int LOSS, bool FULL, bool HESS>
+__device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], int64_t base, bool first, int d) {
+  const int tid = threadIdx.x;
+  const int64_t row = base + tid;
+  const bool ok = FULL || row < a.n;
+  const int64_t rc = ok ? row : a.n - 1;  // rows past the end read row n-1 and store nothing
+  float m = -INFINITY, s = 0.0f, inv = 0.0f;
+  int y = -1;
+  if constexpr (LOSS == SB_LOSS_SOFTMAX_CE) {
+    y = a.labels[rc];
+    for (int j0 = 0; j0 < d; j0 += GRAD_JA) {
+      float x[GRAD_JA];
+      // columns past d (last chunk only) repeat column d-1: a repeat of
+      // the row's own score leaves the maximum unchanged, and its exp is
+      // dropped from the sum below
+#pragma unroll
+      for (int u = 0; u < GRAD_JA; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
+      float cm = x[0];
+#pragma unroll
+      for (int u = 1; u < GRAD_JA; ++u) cm = fmaxf(cm, x[u]);
+      const float mn = fmaxf(m, cm);
+      float add = 0.0f;
+#pragma unroll
+      for (int u = 0; u < GRAD_JA; ++u) add += (j0 + u < d) ? expf(x[u] - mn) : 0.0f;
+      s = s * expf(m - mn) + add;
+      m = mn;
+    }
+    inv = 1.0f / s;
+  }
+  float hsum = 0.0f;
+  for (int j0 = 0; j0 < d; j0 += GRAD_JC) {
+    float x[GRAD_JC];
+#pragma unroll
+    for (int u = 0; u < GRAD_JC; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
+    uint8_t yb[GRAD_JC];
+    if constexpr (LOSS == SB_LOSS_SIGMOID_BCE) {
+#pragma unroll
+      for (int u = 0; u < GRAD_JC; ++u) yb[u] = a.Y[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_y + rc];
+    }
+#pragma unroll
+    for (int u = 0; u < GRAD_JC; ++u) {
+      const int j = j0 + u;
+      const int jj = j < d ? j : d - 1;
+      float g, hh;
+      if constexpr (LOSS == SB_LOSS_SOFTMAX_CE) {
+        const float p = expf(x[u] - m) * inv;
+        g = (jj == y) ? p - 1.0f : p;
+        hh = p * (1.0f - p);
+      } else {
+        // e = exp(-|a|) never overflows, so s keeps its relative accuracy
+        // for scores far below zero (down to fp32's subnormals)
+        const float e = expf(-fabsf(x[u]));
+        const float sg = x[u] >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
+        g = sg - (float)yb[u];
+        hh = sg * (1.0f - sg);
+      }
+      if (ok) {
+        a.G[(int64_t)jj * a.ld_g + row] = g;
+        if (HESS) a.hess[(int64_t)jj * a.ld_h + row] = hh;
+      }
+      hsum += (j < d) ? hh : 0.0f;
+      gbuf[u][tid] = ok ? g : 0.0f;
+    }
+    if (a.npart) {
+      lds_sync();
+      // 16 threads per column, 16 rows each; lanes c*16 .. c*16+15 share column c
+      const int c = tid >> 4, seg = tid & 15;
+      const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
+      double acc = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = src[q];
+        acc += (double)v.x * v.x;
+        acc += (double)v.y * v.y;
+        acc += (double)v.z * v.z;
+        acc += (double)v.w * v.w;
+      }
+      for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+      if (seg == 0 && j0 + c < d) {
+        double* pp = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
+        *pp = first ? acc : *pp + acc;
+      }
+      lds_sync();
+    }
+  }
+  if (a.h_row && ok) a.h_row[row] = hsum * (1.0f / (float)d);
+}
+
+template <int LOSS>
 __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
   __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
-  const int tid = threadIdx.x;
-  const int d = a.d;
-  const float inv_d = 1.0f / (float)d;
   bool first = true;
   for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
-    const int64_t row = (int64_t)tile * GRAD_THREADS + tid;
-    const bool ok = row < a.n;
-    const int64_t rc = ok ? row : a.n - 1;  // rows past the end read row n-1 and store nothing
-    float m = -INFINITY, s = 0.0f, inv = 0.0f;
-    int y = -1;
-    if (a.loss == SB_LOSS_SOFTMAX_CE) {
-      y = a.labels[rc];
-      for (int j0 = 0; j0 < d; j0 += GRAD_JA) {
-        float x[GRAD_JA];
-        // columns past d (last chunk only) repeat column d-1: a repeat of
-        // the row's own score leaves the maximum unchanged, and its exp is
-        // dropped from the sum below
-#pragma unroll
-        for (int u = 0; u < GRAD_JA; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
-        float cm = x[0];
-#pragma unroll
-        for (int u = 1; u < GRAD_JA; ++u) cm = fmaxf(cm, x[u]);
-        const float mn = fmaxf(m, cm);
-        float add = 0.0f;
-#pragma unroll
-        for (int u = 0; u < GRAD_JA; ++u) add += (j0 + u < d) ? expf(x[u] - mn) : 0.0f;
-        s = s * expf(m - mn) + add;
-        m = mn;
-      }
-      inv = 1.0f / s;
+    int d = a.d;
+    asm volatile("" : "+s"(d));
+    const int64_t base = (int64_t)tile * GRAD_THREADS;
+    const bool full = base + GRAD_THREADS <= a.n;
+    if (a.hess) {
+      if (full) grad_tile<LOSS, true, true>(a, gbuf, base, first, d);
+      else grad_tile<LOSS, false, true>(a, gbuf, base, first, d);
+    } else {
+      if (full) grad_tile<LOSS, true, false>(a, gbuf, base, first, d);
+      else grad_tile<LOSS, false, false>(a, gbuf, base, first, d);
     }
-    float hsum = 0.0f;
-    for (int j0 = 0; j0 < d; j0 += GRAD_JC) {
-      float x[GRAD_JC];
-#pragma unroll
-      for (int u = 0; u < GRAD_JC; ++u) x[u] = a.F[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_f + rc];
-      uint8_t yb[GRAD_JC];
-      if (a.loss == SB_LOSS_SIGMOID_BCE) {
-#pragma unroll
-        for (int u = 0; u < GRAD_JC; ++u) yb[u] = a.Y[(int64_t)(j0 + u < d ? j0 + u : d - 1) * a.ld_y + rc];
-      }
-#pragma unroll
-      for (int u = 0; u < GRAD_JC; ++u) {
-        const int j = j0 + u;
-        float g = 0.0f, hh = 0.0f;
-        if (j < d) {
-          if (a.loss == SB_LOSS_SOFTMAX_CE) {
-            const float p = expf(x[u] - m) * inv;
-            g = (j == y) ? p - 1.0f : p;
-            hh = p * (1.0f - p);
-          } else {
-            // e = exp(-|a|) never overflows, so s keeps its relative accuracy
-            // for scores far below zero (down to fp32's subnormals)
-            const float e = expf(-fabsf(x[u]));
-            const float sg = x[u] >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
-            g = sg - (float)yb[u];
-            hh = sg * (1.0f - sg);
-          }
-          if (ok) {
-            a.G[(int64_t)j * a.ld_g + row] = g;
-            if (a.hess) a.hess[(int64_t)j * a.ld_h + row] = hh;
-          }
-          hsum += hh;
-        }
-        gbuf[u][tid] = ok ? g : 0.0f;
-      }
-      if (a.npart) {
-        lds_sync();
-        // 16 threads per column, 16 rows each; lanes c*16 .. c*16+15 share column c
-        const int c = tid >> 4, seg = tid & 15;
-        const float4* src = reinterpret_cast<const float4*>(&gbuf[c][seg * 16]);
-        double acc = 0.0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = src[q];
-          acc += (double)v.x * v.x;
-          acc += (double)v.y * v.y;
-          acc += (double)v.z * v.z;
-          acc += (double)v.w * v.w;
-        }
-        for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-        if (seg == 0 && j0 + c < d) {
-          double* p = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
-          *p = first ? acc : *p + acc;
-        }
-        lds_sync();
-      }
-    }
-    if (a.h_row && ok) a.h_row[row] = hsum * inv_d;
     first = false;
   }
   // a block without tiles still defines its partials
   if (a.npart && first)
-    for (int j = tid; j < d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
+    for (int j = threadIdx.x; j < a.d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
 }
 
 // Softmax cross-entropy with the row's d <= DMAX scores held in registers:
@@ -373,8 +391,10 @@ int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int
     hipLaunchKernelGGL(k_grad_softmax_regs<64>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
   else if (loss == SB_LOSS_SOFTMAX_CE && d <= 104)
     hipLaunchKernelGGL(k_grad_softmax_regs<104>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  else if (loss == SB_LOSS_SOFTMAX_CE)
+    hipLaunchKernelGGL(k_grad<SB_LOSS_SOFTMAX_CE>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
   else
-    hipLaunchKernelGGL(k_grad, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+    hipLaunchKernelGGL(k_grad<SB_LOSS_SIGMOID_BCE>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
   if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, blocks, norm2);
   return check_launch("sb_gradients");
 }

@@ -97,7 +97,9 @@ def check_gradients(loss, F_T, target):
     return G, H, hr, n2
 
 
-@pytest.mark.parametrize("d", [1, 5, 17, 100])
+# d at and around each kernel boundary: rows held in registers for d <= 16,
+# 32, 64, 104, the two-pass kernel above (ragged last column chunks)
+@pytest.mark.parametrize("d", [1, 5, 16, 17, 32, 64, 100, 104, 105, 130, 257])
 def test_softmax_gradients(d):
     F_T, y = scores_and_targets(3 * 256 + 77, d, "softmax", seed=d, scale=2.0)
     G, H, _, _ = check_gradients("softmax", F_T, y)
@@ -105,7 +107,7 @@ def test_softmax_gradients(d):
         assert np.abs(G.astype(np.float64).sum(axis=0)).max() < (d + 24) * U
 
 
-@pytest.mark.parametrize("d", [1, 8, 33])
+@pytest.mark.parametrize("d", [1, 8, 33, 130])
 def test_sigmoid_gradients(d):
     F_T, Y = scores_and_targets(5 * 256 + 3, d, "sigmoid", seed=100 + d, scale=3.0)
     check_gradients("sigmoid", F_T, Y)
@@ -119,6 +121,8 @@ def test_gradients_many_tiles_per_block():
 
 def test_gradients_extreme_scores():
     F_T, y = scores_and_targets(1000, 6, "softmax", seed=8, scale=40.0)
+    check_gradients("softmax", F_T, y)
+    F_T, y = scores_and_targets(1000, 120, "softmax", seed=11, scale=40.0)
     check_gradients("softmax", F_T, y)
     F_T, Y = scores_and_targets(1000, 6, "sigmoid", seed=9, scale=40.0)
     check_gradients("sigmoid", F_T, Y)
