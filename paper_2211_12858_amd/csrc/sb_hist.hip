@@ -273,12 +273,13 @@ __device__ inline void load_run(const uint32_t* p, uint32_t* out) {
 // the 32 banks once and a cell's bank pair is its feature; at step i lane l
 // adds its row's values for feature (i + l) mod 16.  Each step then puts
 // exactly four lanes on every bank pair, whatever the bins.  Measured on
-// MI355X with random bins: 17.8 channel-adds/clk/CU, against 8.8 for the
-// one-feature-per-wave order.  A lane rotates its row's 16 bin bytes once
-// (by l mod 16), so that step i reads byte i.  Features past m come from
-// padding bytes (the row records hold ld_rec >= m bytes, ld_rec % 16 == 0;
-// the quad-major planes are clamped to the last one) and land in feature
-// columns that the reduction never reads.
+// MI355X with random bins: 6.5 clocks per wave instruction (19.75
+// channel-adds/clk/CU), the rate of any 64-bit LDS write or atomic, against
+// 13.9 clocks for the one-feature-per-wave order.  A lane rotates its row's
+// 16 bin bytes once (by l mod 16), so that step i reads byte i.  Features
+// past m come from padding bytes (the row records hold ld_rec >= m bytes,
+// ld_rec % 16 == 0; the quad-major planes are clamped to the last one) and
+// land in feature columns that the reduction never reads.
 
 // Byte i of out = byte (i + r) mod 16 of the 16 bytes in w: whole words by
 // r / 4 in two mask stages (bitfield inserts, so that the compiler keeps the
