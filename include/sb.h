@@ -170,7 +170,9 @@ int32_t sb_layout_bins(const uint8_t* bins, int64_t n, int32_t m, int64_t ld_bin
  *                    accumulation.  cols / scales / norm2 are not written.
  *   IDENTITY         k == d, GH = [G, h].
  * u       RANDOM_SAMPLING only: k uniforms in [0, 1) (fp64, device).  The
- *         random numbers are an input so that results are reproducible.
+ *         paper fixes the distribution of the draws (Section 3.2), not a
+ *         generator; the random numbers are an input so that results are
+ *         reproducible and can be checked draw by draw.
  * Pi      RANDOM_PROJECTION only: d x k, row-major (Pi[j*k + t]), fp32.
  * GH      out: row-major sketch, ld_gh >= k+1 floats per row, 16-byte aligned:
  *         GH[i*ld_gh + t] = fp32(G[i, cols[t]] * scales[t]) for t < k (one
@@ -242,7 +244,10 @@ int32_t sb_hist_exponents(const float* GH, int64_t n, int64_t ld_gh, int32_t k, 
  *   H[((j*m + f)*(k+1) + t)*n_bins + b] = sum over the rows r of node j whose
  *       feature f has bin b of channel t of r's sketch,
  * accumulated exactly in fixed point (see sb_hist_exponents) and written as
- * fp64.  Nodes not in the build list are left untouched.
+ * fp64.  The paper does not fix the histogram arithmetic; fixed point makes
+ * the sums exact and independent of the order of the adds, so results do
+ * not depend on the grid and sibling subtraction is exact.  Nodes not in
+ * the build list are left untouched.
  *
  * The bins come from one of two sources, the sketch always from GH
  * (row-major, ld_gh >= k+1, 16-byte aligned, n rows):
@@ -295,7 +300,9 @@ int32_t sb_subtract_histograms(const double* H_parent, double* H_child, int32_t 
  * valid iff HL > min_child_weight and HR > min_child_weight.  The best valid
  * candidate maximises S; ties go to the lower f, then the lower b.  Scores
  * are evaluated in fp64.  A node without a valid candidate gets
- * (-1, -1, -inf).
+ * (-1, -1, -inf).  The paper states neither the tie rule nor the treatment
+ * of empty children or nodes without a valid split; these are the library's
+ * rules.
  * H: [n_nodes][m][k+1][n_bins] fp64.  lambda > 0, min_child_weight >= 0.
  * best_feature, best_bin, best_score: out, n_nodes entries each.
  */
