@@ -756,7 +756,28 @@ k_subtract(const double* __restrict__ Hp, double* __restrict__ Hc, int64_t cpn, 
     dst[i] = src[i] - built[i];
 }
 
-constexpr int MAX_BPL_F = 4;  // bins per lane in the fused scoring (n_bins <= 256)
+// A double moved across lanes by a DPP control (row shift or row broadcast),
+// both 32-bit halves alike; lanes the control does not write get 0.
+template <int CTRL, int ROW_MASK>
+__device__ inline double dpp_move(double x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, ROW_MASK, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, ROW_MASK, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (all lanes active), in
+// registers: shifts by 1, 2, 4 and 8 lanes inside each row of 16, then the
+// last lane of rows 0 and 2 is added to rows 1 and 3 (row_bcast:15) and
+// lane 31 to rows 2 and 3 (row_bcast:31).
+__device__ inline double wave_inclusive_scan(double x) {
+  x += dpp_move<0x111, 0xf>(x);
+  x += dpp_move<0x112, 0xf>(x);
+  x += dpp_move<0x114, 0xf>(x);
+  x += dpp_move<0x118, 0xf>(x);
+  x += dpp_move<0x142, 0xa>(x);
+  x += dpp_move<0x143, 0xc>(x);
+  return x;
+}
 
 __device__ inline bool score_better(double sa, int ia, double sb_, int ib) {
   return sa > sb_ || (sa == sb_ && ia < ib);
@@ -778,7 +799,10 @@ struct ScoreOut {
 // RQ threads per bin: each sums its share of the node's row groups, and the
 // shares meet in LDS (integers, so the order does not matter).  The first
 // 256 threads then carry the bin through the rest.  RQ = 4 where a node
-// spans many row groups (the first levels), else 1.
+// spans many row groups (the first levels), else 1.  The scan over bins runs
+// in registers (DPP inside each wave, wave totals through LDS), so a block
+// holds under 1 KB of LDS past the quarters' sums and the deep levels, with
+// thousands of blocks, are limited by registers: 4 to 6 blocks per CU.
 template <int PMAX, int RQ>
 __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, ScoreOut so) {
   const int f = blockIdx.x, p = blockIdx.y;
@@ -800,15 +824,21 @@ __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, Scor
   const int64_t qlo = nlo + quarter * per;
   const int64_t qhi = (qlo + per - 1 < nhi) ? qlo + per - 1 : nhi;
   const bool dense = T >= qn;  // every row group holds at least one position
+  // The parent's values for the sibling, loaded first so that this read and
+  // the partials' are in flight together (a block reads them once each).
+  double hp[2 * PMAX];
+#pragma unroll
+  for (int t = 0; t < 2 * PMAX; ++t) {
+    hp[t] = 0.0;
+    if (sib && t < c && on && quarter == 0) hp[t] = a.Hp[(int64_t)p * cpn + ((int64_t)f * c + t) * B + bin];
+  }
   // int64 channel sums of this bin over the node's row groups, from the
   // int32 partials.  Fast path: batches of BQ row groups and every channel
-  // pair, double-buffered (the next batch's loads are issued before this
-  // batch is added, so a node of many row groups waits for about one memory
-  // latency, not one per batch), loads unconditional (groups past the node's
-  // last and pairs past the last repeat it; the extra values are dropped),
-  // no branch on the values: escapes are only flagged.  A lane that met an
-  // escape sums its bin again with the overflow slots (rare: a workgroup's
-  // sum of one bin must pass 2^31).
+  // pair, loads unconditional (groups past the node's last and pairs past
+  // the last repeat it; the extra values are dropped), no branch on the
+  // values: escapes are only flagged.  A lane that met an escape sums its
+  // bin again with the overflow slots (rare: a workgroup's sum of one bin
+  // must pass 2^31).
   int64_t acc_lo[PMAX], acc_hi[PMAX];
 #pragma unroll
   for (int pr = 0; pr < PMAX; ++pr) acc_lo[pr] = acc_hi[pr] = 0;
@@ -841,18 +871,11 @@ __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, Scor
             esc |= use && (x.x == PART_ESC || x.y == PART_ESC);
           }
       };
-      int2 va[BQ][PMAX], vb[BQ][PMAX];
-      int64_t q = qlo;
-      load(q, va);
-      for (; q + BQ <= qhi; q += BQ) {
-        load(q + BQ, vb);
-        add(q, va);
-#pragma unroll
-        for (int u = 0; u < BQ; ++u)
-#pragma unroll
-          for (int pr = 0; pr < PMAX; ++pr) va[u][pr] = vb[u][pr];
+      for (int64_t q = qlo; q <= qhi; q += BQ) {
+        int2 vq[BQ][PMAX];
+        load(q, vq);
+        add(q, vq);
       }
-      add(q, va);
     } else {
       // fewer positions than row groups (tiny levels): empty groups wrote nothing
       for (int64_t q = qlo; q <= qhi; ++q) {
@@ -887,9 +910,8 @@ __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, Scor
     }
   }
   // the quarters meet: quarters 1..3 leave their sums in LDS, quarter 0
-  // adds them (the same LDS then stages the fp64 values for the scan)
-  extern __shared__ double xv[];
-  longlong2* part = reinterpret_cast<longlong2*>(xv);  // [quarter - 1][pair][256]
+  // adds them
+  extern __shared__ longlong2 part[];  // [quarter - 1][pair][256]
   if (RQ > 1 && quarter > 0) {
 #pragma unroll
     for (int pr = 0; pr < PMAX; ++pr) part[((quarter - 1) * PMAX + pr) * 256 + bin] = make_longlong2(acc_lo[pr], acc_hi[pr]);
@@ -905,89 +927,116 @@ __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, Scor
         acc_hi[pr] += v.y;
       }
   }
-  if (RQ > 1) __syncthreads();  // the partial sums are read: the LDS becomes the scan's staging
-  // fp64 histogram values of this bin: written to H (and the sibling by
-  // subtraction) and staged in LDS as [node][channel][bin] for the scan
+  // fp64 histogram values of this bin, v[0] of the built node j and v[1] of
+  // its sibling (by subtraction), written to H and kept in registers for the
+  // scan: the bins are the block's first 256 threads, so the prefix over
+  // bins is a prefix over lanes, then over the block's first waves
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nw = (B + 63) >> 6;  // waves that hold bins
+  const bool scan_wave = quarter == 0 && wave < nw;
+  double v[2][2 * PMAX];
 #pragma unroll
   for (int t = 0; t < 2 * PMAX; ++t) {
+    v[0][t] = v[1][t] = 0.0;
     if (t < c && on && quarter == 0) {
       const int64_t idx = ((int64_t)f * c + t) * B + bin;
       const double x = ldexp((double)((t & 1) ? acc_hi[t >> 1] : acc_lo[t >> 1]), -a.qexp[t]);
       if (a.store_h) a.H[(int64_t)j * cpn + idx] = x;
-      xv[t * B + bin] = x;
+      v[0][t] = x;
       if (sib) {
-        const double xs = a.Hp[(int64_t)p * cpn + idx] - x;
+        const double xs = hp[t] - x;
         if (a.store_h) a.H[(int64_t)(j ^ 1) * cpn + idx] = xs;
-        xv[(c + t) * B + bin] = xs;
+        v[1][t] = xs;
       }
     }
+  }
+  // Every value is a multiple of 2^-qexp below 2^53 of those units in
+  // magnitude (a node's channel sum is at most 2^31 rows of 2^QBITS), so
+  // fp64 sums of them are exact and any order of the scan gives the same
+  // bits.  Wave totals meet in LDS as [node][channel][wave].
+  __shared__ double wtot[2][2 * PMAX][4];
+  __shared__ double wbest_s[2][4];
+  __shared__ int32_t wbest_b[2][4];
+  const int nodes = sib ? 2 : 1;
+  if (scan_wave) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < 2 * PMAX; ++t)
+        if (u < nodes && t < c) {
+          v[u][t] = wave_inclusive_scan(v[u][t]);
+          if (lane == 63) wtot[u][t][wave] = v[u][t];
+        }
+  } else if (quarter == 0 && lane == 0) {
+    // a wave past the last bin adds nothing
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < 2 * PMAX; ++t) wtot[u][t][wave] = 0.0;
   }
   __syncthreads();
-  // one wave per node: lane l owns bins l*bpl .. l*bpl+bpl-1; per channel a
-  // lane prefix plus a wave scan gives the inclusive prefix over bins
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (wave >= (sib ? 2 : 1)) return;
-  const double* xn = xv + wave * c * B;
-  const int bpl = (B + 63) / 64;
-  const int b0 = lane * bpl;
-  double sl[MAX_BPL_F], sr[MAX_BPL_F], hl[MAX_BPL_F];
-  double th = 0.0;
+  if (scan_wave) {
 #pragma unroll
-  for (int i = 0; i < MAX_BPL_F; ++i) sl[i] = sr[i] = hl[i] = 0.0;
-  for (int t = 0; t < c; ++t) {
-    double pfx[MAX_BPL_F];
-    double r = 0.0;
+    for (int u = 0; u < 2; ++u) {
+      if (u < nodes) {
+        // Section 2, eq. 4 for every threshold b (left: bins <= b): gradient
+        // channels t < k add L^2 and R^2, the last channel is the hessian
+        double sl = 0.0, sr = 0.0, HL = 0.0, HR = 0.0;
 #pragma unroll
-    for (int i = 0; i < MAX_BPL_F; ++i) {
-      if (i < bpl && b0 + i < B) r += xn[t * B + b0 + i];
-      pfx[i] = r;
-    }
-    double in = r;
-    for (int off = 1; off < 64; off <<= 1) {
-      const double o = __shfl_up(in, off, 64);
-      if (lane >= off) in += o;
-    }
-    const double ex = in - r;
-    const double tot = __shfl(in, 63, 64);
-    if (t < k) {
+        for (int t = 0; t < 2 * PMAX; ++t) {
+          if (t < c) {
+            double before = 0.0, tot = 0.0;
 #pragma unroll
-      for (int i = 0; i < MAX_BPL_F; ++i) {
-        const double L = pfx[i] + ex, R = tot - L;
-        sl[i] += L * L;
-        sr[i] += R * R;
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < MAX_BPL_F; ++i) hl[i] = pfx[i] + ex;
-      th = tot;
-    }
-  }
-  double best_s = -INFINITY;
-  int best_b = -1;
-#pragma unroll
-  for (int i = 0; i < MAX_BPL_F; ++i) {
-    const int b = b0 + i;
-    if (i < bpl && b <= B - 2) {
-      const double HL = hl[i], HR = th - hl[i];
-      if (HL > so.mcw && HR > so.mcw) {
-        const double S = sl[i] / (HL + so.lam) + sr[i] / (HR + so.lam);
-        if (S > best_s) {
-          best_s = S;
-          best_b = b;
+            for (int w = 0; w < 4; ++w) {
+              const double x = wtot[u][t][w];
+              tot += x;
+              before += w < wave ? x : 0.0;
+            }
+            const double L = v[u][t] + before, R = tot - L;
+            if (t < k) {
+              sl += L * L;
+              sr += R * R;
+            } else {
+              HL = L;
+              HR = R;
+            }
+          }
+        }
+        double best_s = -INFINITY;
+        int best_b = -1;
+        if (on && bin <= B - 2 && HL > so.mcw && HR > so.mcw) {
+          best_s = sl / (HL + so.lam) + sr / (HR + so.lam);
+          best_b = bin;
+        }
+        for (int off = 32; off > 0; off >>= 1) {
+          const double os = __shfl_xor(best_s, off, 64);
+          const int ob = __shfl_xor(best_b, off, 64);
+          if (ob >= 0 && (best_b < 0 || score_better(os, ob, best_s, best_b))) {
+            best_s = os;
+            best_b = ob;
+          }
+        }
+        if (lane == 0) {
+          wbest_s[u][wave] = best_s;
+          wbest_b[u][wave] = best_b;
         }
       }
     }
   }
-  for (int off = 32; off > 0; off >>= 1) {
-    const double os = __shfl_xor(best_s, off, 64);
-    const int ob = __shfl_xor(best_b, off, 64);
-    if (ob >= 0 && (best_b < 0 || score_better(os, ob, best_s, best_b))) {
-      best_s = os;
-      best_b = ob;
+  __syncthreads();
+  if (threadIdx.x < nodes) {
+    const int u = threadIdx.x;
+    double best_s = -INFINITY;
+    int best_b = -1;
+    for (int w = 0; w < nw; ++w) {
+      const double os = wbest_s[u][w];
+      const int ob = wbest_b[u][w];
+      if (ob >= 0 && (best_b < 0 || score_better(os, ob, best_s, best_b))) {
+        best_s = os;
+        best_b = ob;
+      }
     }
-  }
-  if (lane == 0) {
-    const int32_t nd = wave ? (j ^ 1) : j;
+    const int32_t nd = u ? (j ^ 1) : j;
     so.s[(int64_t)nd * a.m + f] = best_s;
     so.b[(int64_t)nd * a.m + f] = best_b;
   }
@@ -1096,16 +1145,15 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
   if (feat_s) {
     ScoreOut so{feat_s, feat_b, lam, mcw};
     const dim3 g(m, n_build);
-    // [node][channel][bin] fp64 values of the built node and its sibling, or
-    // before them the partial sums of quarters 1..3 ([quarter][pair][256])
-    const int pm = pl.pairs <= 3 ? 3 : pl.pairs <= 4 ? 4 : 8;
+    // dynamic LDS: the partial sums of quarters 1..3 ([quarter][pair][256])
+    const int pm = pl.pairs <= 3 ? 3 : pl.pairs <= 4 ? 4 : pl.pairs <= 6 ? 6 : 8;
     const bool wide = pl.q >= 12 * n_build;  // a node spans about q / n_build row groups
     const int rq = wide ? 4 : 1;
-    const size_t lv = (size_t)2 * pl.c * n_bins * 8, lp = (size_t)(rq - 1) * pm * 256 * 16;
-    const size_t lds = lv > lp ? lv : lp;
+    const size_t lds = (size_t)(rq - 1) * pm * 256 * 16;
 #define SB_RS(P, R) hipLaunchKernelGGL((k_hist_reduce_score<P, R>), g, dim3(256 * R), lds, st, a, so)
     if (pm == 3) { if (wide) SB_RS(3, 4); else SB_RS(3, 1); }
     else if (pm == 4) { if (wide) SB_RS(4, 4); else SB_RS(4, 1); }
+    else if (pm == 6) { if (wide) SB_RS(6, 4); else SB_RS(6, 1); }
     else if (pl.pairs <= 8) { if (wide) SB_RS(8, 4); else SB_RS(8, 1); }
 #undef SB_RS
     else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 16 channels");
