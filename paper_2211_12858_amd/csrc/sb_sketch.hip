@@ -204,9 +204,13 @@ constexpr int PACK_THREADS = 256;
 constexpr int PACK_ROWS = 4;                           // rows per thread per pass
 constexpr int64_t PACK_ROWS_PER_BLOCK = PACK_THREADS * PACK_ROWS;
 constexpr int PACK_CG = 16;                            // floats of a row written per pass
-// Grid cap of the sketch kernels: block b writes its per-channel maxima to
-// blockmax[b*(k+1) + t], reduced afterwards by k_qexp (no atomics).
-constexpr int SKETCH_MAX_BLOCKS = 2048;
+// Grid caps of the sketch kernels: block b writes its per-channel maxima to
+// blockmax[b*(k+1) + t], reduced afterwards by k_qexp (no atomics), so the
+// workspace holds SKETCH_MAX_BLOCKS rows of maxima.  The streaming kernels
+// loop over rows in at most SKETCH_GRID_BLOCKS blocks; the matrix-core
+// projection takes one block per 512-row tile up to SKETCH_MAX_BLOCKS.
+constexpr int SKETCH_MAX_BLOCKS = 4096;
+constexpr int SKETCH_GRID_BLOCKS = 2048;
 
 // The floats g0..g0+gn-1 of row i, 16-byte stores when the row allows (every
 // row of a multiple-of-4 stride starts 16-byte aligned).
@@ -560,94 +564,111 @@ k_project_sparse(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, co
   }
 }
 
-// Dense projection on the matrix cores: G (n x d) times Pi (d x k) with
-// v_mfma_f32_32x32x2f32, fp32 products accumulated in fp32 (MI355X's fp32
-// MFMA rate is twice its fp32 vector rate without packed instructions, so at
-// k >= 8 the product stops being bound by the VALU).  A wave computes
-// MF_MT * 32 rows x the pass's 32 output columns.  Operands:
-//   A (32 x 2): lane l holds G[row0 + l % 32, j + l / 32] -- lanes 0-31 and
-//     32-63 each read 32 consecutive rows of one column (one 128-byte line);
-//   B (2 x 32): lane l holds Pi[j + l / 32, t0 + l % 32], from a block of Pi
-//     staged in LDS (zero past d and past the pass's kt columns);
-//   D (32 x 32): register r of lane l holds row (r / 4) * 8 + (l / 32) * 4 +
-//     r % 4, column l % 32.
-// Eight 2-column steps of A are loaded before their MFMAs.  The order in
-// which the hardware adds the products is its own, so the result is checked
-// against the exact product with the dot-product error bound.
-constexpr int MF_THREADS = 256;
-constexpr int MF_JC = 256;  // columns of G per staged block of Pi (32 KB)
-constexpr int MF_KU = 8;    // 2-column steps per batch of loads
-constexpr int MF_MT = 2;    // 32-row tiles per wave
-typedef float mf_v16 __attribute__((ext_vector_type(16)));
+// Dense projection on the matrix cores with v_mfma_f32_4x4x1f32, whose 16
+// blocks of 4 x 4 x 1 are here 16 groups of 4 consecutive rows of G sharing
+// one column j: one instruction multiplies 64 rows of column j by row j of
+// Pi for 4 sketch columns, so k columns take ceil(k / 4) instructions and
+// nothing is padded past a multiple of 4 (the 32 x 32 tile pads 20 columns
+// to 32).  It runs at the same flops per clock as the 32 x 32 x 2 form, and
+// MI355X's fp32 MFMA rate is twice its fp32 vector rate without packed
+// instructions, so at k >= 8 the product stops being bound by the VALU.
+// A wave computes M4_MT * 64 rows x 4 * NG sketch columns.  Operands:
+//   A (block b, 4 x 1): lane l holds G[row0 + l, j] (64 consecutive rows of
+//     one column: two 128-byte lines);
+//   B (block b, 1 x 4): lane l holds Pi[j, t0 + 4g + l % 4], the same in
+//     every block, read from a block of Pi staged in LDS (zero past d and
+//     past the pass's kt columns: four addresses per read, a broadcast);
+//   D (block b, 4 x 4): register r of lane l holds row row0 + 4 (l / 4) + r,
+//     column t0 + 4g + l % 4.
+// M4_KU columns of G are loaded before their MFMAs.  The order in which the
+// hardware adds the products is its own, so the result is checked against
+// the exact product with the dot-product error bound.
+constexpr int M4_THREADS = 256;
+constexpr int M4_MT = 2;    // 64-row tiles per wave
+constexpr int M4_JC = 256;  // columns of G per staged block of Pi
+constexpr int M4_KU = 16;   // columns of G per batch of loads
+static_assert(M4_JC % M4_KU == 0, "a batch of columns never passes the staged block");
+typedef float mf_v4 __attribute__((ext_vector_type(4)));
 
-__global__ void __launch_bounds__(MF_THREADS)
-k_project_mfma(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k,
-               int t0, const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh,
-               uint32_t* __restrict__ blockmax) {
-  __shared__ float sPi[MF_JC * 32];
-  __shared__ uint32_t smax[MF_THREADS / 64][33];
+template <int NG>
+__global__ void __launch_bounds__(M4_THREADS)
+k_project_mfma4(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, const float* __restrict__ Pi, int k,
+                int t0, const float* __restrict__ h, float* __restrict__ GH, int64_t ld_gh,
+                uint32_t* __restrict__ blockmax) {
+  constexpr int W = 4 * NG;  // sketch columns of the pass, padded to a multiple of 4
+  __shared__ float sPi[M4_JC * W];
+  __shared__ uint32_t smax[M4_THREADS / 64][W + 1];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int kt = (k - t0 < 32) ? k - t0 : 32;
-  const bool last = t0 + 32 >= k;
-  const int col = lane & 31, khalf = lane >> 5;
-  uint32_t mxc = 0u, mxh = 0u;
-  constexpr int64_t ROWS = (MF_THREADS / 64) * MF_MT * 32;  // rows per block per pass
-  for (int64_t base = (int64_t)blockIdx.x * ROWS; base < n; base += (int64_t)gridDim.x * ROWS) {
-    const int64_t rw = base + (int64_t)wave * MF_MT * 32;
-    int64_t rc[MF_MT];
+  const int kt = (k - t0 < W) ? k - t0 : W;
+  const bool last = t0 + kt >= k;
+  const int cq = lane & 3;  // this lane's column within each group of 4
+  uint32_t mx[NG], mxh = 0u;
 #pragma unroll
-    for (int mt = 0; mt < MF_MT; ++mt) {
-      const int64_t r = rw + mt * 32 + col;
+  for (int g = 0; g < NG; ++g) mx[g] = 0u;
+  constexpr int64_t ROWS = (M4_THREADS / 64) * M4_MT * 64;  // rows per block per pass
+  for (int64_t base = (int64_t)blockIdx.x * ROWS; base < n; base += (int64_t)gridDim.x * ROWS) {
+    const int64_t rw = base + (int64_t)wave * M4_MT * 64;
+    int64_t rc[M4_MT];
+#pragma unroll
+    for (int mt = 0; mt < M4_MT; ++mt) {
+      const int64_t r = rw + mt * 64 + lane;
       rc[mt] = r < n ? r : n - 1;  // rows past the end read row n-1 and store nothing
     }
-    mf_v16 acc[MF_MT];
+    mf_v4 acc[M4_MT][NG];
 #pragma unroll
-    for (int mt = 0; mt < MF_MT; ++mt)
+    for (int mt = 0; mt < M4_MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
-    for (int j0 = 0; j0 < d; j0 += MF_JC) {
-      const int jc = (d - j0 < MF_JC) ? d - j0 : MF_JC;
+      for (int g = 0; g < NG; ++g) acc[mt][g] = mf_v4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int j0 = 0; j0 < d; j0 += M4_JC) {
+      const int jc = (d - j0 < M4_JC) ? d - j0 : M4_JC;
       __syncthreads();  // the previous block of Pi is no longer read
-      for (int e = threadIdx.x; e < MF_JC * 32; e += MF_THREADS) {
-        const int jj = e >> 5, c = e & 31;
-        sPi[e] = (jj < jc && c < kt) ? Pi[(int64_t)(j0 + jj) * k + t0 + c] : 0.0f;
+      for (int e = threadIdx.x; e < M4_JC * W; e += M4_THREADS) {
+        const int jr = e / W, c = e - jr * W;
+        sPi[e] = (jr < jc && c < kt) ? Pi[(int64_t)(j0 + jr) * k + t0 + c] : 0.0f;
       }
       __syncthreads();
-      for (int kk = 0; kk < jc; kk += 2 * MF_KU) {
-        float a[MF_KU][MF_MT];
+      for (int kk = 0; kk < jc; kk += M4_KU) {
+        float a[M4_KU][M4_MT];
 #pragma unroll
-        for (int u = 0; u < MF_KU; ++u) {
-          const int jj = kk + 2 * u + khalf;
-          const int64_t jg = j0 + (jj < jc ? jj : jc - 1);  // past the block: a finite value times a zero of Pi
+        for (int u = 0; u < M4_KU; ++u) {
+          // past the block: a finite value of column jc - 1 times a zero of Pi
+          const int64_t jg = j0 + (kk + u < jc ? kk + u : jc - 1);
 #pragma unroll
-          for (int mt = 0; mt < MF_MT; ++mt) a[u][mt] = ld_stream(G + jg * ld_g + rc[mt]);
+          for (int mt = 0; mt < M4_MT; ++mt) a[u][mt] = ld_stream(G + jg * ld_g + rc[mt]);
         }
 #pragma unroll
-        for (int u = 0; u < MF_KU; ++u) {
-          const int jj = kk + 2 * u + khalf;
-          const float b = sPi[(jj < MF_JC ? jj : MF_JC - 1) * 32 + col] * (jj < jc ? 1.0f : 0.0f);
+        for (int u = 0; u < M4_KU; ++u) {
+          const float* pr = sPi + (kk + u) * W + cq;
 #pragma unroll
-          for (int mt = 0; mt < MF_MT; ++mt)
-            acc[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u][mt], b, acc[mt], 0, 0, 0);
+          for (int g = 0; g < NG; ++g) {
+            const float b = pr[4 * g];
+#pragma unroll
+            for (int mt = 0; mt < M4_MT; ++mt)
+              acc[mt][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[u][mt], b, acc[mt][g], 0, 0, 0);
+          }
         }
       }
     }
 #pragma unroll
-    for (int mt = 0; mt < MF_MT; ++mt)
+    for (int mt = 0; mt < M4_MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = rw + mt * 32 + (r / 4) * 8 + khalf * 4 + (r % 4);
-        if (row < n && col < kt) {
-          const float v = acc[mt][r];
-          GH[row * ld_gh + t0 + col] = v;
-          const uint32_t m = __float_as_uint(v) & 0x7fffffffu;
-          mxc = m > mxc ? m : mxc;
+      for (int g = 0; g < NG; ++g) {
+        const int col = 4 * g + cq;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t row = rw + mt * 64 + 4 * (lane >> 2) + r;
+          if (row < n && col < kt) {
+            const float v = acc[mt][g][r];
+            GH[row * ld_gh + t0 + col] = v;
+            const uint32_t m = __float_as_uint(v) & 0x7fffffffu;
+            mx[g] = m > mx[g] ? m : mx[g];
+          }
         }
       }
     if (last) {
 #pragma unroll
-      for (int q = 0; q < MF_MT / 2; ++q) {
-        const int64_t row = rw + q * 64 + lane;
+      for (int mt = 0; mt < M4_MT; ++mt) {
+        const int64_t row = rw + mt * 64 + lane;
         if (row < n) {
           const float hv = h[row];
           GH[row * ld_gh + k] = hv;
@@ -658,21 +679,24 @@ k_project_mfma(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, cons
       }
     }
   }
-  // block maxima: column col's lanes are l and l + 32; then the waves
-  {
-    const uint32_t o = __shfl_xor(mxc, 32, 64);
-    mxc = o > mxc ? o : mxc;
-    mxh = wave_max_u32(mxh);
-    if (lane < 32) smax[wave][lane] = mxc;
-    if (lane == 0) smax[wave][32] = mxh;
+  // block maxima: column 4g + cq's lanes are those with the same cq; then the waves
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    for (int off = 4; off < 64; off <<= 1) {
+      const uint32_t o = __shfl_xor(mx[g], off, 64);
+      mx[g] = o > mx[g] ? o : mx[g];
+    }
+    if (lane < 4) smax[wave][4 * g + lane] = mx[g];
   }
+  mxh = wave_max_u32(mxh);
+  if (lane == 0) smax[wave][W] = mxh;
   __syncthreads();
-  if (threadIdx.x <= 32) {
+  if (threadIdx.x <= W) {
     uint32_t r = 0u;
 #pragma unroll
-    for (int w = 0; w < MF_THREADS / 64; ++w) r = smax[w][threadIdx.x] > r ? smax[w][threadIdx.x] : r;
+    for (int w = 0; w < M4_THREADS / 64; ++w) r = smax[w][threadIdx.x] > r ? smax[w][threadIdx.x] : r;
     if (threadIdx.x < kt) blockmax[(int64_t)blockIdx.x * (k + 1) + t0 + threadIdx.x] = r;
-    if (threadIdx.x == 32 && last) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = r;
+    if (threadIdx.x == W && last) blockmax[(int64_t)blockIdx.x * (k + 1) + k] = r;
   }
 }
 
@@ -738,10 +762,10 @@ k_qexp(const uint32_t* __restrict__ blockmax, int nblocks, int c, int32_t* __res
   }
 }
 
-int sketch_blocks(int64_t n, int64_t rows_per_block) {
+int sketch_blocks(int64_t n, int64_t rows_per_block, int cap = SKETCH_GRID_BLOCKS) {
   int64_t b = (n + rows_per_block - 1) / rows_per_block;
   if (b < 1) b = 1;
-  if (b > SKETCH_MAX_BLOCKS) b = SKETCH_MAX_BLOCKS;
+  if (b > cap) b = cap;
   return (int)b;
 }
 
@@ -780,10 +804,17 @@ SketchWs sketch_ws_layout(int64_t n, int32_t d, int32_t k) {
 int launch_dense_projection(const float* G, int64_t n, int32_t d, int64_t ld_g, const float* h, int32_t k,
                             const float* Pi, float* GH, int64_t ld_gh, uint32_t* blockmax, hipStream_t st) {
   if (k >= PROJ_MFMA_MIN_K) {
-    const int nb = sketch_blocks(n, (MF_THREADS / 64) * MF_MT * 32);
-    for (int t0 = 0; t0 < k; t0 += 32)
-      hipLaunchKernelGGL(k_project_mfma, dim3(nb), dim3(MF_THREADS), 0, st, G, n, d, ld_g, Pi, k, t0, h, GH, ld_gh,
-                         blockmax);
+    const int nb = sketch_blocks(n, (M4_THREADS / 64) * M4_MT * 64, SKETCH_MAX_BLOCKS);
+    for (int t0 = 0; t0 < k; t0 += 32) {
+      const int ng = (k - t0 < 32 ? k - t0 + 3 : 32 + 3) / 4;
+#define SB_P4(NG)                                                                                                 \
+  case NG:                                                                                                        \
+    hipLaunchKernelGGL((k_project_mfma4<NG>), dim3(nb), dim3(M4_THREADS), 0, st, G, n, d, ld_g, Pi, k, t0, h, GH, \
+                       ld_gh, blockmax);                                                                          \
+    break;
+      switch (ng) { SB_P4(1) SB_P4(2) SB_P4(3) SB_P4(4) SB_P4(5) SB_P4(6) SB_P4(7) SB_P4(8) }
+#undef SB_P4
+    }
     return nb;
   }
   const int nb = sketch_blocks(n, PROJ_THREADS);

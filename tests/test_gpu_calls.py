@@ -68,7 +68,10 @@ def test_sketch_row_strides(kind, k, ld_gh):
         assert np.array_equal(GH_g[:, k], case.h)
 
 
-@pytest.mark.parametrize("n,d,k,seed", [(5000, 40, 5, 0), (20001, 200, 20, 1), (777, 3, 8, 2)])
+# k = 13 leaves a partial group of four columns and d = 300 a second, partial
+# block of staged Pi rows; k = 33 takes a second pass of one column
+@pytest.mark.parametrize("n,d,k,seed", [(5000, 40, 5, 0), (20001, 200, 20, 1), (777, 3, 8, 2), (3001, 300, 13, 3),
+                                        (2000, 40, 33, 4)])
 def test_random_projection_error_bound(n, d, k, seed):
     # fp32 accumulation against the exact product: Higham's dot-product bound
     # |fl(x.y) - x.y| <= gamma_d |x|.|y| with gamma_d = d u / (1 - d u), u = 2^-24,
