@@ -109,7 +109,10 @@ def boost_leg(wl, inp, dev, L, warm=100, timed=100):
     b.record()
     torch.cuda.synchronize()
     it_ms = a.elapsed_time(b) / timed
-    # the gradient pass on its own (scores and labels in; G and the norms out)
+    # the gradient pass on its own (scores and labels in; G and the norms out),
+    # after the last tree's held update
+    bst.flush()
+    torch.cuda.synchronize()
     a.record()
     for _ in range(10):
         bst.gradients()
@@ -124,7 +127,7 @@ def boost_leg(wl, inp, dev, L, warm=100, timed=100):
         "iterations": "%d-%d (the difference protocol of the synthetic experiment)" % (warm + 1, warm + timed),
         "what": "softmax-CE gradients with column norms, sketch from those norms, tree, leaf values with the "
                 "full G and per-element hessians formed from G and the labels, score update; lr 0.01, zero "
-                "initial scores",
+                "initial scores; each tree's update runs in one pass with the next iteration's gradients",
         "gradient_pass_ms": g_ms,
         "gradient_pass_bytes": g_bytes,
         "gradient_pass_GBps": g_bytes / (g_ms * 1e-3) / 1e9,

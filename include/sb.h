@@ -75,7 +75,7 @@
 extern "C" {
 #endif
 
-#define SB_ABI_VERSION 3
+#define SB_ABI_VERSION 4
 
 /* Status codes. */
 enum {
@@ -104,7 +104,8 @@ enum {
   SB_CALL_HIST_EXPONENTS = 5,
   SB_CALL_LEAF_VALUES = 6,
   SB_CALL_GRADIENTS = 7,
-  SB_CALL_UPDATE_PREDICTIONS = 8
+  SB_CALL_UPDATE_PREDICTIONS = 8,
+  SB_CALL_UPDATE_AND_GRADIENTS = 9
 };
 
 /* Losses of sb_gradients (the cross-entropies of the paper's experiments). */
@@ -124,12 +125,12 @@ int32_t sb_abi_version(void);
  * ignored (pass 0).  n: rows (every call that takes rows, BUILD_HISTOGRAMS
  * included).  n_nodes: nodes of the level (BUILD_HISTOGRAMS,
  * SCORE_SPLITS, PARTITION_ROWS), leaves (LEAF_VALUES).  depth: tree depth
- * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES, GRADIENTS; the
- * LEAF_VALUES size covers all three hessian forms).  UPDATE_PREDICTIONS needs
- * only n.  Returns -1 (and sets the error text) for sizes outside the
- * range the call itself accepts (n < 2^31, m and d <= 65535, k <= 255,
- * n_bins in [2, 256], nodes as documented per call).  sb_layout_bins and
- * sb_subtract_histograms need no workspace.
+ * (GROW_TREE).  d: output dimension (SKETCH, LEAF_VALUES, GRADIENTS,
+ * UPDATE_AND_GRADIENTS; the LEAF_VALUES size covers all three hessian
+ * forms).  UPDATE_PREDICTIONS needs only n.  Returns -1 (and sets the error
+ * text) for sizes outside the range the call itself accepts (n < 2^31, m and
+ * d <= 65535, k <= 255, n_bins in [2, 256], nodes as documented per call).
+ * sb_layout_bins and sb_subtract_histograms need no workspace.
  */
 int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, int32_t d, int32_t k,
                            int32_t n_nodes, int32_t depth);
@@ -456,6 +457,25 @@ int32_t sb_leaf_values_from_loss(int32_t loss, const float* G, int64_t n, int32_
 int32_t sb_update_predictions(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
                               const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
                               void* ws, int64_t ws_bytes, void* stream);
+
+/*
+ * sb_update_and_gradients -- the update of one tree followed by the
+ * derivatives at the new scores, the two consecutive steps of the boosting
+ * loop (Section 2: a_t = a_{t-1} + lr * f_t, then eq. 2 at a_t).  The result
+ * is bit-identical to sb_update_predictions(F, ..., V, ld_v, lr) followed by
+ * sb_gradients(loss, F, ...): F is updated in place, and G, hess, h_row and
+ * norm2 are those of the updated F.  Every argument means what it means in
+ * those two calls, with the same ranges and errors.
+ * For the softmax loss with d <= 104 and at most 256 leaves whose lr * V
+ * table (n_leaves x (d | 1) doubles) fits 64 KB, the two run as one pass
+ * that reads F once; otherwise as the two calls.
+ * Workspace: sb_workspace_bytes(SB_CALL_UPDATE_AND_GRADIENTS, n, d).
+ */
+int32_t sb_update_and_gradients(int32_t loss, float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                                const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                                const int32_t* labels, const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g,
+                                float* hess, int64_t ld_hess, float* h_row, double* norm2, void* ws,
+                                int64_t ws_bytes, void* stream);
 
 /*
  * Kernel timing for benchmarks.  Between sb_profile_begin() and

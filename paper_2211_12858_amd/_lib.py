@@ -20,7 +20,8 @@ LIB_PATH = os.environ.get("SKETCHBOOST_LIB") or os.path.join(HERE, "libsketchboo
 SB_OK, SB_E_ARG, SB_E_SHAPE, SB_E_UNSUPPORTED, SB_E_DEVICE = 0, 1, 2, 3, 4
 SB_SKETCH_TOP_OUTPUTS, SB_SKETCH_RANDOM_SAMPLING, SB_SKETCH_RANDOM_PROJECTION, SB_SKETCH_IDENTITY = 0, 1, 2, 3
 (SB_CALL_SKETCH, SB_CALL_BUILD_HISTOGRAMS, SB_CALL_SCORE_SPLITS, SB_CALL_PARTITION_ROWS, SB_CALL_GROW_TREE,
- SB_CALL_HIST_EXPONENTS, SB_CALL_LEAF_VALUES, SB_CALL_GRADIENTS, SB_CALL_UPDATE_PREDICTIONS) = range(9)
+ SB_CALL_HIST_EXPONENTS, SB_CALL_LEAF_VALUES, SB_CALL_GRADIENTS, SB_CALL_UPDATE_PREDICTIONS,
+ SB_CALL_UPDATE_AND_GRADIENTS) = range(10)
 SB_LOSS_SOFTMAX_CE, SB_LOSS_SIGMOID_BCE = 0, 1
 LOSS = {"softmax": SB_LOSS_SOFTMAX_CE, "sigmoid": SB_LOSS_SIGMOID_BCE}
 
@@ -51,6 +52,7 @@ SYMBOLS = (
     "sb_leaf_values_from_loss",
     "sb_gradients",
     "sb_update_predictions",
+    "sb_update_and_gradients",
     "sb_profile_begin",
     "sb_profile_end",
 )
@@ -94,6 +96,8 @@ _PROTOS["sb_gradients"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, 
 _PROTOS["sb_leaf_values_from_loss"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I64, _P, _P, _I32, _F64, _P,
                                                _I64, _P, _I64, _P])
 _PROTOS["sb_update_predictions"] = (_I32, [_P, _I64, _I32, _I64, _P, _P, _I32, _P, _I64, _F64, _P, _I64, _P])
+_PROTOS["sb_update_and_gradients"] = (_I32, [_I32, _P, _I64, _I32, _I64, _P, _P, _I32, _P, _I64, _F64, _P, _P, _I64,
+                                             _P, _I64, _P, _I64, _P, _P, _P, _I64, _P])
 _PROTOS["sb_profile_begin"] = (_I32, [])
 _PROTOS["sb_profile_end"] = (_I32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)])
 
@@ -248,6 +252,14 @@ def sb_leaf_values_from_loss(loss, G, n, d, ld_g, labels, Y, ld_y, row_idx, leaf
 def sb_update_predictions(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws, ws_bytes, stream=None):
     return _check(load().sb_update_predictions(_ptr(F), n, d, ld_f, _ptr(row_idx), _ptr(leaf_off), n_leaves, _ptr(V),
                                                ld_v, lr, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def sb_update_and_gradients(loss, F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, labels, Y, ld_y, G, ld_g,
+                            hess, ld_hess, h_row, norm2, ws, ws_bytes, stream=None):
+    return _check(load().sb_update_and_gradients(loss, _ptr(F), n, d, ld_f, _ptr(row_idx), _ptr(leaf_off), n_leaves,
+                                                 _ptr(V), ld_v, lr, _ptr(labels), _ptr(Y), ld_y, _ptr(G), ld_g,
+                                                 _ptr(hess), ld_hess, _ptr(h_row), _ptr(norm2), _ptr(ws), ws_bytes,
+                                                 _stream(stream)))
 
 
 def sb_profile_begin():

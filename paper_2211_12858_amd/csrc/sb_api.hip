@@ -199,6 +199,9 @@ int64_t sb_workspace_bytes(int32_t call, int64_t n, int32_t m, int32_t n_bins, i
     case SB_CALL_UPDATE_PREDICTIONS:
       if (n < 1 || n > MAX_ROWS) break;
       return update_ws_bytes(n);
+    case SB_CALL_UPDATE_AND_GRADIENTS:
+      if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535) break;
+      return update_gradients_ws_bytes(n, d);
     case SB_CALL_LEAF_VALUES:
       if (n < 1 || n > MAX_ROWS || d < 1 || d > 65535 || n_nodes < 1 || n_nodes > MAX_LEAVES) break;
       return leaf_ws_bytes(n, d, n_nodes);
@@ -405,6 +408,40 @@ int32_t check_partition(const char* call, const uint8_t* bins_cm, int64_t n, int
   return SB_OK;
 }
 
+int32_t check_gradients(const char* call, int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f,
+                        const int32_t* labels, const uint8_t* Y, int64_t ld_y, const float* G, int64_t ld_g,
+                        const float* hess, int64_t ld_hess) {
+  const std::string c(call);
+  if (loss != SB_LOSS_SOFTMAX_CE && loss != SB_LOSS_SIGMOID_BCE)
+    return fail(SB_E_UNSUPPORTED, c + ": unknown loss " + std::to_string(loss));
+  if (!F || !G) return fail(SB_E_ARG, c + ": F and G must not be NULL");
+  if (loss == SB_LOSS_SOFTMAX_CE && !labels) return fail(SB_E_ARG, c + ": softmax needs labels");
+  if (loss == SB_LOSS_SIGMOID_BCE && !Y) return fail(SB_E_ARG, c + ": sigmoid needs the targets Y");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, c + ": n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, c + ": d must be in [1, 65535]");
+  if (ld_f < n || ld_g < n) return fail(SB_E_SHAPE, c + ": ld_f and ld_g must be >= n");
+  if (hess && ld_hess < n) return fail(SB_E_SHAPE, c + ": ld_hess must be >= n");
+  if (loss == SB_LOSS_SIGMOID_BCE && ld_y < n) return fail(SB_E_SHAPE, c + ": ld_y must be >= n");
+  const char* f0 = reinterpret_cast<const char*>(F);
+  const char* g0 = reinterpret_cast<const char*>(G);
+  const int64_t fb = ((int64_t)(d - 1) * ld_f + n) * 4, gb = ((int64_t)(d - 1) * ld_g + n) * 4;
+  if (f0 < g0 + gb && g0 < f0 + fb) return fail(SB_E_SHAPE, c + ": F and G overlap");
+  return SB_OK;
+}
+
+int32_t check_update(const char* call, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                     const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr) {
+  const std::string c(call);
+  if (!F || !row_idx || !leaf_off || !V) return fail(SB_E_ARG, c + ": F, row_idx, leaf_off and V must not be NULL");
+  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, c + ": n must be in [1, 2^31)");
+  if (d < 1 || d > 65535) return fail(SB_E_ARG, c + ": d must be in [1, 65535]");
+  if (n_leaves < 1 || n_leaves > MAX_LEAVES) return fail(SB_E_ARG, c + ": n_leaves must be in [1, 4096]");
+  if (ld_f < n) return fail(SB_E_SHAPE, c + ": ld_f must be >= n");
+  if (ld_v < d) return fail(SB_E_SHAPE, c + ": ld_v must be >= d");
+  if (!std::isfinite(lr)) return fail(SB_E_ARG, c + ": lr must be finite");
+  return SB_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -555,23 +592,9 @@ int32_t sb_leaf_values(const float* G, int64_t n, int32_t d, int64_t ld_g, const
 int32_t sb_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
                      const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
                      float* h_row, double* norm2, void* ws, int64_t ws_bytes, void* stream) {
-  if (loss != SB_LOSS_SOFTMAX_CE && loss != SB_LOSS_SIGMOID_BCE)
-    return fail(SB_E_UNSUPPORTED, "sb_gradients: unknown loss " + std::to_string(loss));
-  if (!F || !G) return fail(SB_E_ARG, "sb_gradients: F and G must not be NULL");
-  if (loss == SB_LOSS_SOFTMAX_CE && !labels) return fail(SB_E_ARG, "sb_gradients: softmax needs labels");
-  if (loss == SB_LOSS_SIGMOID_BCE && !Y) return fail(SB_E_ARG, "sb_gradients: sigmoid needs the targets Y");
-  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_gradients: n must be in [1, 2^31)");
-  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_gradients: d must be in [1, 65535]");
-  if (ld_f < n || ld_g < n) return fail(SB_E_SHAPE, "sb_gradients: ld_f and ld_g must be >= n");
-  if (hess && ld_hess < n) return fail(SB_E_SHAPE, "sb_gradients: ld_hess must be >= n");
-  if (loss == SB_LOSS_SIGMOID_BCE && ld_y < n) return fail(SB_E_SHAPE, "sb_gradients: ld_y must be >= n");
-  {
-    const char* f0 = reinterpret_cast<const char*>(F);
-    const char* g0 = reinterpret_cast<const char*>(G);
-    const int64_t fb = ((int64_t)(d - 1) * ld_f + n) * 4, gb = ((int64_t)(d - 1) * ld_g + n) * 4;
-    if (f0 < g0 + gb && g0 < f0 + fb) return fail(SB_E_SHAPE, "sb_gradients: F and G overlap");
-  }
-  const int32_t rc = need_ws(ws, ws_bytes, norm2 ? grad_ws_bytes(n, d) : 0, "sb_gradients");
+  int32_t rc = check_gradients("sb_gradients", loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess);
+  if (rc) return rc;
+  rc = need_ws(ws, ws_bytes, norm2 ? grad_ws_bytes(n, d) : 0, "sb_gradients");
   if (rc) return rc;
   return launch_gradients(loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, norm2, ws,
                           static_cast<hipStream_t>(stream));
@@ -605,18 +628,27 @@ int32_t sb_leaf_values_from_loss(int32_t loss, const float* G, int64_t n, int32_
 int32_t sb_update_predictions(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
                               const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
                               void* ws, int64_t ws_bytes, void* stream) {
-  if (!F || !row_idx || !leaf_off || !V)
-    return fail(SB_E_ARG, "sb_update_predictions: F, row_idx, leaf_off and V must not be NULL");
-  if (n < 1 || n > MAX_ROWS) return fail(SB_E_ARG, "sb_update_predictions: n must be in [1, 2^31)");
-  if (d < 1 || d > 65535) return fail(SB_E_ARG, "sb_update_predictions: d must be in [1, 65535]");
-  if (n_leaves < 1 || n_leaves > MAX_LEAVES)
-    return fail(SB_E_ARG, "sb_update_predictions: n_leaves must be in [1, 4096]");
-  if (ld_f < n) return fail(SB_E_SHAPE, "sb_update_predictions: ld_f must be >= n");
-  if (ld_v < d) return fail(SB_E_SHAPE, "sb_update_predictions: ld_v must be >= d");
-  if (!std::isfinite(lr)) return fail(SB_E_ARG, "sb_update_predictions: lr must be finite");
-  const int32_t rc = need_ws(ws, ws_bytes, update_ws_bytes(n), "sb_update_predictions");
+  int32_t rc = check_update("sb_update_predictions", F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr);
+  if (rc) return rc;
+  rc = need_ws(ws, ws_bytes, update_ws_bytes(n), "sb_update_predictions");
   if (rc) return rc;
   return launch_update(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws, static_cast<hipStream_t>(stream));
+}
+
+int32_t sb_update_and_gradients(int32_t loss, float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                                const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                                const int32_t* labels, const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g,
+                                float* hess, int64_t ld_hess, float* h_row, double* norm2, void* ws,
+                                int64_t ws_bytes, void* stream) {
+  const char* call = "sb_update_and_gradients";
+  int32_t rc = check_update(call, F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr);
+  if (rc) return rc;
+  rc = check_gradients(call, loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess);
+  if (rc) return rc;
+  rc = need_ws(ws, ws_bytes, update_gradients_ws_bytes(n, d), call);
+  if (rc) return rc;
+  return launch_update_gradients(loss, F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, labels, Y, ld_y, G,
+                                 ld_g, hess, ld_hess, h_row, norm2, ws, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -124,6 +124,11 @@ int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int
 int64_t update_ws_bytes(int64_t n);
 int32_t launch_update(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx, const int32_t* leaf_off,
                       int32_t n_leaves, const double* V, int64_t ld_v, double lr, void* ws, hipStream_t st);
+int64_t update_gradients_ws_bytes(int64_t n, int32_t d);
+int32_t launch_update_gradients(int32_t loss, float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                                const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                                const int32_t* labels, const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g,
+                                float* hess, int64_t ld_hess, float* h_row, double* norm2, void* ws, hipStream_t st);
 
 // ---------------------------------------------------------------- profiling
 // Event pairs around histogram-kernel launches while profiling is on (per thread).

@@ -13,11 +13,20 @@
 //   Sampling rank and draw by, Sections 3.1, 3.2) are summed in the same pass:
 //   each 16-column chunk of g goes through LDS, 16 threads per column add 16
 //   rows each in fp64, a fixed butterfly joins them, and one thread adds the
-//   tile's sum to the block's partial (a fixed order).  k_grad_norm_final adds
-//   the blocks' partials in a fixed order, so the norms are deterministic.
+//   tile's sum to its slot's partial (slot = tile mod GRAD_PARTS, always the
+//   same thread of the same block, in tile order).  k_grad_norm_final adds the
+//   slots in a fixed order, so the norms are deterministic and the same for
+//   every grid that divides the slot count (the fused update below launches
+//   fewer blocks than the derivatives alone).
 // k_update: F[i, j] += lr * V[leaf of i, j] in fp64, rounded once to fp32.
 //   lr * V of a chunk of columns is staged in LDS; the leaf ids come from the
 //   leaf segments (k_leaf_ids, shared with the leaf values).
+// The update of one tree followed by the derivatives of the next (the two
+// consecutive steps of the boosting loop) can run as one pass for softmax
+// with d <= 104: k_grad_softmax_regs with UPD loads a row's scores, adds
+// lr * V of the row's leaf (all of lr * V staged in LDS), stores the new
+// scores and goes on from them, so F is read once instead of twice.  The
+// arithmetic is k_update's, so the result is bit-identical to the two calls.
 #include <cmath>
 
 #include "sb_common.h"
@@ -29,7 +38,12 @@ namespace {
 constexpr int GRAD_THREADS = 256;
 constexpr int GRAD_JA = 8;          // columns per load batch of the softmax first pass
 constexpr int GRAD_JC = 16;         // columns per chunk of the second pass (norm staging)
-constexpr int GRAD_MAX_BLOCKS = 2048;
+// Column-norm partial slots: tile t adds into slot t % GRAD_PARTS, and the
+// grid divides the slot count (or is one block per tile), so every slot
+// belongs to one block and sums its tiles in tile order: the norms do not
+// depend on the grid.  1536 = 2^9 * 3 has the divisors 512 and 768 (two and
+// three blocks per CU of MI355X).
+constexpr int GRAD_PARTS = 1536;
 constexpr int UPD_THREADS = 256;
 constexpr int UPD_LDS_DOUBLES = 8192;  // lr * V of one column chunk: at most 64 KB
 constexpr int UPD_JC = 16;             // columns per chunk at most
@@ -49,8 +63,19 @@ struct GradArgs {
   float* hess;
   int64_t ld_h;
   float* h_row;
-  double* npart;  // [d][blocks] or NULL
+  double* npart;  // [d][n_parts] or NULL: sums of g^2 per column and slot
   int32_t n_tiles;
+  int32_t n_parts;  // min(n_tiles, GRAD_PARTS)
+  // update before the derivatives (k_grad_softmax_regs with UPD): F_upd is F
+  // (updated in place), ids the leaf of every row, lv_stride the doubles per
+  // leaf of lr * V in LDS
+  float* F_upd;
+  const uint8_t* ids;
+  int32_t n_leaves;
+  int32_t lv_stride;
+  const double* V;
+  int64_t ld_v;
+  double lr;
 };
 
 // Barrier for the norm staging: waits for this wave's LDS operations only.
@@ -70,7 +95,7 @@ __device__ inline void lds_sync() {
 // store column d-1's own values there (same address, same value), and d is
 // passed in opaque to the compiler, as in grad_softmax_tile below.
 template <int LOSS, bool FULL, bool HESS>
-__device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], int64_t base, bool first, int d) {
+__device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], int64_t base, int d) {
   const int tid = threadIdx.x;
   const int64_t row = base + tid;
   const bool ok = FULL || row < a.n;
@@ -148,8 +173,9 @@ __device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS],
       }
       for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
       if (seg == 0 && j0 + c < d) {
-        double* pp = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
-        *pp = first ? acc : *pp + acc;
+        const int tile = (int)(base / GRAD_THREADS);
+        double* pp = a.npart + (int64_t)(j0 + c) * a.n_parts + tile % a.n_parts;
+        *pp = tile < a.n_parts ? acc : *pp + acc;  // the slot's first tile writes it
       }
       lds_sync();
     }
@@ -160,24 +186,19 @@ __device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS],
 template <int LOSS>
 __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
   __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
-  bool first = true;
   for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
     int d = a.d;
     asm volatile("" : "+s"(d));
     const int64_t base = (int64_t)tile * GRAD_THREADS;
     const bool full = base + GRAD_THREADS <= a.n;
     if (a.hess) {
-      if (full) grad_tile<LOSS, true, true>(a, gbuf, base, first, d);
-      else grad_tile<LOSS, false, true>(a, gbuf, base, first, d);
+      if (full) grad_tile<LOSS, true, true>(a, gbuf, base, d);
+      else grad_tile<LOSS, false, true>(a, gbuf, base, d);
     } else {
-      if (full) grad_tile<LOSS, true, false>(a, gbuf, base, first, d);
-      else grad_tile<LOSS, false, false>(a, gbuf, base, first, d);
+      if (full) grad_tile<LOSS, true, false>(a, gbuf, base, d);
+      else grad_tile<LOSS, false, false>(a, gbuf, base, d);
     }
-    first = false;
   }
-  // a block without tiles still defines its partials
-  if (a.npart && first)
-    for (int j = threadIdx.x; j < a.d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
 }
 
 // Softmax cross-entropy with the row's d <= DMAX scores held in registers:
@@ -196,9 +217,9 @@ __global__ void __launch_bounds__(GRAD_THREADS) k_grad(GradArgs a) {
 // phase or the tile loop.  Columns past d stay on column d-1 and store
 // column d-1's own values there (same address, same value), so the stores
 // need no branch; a full tile stores without a row guard.
-template <int DMAX, bool FULL, bool HESS>
-__device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], int64_t base, bool first,
-                                         int64_t ld_f, int64_t ld_g, int64_t ld_h, int d) {
+template <int DMAX, bool FULL, bool HESS, bool UPD>
+__device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS], const double* lv,
+                                         int64_t base, int64_t ld_f, int64_t ld_g, int64_t ld_h, int d) {
   const int tid = threadIdx.x;
   const int64_t row = base + tid;
   const bool ok = FULL || row < a.n;
@@ -208,6 +229,22 @@ __device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_T
   float x[DMAX];
 #pragma unroll
   for (int j = 0; j < DMAX; ++j) x[j] = Fb[(int64_t)(j < d ? j : d - 1) * ld_f + loc];
+  if constexpr (UPD) {
+    // the update of the previous tree, as k_update: fp64 sum, rounded once;
+    // columns past d repeat column d-1 and store its own value there
+    int L = a.ids[base + loc];
+    L = L < a.n_leaves ? L : a.n_leaves - 1;
+    const double* lvL = lv + L * a.lv_stride;
+    asm volatile("" : "+s"(d));
+#pragma unroll
+    for (int j = 0; j < DMAX; ++j) x[j] = (float)((double)x[j] + lvL[j < d ? j : d - 1]);
+    asm volatile("" : "+s"(d));
+    float* Fw = a.F_upd + base;
+#pragma unroll
+    for (int j = 0; j < DMAX; ++j)
+      if (ok) Fw[(int64_t)(j < d ? j : d - 1) * ld_f + tid] = x[j];
+    asm volatile("" : "+s"(d));
+  }
   float m = x[0];
 #pragma unroll
   for (int j = 1; j < DMAX; ++j) m = fmaxf(m, x[j]);
@@ -255,8 +292,9 @@ __device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_T
       }
       for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
       if (seg == 0 && j0 + c < d) {
-        double* pp = a.npart + (int64_t)(j0 + c) * gridDim.x + blockIdx.x;
-        *pp = first ? acc : *pp + acc;
+        const int tile = (int)(base / GRAD_THREADS);
+        double* pp = a.npart + (int64_t)(j0 + c) * a.n_parts + tile % a.n_parts;
+        *pp = tile < a.n_parts ? acc : *pp + acc;  // the slot's first tile writes it
       }
       lds_sync();
     }
@@ -264,10 +302,17 @@ __device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_T
   if (a.h_row && ok) a.h_row[row] = hsum * (1.0f / (float)d);
 }
 
-template <int DMAX>
+template <int DMAX, bool UPD>
 __global__ void __launch_bounds__(GRAD_THREADS) k_grad_softmax_regs(GradArgs a) {
   __shared__ __align__(16) float gbuf[GRAD_JC][GRAD_THREADS];
-  bool first = true;
+  extern __shared__ double lv[];  // UPD: lr * V, [leaf][lv_stride]
+  if constexpr (UPD) {
+    for (int e = threadIdx.x; e < a.n_leaves * a.d; e += GRAD_THREADS) {
+      const int L = e / a.d, j = e - L * a.d;
+      lv[L * a.lv_stride + j] = a.lr * a.V[(int64_t)L * a.ld_v + j];
+    }
+    __syncthreads();
+  }
   for (int tile = blockIdx.x; tile < a.n_tiles; tile += gridDim.x) {
     const int64_t ld_f = a.ld_f, ld_g = a.ld_g, ld_h = a.ld_h;
     // d as seen by the compiler changes at every tile: the per-column tests
@@ -278,16 +323,13 @@ __global__ void __launch_bounds__(GRAD_THREADS) k_grad_softmax_regs(GradArgs a) 
     const int64_t base = (int64_t)tile * GRAD_THREADS;
     const bool full = base + GRAD_THREADS <= a.n;
     if (a.hess) {
-      if (full) grad_softmax_tile<DMAX, true, true>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
-      else grad_softmax_tile<DMAX, false, true>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
+      if (full) grad_softmax_tile<DMAX, true, true, UPD>(a, gbuf, lv, base, ld_f, ld_g, ld_h, d);
+      else grad_softmax_tile<DMAX, false, true, UPD>(a, gbuf, lv, base, ld_f, ld_g, ld_h, d);
     } else {
-      if (full) grad_softmax_tile<DMAX, true, false>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
-      else grad_softmax_tile<DMAX, false, false>(a, gbuf, base, first, ld_f, ld_g, ld_h, d);
+      if (full) grad_softmax_tile<DMAX, true, false, UPD>(a, gbuf, lv, base, ld_f, ld_g, ld_h, d);
+      else grad_softmax_tile<DMAX, false, false, UPD>(a, gbuf, lv, base, ld_f, ld_g, ld_h, d);
     }
-    first = false;
   }
-  if (a.npart && first)
-    for (int j = threadIdx.x; j < a.d; j += GRAD_THREADS) a.npart[(int64_t)j * gridDim.x + blockIdx.x] = 0.0;
 }
 
 // One wave per column: lane l adds partials l, l+64, ... in order, then a fixed butterfly.
@@ -352,50 +394,84 @@ __global__ void __launch_bounds__(UPD_THREADS) k_update(UpdArgs a) {
   }
 }
 
+// Blocks of a kernel that fit on the current device at once (at least 1),
+// with lds bytes of dynamic LDS per block.
+template <typename K>
+int resident_blocks(K kernel, int threads, size_t lds = 0) {
+  int dev = 0, cus = 0, per = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, lds) != hipSuccess)
+    return GRAD_PARTS;
+  const int r = cus * per;
+  return r > 0 ? r : 1;
+}
+
+// Largest lr * V table (n_leaves x lv_stride doubles) the fused update takes.
+constexpr int64_t UPDGRAD_LDS_BYTES = 64 * 1024;
+
+// Grid of a gradient launch over `tiles` tiles, at most `cap` blocks: one
+// block per tile up to GRAD_PARTS tiles, else the largest divisor of
+// GRAD_PARTS within the cap, so that block b owns the slots b mod grid.
+int grad_grid(int64_t tiles, int cap) {
+  if (tiles <= GRAD_PARTS) return (int)tiles;
+  int g = cap < GRAD_PARTS ? (cap > 1 ? cap : 1) : GRAD_PARTS;
+  while (GRAD_PARTS % g) --g;
+  return g;
+}
+
+// The register softmax kernel for d <= 104, with or without the update (lds:
+// the update's table).  Where the rows are wide (DMAX = 104) or the update's
+// table takes LDS, the grid is capped at the blocks that fit at once, each
+// looping over tiles.
+template <bool UPD>
+void launch_softmax_regs(const GradArgs& a, size_t lds, hipStream_t st) {
+  auto grid = [&](auto kernel, bool wide) {
+    if (!wide && !UPD) return grad_grid(a.n_tiles, GRAD_PARTS);
+    static thread_local size_t fit_lds = ~size_t(0);  // per-thread cache of the occupancy query
+    static thread_local int fit = 0;
+    if (fit_lds != lds) {
+      fit = resident_blocks(kernel, GRAD_THREADS, lds);
+      fit_lds = lds;
+    }
+    return grad_grid(a.n_tiles, fit);
+  };
+  if (a.d <= 16) {
+    const int b = grid(k_grad_softmax_regs<16, UPD>, false);
+    hipLaunchKernelGGL((k_grad_softmax_regs<16, UPD>), dim3(b), dim3(GRAD_THREADS), lds, st, a);
+  } else if (a.d <= 32) {
+    const int b = grid(k_grad_softmax_regs<32, UPD>, false);
+    hipLaunchKernelGGL((k_grad_softmax_regs<32, UPD>), dim3(b), dim3(GRAD_THREADS), lds, st, a);
+  } else if (a.d <= 64) {
+    const int b = grid(k_grad_softmax_regs<64, UPD>, false);
+    hipLaunchKernelGGL((k_grad_softmax_regs<64, UPD>), dim3(b), dim3(GRAD_THREADS), lds, st, a);
+  } else {
+    const int b = grid(k_grad_softmax_regs<104, UPD>, true);
+    hipLaunchKernelGGL((k_grad_softmax_regs<104, UPD>), dim3(b), dim3(GRAD_THREADS), lds, st, a);
+  }
+}
+
 }  // namespace
 
 int64_t grad_ws_bytes(int64_t n, int32_t d) {
   const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
-  const int64_t blocks = tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS;
-  return align256((int64_t)d * blocks * 8);
-}
-
-// Blocks of a kernel that fit on the current device at once (at least 1).
-template <typename K>
-int resident_blocks(K kernel, int threads) {
-  int dev = 0, cus = 0, per = 0;
-  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) != hipSuccess)
-    return GRAD_MAX_BLOCKS;
-  const int r = cus * per;
-  return r > 0 ? r : 1;
+  return align256((int64_t)d * (tiles < GRAD_PARTS ? tiles : GRAD_PARTS) * 8);
 }
 
 int32_t launch_gradients(int32_t loss, const float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* labels,
                          const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g, float* hess, int64_t ld_hess,
                          float* h_row, double* norm2, void* ws, hipStream_t st) {
   const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
-  int blocks = (int)(tiles < GRAD_MAX_BLOCKS ? tiles : GRAD_MAX_BLOCKS);
-  if (loss == SB_LOSS_SOFTMAX_CE && d <= 104 && d > 64) {
-    static thread_local int fit = 0;  // per-thread cache of the occupancy query
-    if (!fit) fit = resident_blocks(k_grad_softmax_regs<104>, GRAD_THREADS);
-    if (fit < blocks) blocks = fit;
-  }
+  const int parts = (int)(tiles < GRAD_PARTS ? tiles : GRAD_PARTS);
   double* npart = norm2 ? static_cast<double*>(ws) : nullptr;
-  const GradArgs a{loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, npart, (int32_t)tiles};
-  if (loss == SB_LOSS_SOFTMAX_CE && d <= 16)
-    hipLaunchKernelGGL(k_grad_softmax_regs<16>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
-  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 32)
-    hipLaunchKernelGGL(k_grad_softmax_regs<32>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
-  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 64)
-    hipLaunchKernelGGL(k_grad_softmax_regs<64>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
-  else if (loss == SB_LOSS_SOFTMAX_CE && d <= 104)
-    hipLaunchKernelGGL(k_grad_softmax_regs<104>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
+  GradArgs a{loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, npart, (int32_t)tiles, parts};
+  const int blocks = grad_grid(tiles, GRAD_PARTS);
+  if (loss == SB_LOSS_SOFTMAX_CE && d <= 104)
+    launch_softmax_regs<false>(a, 0, st);
   else if (loss == SB_LOSS_SOFTMAX_CE)
     hipLaunchKernelGGL(k_grad<SB_LOSS_SOFTMAX_CE>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
   else
     hipLaunchKernelGGL(k_grad<SB_LOSS_SIGMOID_BCE>, dim3(blocks), dim3(GRAD_THREADS), 0, st, a);
-  if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, blocks, norm2);
+  if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, parts, norm2);
   return check_launch("sb_gradients");
 }
 
@@ -416,6 +492,40 @@ int32_t launch_update(float* F, int64_t n, int32_t d, int64_t ld_f, const int32_
   else
     hipLaunchKernelGGL(k_update<uint16_t>, dim3(blocks), dim3(UPD_THREADS), lds, st, a);
   return check_launch("sb_update_predictions");
+}
+
+// Workspace: [norm partials (grad_ws_bytes)][leaf ids (update_ws_bytes)]
+int64_t update_gradients_ws_bytes(int64_t n, int32_t d) { return grad_ws_bytes(n, d) + update_ws_bytes(n); }
+
+int32_t launch_update_gradients(int32_t loss, float* F, int64_t n, int32_t d, int64_t ld_f, const int32_t* row_idx,
+                                const int32_t* leaf_off, int32_t n_leaves, const double* V, int64_t ld_v, double lr,
+                                const int32_t* labels, const uint8_t* Y, int64_t ld_y, float* G, int64_t ld_g,
+                                float* hess, int64_t ld_hess, float* h_row, double* norm2, void* ws,
+                                hipStream_t st) {
+  char* w = static_cast<char*>(ws);
+  void* ws_ids = w + grad_ws_bytes(n, d);
+  const int stride = d | 1;  // odd: lanes of different leaves fall on different banks
+  const int64_t table = (int64_t)n_leaves * stride * 8;
+  if (!(loss == SB_LOSS_SOFTMAX_CE && d <= 104 && n_leaves <= 256 && table <= UPDGRAD_LDS_BYTES)) {
+    const int32_t rc = launch_update(F, n, d, ld_f, row_idx, leaf_off, n_leaves, V, ld_v, lr, ws_ids, st);
+    if (rc) return rc;
+    return launch_gradients(loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, norm2, ws, st);
+  }
+  launch_leaf_ids(row_idx, leaf_off, n_leaves, n, ws_ids, st);
+  const int64_t tiles = (n + GRAD_THREADS - 1) / GRAD_THREADS;
+  const int parts = (int)(tiles < GRAD_PARTS ? tiles : GRAD_PARTS);
+  double* npart = norm2 ? reinterpret_cast<double*>(w) : nullptr;
+  GradArgs a{loss, F, n, d, ld_f, labels, Y, ld_y, G, ld_g, hess, ld_hess, h_row, npart, (int32_t)tiles, parts};
+  a.F_upd = F;
+  a.ids = static_cast<const uint8_t*>(ws_ids);
+  a.n_leaves = n_leaves;
+  a.lv_stride = stride;
+  a.V = V;
+  a.ld_v = ld_v;
+  a.lr = lr;
+  launch_softmax_regs<true>(a, (size_t)table, st);
+  if (norm2) hipLaunchKernelGGL(k_grad_norm_final, dim3((d + 3) / 4), dim3(256), 0, st, npart, d, parts, norm2);
+  return check_launch("sb_update_and_gradients");
 }
 
 }  // namespace sb

@@ -229,7 +229,10 @@ class Booster:
     4. leaf values from the full G and the per-element hessians (eq. 3),
        which ``sb_leaf_values_from_loss`` forms from G and the targets
        instead of storing them;
-    5. F += lr * f_t (``sb_update_predictions``).
+    5. F += lr * f_t.  The update is held until the next step, whose first
+       call applies it and takes the derivatives at the new scores in one pass
+       (``sb_update_and_gradients``); reading ``F`` (or ``flush()``) applies a
+       held update on its own (``sb_update_predictions``).
 
     F, G and the hessians are (d, n) float32 device tensors (column-major).
     """
@@ -239,15 +242,31 @@ class Booster:
         self.ss = SplitSearch(bins, n_bins, k, depth, lam, min_child_weight, device=device)
         dev, n = self.ss.device, self.ss.n
         self.n, self.d, self.loss, self.kind, self.lr = n, d, loss, kind, float(lr)
-        self.F = torch.zeros((d, n), dtype=torch.float32, device=dev) if F0 is None else F0.clone()
+        self._F = torch.zeros((d, n), dtype=torch.float32, device=dev) if F0 is None else F0.clone()
         self.G = torch.empty((d, n), dtype=torch.float32, device=dev)
         self.h_row = torch.empty(n, dtype=torch.float32, device=dev)
         self.ones = torch.ones(n, dtype=torch.float32, device=dev)
         self.norm2 = torch.zeros(d, dtype=torch.float64, device=dev)
         self.ws_grad = workspace(L.sb_workspace_bytes(L.SB_CALL_GRADIENTS, n=n, d=d), dev)
         self.ws_upd = workspace(L.sb_workspace_bytes(L.SB_CALL_UPDATE_PREDICTIONS, n=n), dev)
+        self.ws_upd_grad = workspace(L.sb_workspace_bytes(L.SB_CALL_UPDATE_AND_GRADIENTS, n=n, d=d), dev)
         self.labels = None
         self.Y = None
+        self.pending = None  # leaf values of the last tree, not yet added to F
+
+    @property
+    def F(self):
+        """The scores, with every grown tree added."""
+        self.flush()
+        return self._F
+
+    def flush(self, stream=None):
+        """Add a held update (the last tree's leaf values) to F."""
+        if self.pending is not None:
+            V = self.pending
+            L.sb_update_predictions(self._F, self.n, self.d, self.n, self.ss.row_idx, self.ss.leaf_off, V.shape[0], V,
+                                    self.d, self.lr, self.ws_upd, self.ws_upd.numel(), stream)
+            self.pending = None
 
     def set_target(self, target):
         """Labels (n,) int32 for softmax, or a (d, n) uint8 0/1 matrix for sigmoid (device tensors)."""
@@ -257,16 +276,23 @@ class Booster:
             self.Y = target
 
     def gradients(self, stream=None):
+        """Derivatives at the current scores (a held update is applied first, in the same pass)."""
         n, d = self.n, self.d
-        L.sb_gradients(L.LOSS[self.loss], self.F, n, d, n, self.labels, self.Y, n, self.G, n, None, 0,
-                       self.h_row if self.loss == "sigmoid" else None, self.norm2, self.ws_grad,
-                       self.ws_grad.numel(), stream)
+        h_row = self.h_row if self.loss == "sigmoid" else None
+        if self.pending is not None:
+            V = self.pending
+            L.sb_update_and_gradients(L.LOSS[self.loss], self._F, n, d, n, self.ss.row_idx, self.ss.leaf_off,
+                                      V.shape[0], V, d, self.lr, self.labels, self.Y, n, self.G, n, None, 0, h_row,
+                                      self.norm2, self.ws_upd_grad, self.ws_upd_grad.numel(), stream)
+            self.pending = None
+        else:
+            L.sb_gradients(L.LOSS[self.loss], self._F, n, d, n, self.labels, self.Y, n, self.G, n, None, 0, h_row,
+                           self.norm2, self.ws_grad, self.ws_grad.numel(), stream)
 
     def step(self, u=None, Pi=None, stream=None):
         self.gradients(stream)
         h = self.ones if self.loss == "softmax" else self.h_row
         self.ss.sketch(self.kind, self.G, h, u=u, Pi=Pi, stream=stream, norm2_in=self.norm2)
         self.ss.grow(stream)
-        V = self.ss.leaf_values_from_loss(self.loss, self.G, self.labels, self.Y, stream=stream)
-        L.sb_update_predictions(self.F, self.n, self.d, self.n, self.ss.row_idx, self.ss.leaf_off, V.shape[0], V,
-                                self.d, self.lr, self.ws_upd, self.ws_upd.numel(), stream)
+        # the tree's leaf segments stay in ss.row_idx / ss.leaf_off until the next grow
+        self.pending = self.ss.leaf_values_from_loss(self.loss, self.G, self.labels, self.Y, stream=stream)

@@ -35,7 +35,8 @@ def test_header_declares_the_boundary():
     fns = header_functions()
     for name in ("sb_sketch", "sb_build_histograms", "sb_subtract_histograms", "sb_score_splits",
                  "sb_partition_rows", "sb_layout_bins", "sb_grow_tree", "sb_leaf_values", "sb_gradients",
-                 "sb_update_predictions", "sb_sketch_given_norms", "sb_sketch_sparse_projection", "sb_last_error",
+                 "sb_update_predictions", "sb_update_and_gradients", "sb_sketch_given_norms",
+                 "sb_sketch_sparse_projection", "sb_last_error",
                  "sb_abi_version", "sb_workspace_bytes"):
         assert name in fns
 
@@ -50,7 +51,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version_and_error_text(L):
-    assert L.sb_abi_version() == 3
+    assert L.sb_abi_version() == 4
     assert isinstance(L.sb_last_error(), str)
 
 
@@ -411,6 +412,35 @@ def upd_args(**kw):
 def test_update_rejects(L, kw, code):
     assert _code(L.sb_update_predictions, *upd_args(**kw)) == code
     assert L.sb_last_error().startswith("sb_update_predictions")
+
+
+def upd_grad_args(**kw):
+    a = dict(loss=0, F=F, n=1000, d=10, ld_f=1000, row_idx=F, leaf_off=F, n_leaves=64, V=F, ld_v=10, lr=0.1,
+             labels=F, Y=None, ld_y=0, G=F + 10 ** 6, ld_g=1000, hess=None, ld_hess=0, h_row=None, norm2=None, ws=F,
+             ws_bytes=1 << 20, stream=0)
+    a.update(kw)
+    return list(a.values())
+
+
+# The fused call refuses what either of its two steps refuses, with its own name.
+@pytest.mark.parametrize("kw,code", [
+    (dict(loss=2), 3),
+    (dict(F=None), 1),
+    (dict(V=None), 1),
+    (dict(labels=None), 1),
+    (dict(n=0), 1),
+    (dict(d=0), 1),
+    (dict(n_leaves=5000), 1),
+    (dict(ld_f=999), 2),
+    (dict(ld_g=999), 2),
+    (dict(ld_v=9), 2),
+    (dict(lr=float("inf")), 1),
+    (dict(G=F + 400), 2),
+    (dict(ws_bytes=16), 1),
+])
+def test_update_and_gradients_rejects(L, kw, code):
+    assert _code(L.sb_update_and_gradients, *upd_grad_args(**kw)) == code
+    assert L.sb_last_error().startswith("sb_update_and_gradients")
 
 
 def test_error_text_is_per_thread(L):

@@ -156,6 +156,60 @@ def test_update_predictions_bit_exact(n_leaves, d):
     assert np.array_equal(Fd.cpu().numpy().T.view(np.uint32), want.view(np.uint32))
 
 
+# The fused update + derivatives against the two calls it stands for, bit for
+# bit: the one-pass kernel (softmax, d <= 104, <= 256 leaves whose lr * V
+# table fits 64 KB) at each register-kernel width and ragged tiles, and the
+# two-call route (sigmoid, d > 104, wider tables, more leaves).
+@pytest.mark.parametrize("loss,d,n_leaves,n", [
+    ("softmax", 1, 1, 1000), ("softmax", 5, 64, 3 * 256 + 77), ("softmax", 17, 3, 2000), ("softmax", 33, 64, 2500),
+    ("softmax", 64, 100, 1500), ("softmax", 100, 64, 2048 * 256 + 1000), ("softmax", 104, 78, 5000),
+    ("softmax", 100, 82, 3000), ("softmax", 105, 64, 3000), ("softmax", 16, 300, 3000), ("sigmoid", 8, 64, 3000),
+])
+def test_update_and_gradients_bit_exact(loss, d, n_leaves, n):
+    print("update+gradients case: %s d=%d leaves=%d n=%d" % (loss, d, n_leaves, n), flush=True)
+    rng = np.random.default_rng(d * 1000 + n_leaves)
+    F_T = (rng.standard_normal((d, n)) * 2.0).astype(np.float32)
+    tgt = rng.integers(0, d, n).astype(np.int32) if loss == "softmax" else \
+        (rng.random((d, n)) < 0.3).astype(np.uint8)
+    leaf_of = rng.integers(0, n_leaves, n)
+    row_idx = np.argsort(leaf_of, kind="stable").astype(np.int32)
+    leaf_off = np.concatenate([[0], np.cumsum(np.bincount(leaf_of, minlength=n_leaves))]).astype(np.int32)
+    V = np.ascontiguousarray(rng.standard_normal((n_leaves, d)) * 3.0)
+    lr = 0.1
+    labels = gu.up(tgt) if loss == "softmax" else None
+    Y = gu.up(tgt) if loss == "sigmoid" else None
+    ri, lo, Vd = gu.up(row_idx), gu.up(leaf_off), gu.up(V)
+
+    def outputs():
+        G = torch.full((d, n), float("nan"), dtype=torch.float32, device=gu.DEV)
+        H = torch.full((d, n), float("nan"), dtype=torch.float32, device=gu.DEV)
+        hr = torch.full((n,), float("nan"), dtype=torch.float32, device=gu.DEV)
+        n2 = torch.full((d,), float("nan"), dtype=torch.float64, device=gu.DEV)
+        return G, H, hr, n2
+
+    # the two calls
+    F1 = gu.up(F_T)
+    G1, H1, hr1, n21 = outputs()
+    wu = workspace(L.sb_workspace_bytes(L.SB_CALL_UPDATE_PREDICTIONS, n=n), gu.DEV)
+    wg = workspace(L.sb_workspace_bytes(L.SB_CALL_GRADIENTS, n=n, d=d), gu.DEV)
+    L.sb_update_predictions(F1, n, d, n, ri, lo, n_leaves, Vd, d, lr, wu, wu.numel())
+    L.sb_gradients(L.LOSS[loss], F1, n, d, n, labels, Y, n, G1, n, H1, n, hr1, n21, wg, wg.numel())
+    # the fused call, twice (its workspace keeps nothing between calls)
+    wf = workspace(L.sb_workspace_bytes(L.SB_CALL_UPDATE_AND_GRADIENTS, n=n, d=d), gu.DEV)
+    for _ in range(2):
+        F2 = gu.up(F_T)
+        G2, H2, hr2, n22 = outputs()
+        L.sb_update_and_gradients(L.LOSS[loss], F2, n, d, n, ri, lo, n_leaves, Vd, d, lr, labels, Y, n, G2, n, H2, n,
+                                  hr2, n22, wf, wf.numel())
+        gu.sync()
+        for a, b in ((F1, F2), (G1, G2), (H1, H2), (hr1, hr2)):
+            assert np.array_equal(a.cpu().numpy().view(np.uint32), b.cpu().numpy().view(np.uint32))
+        assert np.array_equal(n21.cpu().numpy().view(np.uint64), n22.cpu().numpy().view(np.uint64))
+    # and the update itself is the oracle's
+    want = ob.update_predictions(F_T.T, row_idx, leaf_off, V, lr)
+    assert np.array_equal(F2.cpu().numpy().T.view(np.uint32), want.view(np.uint32))
+
+
 @pytest.mark.parametrize("kind", ["top_outputs", "random_sampling"])
 def test_sketch_given_norms_matches_sketch(kind):
     from workloads import small_case
