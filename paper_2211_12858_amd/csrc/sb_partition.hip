@@ -389,9 +389,10 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scatter(PartArgs a) {
 //                       j = b (mod grid);
 //   k_part_scan_scatter : every block scans the tile counts into LDS, derives
 //                       the left-count bases Lb of the node boundaries it
-//                       needs from the ballots, and scatters its tile; block
-//                       0 also writes the child offsets, the build list and
-//                       the built-size prefix.
+//                       needs from the ballots, and scatters its tiles (one,
+//                       or two from about 1.5M rows); block 0 also writes the
+//                       child offsets, the build list and the built-size
+//                       prefix.
 // This replaces the one-block bounds kernel (and the node argmax kernel),
 // whose launches and dependent load chains dominated the small levels.
 
@@ -520,48 +521,62 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_flags_pick(PartArgs a) {
   }
 }
 
+template <int TPB>
 __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
-  __shared__ uint64_t mk[PT_MASKS];
-  __shared__ int32_t pre[PT_MASKS];
+  constexpr int NM = PT_MASKS * TPB;  // ballots of the block's tiles
+  static_assert(NM <= 64, "one wave scans the block's ballots");
+  __shared__ uint64_t mk[NM];
+  __shared__ int32_t pre[NM];
   __shared__ int64_t sh[PT_THREADS / 64];
   __shared__ int32_t span[2];
   extern __shared__ int32_t pt_lds[];  // [toff: n_tiles][off: n_nodes + 1][lb: n_nodes + 1]
   int32_t* s_toff = pt_lds;
   int32_t* s_off = s_toff + a.n_tiles;
   int32_t* s_lb = s_off + a.n_nodes + 1;
-  const int64_t t0 = (int64_t)blockIdx.x * PT_TILE;
+  const int64_t tile0 = (int64_t)blockIdx.x * TPB;  // the block's first tile
+  const int64_t t0 = tile0 * PT_TILE;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  int64_t row[PT_ITERS];
+  int64_t row[PT_ITERS * TPB];
 #pragma unroll
-  for (int it = 0; it < PT_ITERS; ++it) {
+  for (int it = 0; it < PT_ITERS * TPB; ++it) {
     const int64_t i = t0 + threadIdx.x + (int64_t)it * PT_THREADS;
     const int64_t ic = i < a.n ? i : a.n - 1;
     row[it] = a.row_in ? (int64_t)a.row_in[ic] : ic;
   }
   for (int j = threadIdx.x; j <= a.n_nodes; j += PT_THREADS) s_off[j] = (int32_t)off_at(a, j);
   uint64_t my_mask = 0;
-  if (wave == 0 && lane < PT_MASKS) my_mask = a.masks[(int64_t)blockIdx.x * PT_MASKS + lane];
+  if (wave == 0 && lane < NM && tile0 + lane / PT_MASKS < a.n_tiles) my_mask = a.masks[tile0 * PT_MASKS + lane];
   // 1. exclusive prefix of the tile counts (every block its own copy): the
   // counts are staged into LDS with eight loads in flight per thread, then
-  // each thread scans a contiguous run of them in place
-  for (int t0s = 0; t0s < a.n_tiles; t0s += 8 * PT_THREADS) {
+  // each thread scans a contiguous run of them in place.  With two tiles per
+  // block the entries are the counts of tile pairs (half the scan): entry e
+  // is the prefix before tile TPB * e
+  const int ns = TPB == 1 ? a.n_tiles : (a.n_tiles + 1) / 2;
+  for (int t0s = 0; t0s < ns; t0s += 8 * PT_THREADS) {
     int32_t v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int t = t0s + u * PT_THREADS + threadIdx.x;
-      v[u] = t < a.n_tiles ? a.tile_cnt[t] : 0;
+      v[u] = 0;
+      if (TPB == 1) {
+        if (t < ns) v[u] = a.tile_cnt[t];
+      } else if (t < ns) {
+        // the slot past an odd last tile is allocated; its value is not used
+        const int2 pr = reinterpret_cast<const int2*>(a.tile_cnt)[t];
+        v[u] = pr.x + (2 * t + 1 < a.n_tiles ? pr.y : 0);
+      }
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int t = t0s + u * PT_THREADS + threadIdx.x;
-      if (t < a.n_tiles) s_toff[t] = v[u];
+      if (t < ns) s_toff[t] = v[u];
     }
   }
   __syncthreads();
   const int64_t total = block_scan_nt<PT_THREADS>(
-      a.n_tiles, [&](int t) -> int64_t { return s_toff[t]; }, [&](int t, int64_t p) { s_toff[t] = (int32_t)p; }, sh);
+      ns, [&](int t) -> int64_t { return s_toff[t]; }, [&](int t, int64_t p) { s_toff[t] = (int32_t)p; }, sh);
   __syncthreads();  // s_toff complete
-  // this tile's ballots and their prefix
+  // the block's ballots and their prefix
   if (wave == 0) {
     const int32_t c = popc64(my_mask);
     int32_t incl = c;
@@ -569,7 +584,7 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
       const int32_t o = __shfl_up(incl, off, 64);
       if (lane >= off) incl += o;
     }
-    if (lane < PT_MASKS) {
+    if (lane < NM) {
       mk[lane] = my_mask;
       pre[lane] = s_toff[blockIdx.x] + incl - c;
     }
@@ -583,7 +598,7 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
       span[0] = 0;
       span[1] = a.n_nodes;
     } else {
-      const int64_t last_pos = (t0 + PT_TILE < a.n ? t0 + PT_TILE : a.n) - 1;
+      const int64_t last_pos = (t0 + PT_TILE * TPB < a.n ? t0 + PT_TILE * TPB : a.n) - 1;
       span[0] = find_node<true>(tab, a.n_nodes, t0);
       span[1] = find_node<true>(tab, a.n_nodes, last_pos) + 1;
     }
@@ -611,10 +626,11 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
           const uint64_t mq = a.masks[tx * PT_MASKS + q];
           c = q < (w >> 6) ? popc64(mq) : popc64(mq & ((uint64_t(1) << (w & 63)) - 1));
         }
+        if (TPB == 2 && q == 0 && (tx & 1)) c += a.tile_cnt[tx - 1];  // the pair's first tile
       }
     }
     for (int o = PT_MASKS / 2; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
-    if (e < nb * PT_MASKS && q == 0) s_lb[jb] = in ? s_toff[tx] + c : (int32_t)total;
+    if (e < nb * PT_MASKS && q == 0) s_lb[jb] = in ? s_toff[tx / TPB] + c : (int32_t)total;
   }
   __syncthreads();
   // 3. block 0: child offsets, build list and the built-size prefix
@@ -648,7 +664,7 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
   int64_t jstart = tab.at(j), jend = tab.at(j + 1);
   int64_t lbj = s_lb[j], nleft = (int64_t)s_lb[j + 1] - lbj;
 #pragma unroll
-  for (int it = 0; it < PT_ITERS; ++it, i += PT_THREADS) {
+  for (int it = 0; it < PT_ITERS * TPB; ++it, i += PT_THREADS) {
     if (i < a.n && i >= first && i < last) {
       while (i >= jend && j < a.n_nodes - 1) {
         ++j;
@@ -744,7 +760,14 @@ int32_t launch_partition(const uint8_t* bins_cm, int64_t n, int32_t m, int64_t l
     } else {
       hipLaunchKernelGGL(k_part_flags_pick<false>, dim3((unsigned)tiles), dim3(PT_THREADS), lf, st, a);
     }
-    hipLaunchKernelGGL(k_part_scan_scatter, dim3((unsigned)tiles), dim3(PT_THREADS), ls, st, a);
+    // from about 1.5M rows, two tiles per scatter block: every block scans
+    // the tile counts, here in pairs, so the scan is half as long and half as
+    // many blocks run it (2M rows: 14.4 -> 11.7 us per level; at 1M rows one
+    // tile per block is faster)
+    if (tiles >= 1536)
+      hipLaunchKernelGGL(k_part_scan_scatter<2>, dim3((unsigned)((tiles + 1) / 2)), dim3(PT_THREADS), ls, st, a);
+    else
+      hipLaunchKernelGGL(k_part_scan_scatter<1>, dim3((unsigned)tiles), dim3(PT_THREADS), ls, st, a);
     return check_launch("sb_partition_rows");
   }
   if (feat_s) return fail(SB_E_UNSUPPORTED, "partition: picking splits needs <= 2048 nodes and <= 8192 tiles");

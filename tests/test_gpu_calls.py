@@ -260,9 +260,13 @@ def test_score_ties_and_min_child_weight():
 
 # ---------------------------------------------------------------- partition
 # 2048 nodes: the largest level whose node table the flags and scatter blocks
-# stage in LDS; 3000: the same kernels reading it from global memory
+# stage in LDS; 3000: the same kernels reading it from global memory; from
+# 1536 tiles of 1024 rows the scatter blocks take two tiles each (1537 tiles:
+# the last block has one)
 @pytest.mark.parametrize("n,m,n_nodes,seed", [(1, 1, 1, 0), (4095, 3, 1, 1), (4097, 5, 2, 2), (100003, 20, 16, 3),
-                                               (50000, 7, 64, 4), (60000, 4, 2048, 5), (70001, 6, 3000, 6)])
+                                               (50000, 7, 64, 4), (60000, 4, 2048, 5), (70001, 6, 3000, 6),
+                                               (1536 * 1024 + 1, 3, 32, 7), (2_000_000, 2, 1, 8),
+                                               (1536 * 1024 + 5000, 2, 2048, 9)])
 def test_partition_bit_exact(n, m, n_nodes, seed):
     rng = np.random.default_rng(seed)
     bins = rng.integers(0, 256, (n, m), dtype=np.uint8)
