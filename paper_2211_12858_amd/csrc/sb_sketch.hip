@@ -111,26 +111,48 @@ k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __res
   }
 }
 
-// One block.
+// One block (Top Outputs: one block per 64 columns).
 constexpr int SELECT_LDS_D = 4096;  // Random Sampling prefix sums held in LDS up to this d
 
 __global__ void __launch_bounds__(1024)
 k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __restrict__ u,
          int32_t* __restrict__ cols, float* __restrict__ scales, double* __restrict__ C) {
+  __shared__ double sbuf[SELECT_LDS_D];  // the norms (Top Outputs) or their prefix sums (Random Sampling)
+  if (kind != SB_SKETCH_TOP_OUTPUTS && blockIdx.x > 0) return;  // one block but for Top Outputs
   if (kind == SB_SKETCH_IDENTITY) {
     for (int t = threadIdx.x; t < k; t += blockDim.x) {
       cols[t] = t;
       scales[t] = 1.0f;
     }
   } else if (kind == SB_SKETCH_TOP_OUTPUTS) {
-    // rank of column j in the order (norm descending, index ascending)
-    for (int j = threadIdx.x; j < d; j += blockDim.x) {
-      const double v = n2[j];
-      int rank = 0;
-      for (int l = 0; l < d; ++l) {
-        const double w = n2[l];
-        rank += (w > v) || (w == v && l < j);
+    // rank of column j in the order (norm descending, index ascending).
+    // Block b ranks columns 64b .. 64b+63; its 16 waves count the columns
+    // ahead of them in 16 parts of [0, d) and the parts meet in LDS.  Up to
+    // SELECT_LDS_D norms are read from LDS (a wave reads one l at a time: a
+    // broadcast).
+    __shared__ int32_t cnt[16][64];
+    const bool in_lds = d <= SELECT_LDS_D;
+    if (in_lds) {
+      for (int l = threadIdx.x; l < d; l += blockDim.x) sbuf[l] = n2[l];
+      __syncthreads();
+    }
+    const double* N = in_lds ? sbuf : n2;
+    const int lane = threadIdx.x & 63, part = threadIdx.x >> 6;
+    const int j = blockIdx.x * 64 + lane;
+    const int per = (d + 15) / 16, l0 = part * per, l1 = l0 + per < d ? l0 + per : d;
+    int ahead = 0;
+    if (j < d) {
+      const double v = N[j];
+      for (int l = l0; l < l1; ++l) {
+        const double w = N[l];
+        ahead += (w > v) || (w == v && l < j);
       }
+    }
+    cnt[part][lane] = ahead;
+    __syncthreads();
+    if (part == 0 && j < d) {
+      int rank = 0;
+      for (int q = 0; q < 16; ++q) rank += cnt[q][lane];
       if (rank < k) {
         cols[rank] = j;
         scales[rank] = 1.0f;
@@ -140,17 +162,16 @@ k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __
     // the prefix sums are formed sequentially (the order the draws are
     // defined with); up to SELECT_LDS_D norms they live in LDS, so the
     // sum and the searches wait on LDS instead of global memory
-    __shared__ double sC[SELECT_LDS_D];
     const bool in_lds = d <= SELECT_LDS_D;
-    double* Cw = in_lds ? sC : C;
+    double* Cw = in_lds ? sbuf : C;
     if (in_lds) {
-      for (int j = threadIdx.x; j < d; j += blockDim.x) sC[j] = n2[j];
+      for (int j = threadIdx.x; j < d; j += blockDim.x) sbuf[j] = n2[j];
       __syncthreads();
     }
     if (threadIdx.x == 0) {
       double acc = 0.0;
       for (int j = 0; j < d; ++j) {
-        acc = acc + (in_lds ? sC[j] : n2[j]);
+        acc = acc + (in_lds ? sbuf[j] : n2[j]);
         Cw[j] = acc;
       }
     }
@@ -866,8 +887,9 @@ int32_t launch_sketch(int32_t kind, const float* G, int64_t n, int32_t d, int64_
       hipLaunchKernelGGL(k_colnorm_partial, dim3(P, d), dim3(NORM_THREADS), 0, st, G, n, ld_g, P, chunk, part);
       hipLaunchKernelGGL(k_colnorm_final, dim3((d + 3) / 4), dim3(256), 0, st, part, d, P, n2, norm2);
     }
-    hipLaunchKernelGGL(k_select, dim3(1), dim3(1024), 0, st, kind, norm2_in ? norm2_in : n2, d, k, u, cols, scales,
-                       C);
+    const unsigned sel_blocks = kind == SB_SKETCH_TOP_OUTPUTS ? (unsigned)((d + 63) / 64) : 1u;
+    hipLaunchKernelGGL(k_select, dim3(sel_blocks), dim3(1024), 0, st, kind, norm2_in ? norm2_in : n2, d, k, u, cols,
+                       scales, C);
     nb = sketch_blocks(n, PACK_ROWS_PER_BLOCK);
     if (k < PACK_CG && ld_gh <= PACK_CG) {
 #define SB_PACK(K)                                                                                               \
