@@ -79,9 +79,9 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
                                 double mcw = 0.0, uint32_t* qrow = nullptr, bool qrow_ready = false,
                                 bool store_h = true, int32_t* root_off = nullptr);
 // The fused level end (reduction, subtraction and per-feature scoring in one
-// kernel) stages both nodes' values of one feature in LDS: channels up to
-// this many (64 KB at 256 bins).
-constexpr int FUSED_SCORE_MAX_C = 16;
+// kernel) holds a bin's channel sums of both nodes in registers: channels up
+// to this many (every sketch the histogram kernel takes).
+constexpr int FUSED_SCORE_MAX_C = 24;
 int32_t launch_subtract(const double* Hp, double* Hc, int32_t n_parents, int64_t cells_per_node,
                         const int32_t* build_list, hipStream_t st);
 

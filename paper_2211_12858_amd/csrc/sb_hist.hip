@@ -1146,17 +1146,20 @@ int32_t launch_build_histograms(const uint32_t* bins4, int64_t ld4, const uint8_
     ScoreOut so{feat_s, feat_b, lam, mcw};
     const dim3 g(m, n_build);
     // dynamic LDS: the partial sums of quarters 1..3 ([quarter][pair][256])
-    const int pm = pl.pairs <= 3 ? 3 : pl.pairs <= 4 ? 4 : pl.pairs <= 6 ? 6 : 8;
-    const bool wide = pl.q >= 12 * n_build;  // a node spans about q / n_build row groups
+    const int pm = pl.pairs <= 3 ? 3 : pl.pairs <= 4 ? 4 : pl.pairs <= 6 ? 6 : pl.pairs <= 8 ? 8 : 12;
+    // four threads per bin where a node spans about q / n_build >= 12 row
+    // groups; not at 12 pairs, where the 1024-thread block would spill
+    const bool wide = pl.q >= 12 * n_build && pm < 12;
     const int rq = wide ? 4 : 1;
     const size_t lds = (size_t)(rq - 1) * pm * 256 * 16;
 #define SB_RS(P, R) hipLaunchKernelGGL((k_hist_reduce_score<P, R>), g, dim3(256 * R), lds, st, a, so)
     if (pm == 3) { if (wide) SB_RS(3, 4); else SB_RS(3, 1); }
     else if (pm == 4) { if (wide) SB_RS(4, 4); else SB_RS(4, 1); }
     else if (pm == 6) { if (wide) SB_RS(6, 4); else SB_RS(6, 1); }
-    else if (pl.pairs <= 8) { if (wide) SB_RS(8, 4); else SB_RS(8, 1); }
+    else if (pm == 8) { if (wide) SB_RS(8, 4); else SB_RS(8, 1); }
+    else if (pl.pairs <= 12) SB_RS(12, 1);
 #undef SB_RS
-    else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 16 channels");
+    else return fail(SB_E_UNSUPPORTED, "sb_grow_tree: the fused histogram scoring takes at most 24 channels");
   } else {
     dim3 rg((pl.cells + 255) / 256, n_build, pl.slices);
     hipLaunchKernelGGL(k_hist_reduce, rg, dim3(256), 0, st, a);
