@@ -517,9 +517,10 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
   double* feat_s = reinterpret_cast<double*>(w + G.feat_s);
   int32_t* feat_b = reinterpret_cast<int32_t*>(w + G.feat_b);
   uint32_t* qrow = reinterpret_cast<uint32_t*>(w + G.qrow);
-  // the fused level end (histogram reduction, subtraction and per-feature
-  // scoring in one kernel) holds its per-bin channel sums in registers
-  const bool fused = k + 1 <= FUSED_SCORE_MAX_C;
+  // every level ends with the fused kernel (histogram reduction, subtraction
+  // and per-feature scoring), which takes every sketch the histogram kernel
+  // takes
+  static_assert(FUSED_SCORE_MAX_C >= ROT_MAX_C, "the fused level end covers every histogram shape");
   void* cws = w + G.call;
 
   // level l node offsets start at offs + (2^l - 1) + l (2^l + 1 entries), its
@@ -543,24 +544,22 @@ int32_t sb_grow_tree(const uint32_t* bins4, int64_t ld4, const uint8_t* bins_cm,
     const int64_t base = (int64_t(1) << l) - 1;
     if (l == 0) {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, nullptr, off_l, 1,
-                                   nullptr, 1, Hcur, cws, st, pre, nullptr, fused ? feat_s : nullptr, feat_b, lambda,
+                                   nullptr, 1, Hcur, cws, st, pre, nullptr, feat_s, feat_b, lambda,
                                    min_child_weight, qrow, false, depth > 1, const_cast<int32_t*>(off_l));
     } else {
       rc = launch_build_histograms(bins4, ld4, rec, ld_rec, n, m, n_bins, GH, ld_gh, k, qexp, row_in, off_l, nn,
                                    level_build(l), nn / 2, Hcur, cws, st, pre, Hbuf[(l - 1) & 1],
-                                   fused ? feat_s : nullptr, feat_b, lambda, min_child_weight, qrow, true,
+                                   feat_s, feat_b, lambda, min_child_weight, qrow, true,
                                    l < depth - 1);
     }
     if (rc) return rc;
     // node splits: picked by the partition from the fused level end's
-    // per-feature results where it can, else by the scoring kernels first
-    const bool pick = fused && partition_picks_splits(n, nn);
-    if (fused && !pick)
+    // per-feature results where it can, else by the node argmax kernel first
+    const bool pick = partition_picks_splits(n, nn);
+    if (!pick) {
       rc = launch_score_node(feat_s, feat_b, nn, m, tree_feature + base, tree_bin + base, tree_score + base, st);
-    else if (!fused)
-      rc = launch_score(Hcur, nn, m, n_bins, k, lambda, min_child_weight, tree_feature + base, tree_bin + base,
-                        tree_score + base, cws, st);
-    if (rc) return rc;
+      if (rc) return rc;
+    }
     const bool last = l == depth - 1;
     rc = launch_partition(bins_cm, n, m, ld_cm, row_in, off_l, nn, tree_feature + base, tree_bin + base,
                           level_rows(l + 1), last ? leaf_off_out : level_off(l + 1), level_build(l + 1), cws, st,
