@@ -28,6 +28,10 @@ SKETCH_CASES = [
     (70001, 100, 5, "random_sampling", 4),
     (5000, 7, 1, "random_sampling", 5),
     (33333, 50, 10, "top_outputs", 6),
+    # more outputs than the selection holds in LDS (4096): norms read from
+    # global memory; Top Outputs over 79 blocks of 64 columns
+    (1000, 5000, 7, "top_outputs", 7),
+    (1000, 5000, 3, "random_sampling", 8),
 ]
 
 
