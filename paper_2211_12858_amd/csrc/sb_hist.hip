@@ -411,9 +411,12 @@ k_quant_rows_wide(const float* __restrict__ GH, int64_t ld_gh, int64_t n, int c,
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const uint32_t* p = reinterpret_cast<const uint32_t*>(GH + i * ld_gh);
-  uint32_t w[CM];
+  // the values come in fours, so the row buffer is a whole number of fours
+  // (CM = 18 is not)
+  constexpr int CW = (CM + 3) / 4 * 4;
+  uint32_t w[CW];
 #pragma unroll
-  for (int j = 0; j < CM; j += 4) {
+  for (int j = 0; j < CW; j += 4) {
     if (j + 3 < c) {
       const u32x4_a4 v = *reinterpret_cast<const u32x4_a4*>(p + j);
       w[j] = v.x;

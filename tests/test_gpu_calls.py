@@ -123,6 +123,14 @@ HIST_CASES = [
     (6000, 7, 32, 3, 2, False, 10),         # only a thin slice of 8 features, root
     (9001, 40, 256, 4, 8, True, 11),        # two full slices and a thin slice of 8, odd channel count
     (4000, 2, 256, 5, 1, False, 12),        # thin slice of 2 features (eight copies)
+    # channel groups of six: every group count and the partial last groups
+    (6000, 17, 64, 6, 4, True, 13),         # k=6: two groups, the last of one channel
+    (6000, 17, 64, 11, 1, False, 14),       # k=11: two full groups, root
+    (5000, 9, 32, 12, 2, False, 15),        # k=12: three groups, the last of one channel
+    (9000, 13, 256, 15, 8, True, 16),       # k=15: three groups, the last of four channels
+    (7000, 20, 64, 17, 4, True, 17),        # k=17: three full groups
+    (6000, 18, 128, 18, 2, True, 18),       # k=18: four groups, the last of one channel
+    (6000, 18, 256, 23, 1, False, 19),      # k=23: 24 channels, the widest sketch taken
 ]
 
 
@@ -160,12 +168,14 @@ def test_histograms(n, m, B, k, n_nodes, build, seed):
         assert np.isnan(Hg[others]).all()
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 11, 12, 15, 17, 23])
 @pytest.mark.parametrize("gathered", [False, True])
 def test_histograms_quantised_extremes(k, gathered):
     # values whose fixed-point images reach the largest magnitude, 2^18
     # (1 - 2^-24 with exponent 18), mixed with both signs of small values, on
-    # every channel count the 16-byte quantised rows hold (c = 2 .. 6)
+    # every channel count one 16-byte quantised row holds (c = 2 .. 6) and on
+    # one, two, three and four such words per row with full and partial last
+    # words (c = 7 .. 24)
     rng = np.random.default_rng(100 + k)
     n, m, B = 3001, 9, 16
     c = k + 1

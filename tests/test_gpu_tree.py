@@ -103,6 +103,14 @@ def test_tree_edge_shapes(n, m, B, d, depth):
     check_tree(small_case(n, m, B, d, seed=n), "identity", d, depth, n_bins=B)
 
 
+@pytest.mark.parametrize("d", [7, 15, 23])
+def test_tree_every_level_end_width(d):
+    # 8, 16 and 24 channels (k = d = 7, 15, 23): the register widths of the
+    # fused level end not met by the workloads above; 24 channels is the
+    # widest sketch the histogram calls take
+    check_tree(small_case(30_000, 20, 32, d, seed=d, h_kind="uniform"), "identity", d, 5, n_bins=32)
+
+
 def test_tree_constant_features_are_terminal():
     case = small_case(5000, 4, 8, 3, seed=1)
     case.bins[:] = 3
@@ -152,6 +160,25 @@ def test_per_step_calls_grow_the_same_tree(name, kw):
         assert np.array_equal(fused["score"][l].view(np.uint64), steps["score"][l].view(np.uint64)), l
     assert np.array_equal(fused["row_idx"], steps["row_idx"])
     assert np.array_equal(fused["leaf_off"], steps["leaf_off"])
+
+
+@pytest.mark.parametrize("d", [7, 15, 23])
+def test_per_step_calls_grow_the_same_tree_wide(d):
+    """As above for 8, 16 and 24 channels on 400,000 rows, so that the first
+    levels take the level end's four-threads-per-bin form where it exists."""
+    case = small_case(400_000, 40, 64, d, seed=100 + d, h_kind="uniform")
+    ss = grow_on_device(case, "identity", d, 6, n_bins=64)
+    fused = ss.tree()
+    ss.grow_levelwise()
+    gu.sync()
+    steps = ss.tree()
+    for l in range(6):
+        assert np.array_equal(fused["feature"][l], steps["feature"][l]), l
+        assert np.array_equal(fused["bin"][l], steps["bin"][l]), l
+        assert np.array_equal(fused["score"][l].view(np.uint64), steps["score"][l].view(np.uint64)), l
+    assert np.array_equal(fused["row_idx"], steps["row_idx"])
+    assert np.array_equal(fused["leaf_off"], steps["leaf_off"])
+    assert (fused["feature"][0] >= 0).all()
 
 
 def test_fused_level_end_escaped_partials():
