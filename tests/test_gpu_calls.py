@@ -48,6 +48,19 @@ def test_sketch_bit_exact(n, d, k, kind, seed):
     assert not pad.any()  # the rows are written whole: padding floats are 0
 
 
+@pytest.mark.parametrize("k", range(1, 24))
+def test_sketch_every_width(k):
+    # every sketch width the histogram calls take (k + 1 <= 24): the packing
+    # kernel's per-width instantiations, odd row counts, bit for bit
+    case = small_case(1031, 1, 2, 30, seed=200 + k, h_kind="random", k=k)
+    GH_g, cols_g, sc_g, _, qexp_g, pad = gu.run_sketch("top_outputs", case.G_T, case.h, k)
+    GH_o, cols_o, sc_o, _ = oracle.sketch("top_outputs", case.G, case.h, k)
+    assert np.array_equal(cols_g, cols_o)
+    assert np.array_equal(GH_g.view(np.uint32), GH_o.view(np.uint32))
+    assert np.array_equal(qexp_g, gu.qexp_rule(GH_o))
+    assert not pad.any()
+
+
 def test_sketch_random_sampling_zero_gradients():
     n, d, k = 3000, 6, 4
     G_T = np.zeros((d, n), dtype=np.float32)
@@ -90,6 +103,25 @@ def test_random_projection_error_bound(n, d, k, seed):
     assert np.all(err <= gamma * absprod + u * np.abs(GH_o[:, :k]) + 1e-30)
     assert np.array_equal(GH_g[:, k], case.h)
     assert np.array_equal(qexp_g, gu.qexp_rule(GH_g))
+
+
+@pytest.mark.parametrize("k", range(1, 34))
+def test_random_projection_every_width(k):
+    # every column count of one 32-column pass and a second pass of one: the
+    # vector kernel below 8 columns, the matrix-core kernel with 1 to 8 groups
+    # of four columns (partial last groups), within the dot-product bound
+    d = 37
+    case = small_case(1500, 1, 2, d, seed=300 + k, k=k)
+    GH_g, _, _, _, qexp_g, pad = gu.run_sketch("random_projection", case.G_T, case.h, k, Pi=case.Pi)
+    GH_o = oracle.random_projection(case.G, case.h, case.Pi)
+    u = 2.0 ** -24
+    gamma = d * u / (1 - d * u)
+    absprod = np.abs(np.asarray(case.G, dtype=np.float64)) @ np.abs(case.Pi.astype(np.float64))
+    err = np.abs(GH_g[:, :k].astype(np.float64) - GH_o[:, :k])
+    assert np.all(err <= gamma * absprod + u * np.abs(GH_o[:, :k]) + 1e-30)
+    assert np.array_equal(GH_g[:, k], case.h)
+    assert np.array_equal(qexp_g, gu.qexp_rule(GH_g))
+    assert not pad.any()
 
 
 # ---------------------------------------------------------------- histograms
