@@ -101,21 +101,23 @@ def test_leaf_values_of_a_grown_tree():
     check(case.G_T, tree["row_idx"], tree["leaf_off"], 1.0)
 
 
+@pytest.mark.parametrize("n_leaves", [16, 1000, 4096])
 @pytest.mark.parametrize("loss", ["softmax", "sigmoid"])
-def test_leaf_values_from_loss(loss):
+def test_leaf_values_from_loss(loss, n_leaves):
     # hessians formed from G and the targets on the device; the oracle uses the
     # fp32-rounded hessians of the same scores.  g carries at most 2^-24 of
     # rounding, p = g + target and h = p (1 - p) one more each, and the
-    # oracle's stored h one: at most 3.5 * 2^-24 < 2^-22 per element.
+    # oracle's stored h one: at most 3.5 * 2^-24 < 2^-22 per element.  1000
+    # and 4096 leaves take narrower blocks (4 and 1 channel pairs) and 16-bit
+    # leaf ids.
     from oracle import boost as ob
     from workloads import scores_and_targets
     n, d = 2 * 2048 + 901, 6
     F_T, tgt = scores_and_targets(n, d, loss, seed=71, scale=2.0)
     tgt_o = tgt if loss == "softmax" else tgt.T
     G, Hd, _, _ = ob.gradients(loss, F_T.T, tgt_o)
-    row_idx, leaf_off = grouping(n, 16, seed=72, empty=(5,))
+    row_idx, leaf_off = grouping(n, n_leaves, seed=72, empty=(5,))
     G_T = np.ascontiguousarray(G.T)
-    n_leaves = 16
     V = torch.full((n_leaves, d), float("nan"), dtype=torch.float64, device=gu.DEV)
     ws = gu.workspace(gu.L.sb_workspace_bytes(gu.L.SB_CALL_LEAF_VALUES, n=n, d=d, n_nodes=n_leaves), gu.DEV)
     labels = gu.up(tgt) if loss == "softmax" else None

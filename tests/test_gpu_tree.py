@@ -96,10 +96,12 @@ def test_tree_wide_row_records():
     check_tree(make_inputs(wl), "top_outputs", wl.k, wl.depth, ld_rec=256)
 
 
-@pytest.mark.parametrize("n,m,B,d,depth", [(1, 1, 2, 2, 3), (7, 2, 2, 3, 4), (300, 5, 3, 2, 5), (4099, 9, 16, 4, 7)])
+@pytest.mark.parametrize("n,m,B,d,depth", [(1, 1, 2, 2, 3), (7, 2, 2, 3, 4), (300, 5, 3, 2, 5), (4099, 9, 16, 4, 7),
+                                           (20000, 6, 16, 3, 12), (200_000, 12, 32, 5, 12)])
 def test_tree_edge_shapes(n, m, B, d, depth):
     # tiny and ragged inputs, depth beyond what the rows can split (terminal
-    # nodes and empty children on deep levels)
+    # nodes and empty children on deep levels), and the deepest tree taken
+    # (depth 12: 2048 nodes on the last level)
     check_tree(small_case(n, m, B, d, seed=n), "identity", d, depth, n_bins=B)
 
 
