@@ -113,6 +113,13 @@ def test_tree_every_level_end_width(d):
     check_tree(small_case(30_000, 20, 32, d, seed=d, h_kind="uniform"), "identity", d, 5, n_bins=32)
 
 
+@pytest.mark.parametrize("B", [65, 100, 200, 255])
+def test_tree_bin_counts_past_one_wave(B):
+    # the level end's scan over bins crosses waves (64 bins each) and the last
+    # wave is partial
+    check_tree(small_case(30_000, 10, B, 5, seed=B, h_kind="uniform"), "identity", 5, 5, n_bins=B)
+
+
 def test_tree_constant_features_are_terminal():
     case = small_case(5000, 4, 8, 3, seed=1)
     case.bins[:] = 3
