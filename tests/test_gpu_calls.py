@@ -163,6 +163,9 @@ HIST_CASES = [
     (7000, 20, 64, 17, 4, True, 17),        # k=17: three full groups
     (6000, 18, 128, 18, 2, True, 18),       # k=18: four groups, the last of one channel
     (6000, 18, 256, 23, 1, False, 19),      # k=23: 24 channels, the widest sketch taken
+    # more slices than an XCD has CUs (one row group per XCD)
+    (5000, 1000, 256, 5, 2, True, 20),      # 62 full slices and a padded one
+    (3000, 333, 64, 15, 1, False, 21),      # 20 full slices and a padded one of 13 features, three channel groups
 ]
 
 

@@ -120,6 +120,12 @@ def test_tree_bin_counts_past_one_wave(B):
     check_tree(small_case(30_000, 10, B, 5, seed=B, h_kind="uniform"), "identity", 5, 5, n_bins=B)
 
 
+def test_tree_many_features():
+    # 500 features: 31 full slices, then a thin slice of 4 at the root and a
+    # padded one below it; one row group per XCD
+    check_tree(small_case(20_000, 500, 64, 5, seed=500, h_kind="uniform"), "identity", 5, 4, n_bins=64)
+
+
 def test_tree_constant_features_are_terminal():
     case = small_case(5000, 4, 8, 3, seed=1)
     case.bins[:] = 3
