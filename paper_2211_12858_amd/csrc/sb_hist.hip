@@ -1,7 +1,9 @@
 // Per-node histograms of one tree level (Section 3.4) and sibling subtraction.
 //
 // Design for gfx950.  The scatter-add of random bins into LDS bounds this
-// kernel, so every choice below serves the LDS data path:
+// kernel where rows are contiguous (the root); below it the gathered loads
+// of scattered rows weigh as much.  Every choice below serves the LDS data
+// path:
 //  * every sketch value is quantised to an integer rint(v * 2^qexp[t]) of
 //    magnitude <= 2^QBITS (written once per tree as 21-bit fields of one
 //    16-byte word per row and channel group of six);
@@ -787,12 +789,14 @@ __device__ inline bool score_better(double sa, int ia, double sb_, int ib) {
 }
 
 // Fused end of a level (the level loop's path): one block per (feature f,
-// built node p), one thread per bin.  The block sums feature f's int64
-// partials of node p, writes the fp64 histogram of the built node j (and,
-// with the parent level given, of its sibling by exact subtraction), then
-// scores every threshold of f for both nodes as k_score_feature does
-// (Section 2, eq. 4: prefix sums over bins, fp64, ties to the lower bin)
-// and writes the best (score, bin) per (node, feature) for k_score_node.
+// built node p), one thread per bin.  The block sums feature f's int32
+// partials of node p (with the int64 overflow slots where a sum escaped),
+// writes the fp64 histogram of the built node j (and, with the parent level
+// given, of its sibling by exact subtraction), then scores every threshold
+// of f for both nodes as k_score_feature does (Section 2, eq. 4: prefix sums
+// over bins, fp64, ties to the lower bin) and writes the best (score, bin)
+// per (node, feature) for the node argmax (in the partition's first kernel,
+// or k_score_node).
 struct ScoreOut {
   double* s;
   int32_t* b;
