@@ -126,6 +126,15 @@ def test_tree_many_features():
     check_tree(small_case(20_000, 500, 64, 5, seed=500, h_kind="uniform"), "identity", 5, 4, n_bins=64)
 
 
+@pytest.mark.parametrize("lam,mcw", [(1e-3, 0.0), (0.1, 5.0), (10.0, 100.0)])
+def test_tree_lambda_and_min_child_weight(lam, mcw):
+    # the level end's lambda and min_child_weight (hessians in [0.05, 0.25],
+    # so that 100 leaves some deep nodes without a valid split)
+    stats = check_tree(small_case(30_000, 12, 64, 6, seed=40, h_kind="uniform"), "identity", 6, 6, lam=lam, mcw=mcw,
+                       n_bins=64)
+    assert stats["nodes"] > 0
+
+
 def test_tree_constant_features_are_terminal():
     case = small_case(5000, 4, 8, 3, seed=1)
     case.bins[:] = 3
