@@ -164,6 +164,29 @@ __device__ inline void leaf_load(const LeafArgs& a, const float* const (&col)[J]
   }
 }
 
+// A float moved across lanes by a DPP control (row shift or row broadcast);
+// lanes the control does not write get 0.
+template <int CTRL, int ROW_MASK>
+__device__ inline float dpp_f32(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, false));
+}
+
+// Maximum of non-negative values over the 64 lanes of a wave, in registers
+// (no LDS traffic): shifts by 1, 2, 4 and 8 lanes inside each row of 16, then
+// the last lane of rows 0 and 2 into rows 1 and 3 (row_bcast:15) and lane 31
+// into rows 2 and 3 (row_bcast:31).  Lanes a step does not write take 0,
+// which leaves a maximum of non-negative values unchanged.  Lane 63 ends
+// with the wave's maximum.
+__device__ inline float wave_max_nonneg(float x) {
+  x = fmaxf(x, dpp_f32<0x111, 0xf>(x));
+  x = fmaxf(x, dpp_f32<0x112, 0xf>(x));
+  x = fmaxf(x, dpp_f32<0x114, 0xf>(x));
+  x = fmaxf(x, dpp_f32<0x118, 0xf>(x));
+  x = fmaxf(x, dpp_f32<0x142, 0xa>(x));
+  x = fmaxf(x, dpp_f32<0x143, 0xc>(x));
+  return x;
+}
+
 // One tile: block-wide maximum per channel, quantisation, integer adds into
 // the LDS cells, then the exact fp64 conversion into the accumulators.
 template <int J, int SPT>
@@ -177,8 +200,8 @@ __device__ inline void leaf_tile(const LeafTile<J, SPT>& x, const bool (&live)[J
     float mx = 0.0f;
 #pragma unroll
     for (int s = 0; s < SPT; ++s) mx = fmaxf(mx, fabsf(x.v[s][j]));
-    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
-    if (lane == 0) wmax[wave][j] = mx;
+    mx = wave_max_nonneg(mx);
+    if (lane == 63) wmax[wave][j] = mx;
   }
   __syncthreads();
   double sc[J];
