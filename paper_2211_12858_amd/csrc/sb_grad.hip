@@ -12,7 +12,8 @@
 //   The squared column norms of the stored G (what Top Outputs and Random
 //   Sampling rank and draw by, Sections 3.1, 3.2) are summed in the same pass:
 //   each 16-column chunk of g goes through LDS, 16 threads per column add 16
-//   rows each in fp64, a fixed butterfly joins them, and one thread adds the
+//   rows each in fp64, a fixed shift-and-add over their 16 lanes (DPP, in
+//   registers) joins them, and one thread adds the
 //   tile's sum to its slot's partial (slot = tile mod GRAD_PARTS, always the
 //   same thread of the same block, in tile order).  k_grad_norm_final adds the
 //   slots in a fixed order, so the norms are deterministic and the same for
@@ -34,6 +35,24 @@
 
 namespace sb {
 namespace {
+
+// Sum over each row of 16 lanes, in registers (no LDS traffic): shifts by 1,
+// 2, 4 and 8 lanes (lanes a shift does not write add 0), so the last lane of
+// each row ends with the row's sum, always added in the same order.
+template <int CTRL>
+__device__ inline double dpp_row_shr(double x) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(x), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(x), CTRL, 0xf, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+
+__device__ inline double row16_sum(double x) {
+  x += dpp_row_shr<0x111>(x);
+  x += dpp_row_shr<0x112>(x);
+  x += dpp_row_shr<0x114>(x);
+  x += dpp_row_shr<0x118>(x);
+  return x;
+}
 
 constexpr int GRAD_THREADS = 256;
 constexpr int GRAD_JA = 8;          // columns per load batch of the softmax first pass
@@ -171,8 +190,8 @@ __device__ inline void grad_tile(const GradArgs& a, float (*gbuf)[GRAD_THREADS],
         acc += (double)v.z * v.z;
         acc += (double)v.w * v.w;
       }
-      for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-      if (seg == 0 && j0 + c < d) {
+      acc = row16_sum(acc);  // in the row's last lane
+      if (seg == 15 && j0 + c < d) {
         const int tile = (int)(base / GRAD_THREADS);
         double* pp = a.npart + (int64_t)(j0 + c) * a.n_parts + tile % a.n_parts;
         *pp = tile < a.n_parts ? acc : *pp + acc;  // the slot's first tile writes it
@@ -290,8 +309,8 @@ __device__ inline void grad_softmax_tile(const GradArgs& a, float (*gbuf)[GRAD_T
         acc += (double)v.z * v.z;
         acc += (double)v.w * v.w;
       }
-      for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-      if (seg == 0 && j0 + c < d) {
+      acc = row16_sum(acc);  // in the row's last lane
+      if (seg == 15 && j0 + c < d) {
         const int tile = (int)(base / GRAD_THREADS);
         double* pp = a.npart + (int64_t)(j0 + c) * a.n_parts + tile % a.n_parts;
         *pp = tile < a.n_parts ? acc : *pp + acc;  // the slot's first tile writes it

@@ -198,11 +198,26 @@ k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __
   }
 }
 
+// A value moved across lanes by a DPP control (row shift or row broadcast);
+// lanes the control does not write get 0.
+template <int CTRL, int ROW_MASK>
+__device__ inline uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Maximum over the 64 lanes of a wave, in registers (no LDS traffic):
+// shifts by 1, 2, 4 and 8 lanes inside each row of 16, then the last lane of
+// rows 0 and 2 into rows 1 and 3 (row_bcast:15) and lane 31 into rows 2 and 3
+// (row_bcast:31).  Lanes a step does not write take 0, the smallest value,
+// so lane 63 ends with the wave's maximum.
 __device__ inline uint32_t wave_max_u32(uint32_t v) {
-  for (int off = 32; off > 0; off >>= 1) {
-    uint32_t o = __shfl_down(v, off, 64);
-    v = o > v ? o : v;
-  }
+  uint32_t o;
+  o = dpp_u32<0x111, 0xf>(v); v = o > v ? o : v;
+  o = dpp_u32<0x112, 0xf>(v); v = o > v ? o : v;
+  o = dpp_u32<0x114, 0xf>(v); v = o > v ? o : v;
+  o = dpp_u32<0x118, 0xf>(v); v = o > v ? o : v;
+  o = dpp_u32<0x142, 0xa>(v); v = o > v ? o : v;
+  o = dpp_u32<0x143, 0xc>(v); v = o > v ? o : v;
   return v;
 }
 
@@ -213,7 +228,7 @@ __device__ inline uint32_t block_max_u32(uint32_t v, uint32_t* sh) {
   v = wave_max_u32(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
-  if (lane == 0) sh[wave] = v;
+  if (lane == 63) sh[wave] = v;
   __syncthreads();
   uint32_t r = 0u;
 #pragma unroll
@@ -709,8 +724,8 @@ k_project_mfma4(const float* __restrict__ G, int64_t n, int d, int64_t ld_g, con
     }
     if (lane < 4) smax[wave][4 * g + lane] = mx[g];
   }
-  mxh = wave_max_u32(mxh);
-  if (lane == 0) smax[wave][W] = mxh;
+  mxh = wave_max_u32(mxh);  // in lane 63
+  if (lane == 63) smax[wave][W] = mxh;
   __syncthreads();
   if (threadIdx.x <= W) {
     uint32_t r = 0u;
