@@ -14,35 +14,83 @@ namespace sb {
 // A load of data that is streamed once: it does not allocate in the caches.
 __device__ inline float ld_stream(const float* p) { return __builtin_nontemporal_load(p); }
 
+// A 32-bit value moved across lanes by a DPP control (row shift or row
+// broadcast); lanes the control does not write get `old`.
+template <int CTRL, int ROW_MASK>
+__device__ inline int32_t dpp_i32(int32_t old, int32_t x) {
+  return __builtin_amdgcn_update_dpp(old, x, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (all lanes active), in
+// registers: shifts by 1, 2, 4 and 8 lanes inside each row of 16, then the
+// last lane of rows 0 and 2 into rows 1 and 3 (row_bcast:15) and lane 31
+// into rows 2 and 3 (row_bcast:31); lanes a step does not write add 0.
+__device__ inline int32_t wave_incl_scan_i32(int32_t x) {
+  x += dpp_i32<0x111, 0xf>(0, x);
+  x += dpp_i32<0x112, 0xf>(0, x);
+  x += dpp_i32<0x114, 0xf>(0, x);
+  x += dpp_i32<0x118, 0xf>(0, x);
+  x += dpp_i32<0x142, 0xa>(0, x);
+  x += dpp_i32<0x143, 0xc>(0, x);
+  return x;
+}
+
+// Sum over each row of 16 lanes (all lanes active), in the row's last lane.
+__device__ inline int32_t row16_sum_i32(int32_t x) {
+  x += dpp_i32<0x111, 0xf>(0, x);
+  x += dpp_i32<0x112, 0xf>(0, x);
+  x += dpp_i32<0x114, 0xf>(0, x);
+  x += dpp_i32<0x118, 0xf>(0, x);
+  return x;
+}
+
+// One step of the wave argmax below: the candidate of the lane the DPP
+// control names, where there is one ((-inf, -1), no candidate, elsewhere).
+template <int CTRL, int ROW_MASK>
+__device__ inline void best_step(double& s, int& f, int& b) {
+  const int lo = dpp_i32<CTRL, ROW_MASK>(__double2loint(-INFINITY), __double2loint(s));
+  const int hi = dpp_i32<CTRL, ROW_MASK>(__double2hiint(-INFINITY), __double2hiint(s));
+  const int of = dpp_i32<CTRL, ROW_MASK>(-1, f);
+  const int ob = dpp_i32<CTRL, ROW_MASK>(-1, b);
+  const double os = __hiloint2double(hi, lo);
+  if (of >= 0 && (f < 0 || os > s || (os == s && of < f))) {
+    s = os;
+    f = of;
+    b = ob;
+  }
+}
+
 // Best feature of one node from its per-feature results (score s_f, bin b_f;
-// b_f < 0: no valid threshold), by one wave: larger score first, then the
-// smaller feature.  Fixed reduction order, so every caller gets the same
-// answer.  Outputs (-1, -1, -inf) when no feature has a valid threshold.
+// b_f < 0: no valid threshold), by one wave (all lanes active): larger score
+// first, then the smaller feature.  This is a maximum under a total order,
+// so the result does not depend on the reduction order; the lanes' bests
+// meet in registers (DPP row shifts and broadcasts, ending in lane 63) and
+// every lane gets the result.  Outputs (-1, -1, -inf) when no feature has a
+// valid threshold.
 __device__ inline void wave_best_feature(const double* fs, const int32_t* fb, int m, int32_t* out_f, int32_t* out_b,
                                          double* out_s) {
   const int lane = threadIdx.x & 63;
   double best_s = -INFINITY;
   int best_f = -1, best_bin = -1;
-  auto better = [](double sa, int ia, double sb_, int ib) { return sa > sb_ || (sa == sb_ && ia < ib); };
   for (int f = lane; f < m; f += 64) {
     const int b = fb[f];
     const double s = fs[f];
-    if (b >= 0 && (best_f < 0 || better(s, f, best_s, best_f))) {
+    if (b >= 0 && (best_f < 0 || s > best_s || (s == best_s && f < best_f))) {
       best_s = s;
       best_f = f;
       best_bin = b;
     }
   }
-  for (int off = 32; off > 0; off >>= 1) {
-    const double os = __shfl_xor(best_s, off, 64);
-    const int of = __shfl_xor(best_f, off, 64);
-    const int ob = __shfl_xor(best_bin, off, 64);
-    if (of >= 0 && (best_f < 0 || better(os, of, best_s, best_f))) {
-      best_s = os;
-      best_f = of;
-      best_bin = ob;
-    }
-  }
+  best_step<0x111, 0xf>(best_s, best_f, best_bin);
+  best_step<0x112, 0xf>(best_s, best_f, best_bin);
+  best_step<0x114, 0xf>(best_s, best_f, best_bin);
+  best_step<0x118, 0xf>(best_s, best_f, best_bin);
+  best_step<0x142, 0xa>(best_s, best_f, best_bin);
+  best_step<0x143, 0xc>(best_s, best_f, best_bin);
+  best_f = __builtin_amdgcn_readlane(best_f, 63);
+  best_bin = __builtin_amdgcn_readlane(best_bin, 63);
+  best_s = __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(best_s), 63),
+                            __builtin_amdgcn_readlane(__double2loint(best_s), 63));
   *out_f = best_f;
   *out_b = best_f >= 0 ? best_bin : -1;
   *out_s = best_f >= 0 ? best_s : -INFINITY;

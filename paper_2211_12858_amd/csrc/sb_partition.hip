@@ -408,11 +408,8 @@ __device__ int64_t block_scan_nt(int N, V v, O out, int64_t* sh) {
   int64_t local = 0;
   for (int i = 0; i < per; ++i)
     if (p0 + i < N) local += v(p0 + i);
-  int64_t incl = local;
-  for (int off = 1; off < 64; off <<= 1) {
-    const int64_t o = __shfl_up(incl, off, 64);
-    if (lane >= off) incl += o;
-  }
+  // every partial sum is a count of positions, below 2^31
+  const int64_t incl = wave_incl_scan_i32((int32_t)local);
   __syncthreads();
   if (lane == 63) sh[wave] = incl;
   __syncthreads();
@@ -579,11 +576,7 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
   // the block's ballots and their prefix
   if (wave == 0) {
     const int32_t c = popc64(my_mask);
-    int32_t incl = c;
-    for (int off = 1; off < 64; off <<= 1) {
-      const int32_t o = __shfl_up(incl, off, 64);
-      if (lane >= off) incl += o;
-    }
+    const int32_t incl = wave_incl_scan_i32(c);
     if (lane < NM) {
       mk[lane] = my_mask;
       pre[lane] = s_toff[blockIdx.x] + incl - c;
@@ -607,8 +600,9 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
   const int J0 = span[0], J1 = span[1];
   // Lb_j = left flags before position off[j]: the tile offset of its tile
   // plus the popcounts of the ballots before it.  PT_MASKS consecutive lanes
-  // share a boundary (one ballot each) and add their counts with shuffles.
-  static_assert(PT_THREADS % PT_MASKS == 0 && 64 % PT_MASKS == 0, "a boundary's ballots share one wave");
+  // share a boundary (one ballot each, one row of 16 lanes) and add their
+  // counts in registers, the sum ending in the row's last lane.
+  static_assert(PT_MASKS == 16 && PT_THREADS % 64 == 0, "a boundary's ballots fill one row of 16 lanes");
   const int nb = J1 - J0 + 1;
   for (int e0 = 0; e0 < nb * PT_MASKS; e0 += PT_THREADS) {
     const int e = e0 + threadIdx.x;
@@ -629,8 +623,8 @@ __global__ void __launch_bounds__(PT_THREADS) k_part_scan_scatter(PartArgs a) {
         if (TPB == 2 && q == 0 && (tx & 1)) c += a.tile_cnt[tx - 1];  // the pair's first tile
       }
     }
-    for (int o = PT_MASKS / 2; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
-    if (e < nb * PT_MASKS && q == 0) s_lb[jb] = in ? s_toff[tx / TPB] + c : (int32_t)total;
+    c = row16_sum_i32(c);
+    if (e < nb * PT_MASKS && q == PT_MASKS - 1) s_lb[jb] = in ? s_toff[tx / TPB] + c : (int32_t)total;
   }
   __syncthreads();
   // 3. block 0: child offsets, build list and the built-size prefix
