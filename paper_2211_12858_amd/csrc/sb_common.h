@@ -60,6 +60,31 @@ __device__ inline void best_step(double& s, int& f, int& b) {
   }
 }
 
+// One step of a wave maximum of (score, index) pairs, larger score first,
+// then the smaller index (index < 0: no candidate): the pair of the lane the
+// DPP control names, where there is one ((-inf, -1) elsewhere).
+template <int CTRL, int ROW_MASK>
+__device__ inline void best_step_si(double& s, int& i) {
+  const int lo = dpp_i32<CTRL, ROW_MASK>(__double2loint(-INFINITY), __double2loint(s));
+  const int hi = dpp_i32<CTRL, ROW_MASK>(__double2hiint(-INFINITY), __double2hiint(s));
+  const int oi = dpp_i32<CTRL, ROW_MASK>(-1, i);
+  const double os = __hiloint2double(hi, lo);
+  if (oi >= 0 && (i < 0 || os > s || (os == s && oi < i))) {
+    s = os;
+    i = oi;
+  }
+}
+
+// The best (score, index) pair of a wave (all lanes active), in lane 63.
+__device__ inline void wave_best_si(double& s, int& i) {
+  best_step_si<0x111, 0xf>(s, i);
+  best_step_si<0x112, 0xf>(s, i);
+  best_step_si<0x114, 0xf>(s, i);
+  best_step_si<0x118, 0xf>(s, i);
+  best_step_si<0x142, 0xa>(s, i);
+  best_step_si<0x143, 0xc>(s, i);
+}
+
 // Best feature of one node from its per-feature results (score s_f, bin b_f;
 // b_f < 0: no valid threshold), by one wave (all lanes active): larger score
 // first, then the smaller feature.  This is a maximum under a total order,

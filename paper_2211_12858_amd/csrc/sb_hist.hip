@@ -1015,15 +1015,8 @@ __global__ void __launch_bounds__(256 * RQ) k_hist_reduce_score(HistArgs a, Scor
           best_s = sl / (HL + so.lam) + sr / (HR + so.lam);
           best_b = bin;
         }
-        for (int off = 32; off > 0; off >>= 1) {
-          const double os = __shfl_xor(best_s, off, 64);
-          const int ob = __shfl_xor(best_b, off, 64);
-          if (ob >= 0 && (best_b < 0 || score_better(os, ob, best_s, best_b))) {
-            best_s = os;
-            best_b = ob;
-          }
-        }
-        if (lane == 0) {
+        wave_best_si(best_s, best_b);  // in lane 63, the reduction in registers
+        if (lane == 63) {
           wbest_s[u][wave] = best_s;
           wbest_b[u][wave] = best_b;
         }
