@@ -169,9 +169,24 @@ k_select(int kind, const double* __restrict__ n2, int d, int k, const double* __
       __syncthreads();
     }
     if (threadIdx.x == 0) {
+      // eight norms are read ahead of their adds (the adds stay in order),
+      // so the chain waits on the fp64 adds rather than on each read; in LDS
+      // the prefix overwrites the norms already read
+      const double* src = in_lds ? sbuf : n2;
       double acc = 0.0;
-      for (int j = 0; j < d; ++j) {
-        acc = acc + (in_lds ? sbuf[j] : n2[j]);
+      int j = 0;
+      for (; j + 8 <= d; j += 8) {
+        double v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = src[j + q];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          acc = acc + v[q];
+          Cw[j + q] = acc;
+        }
+      }
+      for (; j < d; ++j) {
+        acc = acc + src[j];
         Cw[j] = acc;
       }
     }
