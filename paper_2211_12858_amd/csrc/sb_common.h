@@ -14,6 +14,24 @@ namespace sb {
 // A load of data that is streamed once: it does not allocate in the caches.
 __device__ inline float ld_stream(const float* p) { return __builtin_nontemporal_load(p); }
 
+// Sum of x[p] over p = lane, lane + 64, ... < count, added in that order
+// from 0.0 (a fixed order: the result depends only on the values); eight
+// loads are issued before their adds, so the chain waits once per eight
+// values rather than once per value.
+__device__ inline double lane_strided_sum(const double* x, int count, int lane) {
+  double s = 0.0;
+  int p = lane;
+  for (; p + 7 * 64 < count; p += 8 * 64) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = x[p + u * 64];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; p < count; p += 64) s += x[p];
+  return s;
+}
+
 // A 32-bit value moved across lanes by a DPP control (row shift or row
 // broadcast); lanes the control does not write get `old`.
 template <int CTRL, int ROW_MASK>

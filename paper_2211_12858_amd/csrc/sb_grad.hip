@@ -357,8 +357,7 @@ __global__ void __launch_bounds__(256) k_grad_norm_final(const double* __restric
   const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (j >= d) return;
-  double s = 0.0;
-  for (int p = lane; p < parts; p += 64) s += npart[(int64_t)j * parts + p];
+  double s = lane_strided_sum(npart + (int64_t)j * parts, parts, lane);
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
   if (lane == 0) norm2[j] = s;
 }

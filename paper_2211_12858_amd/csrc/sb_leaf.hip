@@ -300,11 +300,9 @@ __global__ void __launch_bounds__(256) k_leaf_final(const double* __restrict__ p
   const double* ph = hmode == 3   ? part + ((int64_t)L * nch + 2 * j + 1) * n_splits
                      : hmode == 1 ? part + ((int64_t)L * nch + d + j) * n_splits
                                   : part + ((int64_t)L * nch + d) * n_splits;
-  double gs = 0.0, hs = 0.0;
-  for (int s = lane; s < n_splits; s += 64) {
-    gs += pg[s];
-    if (hmode != 0) hs += ph[s];
-  }
+  const double gs0 = lane_strided_sum(pg, n_splits, lane);
+  const double hs0 = hmode != 0 ? lane_strided_sum(ph, n_splits, lane) : 0.0;
+  double gs = gs0, hs = hs0;
   for (int off = 32; off > 0; off >>= 1) {
     gs += __shfl_xor(gs, off, 64);
     hs += __shfl_xor(hs, off, 64);

@@ -102,8 +102,7 @@ k_colnorm_final(const double* __restrict__ part, int d, int parts, double* __res
   const int j = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (j >= d) return;
-  double s = 0.0;
-  for (int p = lane; p < parts; p += 64) s += part[(int64_t)j * parts + p];
+  double s = lane_strided_sum(part + (int64_t)j * parts, parts, lane);
   s = wave_sum(s);
   if (lane == 0) {
     n2[j] = s;
@@ -802,7 +801,15 @@ k_qexp(const uint32_t* __restrict__ blockmax, int nblocks, int c, int32_t* __res
   __shared__ uint32_t sh[4];
   const int t = blockIdx.x;
   uint32_t mx = 0u;
-  for (int b = threadIdx.x; b < nblocks; b += 256) {
+  int b = threadIdx.x;
+  for (; b + 7 * 256 < nblocks; b += 8 * 256) {  // eight loads in flight
+    uint32_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = blockmax[(int64_t)(b + u * 256) * c + t];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) mx = v[u] > mx ? v[u] : mx;
+  }
+  for (; b < nblocks; b += 256) {
     const uint32_t v = blockmax[(int64_t)b * c + t];
     mx = v > mx ? v : mx;
   }
